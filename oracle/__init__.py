@@ -1,0 +1,210 @@
+"""Plain fp64 CPU oracle for batched iteration-period detection.
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the bench's
+CPU-baseline leg are the only users.  The product path (the HIP library and its
+binding) never imports or calls this package, and this package imports nothing
+from the product.
+
+``oracle.c`` (built by ``build()`` with gcc, contraction off, OpenMP) holds the
+score, reference and selection definitions; ``brute.py`` holds exact-rational
+evaluations used to pin it on tiny inputs.  The definitions follow the paper's
+Sec. 4.1.2 (Algorithms 1 and 2) as documented in ``oracle.h``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liboracle_pd.so")
+
+PERIODIC, APERIODIC, CONSTANT = 0, 1, 2
+DEFAULT_C_LAG = 0.9
+DEFAULT_ERR_MAX = 1.0
+
+
+def build(verbose: bool = False) -> str:
+    """Compile oracle.c into liboracle_pd.so (always recompiles)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+           "-fPIC", "-shared", "-Wall", "-Wextra", "-Werror",
+           os.path.join(HERE, "oracle.c"), "-o", LIB_PATH + ".tmp", "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(LIB_PATH + ".tmp", LIB_PATH)
+    return LIB_PATH
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [("num_windows", ctypes.c_int64), ("num_channels", ctypes.c_int32),
+                ("n", ctypes.c_int64), ("window_stride", ctypes.c_int64),
+                ("channel_stride", ctypes.c_int64), ("tmin", ctypes.c_int32),
+                ("tmax", ctypes.c_int32), ("c_lag", ctypes.c_double),
+                ("err_max", ctypes.c_double), ("channel_weights", ctypes.c_void_p)]
+
+
+class _Out(ctypes.Structure):
+    _fields_ = [("period", ctypes.c_int32), ("verdict", ctypes.c_int32), ("err", ctypes.c_double),
+                ("n_candidates", ctypes.c_int32), ("t_cand", ctypes.c_int32),
+                ("t_low", ctypes.c_int32), ("t_up", ctypes.c_int32), ("n_peaks", ctypes.c_int32),
+                ("r", ctypes.c_double), ("s_pk", ctypes.c_double)]
+
+
+OUT_DTYPE = np.dtype([("period", np.int32), ("verdict", np.int32), ("err", np.float64),
+                      ("n_candidates", np.int32), ("t_cand", np.int32), ("t_low", np.int32),
+                      ("t_up", np.int32), ("n_peaks", np.int32), ("r", np.float64),
+                      ("s_pk", np.float64)], align=True)
+assert OUT_DTYPE.itemsize == ctypes.sizeof(_Out)
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            build()
+        lib = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER
+        lib.oracle_pd_reference.restype = ctypes.c_double
+        lib.oracle_pd_reference.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                            ctypes.c_int64, ctypes.c_void_p]
+        lib.oracle_pd_score.restype = ctypes.c_double
+        lib.oracle_pd_score.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                        ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
+        lib.oracle_pd_select.restype = None
+        lib.oracle_pd_select.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                         ctypes.c_int32, ctypes.c_double, ctypes.c_double,
+                                         ctypes.c_double, P(_Out)]
+        lib.oracle_pd_detect.restype = ctypes.c_int
+        lib.oracle_pd_detect.argtypes = [P(_Params), ctypes.c_void_p, ctypes.c_void_p,
+                                         ctypes.c_void_p]
+        lib.oracle_pd_score_list.restype = ctypes.c_int
+        lib.oracle_pd_score_list.argtypes = [P(_Params), ctypes.c_void_p, ctypes.c_void_p,
+                                             ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+        lib.oracle_pd_threads.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def threads() -> int:
+    return int(_load().oracle_pd_threads())
+
+
+@dataclass
+class Layout:
+    num_windows: int
+    num_channels: int
+    n: int
+    window_stride: int
+    channel_stride: int
+    tmin: int
+    tmax: int
+    c_lag: float = DEFAULT_C_LAG
+    err_max: float = DEFAULT_ERR_MAX
+    weights: np.ndarray | None = None
+
+    @classmethod
+    def of(cls, wl, **kw) -> "Layout":
+        """Layout of a gen.Workload (duck-typed), optionally overriding fields."""
+        d = dict(num_windows=wl.num_windows, num_channels=wl.num_channels, n=wl.n,
+                 window_stride=wl.window_stride, channel_stride=wl.channel_stride,
+                 tmin=wl.tmin, tmax=wl.tmax, weights=wl.weights)
+        d.update(kw)
+        return cls(**d)
+
+    @property
+    def lags(self) -> int:
+        return self.tmax - self.tmin + 1
+
+
+def _params(lay: Layout, keep: list) -> _Params:
+    w = None
+    if lay.weights is not None:
+        w = np.ascontiguousarray(lay.weights, dtype=np.float32)
+        keep.append(w)
+    return _Params(lay.num_windows, lay.num_channels, lay.n, lay.window_stride,
+                   lay.channel_stride, lay.tmin, lay.tmax, float(lay.c_lag), float(lay.err_max),
+                   None if w is None else w.ctypes.data)
+
+
+def _as_f32(x: np.ndarray) -> np.ndarray:
+    x = np.ascontiguousarray(x)
+    if x.dtype != np.float32:
+        raise TypeError("oracle inputs are float32 sample buffers")
+    return x.reshape(-1)
+
+
+def _check_extent(x: np.ndarray, lay: Layout) -> None:
+    need = ((lay.num_windows - 1) * lay.window_stride
+            + (lay.num_channels - 1) * lay.channel_stride + lay.n)
+    if x.size < need:
+        raise ValueError(f"buffer has {x.size} samples, layout needs {need}")
+
+
+def detect(x: np.ndarray, lay: Layout, want_scores: bool = True):
+    """Scores [B][L] (fp64, or None) and one result record per window."""
+    x = _as_f32(x)
+    _check_extent(x, lay)
+    keep: list = []
+    p = _params(lay, keep)
+    scores = np.empty((lay.num_windows, lay.lags), dtype=np.float64) if want_scores else None
+    out = np.zeros(lay.num_windows, dtype=OUT_DTYPE)
+    rc = _load().oracle_pd_detect(ctypes.byref(p), x.ctypes.data,
+                                  None if scores is None else scores.ctypes.data,
+                                  out.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle rejected the parameters")
+    return scores, out
+
+
+def score_list(x: np.ndarray, lay: Layout, windows, lags) -> np.ndarray:
+    """S(T) for the given (window, lag) pairs, each one plain sequential fp64 sum."""
+    x = _as_f32(x)
+    _check_extent(x, lay)
+    w = np.ascontiguousarray(windows, dtype=np.int64)
+    t = np.ascontiguousarray(lags, dtype=np.int32)
+    if w.shape != t.shape:
+        raise ValueError("windows and lags differ in length")
+    keep: list = []
+    p = _params(lay, keep)
+    out = np.empty(w.shape, dtype=np.float64)
+    rc = _load().oracle_pd_score_list(ctypes.byref(p), x.ctypes.data, w.ctypes.data,
+                                      t.ctypes.data, int(w.size), out.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle rejected the parameters")
+    return out
+
+
+def score(xw: np.ndarray, t: int, weights=None) -> float:
+    """S(T) of one window given as [C][N] (or [N]) float32."""
+    xw = np.ascontiguousarray(np.atleast_2d(xw), dtype=np.float32)
+    c, n = xw.shape
+    w = None if weights is None else np.ascontiguousarray(weights, dtype=np.float32)
+    return float(_load().oracle_pd_score(xw.ctypes.data, c, n, n, int(t),
+                                         None if w is None else w.ctypes.data))
+
+
+def reference(xw: np.ndarray, weights=None) -> float:
+    """R = 2 * sum_c w_c * Var_c of one window given as [C][N] (or [N]) float32."""
+    xw = np.ascontiguousarray(np.atleast_2d(xw), dtype=np.float32)
+    c, n = xw.shape
+    w = None if weights is None else np.ascontiguousarray(weights, dtype=np.float32)
+    return float(_load().oracle_pd_reference(xw.ctypes.data, c, n, n,
+                                             None if w is None else w.ctypes.data))
+
+
+def select(s: np.ndarray, n: int, tmin: int, tmax: int, r: float,
+           c_lag: float = DEFAULT_C_LAG, err_max: float = DEFAULT_ERR_MAX) -> dict:
+    """The selection rule on one score row s[j] = S(tmin + j)."""
+    s = np.ascontiguousarray(s, dtype=np.float64)
+    if s.shape != (tmax - tmin + 1,):
+        raise ValueError("score row length must be tmax - tmin + 1")
+    o = _Out()
+    _load().oracle_pd_select(s.ctypes.data, int(n), int(tmin), int(tmax), float(r),
+                             float(c_lag), float(err_max), ctypes.byref(o))
+    return {name: getattr(o, name) for name, _ in _Out._fields_}
