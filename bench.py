@@ -1,0 +1,216 @@
+#!/usr/bin/env python3
+"""Throughput of batched iteration-period detection on one MI355X.
+
+One step = one gpoeo_pd_detect call over the whole batch: window statistics,
+lag scores for every T in [Tmin, Tmax] of every window, finalisation and the
+per-window selection.  Inputs are generated (seeded) on the host, copied to HBM
+once, and resident there before the timed region starts.
+
+Prints one JSON line with the throughput (lag*samples/s), traces/s, the
+roofline of the lag-score kernel (timed with HIP events recorded around it on
+the stream it runs on) and the CPU oracle timed on a bounded sample of the same
+workload.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+FP32_VECTOR_PEAK_TFLOPS = 157.3   # MI355X published FP32 vector peak
+FLOP_PER_PAIR = 3                 # one subtraction, one multiply, one add per (x[i], x[i+T])
+METRIC = "lag·samples/sec and traces/sec for batched period detection; % FP32 peak"
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "lag_score_w3_counters.json")
+SCORE_SOURCE = os.path.join(ROOT, "paper_2201_01684_amd", "csrc", "lag_score.hip")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="w3", help="w1..w5 (default w3, the 1024-trace batch)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="approximate CPU time budget of the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+class HipEvents:
+    """hipEvent_t handles from the HIP runtime torch loaded (one runtime per process)."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so.7")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventCreate.restype = ctypes.c_int
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventElapsedTime.restype = ctypes.c_int
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventDestroy.restype = ctypes.c_int
+
+    def create(self, count):
+        arr = (ctypes.c_void_p * count)()
+        for k in range(count):
+            h = ctypes.c_void_p()
+            rc = self.hip.hipEventCreate(ctypes.byref(h))
+            if rc != 0:
+                raise RuntimeError(f"hipEventCreate failed ({rc})")
+            arr[k] = h.value
+        return arr
+
+    def elapsed_ms(self, a, b) -> float:
+        out = ctypes.c_float()
+        rc = self.hip.hipEventElapsedTime(ctypes.byref(out), a, b)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return float(out.value)
+
+    def destroy(self, arr):
+        for h in arr:
+            self.hip.hipEventDestroy(h)
+
+
+def counters_traffic():
+    """HBM bytes per lag-score launch from the committed rocprofv3 counter summary,
+    or None if there is none or the kernel source changed since it was taken."""
+    try:
+        with open(COUNTERS_FILE) as f:
+            c = json.load(f)
+        src = hashlib.sha256(open(SCORE_SOURCE, "rb").read()).hexdigest()
+        if c.get("source_sha256") != src:
+            return None
+        return float(c["hbm_bytes_per_launch"])
+    except (OSError, ValueError, KeyError):
+        return None
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for "
+              f"--gpus {args.gpus}); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2201_01684_amd as pkg
+    from gen import make_workload
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+
+    t_gen = time.perf_counter()
+    wl = make_workload(args.workload)
+    sha = wl.sha256
+    t_gen = time.perf_counter() - t_gen
+    pairs = wl.pairs()
+    x = torch.from_numpy(wl.x).to(dev)
+    desc, keep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
+                               wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights)
+    det = pkg.Detector(x, desc, keep, want_scores=True)
+    print(f"# {wl.name}: {wl.num_windows} windows x {wl.num_channels} ch x {wl.n} samples, "
+          f"T {wl.tmin}..{wl.tmax}, {pairs:.4e} pairs, generated in {t_gen:.1f}s, "
+          f"workspace {det.ws_bytes / 2**20:.1f} MiB", file=sys.stderr, flush=True)
+
+    for _ in range(args.warmup):
+        det.run()
+    torch.cuda.synchronize()
+
+    ev = HipEvents()
+    sets = [ev.create(5) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        det.run_staged(sets[k])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    stage_ms = np.array([[ev.elapsed_ms(s[j], s[j + 1]) for j in range(4)] for s in sets])
+    for s in sets:
+        ev.destroy(s)
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    value = pairs / (ms_per_step / 1e3)
+    score_ms = float(stage_ms[:, 1].mean())
+    achieved = FLOP_PER_PAIR * pairs / (score_ms / 1e3) / 1e12
+    res = det.results_numpy()
+    scores = det.scores
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "lag·samples/s",
+        "traces_per_sec": wl.num_windows / (ms_per_step / 1e3),
+        "pct_fp32_peak": 100.0 * FLOP_PER_PAIR * value / 1e12 / FP32_VECTOR_PEAK_TFLOPS,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "description": wl.meta["description"],
+                   "windows": wl.num_windows, "channels": wl.num_channels, "n": wl.n,
+                   "tmin": wl.tmin, "tmax": wl.tmax, "pairs": pairs, "sha256": sha},
+        "stage_ms": {"window_stats": float(stage_ms[:, 0].mean()),
+                     "lag_score": score_ms,
+                     "finalize": float(stage_ms[:, 2].mean()),
+                     "select": float(stage_ms[:, 3].mean())},
+        "roofline": {"kernel": "lag_score_kernel", "bound": "alu", "achieved": achieved,
+                     "peak": FP32_VECTOR_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / FP32_VECTOR_PEAK_TFLOPS, "traffic": counters_traffic()},
+        "windows_flagged_unresolved": int(np.count_nonzero(res["flags"] & pkg.UNRESOLVED)),
+        "windows_rescored": int(np.count_nonzero(res["n_rescored"])),
+    }
+    if wl.truth is not None:
+        d = wl.truth > 0
+        if wl.jitter:
+            ok = np.abs(res["period"][d] - wl.truth[d]) <= np.ceil(0.02 * wl.truth[d])
+        else:
+            ok = res["period"][d] == wl.truth[d]
+        line["planted_period_hits"] = f"{int(ok.sum())}/{int(d.sum())}"
+
+    if not args.no_cpu_baseline:
+        import oracle
+        lay = oracle.Layout.of(wl)
+        per_window = pairs // wl.num_windows
+        done, t_cpu, match, worst = 0, 0.0, 0, 0.0
+        s_host = None
+        while done < wl.num_windows and (done == 0 or t_cpu < args.cpu_seconds):
+            b = done
+            base = b * wl.window_stride
+            sub = wl.x[base: base + (wl.num_channels - 1) * wl.channel_stride + wl.n]
+            lay1 = oracle.Layout.of(wl, num_windows=1)
+            t = time.perf_counter()
+            o_scores, o_out = oracle.detect(sub, lay1)
+            t_cpu += time.perf_counter() - t
+            if s_host is None:
+                s_host = scores.double().cpu().numpy()
+            g = s_host[b]
+            o = o_scores[0]
+            nz = o != 0
+            worst = max(worst, float(np.max(np.abs(g[nz] - o[nz]) / o[nz])) if nz.any() else 0.0)
+            match += int(o_out["period"][0] == res["period"][b])
+            done += 1
+        line["cpu_baseline"] = {"value": done * per_window / t_cpu, "unit": "lag·samples/s",
+                                "cores": oracle.threads(), "kind": "oracle",
+                                "sample": f"first {done} of {wl.num_windows} windows, all "
+                                          f"{wl.lags} lags each, {t_cpu:.1f} s"}
+        line["parity_sample"] = {"windows": done, "period_match": match,
+                                 "max_score_rel_err": worst}
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,149 @@
+/*
+ * gpoeo_pd.h - batched iteration-period detection on MI355X (gfx950).
+ *
+ * C ABI of the HIP library libgpoeo_pd.so.  One call scores every candidate
+ * period T in [tmin, tmax] of every window of a batch of sampled feature
+ * traces and selects each window's iteration period, following Sec. 4.1.2 of
+ * Wang et al., "Dynamic GPU Energy Optimization for Machine Learning Training
+ * Workloads" (arXiv 2201.01684):
+ *
+ *   score   (Algorithm 2, read as the Euclidean distance between
+ *           corresponding points of adjacent sub-curves, over all N-T pairs)
+ *             D_c(T) = sum_{i=0}^{N-T-1} (x_c[i] - x_c[i+T])^2
+ *             S(T)   = sum_c w_c * D_c(T) / (N - T)
+ *           channels are combined as a weighted sum, the composite detection
+ *           feature of Sec. 4.2.
+ *
+ *   select  (Algorithm 1: peaks, relative-height candidate filter, choice of
+ *           the fundamental, local search over the neighbouring Fourier-bin
+ *           periods at a one-sample step)
+ *             R      = 2 * sum_c w_c * Var_c   (population variance, fp64)
+ *             peaks  = { Tmin < T < Tmax : S(T) < S(T-1), S(T) <= S(T+1) }
+ *             S_pk   = min S over peaks; thr = R - c_lag * (R - S_pk)
+ *             T_c    = smallest peak with S(T) < thr
+ *             T_low  = max(Tmin, ceil (T_c (N-1) / (N-1+T_c)))
+ *             T_up   = min(Tmax, floor(T_c (N-1) / (N-1-T_c)))
+ *             period = smallest T in [T_low, T_up] attaining min S
+ *             err    = S(period) / R
+ *
+ * Precision.  D_c(T) is accumulated in fp32 over runs of at most 256 samples
+ * and the runs are combined in fp64, so every score is within 2e-5 relative of
+ * the exact value (scores are sums of non-negative terms; an exact zero stays
+ * exactly zero).  The selection compares these bounded values; any comparison
+ * the bound cannot decide is re-decided on scores (and R) recomputed on the
+ * GPU as plain sequential fp64 sums over ascending i, with no fused
+ * multiply-add, i.e. on the same values a straightforward fp64 evaluation of
+ * the definitions gives.
+ *
+ * Threading and ownership.  All buffers except `desc` and `desc->channel_weights`
+ * are DEVICE memory owned by the caller.  The library never allocates or frees
+ * memory and keeps no mutable global state: calls on different streams with
+ * different workspaces may run concurrently.  `gpoeo_pd_detect` validates its
+ * arguments on the host, enqueues its kernels on `stream` and returns; outputs
+ * are valid once the stream has been synchronised.
+ *
+ * Inputs must be finite (no NaN or Inf); otherwise the outputs are unspecified.
+ */
+#ifndef GPOEO_PD_H
+#define GPOEO_PD_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GPOEO_PD_ABI_VERSION 1
+
+/* Status codes returned by every entry point. */
+#define GPOEO_PD_OK 0
+#define GPOEO_PD_EINVAL (-1)   /* invalid descriptor or pointer; nothing was launched      */
+#define GPOEO_PD_ENOMEM (-2)   /* workspace smaller than gpoeo_pd_workspace_bytes()        */
+#define GPOEO_PD_EHIP (-3)     /* a HIP launch failed (hipGetLastError after enqueueing)    */
+
+/* Per-window verdicts. */
+#define GPOEO_PD_PERIODIC 0    /* a period was selected and err < err_max                  */
+#define GPOEO_PD_APERIODIC 1   /* no candidate period, or err >= err_max                   */
+#define GPOEO_PD_CONSTANT 2    /* R == 0: every weighted channel is constant               */
+
+/* desc->flags */
+#define GPOEO_PD_SCORES_ONLY 1u  /* compute scores only; `results` is not written           */
+#define GPOEO_PD_NO_RESCUE 2u    /* decide on the bounded fp32-accumulated scores only       */
+
+/* result->flags */
+#define GPOEO_PD_UNRESOLVED 1u   /* some comparison stayed undecided after the exact
+                                    re-scoring limit; the result uses bounded scores       */
+
+typedef struct {
+    int64_t num_windows;     /* B >= 1: traces, or sliding windows of one long trace        */
+    int32_t num_channels;    /* C >= 1: per-lag channel scores are summed with weights      */
+    int32_t reserved0;       /* must be 0                                                   */
+    int64_t n;               /* N >= 8 samples per window                                   */
+    int64_t window_stride;   /* samples between window starts (N*C when packed)            */
+    int64_t channel_stride;  /* samples between channels of one window (>= N if C > 1)     */
+    int32_t tmin, tmax;      /* inclusive lag range: 1 <= tmin, tmin + 2 <= tmax <= N / 2   */
+    double c_lag;            /* relative-height factor of the candidate filter, in (0, 1);
+                                the lag-domain counterpart of Algorithm 1's c_peak.
+                                Recommended 0.9                                             */
+    double err_max;          /* APERIODIC if S(period)/R >= err_max (1.0: never for a
+                                selected period)                                            */
+    const float* channel_weights; /* HOST array of C weights > 0, or NULL for all 1          */
+    uint32_t flags;          /* GPOEO_PD_SCORES_ONLY | GPOEO_PD_NO_RESCUE                   */
+    uint32_t reserved1;      /* must be 0                                                   */
+} gpoeo_pd_desc;
+
+typedef struct {
+    int32_t period;          /* selected period in samples (times T_s for seconds); 0 if none */
+    int32_t verdict;         /* GPOEO_PD_PERIODIC / _APERIODIC / _CONSTANT                   */
+    float err;               /* S(period) / R, Algorithm 1's "error of period"; 0 if none    */
+    int32_t n_candidates;    /* peaks passing the relative-height filter                     */
+    int32_t t_cand;          /* T_c, the smallest candidate; 0 if none                       */
+    int32_t t_low, t_up;     /* local-search window; 0 if none                               */
+    int32_t n_rescored;      /* scores recomputed as sequential fp64 sums for this window    */
+    uint32_t flags;          /* GPOEO_PD_UNRESOLVED                                          */
+} gpoeo_pd_result;
+
+/* ABI version the library was built with (GPOEO_PD_ABI_VERSION). */
+int gpoeo_pd_abi_version(void);
+
+/* Static message for a status code; never NULL. */
+const char* gpoeo_pd_strerror(int status);
+
+/* Validates `desc` and writes the device workspace size gpoeo_pd_detect needs.
+ * Returns GPOEO_PD_OK or GPOEO_PD_EINVAL.  Host-only: launches nothing. */
+int gpoeo_pd_workspace_bytes(const gpoeo_pd_desc* desc, size_t* bytes);
+
+/* Scores and selects every window of the batch.
+ *   x          device, fp32; window b, channel c, sample i at
+ *              x[b*window_stride + c*channel_stride + i]; windows may overlap.
+ *   scores     device, fp32 [B][tmax-tmin+1] row-major, scores[b][T-tmin] = S(T);
+ *              may be NULL.
+ *   results    device, one gpoeo_pd_result per window; may be NULL only with
+ *              GPOEO_PD_SCORES_ONLY.
+ *   workspace  device, at least gpoeo_pd_workspace_bytes() bytes, 256-byte
+ *              aligned; its contents on entry are ignored.
+ *   stream     HIP stream all kernels are enqueued on (0 = the null stream).
+ * Returns GPOEO_PD_OK, GPOEO_PD_EINVAL or GPOEO_PD_ENOMEM before launching
+ * anything, or GPOEO_PD_EHIP if a launch failed. */
+int gpoeo_pd_detect(const gpoeo_pd_desc* desc, const float* x, float* scores,
+                    gpoeo_pd_result* results, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream);
+
+/* gpoeo_pd_detect, additionally recording stage_events[k] on `stream` right
+ * before stage k is enqueued (0 window statistics, 1 lag scores, 2 score
+ * finalisation, 3 selection) and stage_events[4] after the last one, so that
+ * hipEventElapsedTime between consecutive events gives each stage's device
+ * time.  For measurement tools; the events are created (hipEventCreate) and
+ * owned by the caller.  A stage that the flags skip records its two events
+ * back to back.  Same return values as gpoeo_pd_detect; EINVAL if
+ * stage_events is NULL. */
+int gpoeo_pd_detect_staged(const gpoeo_pd_desc* desc, const float* x, float* scores,
+                           gpoeo_pd_result* results, void* workspace, size_t workspace_bytes,
+                           hipStream_t stream, hipEvent_t stage_events[5]);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GPOEO_PD_H */

@@ -1,0 +1,213 @@
+"""ctypes binding of libgpoeo_pd.so (argument marshalling only).
+
+Every step of the detection runs in the library's HIP kernels; this module
+only builds the descriptor, hands over device pointers of torch tensors and the
+current HIP stream, and allocates the caller-side buffers (scores, results,
+workspace) with torch.  If the library is missing it raises: there is no other
+code path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch  # noqa: F401  (loads the HIP runtime the library must share)
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libgpoeo_pd.so")
+
+OK, EINVAL, ENOMEM, EHIP = 0, -1, -2, -3
+PERIODIC, APERIODIC, CONSTANT = 0, 1, 2
+SCORES_ONLY, NO_RESCUE = 1, 2
+UNRESOLVED = 1
+DEFAULT_C_LAG = 0.9
+DEFAULT_ERR_MAX = 1.0
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [("num_windows", ctypes.c_int64), ("num_channels", ctypes.c_int32),
+                ("reserved0", ctypes.c_int32), ("n", ctypes.c_int64),
+                ("window_stride", ctypes.c_int64), ("channel_stride", ctypes.c_int64),
+                ("tmin", ctypes.c_int32), ("tmax", ctypes.c_int32), ("c_lag", ctypes.c_double),
+                ("err_max", ctypes.c_double), ("channel_weights", ctypes.c_void_p),
+                ("flags", ctypes.c_uint32), ("reserved1", ctypes.c_uint32)]
+
+
+class Result(ctypes.Structure):
+    _fields_ = [("period", ctypes.c_int32), ("verdict", ctypes.c_int32), ("err", ctypes.c_float),
+                ("n_candidates", ctypes.c_int32), ("t_cand", ctypes.c_int32),
+                ("t_low", ctypes.c_int32), ("t_up", ctypes.c_int32), ("n_rescored", ctypes.c_int32),
+                ("flags", ctypes.c_uint32)]
+
+
+RESULT_DTYPE = np.dtype([("period", np.int32), ("verdict", np.int32), ("err", np.float32),
+                         ("n_candidates", np.int32), ("t_cand", np.int32), ("t_low", np.int32),
+                         ("t_up", np.int32), ("n_rescored", np.int32), ("flags", np.uint32)])
+RESULT_WORDS = ctypes.sizeof(Result) // 4
+assert RESULT_DTYPE.itemsize == ctypes.sizeof(Result)
+
+EXPORTS = ("gpoeo_pd_abi_version", "gpoeo_pd_strerror", "gpoeo_pd_workspace_bytes",
+           "gpoeo_pd_detect", "gpoeo_pd_detect_staged")
+
+_lib = None
+
+
+def load_library():
+    """Load libgpoeo_pd.so (built in-tree); raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "(python paper_2201_01684_amd/build.py)")
+        lib = ctypes.CDLL(LIB_PATH)
+        lib.gpoeo_pd_abi_version.restype = ctypes.c_int
+        lib.gpoeo_pd_abi_version.argtypes = []
+        lib.gpoeo_pd_strerror.restype = ctypes.c_char_p
+        lib.gpoeo_pd_strerror.argtypes = [ctypes.c_int]
+        lib.gpoeo_pd_workspace_bytes.restype = ctypes.c_int
+        lib.gpoeo_pd_workspace_bytes.argtypes = [ctypes.POINTER(Desc),
+                                                 ctypes.POINTER(ctypes.c_size_t)]
+        lib.gpoeo_pd_detect.restype = ctypes.c_int
+        lib.gpoeo_pd_detect.argtypes = [ctypes.POINTER(Desc), ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                        ctypes.c_void_p]
+        lib.gpoeo_pd_detect_staged.restype = ctypes.c_int
+        lib.gpoeo_pd_detect_staged.argtypes = [ctypes.POINTER(Desc), ctypes.c_void_p,
+                                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                               ctypes.c_size_t, ctypes.c_void_p,
+                                               ctypes.c_void_p]
+        _lib = lib
+    return _lib
+
+
+def strerror(status: int) -> str:
+    return load_library().gpoeo_pd_strerror(int(status)).decode()
+
+
+class GpoeoError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {strerror(status)} ({status})")
+        self.status = status
+
+
+def make_desc(num_windows, num_channels, n, window_stride, channel_stride, tmin, tmax,
+              c_lag=DEFAULT_C_LAG, err_max=DEFAULT_ERR_MAX, weights=None, flags=0):
+    """Descriptor plus the host weight array it points at (keep both alive)."""
+    w = None
+    if weights is not None:
+        w = np.ascontiguousarray(weights, dtype=np.float32)
+        if w.shape != (num_channels,):
+            raise ValueError("need one weight per channel")
+    d = Desc(int(num_windows), int(num_channels), 0, int(n), int(window_stride),
+             int(channel_stride), int(tmin), int(tmax), float(c_lag), float(err_max),
+             None if w is None else w.ctypes.data, int(flags), 0)
+    return d, w
+
+
+def workspace_bytes(desc: Desc) -> int:
+    size = ctypes.c_size_t(0)
+    rc = load_library().gpoeo_pd_workspace_bytes(ctypes.byref(desc), ctypes.byref(size))
+    if rc != OK:
+        raise GpoeoError(rc, "gpoeo_pd_workspace_bytes")
+    return int(size.value)
+
+
+def _stream_handle(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+class Detector:
+    """Reusable call site: device buffers allocated once, then `run()` only enqueues.
+
+    ``x`` is a float32 device tensor holding all windows (any shape; its
+    storage is addressed with the layout in the descriptor).
+    """
+
+    def __init__(self, x: torch.Tensor, desc: Desc, weights_keepalive=None, want_scores=True):
+        if not isinstance(x, torch.Tensor) or x.dtype != torch.float32 or not x.is_cuda:
+            raise TypeError("x must be a float32 GPU tensor")
+        if not x.is_contiguous():
+            raise ValueError("x must be contiguous")
+        need = ((desc.num_windows - 1) * desc.window_stride
+                + (desc.num_channels - 1) * desc.channel_stride + desc.n)
+        if x.numel() < need:
+            raise ValueError(f"x has {x.numel()} samples, the layout addresses {need}")
+        self.x = x
+        self.desc = desc
+        self._w = weights_keepalive
+        dev = x.device
+        lags = desc.tmax - desc.tmin + 1
+        self.scores = (torch.empty((desc.num_windows, lags), dtype=torch.float32, device=dev)
+                       if want_scores else None)
+        self.results = torch.zeros((desc.num_windows, RESULT_WORDS), dtype=torch.int32,
+                                   device=dev)
+        self.ws_bytes = workspace_bytes(desc)
+        self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=dev)
+        self._lib = load_library()
+
+    def run(self, stream=None) -> None:
+        rc = self._lib.gpoeo_pd_detect(
+            ctypes.byref(self.desc), self.x.data_ptr(),
+            None if self.scores is None else self.scores.data_ptr(),
+            self.results.data_ptr(), self.workspace.data_ptr(), self.ws_bytes,
+            _stream_handle(stream))
+        if rc != OK:
+            raise GpoeoError(rc, "gpoeo_pd_detect")
+
+    def run_staged(self, events, stream=None) -> None:
+        """run(), recording the five caller-created hipEvent_t handles in ``events``
+        (a ctypes array of 5 void pointers) around the four stages."""
+        rc = self._lib.gpoeo_pd_detect_staged(
+            ctypes.byref(self.desc), self.x.data_ptr(),
+            None if self.scores is None else self.scores.data_ptr(),
+            self.results.data_ptr(), self.workspace.data_ptr(), self.ws_bytes,
+            _stream_handle(stream), events)
+        if rc != OK:
+            raise GpoeoError(rc, "gpoeo_pd_detect_staged")
+
+    def results_numpy(self) -> np.ndarray:
+        return results_to_numpy(self.results)
+
+
+def results_to_numpy(results: torch.Tensor) -> np.ndarray:
+    host = results.detach().to("cpu").contiguous().numpy()
+    return host.view(RESULT_DTYPE).reshape(-1)
+
+
+def detect_period(traces: torch.Tensor, tmin: int, tmax: int, *, n: int | None = None,
+                  window_stride: int | None = None, num_windows: int | None = None,
+                  weights=None, c_lag: float = DEFAULT_C_LAG,
+                  err_max: float = DEFAULT_ERR_MAX, flags: int = 0, want_scores: bool = True,
+                  stream=None):
+    """Score every lag in [tmin, tmax] of every window and select each window's period.
+
+    ``traces`` is a float32 GPU tensor shaped [B, N] (one channel), [B, C, N]
+    (channel scores summed with ``weights``), or a 1-D long trace cut into
+    ``num_windows`` windows of ``n`` samples starting every ``window_stride``
+    samples.  Returns ``(scores, results)``: scores is a float32 [B, L] tensor
+    (L = tmax - tmin + 1, scores[b, T - tmin] = S(T)) or None, and results a
+    numpy structured array with one record per window (period, verdict, err, ...).
+    """
+    if traces.dim() == 1:
+        if n is None or window_stride is None:
+            raise ValueError("a 1-D trace needs n and window_stride")
+        if num_windows is None:
+            num_windows = (traces.numel() - n) // window_stride + 1
+        b, c, cs = num_windows, 1, n
+    elif traces.dim() == 2:
+        b, n_ = traces.shape
+        c, n, window_stride, cs = 1, n_, n_, n_
+    elif traces.dim() == 3:
+        b, c, n_ = traces.shape
+        n, window_stride, cs = n_, c * n_, n_
+    else:
+        raise ValueError("traces must be 1-D, 2-D or 3-D")
+    desc, w = make_desc(b, c, n, window_stride, cs, tmin, tmax, c_lag, err_max, weights, flags)
+    det = Detector(traces.contiguous(), desc, w, want_scores=want_scores)
+    det.run(stream)
+    torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
+    res = None if (flags & SCORES_ONLY) else det.results_numpy()
+    return det.scores, res

@@ -1,0 +1,190 @@
+// C ABI of libgpoeo_pd: argument validation, launch plan, workspace layout and
+// the kernel sequence (window statistics, lag scores, finalisation, selection).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "gpoeo_pd.h"
+#include "internal.h"
+
+namespace gpoeo {
+namespace {
+
+constexpr int64_t kTargetWaves = 8192;   // about 8 waves per SIMD on 256 CUs x 4 SIMDs
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+    if (a < 0 || b < 0) return false;
+    if (a != 0 && b > INT64_MAX / a) return false;
+    *out = a * b;
+    return true;
+}
+
+int make_plan(const gpoeo_pd_desc* d, Plan* p) {
+    if (!d) return GPOEO_PD_EINVAL;
+    if (d->reserved0 != 0 || d->reserved1 != 0) return GPOEO_PD_EINVAL;
+    if (d->flags & ~(GPOEO_PD_SCORES_ONLY | GPOEO_PD_NO_RESCUE)) return GPOEO_PD_EINVAL;
+    if (d->num_windows < 1 || d->num_windows > INT32_MAX) return GPOEO_PD_EINVAL;
+    if (d->num_channels < 1 || d->num_channels > kMaxChannels) return GPOEO_PD_EINVAL;
+    if (d->n < 8 || d->n > (int64_t(1) << 40)) return GPOEO_PD_EINVAL;
+    if (d->tmin < 1 || (int64_t)d->tmin + 2 > (int64_t)d->tmax || (int64_t)d->tmax > d->n / 2)
+        return GPOEO_PD_EINVAL;
+    if (d->window_stride < 0 || (d->num_windows > 1 && d->window_stride < 1))
+        return GPOEO_PD_EINVAL;
+    if (d->channel_stride < 0 || (d->num_channels > 1 && d->channel_stride < d->n))
+        return GPOEO_PD_EINVAL;
+    if (!(d->c_lag > 0.0 && d->c_lag < 1.0)) return GPOEO_PD_EINVAL;
+    if (std::isnan(d->err_max)) return GPOEO_PD_EINVAL;
+    if (d->channel_weights)
+        for (int32_t c = 0; c < d->num_channels; ++c) {
+            const float w = d->channel_weights[c];
+            if (!(w > 0.0f) || !std::isfinite(w)) return GPOEO_PD_EINVAL;
+        }
+
+    std::memset(p, 0, sizeof(*p));
+    p->num_windows = d->num_windows;
+    p->num_channels = d->num_channels;
+    p->n = d->n;
+    p->window_stride = d->window_stride;
+    p->channel_stride = d->channel_stride;
+    p->tmin = d->tmin;
+    p->tmax = d->tmax;
+    p->lags = d->tmax - d->tmin + 1;
+    p->c_lag = d->c_lag;
+    p->err_max = d->err_max;
+    p->flags = d->flags;
+
+    // Lag blocks end exactly at tmax when possible, so that no block is mostly
+    // outside [tmin, tmax]; lags below tmin are computed and discarded.
+    p->lag_blocks = (p->lags + kLagsPerWave - 1) / kLagsPerWave;
+    int64_t t0 = (int64_t)d->tmax + 1 - (int64_t)p->lag_blocks * kLagsPerWave;
+    if (t0 < 0) t0 = 0;
+    p->t0 = (int32_t)t0;
+    p->lags_padded = p->lag_blocks * kLagsPerWave;
+
+    int64_t bc, base;
+    if (!mul_ok(d->num_windows, d->num_channels, &bc)) return GPOEO_PD_EINVAL;
+    if (!mul_ok(bc, p->lag_blocks, &base)) return GPOEO_PD_EINVAL;
+    const int64_t span = d->n - p->t0;             // longest sample range of any lag
+    const int64_t max_chunks = (span + kRunSamples - 1) / kRunSamples;
+    int64_t chunks = (kTargetWaves + base - 1) / base;
+    if (chunks < 1) chunks = 1;
+    if (chunks > max_chunks) chunks = max_chunks;
+    int64_t chunk = (span + chunks - 1) / chunks;
+    chunk = (chunk + kRunSamples - 1) / kRunSamples * kRunSamples;
+    chunks = (span + chunk - 1) / chunk;
+    p->chunk = chunk;
+    p->chunks = (int32_t)chunks;
+    if (!mul_ok(base, chunks, &p->tasks)) return GPOEO_PD_EINVAL;
+    if (p->tasks / 4 + 1 > INT32_MAX) return GPOEO_PD_EINVAL;
+    p->bitmap_words = (p->lags + 31) / 32;
+
+    int64_t n_var, n_s, n_bits, n_part;
+    if (!mul_ok(bc, 1, &n_var)) return GPOEO_PD_EINVAL;
+    if (!mul_ok(d->num_windows, p->lags, &n_s)) return GPOEO_PD_EINVAL;
+    if (!mul_ok(d->num_windows, p->bitmap_words, &n_bits)) return GPOEO_PD_EINVAL;
+    int64_t tmp;
+    if (!mul_ok(bc, chunks, &tmp) || !mul_ok(tmp, p->lags_padded, &n_part)) return GPOEO_PD_EINVAL;
+    if (n_part > (INT64_MAX / 16)) return GPOEO_PD_EINVAL;
+    size_t off = 0;
+    p->off_var = off;
+    off = align_up(off + (size_t)n_var * sizeof(double));
+    p->off_s64 = off;
+    off = align_up(off + (size_t)n_s * sizeof(double));
+    p->off_bits = off;
+    off = align_up(off + (size_t)n_bits * sizeof(uint32_t));
+    p->off_part = off;
+    off = align_up(off + (size_t)n_part * sizeof(double));
+    p->bytes = off;
+    return GPOEO_PD_OK;
+}
+
+}  // namespace
+}  // namespace gpoeo
+
+extern "C" {
+
+int gpoeo_pd_abi_version(void) { return GPOEO_PD_ABI_VERSION; }
+
+const char* gpoeo_pd_strerror(int status) {
+    switch (status) {
+        case GPOEO_PD_OK: return "success";
+        case GPOEO_PD_EINVAL: return "invalid argument";
+        case GPOEO_PD_ENOMEM: return "workspace too small";
+        case GPOEO_PD_EHIP: return "HIP launch failed";
+        default: return "unknown status";
+    }
+}
+
+int gpoeo_pd_workspace_bytes(const gpoeo_pd_desc* desc, size_t* bytes) {
+    if (!bytes) return GPOEO_PD_EINVAL;
+    gpoeo::Plan p;
+    const int rc = gpoeo::make_plan(desc, &p);
+    if (rc != GPOEO_PD_OK) return rc;
+    *bytes = p.bytes;
+    return GPOEO_PD_OK;
+}
+
+static int detect_impl(const gpoeo_pd_desc* desc, const float* x, float* scores,
+                       gpoeo_pd_result* results, void* workspace, size_t workspace_bytes,
+                       hipStream_t stream, hipEvent_t* ev) {
+    gpoeo::Plan p;
+    const int rc = gpoeo::make_plan(desc, &p);
+    if (rc != GPOEO_PD_OK) return rc;
+    const bool scores_only = (p.flags & GPOEO_PD_SCORES_ONLY) != 0;
+    if (!x || (!results && !scores_only) || !workspace) return GPOEO_PD_EINVAL;
+    if (reinterpret_cast<uintptr_t>(workspace) % gpoeo::kAlign) return GPOEO_PD_EINVAL;
+    if (reinterpret_cast<uintptr_t>(x) % sizeof(float)) return GPOEO_PD_EINVAL;
+    if (workspace_bytes < p.bytes) return GPOEO_PD_ENOMEM;
+    p.aligned = (reinterpret_cast<uintptr_t>(x) % 16 == 0) &&
+                (p.num_windows == 1 || p.window_stride % 4 == 0) &&
+                (p.num_channels == 1 || p.channel_stride % 4 == 0);
+
+    gpoeo::Weights w;
+    for (int c = 0; c < gpoeo::kMaxChannels; ++c)
+        w.w[c] = (desc->channel_weights && c < p.num_channels) ? desc->channel_weights[c] : 1.0f;
+
+    char* ws = static_cast<char*>(workspace);
+    double* var = reinterpret_cast<double*>(ws + p.off_var);
+    double* s64 = reinterpret_cast<double*>(ws + p.off_s64);
+    uint32_t* bits = reinterpret_cast<uint32_t*>(ws + p.off_bits);
+    double* part = reinterpret_cast<double*>(ws + p.off_part);
+
+    auto mark = [&](int k) { return !ev || hipEventRecord(ev[k], stream) == hipSuccess; };
+    if (!mark(0)) return GPOEO_PD_EHIP;
+    if (!scores_only && gpoeo::launch_window_stats(p, x, var, stream) != hipSuccess)
+        return GPOEO_PD_EHIP;
+    if (!mark(1)) return GPOEO_PD_EHIP;
+    if (gpoeo::launch_lag_score(p, x, part, stream) != hipSuccess) return GPOEO_PD_EHIP;
+    if (!mark(2)) return GPOEO_PD_EHIP;
+    if (gpoeo::launch_finalize(p, w, part, s64, scores, stream) != hipSuccess)
+        return GPOEO_PD_EHIP;
+    if (!mark(3)) return GPOEO_PD_EHIP;
+    if (!scores_only &&
+        gpoeo::launch_select(p, w, x, var, s64, bits, results, stream) != hipSuccess)
+        return GPOEO_PD_EHIP;
+    if (!mark(4)) return GPOEO_PD_EHIP;
+    return GPOEO_PD_OK;
+}
+
+int gpoeo_pd_detect(const gpoeo_pd_desc* desc, const float* x, float* scores,
+                    gpoeo_pd_result* results, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream) {
+    return detect_impl(desc, x, scores, results, workspace, workspace_bytes, stream, nullptr);
+}
+
+int gpoeo_pd_detect_staged(const gpoeo_pd_desc* desc, const float* x, float* scores,
+                           gpoeo_pd_result* results, void* workspace, size_t workspace_bytes,
+                           hipStream_t stream, hipEvent_t stage_events[5]) {
+    if (!stage_events) return GPOEO_PD_EINVAL;
+    for (int k = 0; k < 5; ++k)
+        if (!stage_events[k]) return GPOEO_PD_EINVAL;
+    return detect_impl(desc, x, scores, results, workspace, workspace_bytes, stream,
+                       stage_events);
+}
+
+}  // extern "C"

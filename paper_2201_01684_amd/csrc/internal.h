@@ -1,0 +1,58 @@
+// Internal launch plan and kernel entry points of libgpoeo_pd (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gpoeo {
+
+constexpr int kWave = 64;            // CDNA wavefront width
+constexpr int kLagsPerLane = 16;     // consecutive lags held in one lane's accumulators
+constexpr int kLagsPerWave = kWave * kLagsPerLane;
+constexpr int kBlockSamples = 16;    // samples per register block of the score kernel
+constexpr int kRunSamples = 256;     // samples per fp32 run before the fp64 flush
+constexpr int kMaxChannels = 256;    // channel weights travel as a kernel argument
+
+// Relative error bound of a score accumulated in fp32 runs of kRunSamples
+// non-negative terms (each run: kRunSamples roundings plus the rounding of the
+// difference, about 258 * 2^-24 = 1.54e-5) and combined in fp64; rounded up.
+constexpr double kScoreRelBound = 2.5e-5;
+// Relative error bound of R from a parallel fp64 two-pass variance.
+constexpr double kRefRelBound = 1e-12;
+
+struct Weights {
+    float w[kMaxChannels];
+};
+
+// Everything the kernels need, derived on the host from a validated descriptor.
+struct Plan {
+    int64_t num_windows;
+    int32_t num_channels;
+    int64_t n;
+    int64_t window_stride;
+    int64_t channel_stride;
+    int32_t tmin, tmax;
+    int32_t lags;            // tmax - tmin + 1
+    int32_t t0;              // first lag of lag block 0 (tmin rounded down to a multiple of 4)
+    int32_t lag_blocks;      // blocks of kLagsPerWave lags covering [t0, tmax]
+    int32_t lags_padded;     // lag_blocks * kLagsPerWave
+    int32_t chunks;          // sample chunks per (window, channel, lag block)
+    int64_t chunk;           // samples per chunk, a multiple of kRunSamples
+    int64_t tasks;           // waves of the score kernel
+    bool aligned;            // x and strides allow 16-byte vector loads
+    double c_lag, err_max;
+    uint32_t flags;
+    int32_t bitmap_words;    // 32-bit words per window of the exactness bitmap
+    // workspace layout (byte offsets, 256-byte aligned)
+    size_t off_var, off_s64, off_bits, off_part, bytes;
+};
+
+// Kernel launchers; each returns hipGetLastError() after enqueueing.
+hipError_t launch_window_stats(const Plan& p, const float* x, double* var, hipStream_t s);
+hipError_t launch_lag_score(const Plan& p, const float* x, double* part, hipStream_t s);
+hipError_t launch_finalize(const Plan& p, const Weights& w, const double* part, double* s64,
+                           float* scores, hipStream_t s);
+hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const double* var,
+                         double* s64, uint32_t* bits, void* results, hipStream_t s);
+
+}  // namespace gpoeo

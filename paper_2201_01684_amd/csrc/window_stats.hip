@@ -1,0 +1,97 @@
+// Window statistics and score finalisation.
+//
+// window_stats: per (window, channel), the population variance in fp64 by two
+//   passes (mean, then mean squared deviation), each a fixed-order workgroup
+//   reduction.  The selection forms R = 2 * sum_c w_c * Var_c from it, the
+//   reference the relative-height candidate filter of Algorithm 1 is measured
+//   against in the lag domain.
+// finalize: per (window, lag), combines the fp64 chunk partials of every
+//   channel in ascending chunk order, divides by the N-T pairs and forms the
+//   weighted channel sum S(T) (the composite detection feature of Sec. 4.2).
+#include "internal.h"
+
+namespace gpoeo {
+namespace {
+
+constexpr int kStatsThreads = 256;
+
+__device__ double block_sum(double v, double* red) {
+    red[threadIdx.x] = v;
+    __syncthreads();
+#pragma unroll
+    for (int w = kStatsThreads / 2; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+        __syncthreads();
+    }
+    double r = red[0];
+    __syncthreads();
+    return r;
+}
+
+__global__ __launch_bounds__(kStatsThreads) void window_stats_kernel(
+    const float* __restrict__ x, double* __restrict__ var, int64_t n, int64_t window_stride,
+    int64_t channel_stride, int32_t num_channels) {
+    __shared__ double red[kStatsThreads];
+    const int64_t bc = blockIdx.x;
+    const int64_t b = bc / num_channels;
+    const int32_t c = (int32_t)(bc % num_channels);
+    const float* __restrict__ xw = x + b * window_stride + (int64_t)c * channel_stride;
+    double s = 0.0;
+    for (int64_t i = threadIdx.x; i < n; i += kStatsThreads) s += (double)xw[i];
+    const double mean = block_sum(s, red) / (double)n;
+    double q = 0.0;
+    for (int64_t i = threadIdx.x; i < n; i += kStatsThreads) {
+        const double d = (double)xw[i] - mean;
+        q += d * d;
+    }
+    const double sq = block_sum(q, red);
+    if (threadIdx.x == 0) var[bc] = sq / (double)n;
+}
+
+__global__ __launch_bounds__(256) void finalize_kernel(const double* __restrict__ part,
+                                                       double* __restrict__ s64,
+                                                       float* __restrict__ scores, Weights w,
+                                                       int64_t num_windows, int32_t num_channels,
+                                                       int64_t n, int32_t tmin, int32_t lags,
+                                                       int32_t t0, int32_t lags_padded,
+                                                       int32_t chunks) {
+    const int64_t total = num_windows * (int64_t)lags;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t b = e / lags;
+        const int32_t j = (int32_t)(e % lags);
+        const int64_t t = (int64_t)tmin + j;
+        double s = 0.0;
+        for (int32_t c = 0; c < num_channels; ++c) {
+            const double* p = part + ((b * num_channels + c) * chunks) * (int64_t)lags_padded +
+                              (t - t0);
+            double d = 0.0;
+            for (int32_t k = 0; k < chunks; ++k) d += p[(int64_t)k * lags_padded];
+            s += (double)w.w[c] * (d / (double)(n - t));
+        }
+        s64[e] = s;
+        if (scores) scores[e] = (float)s;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_window_stats(const Plan& p, const float* x, double* var, hipStream_t s) {
+    const int64_t groups = p.num_windows * p.num_channels;
+    hipLaunchKernelGGL(window_stats_kernel, dim3((unsigned)groups), dim3(kStatsThreads), 0, s, x,
+                       var, p.n, p.window_stride, p.channel_stride, p.num_channels);
+    return hipGetLastError();
+}
+
+hipError_t launch_finalize(const Plan& p, const Weights& w, const double* part, double* s64,
+                           float* scores, hipStream_t s) {
+    const int64_t total = p.num_windows * (int64_t)p.lags;
+    int64_t groups = (total + 255) / 256;
+    if (groups > 65536) groups = 65536;
+    hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)groups), dim3(256), 0, s, part, s64,
+                       scores, w, p.num_windows, p.num_channels, p.n, p.tmin, p.lags, p.t0,
+                       p.lags_padded, p.chunks);
+    return hipGetLastError();
+}
+
+}  // namespace gpoeo

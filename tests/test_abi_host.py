@@ -1,0 +1,142 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every
+declared entry point, its structs match the header, and every invalid-argument
+path returns before any launch."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gpoeo_pd.h")
+
+pkg = pytest.importorskip("paper_2201_01684_amd")
+from paper_2201_01684_amd import _binding as B  # noqa: E402
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.fail("libgpoeo_pd.so is not built (run __graft_entry__.build())")
+    return B.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(gpoeo_pd_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert set(names) == set(B.EXPORTS)
+    for name in names:
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", B.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (gpoeo_pd_\w+)$", out, re.M))
+    assert exported == set(names)
+
+
+def test_version_and_messages(lib):
+    assert lib.gpoeo_pd_abi_version() == 1
+    for code in (0, -1, -2, -3, 17):
+        assert isinstance(B.strerror(code), str) and B.strerror(code)
+    assert B.strerror(-2) == "workspace too small"
+
+
+def test_struct_layout_matches_header(tmp_path):
+    src = tmp_path / "layout.c"
+    src.write_text("""
+#include <stdio.h>
+#include <stddef.h>
+#include "gpoeo_pd.h"
+int main(void) {
+  printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(gpoeo_pd_desc), offsetof(gpoeo_pd_desc, c_lag),
+         offsetof(gpoeo_pd_desc, channel_weights), offsetof(gpoeo_pd_desc, flags),
+         sizeof(gpoeo_pd_result), offsetof(gpoeo_pd_result, n_rescored));
+  return 0;
+}
+""")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"),
+                    "-I", "/opt/rocm/include", str(src), "-o", str(exe)], check=True)
+    got = list(map(int, subprocess.run([str(exe)], capture_output=True, text=True,
+                                       check=True).stdout.split()))
+    want = [ctypes.sizeof(B.Desc), B.Desc.c_lag.offset, B.Desc.channel_weights.offset,
+            B.Desc.flags.offset, ctypes.sizeof(B.Result), B.Result.n_rescored.offset]
+    assert got == want
+
+
+def good_desc(**kw):
+    base = dict(num_windows=4, num_channels=2, n=4096, window_stride=8192, channel_stride=4096,
+                tmin=2, tmax=1024)
+    base.update(kw)
+    return B.make_desc(**base)
+
+
+def test_workspace_size_valid_and_monotone(lib):
+    d, _ = good_desc()
+    small = B.workspace_bytes(d)
+    d2, _ = good_desc(num_windows=8, window_stride=8192)
+    assert small > 0 and B.workspace_bytes(d2) > small
+    assert small % 256 == 0
+
+
+@pytest.mark.parametrize("kw", [
+    dict(num_windows=0), dict(num_channels=0), dict(num_channels=257, channel_stride=4096),
+    dict(n=7, tmin=1, tmax=3), dict(tmin=0), dict(tmin=5, tmax=6), dict(tmax=2049),
+    dict(window_stride=0), dict(channel_stride=4095), dict(window_stride=-1),
+    dict(c_lag=0.0), dict(c_lag=1.0), dict(c_lag=float("nan")), dict(err_max=float("nan")),
+    dict(flags=4),
+])
+def test_invalid_descriptors_rejected(lib, kw):
+    d, _ = good_desc(**kw)
+    with pytest.raises(B.GpoeoError) as e:
+        B.workspace_bytes(d)
+    assert e.value.status == B.EINVAL
+
+
+@pytest.mark.parametrize("weights", [[1.0, 0.0], [1.0, -2.0], [1.0, float("inf")],
+                                     [float("nan"), 1.0]])
+def test_invalid_weights_rejected(lib, weights):
+    d, _keep = good_desc(weights=np.array(weights, dtype=np.float32))
+    with pytest.raises(B.GpoeoError):
+        B.workspace_bytes(d)
+
+
+def test_reserved_fields_must_be_zero(lib):
+    d, _ = good_desc()
+    d.reserved0 = 1
+    size = ctypes.c_size_t()
+    assert lib.gpoeo_pd_workspace_bytes(ctypes.byref(d), ctypes.byref(size)) == B.EINVAL
+    assert lib.gpoeo_pd_workspace_bytes(None, ctypes.byref(size)) == B.EINVAL
+    d, _ = good_desc()
+    assert lib.gpoeo_pd_workspace_bytes(ctypes.byref(d), None) == B.EINVAL
+
+
+def test_detect_rejects_bad_pointers_before_launching(lib):
+    # Fake device addresses: every call below must fail validation on the host.
+    d, _ = good_desc()
+    need = B.workspace_bytes(d)
+    x, res, ws = 0x100000, 0x200000, 0x300000
+    call = lib.gpoeo_pd_detect
+    assert call(None, x, None, res, ws, need, None) == B.EINVAL
+    assert call(ctypes.byref(d), None, None, res, ws, need, None) == B.EINVAL
+    assert call(ctypes.byref(d), x, None, None, ws, need, None) == B.EINVAL
+    assert call(ctypes.byref(d), x, None, res, None, need, None) == B.EINVAL
+    assert call(ctypes.byref(d), x, None, res, ws + 8, need, None) == B.EINVAL  # misaligned ws
+    assert call(ctypes.byref(d), x + 2, None, res, ws, need, None) == B.EINVAL  # misaligned x
+    assert call(ctypes.byref(d), x, None, res, ws, need - 1, None) == B.ENOMEM
+    bad, _ = good_desc(tmax=4000)
+    assert call(ctypes.byref(bad), x, None, res, ws, need, None) == B.EINVAL
+
+
+def test_scores_only_needs_no_results_pointer_but_still_a_workspace(lib):
+    d, _ = good_desc(flags=B.SCORES_ONLY)
+    need = B.workspace_bytes(d)
+    assert lib.gpoeo_pd_detect(ctypes.byref(d), 0x100000, None, None, None, need,
+                               None) == B.EINVAL
+    assert lib.gpoeo_pd_detect(ctypes.byref(d), 0x100000, None, None, 0x300000, need - 1,
+                               None) == B.ENOMEM

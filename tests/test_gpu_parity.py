@@ -1,0 +1,171 @@
+"""GPU parity: the HIP path against the fp64 CPU oracle on the same seeded inputs.
+
+Bar (scores): |S_gpu - S_oracle| <= 1e-4 * |S_oracle| for every lag; a zero
+oracle score must be reproduced exactly.  Bar (selection): period, verdict,
+T_c, the local-search window and the candidate count identical; err within
+1e-4 relative.  No window may be flagged UNRESOLVED.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+import oracle  # noqa: E402
+from gen import make_workload, planted_trace  # noqa: E402
+
+SCORE_RTOL = 1e-4
+
+
+def _device():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+def gpu_run(x_np, lay, flags=0, want_scores=True):
+    import paper_2201_01684_amd as pkg
+    dev = _device()
+    x = torch.from_numpy(np.ascontiguousarray(x_np).reshape(-1)).to(dev)
+    desc, keep = pkg.make_desc(lay.num_windows, lay.num_channels, lay.n, lay.window_stride,
+                               lay.channel_stride, lay.tmin, lay.tmax, lay.c_lag, lay.err_max,
+                               lay.weights, flags)
+    det = pkg.Detector(x, desc, keep, want_scores=want_scores)
+    det.run()
+    torch.cuda.synchronize()
+    scores = None if det.scores is None else det.scores.double().cpu().numpy()
+    res = None if flags & pkg.SCORES_ONLY else det.results_numpy()
+    return scores, res
+
+
+def check_scores(g, o, where=""):
+    assert g.shape == o.shape
+    zero = o == 0
+    assert np.all(g[zero] == 0), f"{where}: zero scores not reproduced"
+    rel = np.abs(g - o)[~zero] / np.abs(o[~zero])
+    if rel.size:
+        worst = np.unravel_index(np.argmax(np.where(zero, 0, np.abs(g - o) / np.where(zero, 1, np.abs(o)))), o.shape)
+        assert rel.max() <= SCORE_RTOL, f"{where}: rel err {rel.max():.3e} at {worst}"
+    return float(rel.max()) if rel.size else 0.0
+
+
+def check_results(res, out, where=""):
+    import paper_2201_01684_amd as pkg
+    assert np.all(res["flags"] & pkg.UNRESOLVED == 0), f"{where}: unresolved windows"
+    for f in ("period", "verdict", "t_cand", "t_low", "t_up", "n_candidates"):
+        bad = np.nonzero(res[f] != out[f])[0]
+        assert bad.size == 0, (f"{where}: {f} differs at windows {bad[:10]}: "
+                               f"gpu {res[f][bad[:10]]} oracle {out[f][bad[:10]]}")
+    has = out["period"] > 0
+    rel = np.abs(res["err"][has].astype(np.float64) - out["err"][has]) / out["err"][has]
+    assert np.all(rel <= 1e-4), f"{where}: err rel {rel.max():.3e}"
+
+
+def parity(x, lay, where=""):
+    g, res = gpu_run(x, lay)
+    o, out = oracle.detect(x, lay)
+    check_scores(g, o, where)
+    check_results(res, out, where)
+    return res, out
+
+
+def test_single_hip_runtime_in_process():
+    import paper_2201_01684_amd as pkg
+    _device()
+    pkg.load_library()
+    maps = open("/proc/self/maps").read()
+    paths = {line.split()[-1] for line in maps.splitlines() if "libamdhip64" in line}
+    assert len(paths) == 1, paths
+
+
+def test_small_workload_full_parity():
+    wl = make_workload("w1")
+    res, _ = parity(wl.x, oracle.Layout.of(wl), "w1")
+    assert res["period"][0] == 137
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("w2", dict(traces=6, n=16384, tmax=2048, pmax=1500)),
+    ("w3", dict(traces=4, n=32768, tmax=4096, pmax=3000)),
+    ("w4", dict(total=131072, n=16384, stride=2048, tmax=4096)),
+    ("w5", dict(traces=3, n=16384, tmax=2048, pmax=1500)),
+])
+def test_reduced_workloads_full_parity(name, kw):
+    wl = make_workload(name, **kw)
+    parity(wl.x, oracle.Layout.of(wl), f"{name}{kw}")
+
+
+@pytest.mark.parametrize("n,tmin,tmax", [
+    (4096, 1, 2048),      # tmin = 1, tmax = N/2
+    (8, 1, 4),            # smallest window
+    (4099, 3, 2049),      # ragged N, odd tmin
+    (1001, 5, 500),       # N not a multiple of 4
+    (5000, 2, 7),         # very few lags
+    (3000, 1021, 1500),   # lag range far from zero
+    (20000, 6, 3333),     # several lag blocks, shifted alignment
+])
+def test_edge_shapes(n, tmin, tmax):
+    x = planted_trace(n, max(3, min(97, n // 3)), 3, seed=n + tmin, sigma=1.0)
+    lay = oracle.Layout(1, 1, n, n, n, tmin, tmax)
+    parity(x, lay, f"n={n} T=[{tmin},{tmax}]")
+
+
+def test_unaligned_strides_and_overlapping_windows():
+    # window stride not a multiple of 4 -> the kernel's dword-load path
+    x = planted_trace(40_003, 211, 5, seed=5, sigma=2.0)
+    lay = oracle.Layout(num_windows=9, num_channels=1, n=8000, window_stride=3999,
+                        channel_stride=8000, tmin=2, tmax=3000)
+    parity(x, lay, "stride 3999")
+    # aligned overlapping windows, every lag-start alignment
+    for tmin in (2, 3, 4, 5):
+        lay = oracle.Layout(num_windows=7, num_channels=1, n=8192, window_stride=4096,
+                            channel_stride=8192, tmin=tmin, tmax=2500 + tmin)
+        parity(x, lay, f"overlap tmin={tmin}")
+
+
+def test_weighted_channels():
+    rng = np.random.default_rng(3)
+    b, c, n = 3, 3, 6000
+    base = np.stack([planted_trace(n, 300 + 17 * k, 6, seed=k, sigma=0.5) for k in range(b)])
+    x = np.stack([base * s + rng.normal(0, 0.3, size=(b, n)) for s in (1.0, 0.01, 30.0)], axis=1)
+    x = x.astype(np.float32)
+    lay = oracle.Layout(b, c, n, c * n, n, 2, 3000,
+                        weights=np.array([1.0, 250.0, 0.003], dtype=np.float32))
+    parity(x, lay, "weighted")
+
+
+def test_constant_noise_free_and_white_noise_windows():
+    n = 8192
+    rows = [np.full(n, 123.25, dtype=np.float32),                         # CONSTANT
+            planted_trace(n, 64, 4, seed=1, integer=True),                  # exact zeros, ties
+            planted_trace(n, 301, 9, seed=2, integer=True),
+            np.random.default_rng(4).normal(0, 1, n).astype(np.float32),    # no clear period
+            np.zeros(n, dtype=np.float32)]
+    x = np.stack(rows)
+    lay = oracle.Layout(len(rows), 1, n, n, n, 2, 4096)
+    res, out = parity(x, lay, "special windows")
+    assert res["verdict"][0] == oracle.CONSTANT and res["verdict"][4] == oracle.CONSTANT
+    assert res["period"][1] == 64 and res["period"][2] == 301
+
+
+def test_no_rescue_flag_and_scores_only():
+    import paper_2201_01684_amd as pkg
+    wl = make_workload("w2", traces=4, n=16384, tmax=2048, pmax=1500)
+    lay = oracle.Layout.of(wl)
+    g, _ = gpu_run(wl.x, lay, flags=pkg.SCORES_ONLY)
+    o, out = oracle.detect(wl.x, lay)
+    check_scores(g, o, "scores only")
+    g2, res = gpu_run(wl.x, lay, flags=pkg.NO_RESCUE)
+    assert np.all(res["n_rescored"] == 0)
+    assert np.all(np.abs(res["period"] - out["period"]) <= 2)
+
+
+def test_deterministic_bitwise():
+    wl = make_workload("w3", traces=3, n=32768, tmax=4096, pmax=3000)
+    lay = oracle.Layout.of(wl)
+    a, ra = gpu_run(wl.x, lay)
+    b, rb = gpu_run(wl.x, lay)
+    assert np.array_equal(a, b) and np.array_equal(ra, rb)
