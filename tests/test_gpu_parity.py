@@ -60,7 +60,10 @@ def check_results(res, out, where=""):
         assert bad.size == 0, (f"{where}: {f} differs at windows {bad[:10]}: "
                                f"gpu {res[f][bad[:10]]} oracle {out[f][bad[:10]]}")
     has = out["period"] > 0
-    rel = np.abs(res["err"][has].astype(np.float64) - out["err"][has]) / out["err"][has]
+    g_err, o_err = res["err"][has].astype(np.float64), out["err"][has]
+    assert np.all(g_err[o_err == 0] == 0), f"{where}: zero err not reproduced"
+    nz = o_err != 0
+    rel = np.abs(g_err[nz] - o_err[nz]) / o_err[nz]
     assert np.all(rel <= 1e-4), f"{where}: err rel {rel.max():.3e}"
 
 
