@@ -24,6 +24,9 @@ LIB_NAME = "libgpoeo_pd.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
 
 SOURCES = ["api.cpp", "lag_score.hip", "window_stats.hip", "select.hip"]
+# The selection re-evaluates scores and thresholds as plain fp64 expressions
+# (one rounding per operation, as written); no multiply-add contraction there.
+EXTRA_FLAGS = {"select.hip": ["-ffp-contract=off"]}
 ARCH = os.environ.get("GPOEO_PD_ARCH", "gfx950")
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -53,7 +56,8 @@ def _torch_lib_dir() -> str | None:
 
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(OBJ_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [_hipcc(), *HIP_FLAGS, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [_hipcc(), *HIP_FLAGS, *EXTRA_FLAGS.get(src, []), "-x", "hip", "-c",
+           os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -84,7 +84,7 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
     p->bitmap_words = (p->lags + 31) / 32;
 
     int64_t n_var, n_s, n_bits, n_part;
-    if (!mul_ok(bc, 1, &n_var)) return GPOEO_PD_EINVAL;
+    if (!mul_ok(bc, 2, &n_var)) return GPOEO_PD_EINVAL;      // variance, mean |x|
     if (!mul_ok(d->num_windows, p->lags, &n_s)) return GPOEO_PD_EINVAL;
     if (!mul_ok(d->num_windows, p->bitmap_words, &n_bits)) return GPOEO_PD_EINVAL;
     int64_t tmp;
@@ -95,8 +95,12 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
     off = align_up(off + (size_t)n_var * sizeof(double));
     p->off_s64 = off;
     off = align_up(off + (size_t)n_s * sizeof(double));
-    p->off_bits = off;
-    off = align_up(off + (size_t)n_bits * sizeof(uint32_t));
+    p->off_bits = off;                            // four bitmaps
+    off = align_up(off + 4 * (size_t)n_bits * sizeof(uint32_t));
+    p->off_state = off;
+    off = align_up(off + (size_t)d->num_windows * sizeof(WinState));
+    p->off_queue = off;                           // q_win, q_lag, q_count
+    off = align_up(off + (4 * (size_t)kQueueCap + 2 * kPasses) * sizeof(int32_t));
     p->off_part = off;
     off = align_up(off + (size_t)n_part * sizeof(double));
     p->bytes = off;
@@ -151,7 +155,18 @@ static int detect_impl(const gpoeo_pd_desc* desc, const float* x, float* scores,
     char* ws = static_cast<char*>(workspace);
     double* var = reinterpret_cast<double*>(ws + p.off_var);
     double* s64 = reinterpret_cast<double*>(ws + p.off_s64);
+    const size_t words = (size_t)p.num_windows * p.bitmap_words;
     uint32_t* bits = reinterpret_cast<uint32_t*>(ws + p.off_bits);
+    int32_t* queue = reinterpret_cast<int32_t*>(ws + p.off_queue);
+    gpoeo::SelectBuffers sb;
+    sb.tier1 = bits;
+    sb.tier2 = bits + words;
+    sb.queued1 = bits + 2 * words;
+    sb.queued2 = bits + 3 * words;
+    sb.state = reinterpret_cast<gpoeo::WinState*>(ws + p.off_state);
+    sb.q_win = queue;
+    sb.q_lag = queue + 2 * gpoeo::kQueueCap;
+    sb.q_count = queue + 4 * gpoeo::kQueueCap;
     double* part = reinterpret_cast<double*>(ws + p.off_part);
 
     auto mark = [&](int k) { return !ev || hipEventRecord(ev[k], stream) == hipSuccess; };
@@ -165,7 +180,7 @@ static int detect_impl(const gpoeo_pd_desc* desc, const float* x, float* scores,
         return GPOEO_PD_EHIP;
     if (!mark(3)) return GPOEO_PD_EHIP;
     if (!scores_only &&
-        gpoeo::launch_select(p, w, x, var, s64, bits, results, stream) != hipSuccess)
+        gpoeo::launch_select(p, w, x, var, s64, sb, results, stream) != hipSuccess)
         return GPOEO_PD_EHIP;
     if (!mark(4)) return GPOEO_PD_EHIP;
     return GPOEO_PD_OK;

@@ -17,11 +17,35 @@ constexpr int kMaxChannels = 256;    // channel weights travel as a kernel argum
 // non-negative terms (each run: kRunSamples roundings plus the rounding of the
 // difference, about 258 * 2^-24 = 1.54e-5) and combined in fp64; rounded up.
 constexpr double kScoreRelBound = 2.5e-5;
-// Relative error bound of R from a parallel fp64 two-pass variance.
-constexpr double kRefRelBound = 1e-12;
 
 struct Weights {
     float w[kMaxChannels];
+};
+
+// Selection passes (with one re-score round between consecutive passes) and the
+// capacity of each re-score queue (per tier, per round, all windows together).
+constexpr int kPasses = 4;
+constexpr int kQueueCap = 1 << 16;
+
+// Per-window selection state kept in the workspace between selection passes.
+struct WinState {
+    double r_exact;          // R as a plain sequential fp64 evaluation, once computed
+    int32_t done;            // result written
+    int32_t r_queued;        // R queued for the sequential evaluation
+    int32_t r_is_exact;
+    int32_t rescored;        // lags re-scored in fp64 so far
+};
+
+// Workspace buffers of the selection.
+struct SelectBuffers {
+    uint32_t* tier1;         // [B][words] bitmaps
+    uint32_t* tier2;
+    uint32_t* queued1;
+    uint32_t* queued2;
+    WinState* state;         // [B]
+    int32_t* q_win;          // [2][kQueueCap]
+    int32_t* q_lag;          // [2][kQueueCap]
+    int32_t* q_count;        // [kPasses][2]
 };
 
 // Everything the kernels need, derived on the host from a validated descriptor.
@@ -44,15 +68,16 @@ struct Plan {
     uint32_t flags;
     int32_t bitmap_words;    // 32-bit words per window of the exactness bitmap
     // workspace layout (byte offsets, 256-byte aligned)
-    size_t off_var, off_s64, off_bits, off_part, bytes;
+    size_t off_var, off_s64, off_bits, off_state, off_queue, off_part, bytes;
 };
 
 // Kernel launchers; each returns hipGetLastError() after enqueueing.
+// var: [B][C][2] = population variance, mean |x| per window and channel.
 hipError_t launch_window_stats(const Plan& p, const float* x, double* var, hipStream_t s);
 hipError_t launch_lag_score(const Plan& p, const float* x, double* part, hipStream_t s);
 hipError_t launch_finalize(const Plan& p, const Weights& w, const double* part, double* s64,
                            float* scores, hipStream_t s);
 hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const double* var,
-                         double* s64, uint32_t* bits, void* results, hipStream_t s);
+                         double* s64, const SelectBuffers& sb, void* results, hipStream_t s);
 
 }  // namespace gpoeo

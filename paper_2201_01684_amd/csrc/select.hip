@@ -15,15 +15,23 @@
 //            T_c = D / k, i.e. Algorithm 1's local search at a one-sample step
 //   period = smallest T in the window attaining min S; err = S(period) / R
 //
-// Each score comes from the score kernels with a relative error bound
-// (kScoreRelBound), so it is handled as the interval [v(1-e), v(1+e)] that
-// contains the value a plain sequential fp64 evaluation gives.  A comparison
-// the intervals decide is final.  Otherwise the lags involved (and R, when the
-// threshold or err is involved) are recomputed here as plain sequential fp64
-// sums in ascending index order with no fused multiply-add, which makes them
-// exact points, and the rule runs again.  The number of passes is bounded; if
-// the bound is reached the last pass decides on the unwidened values and the
-// window is flagged GPOEO_PD_UNRESOLVED.
+// Every score carries a tier and is handled as an interval [v(1-e), v(1+e)]
+// that contains the value a plain sequential fp64 evaluation of the definition
+// gives:
+//   tier 0  from the score kernels (fp32 runs, fp64 combine): e = kScoreRelBound
+//   tier 1  re-scored in fp64 by one wavefront (64 strided partial sums and a
+//           fixed-order tree): e = tau1, derived from N (about 3e-11 at
+//           N = 262144) - it covers the rounding of both evaluation orders
+//   tier 2  re-scored as the plain sequential fp64 sum itself (ascending i,
+//           one rounding per operation, no contraction): a point
+// R is an fp64 two-pass value whose distance to the sequential evaluation is
+// bounded from N, the variances and the mean absolute samples (see
+// reference_bound), or a point once recomputed sequentially.  A comparison the intervals decide is final.
+// Otherwise the lags involved are queued for the next tier (R for a point),
+// a re-score kernel spread over the whole GPU raises them, and the rule runs
+// again.  The launcher runs kPasses selection passes with a re-score round
+// between consecutive ones; a window still open in the last pass is decided
+// on the unwidened values and flagged GPOEO_PD_UNRESOLVED.
 #include "internal.h"
 #include "gpoeo_pd.h"
 
@@ -31,22 +39,30 @@ namespace gpoeo {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kNeedCap = 512;
-constexpr int kMaxPasses = 24;
+constexpr int kRescoreGroups = 1024;   // workgroups of one re-score round
 
 struct SelectArgs {
     const float* x;
-    const double* var;       // [B][C]
-    double* s64;             // [B][L], overwritten in place by exact re-scores
-    uint32_t* bits;          // [B][bitmap_words], 1 = exact value in s64
+    const double* var;       // [B][C][2]: variance, mean |x|
+    double* s64;             // [B][L], overwritten in place by re-scores
+    uint32_t* tier1;         // [B][words]: value is tier >= 1
+    uint32_t* tier2;         // [B][words]: value is tier 2
+    uint32_t* queued1;       // [B][words]: queued for a tier-1 re-score
+    uint32_t* queued2;       // [B][words]: queued for a tier-2 re-score
+    WinState* state;         // [B]
+    int32_t* q_win;          // [2][kQueueCap] queued (window, lag) pairs, per tier
+    int32_t* q_lag;          //   lag -1 in the tier-2 queue: R of that window
+    int32_t* q_count;        // [kPasses][2] queue lengths per round and tier
     gpoeo_pd_result* results;
     int64_t n;
     int64_t window_stride;
     int64_t channel_stride;
     int32_t num_channels;
     int32_t tmin, tmax, lags, words;
-    double c_lag, err_max;
+    double c_lag, err_max, tau1;
     uint32_t flags;
+    int32_t pass;
+    int32_t last;
 };
 
 enum Tri : int { kNo = 0, kYes = 1, kUnk = 2 };
@@ -67,30 +83,62 @@ __device__ __forceinline__ Tri le(const Iv& a, const Iv& b) {
     return kUnk;
 }
 
-// Plain sequential fp64 evaluation of S(T), ascending i, no contraction.
+// The exact re-scores below are plain sequential fp64 sums (ascending index,
+// one rounding per addition, no contraction).  Their cost is a chain of
+// dependent additions; to keep it from also waiting on memory at every step,
+// samples are staged through registers in chunks of kChunk and the loads of
+// the next chunk are issued before the additions of the current one.
+constexpr int kChunk = 32;
+
+template <typename F>
+__device__ __forceinline__ void for_pairs(const float* __restrict__ a, const float* __restrict__ b,
+                                          int64_t m, F&& step) {
+    float ca[kChunk], cb[kChunk], na[kChunk], nb[kChunk];
+    const int64_t full = m / kChunk;
+    if (full > 0) {
+#pragma unroll
+        for (int k = 0; k < kChunk; ++k) {
+            ca[k] = a[k];
+            cb[k] = b[k];
+        }
+    }
+    for (int64_t c = 0; c < full; ++c) {
+        const bool more = c + 1 < full;
+        if (more) {
+            const int64_t o = (c + 1) * kChunk;
+#pragma unroll
+            for (int k = 0; k < kChunk; ++k) {
+                na[k] = a[o + k];
+                nb[k] = b[o + k];
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kChunk; ++k) step(ca[k], cb[k]);
+        if (more) {
+#pragma unroll
+            for (int k = 0; k < kChunk; ++k) {
+                ca[k] = na[k];
+                cb[k] = nb[k];
+            }
+        }
+    }
+    for (int64_t i = full * kChunk; i < m; ++i) step(a[i], b[i]);
+}
+
+// Plain sequential fp64 evaluation of S(T) = sum_c w_c * D_c(T) / (N - T).
 __device__ double exact_score(const float* __restrict__ xw, int32_t num_channels,
                               int64_t channel_stride, int64_t n, int64_t t, const Weights& w) {
 #pragma clang fp contract(off)
     double s = 0.0;
     for (int32_t c = 0; c < num_channels; ++c) {
         const float* __restrict__ xc = xw + (int64_t)c * channel_stride;
-        double dsum = 0.0;
         const int64_t m = n - t;
-        int64_t i = 0;
-        for (; i + 4 <= m; i += 4) {
-            const float a0 = xc[i], a1 = xc[i + 1], a2 = xc[i + 2], a3 = xc[i + 3];
-            const float b0 = xc[i + t], b1 = xc[i + t + 1], b2 = xc[i + t + 2],
-                        b3 = xc[i + t + 3];
-            double d;
-            d = (double)a0 - (double)b0; dsum = dsum + d * d;
-            d = (double)a1 - (double)b1; dsum = dsum + d * d;
-            d = (double)a2 - (double)b2; dsum = dsum + d * d;
-            d = (double)a3 - (double)b3; dsum = dsum + d * d;
-        }
-        for (; i < m; ++i) {
-            const double d = (double)xc[i] - (double)xc[i + t];
+        double dsum = 0.0;
+        for_pairs(xc, xc + t, m, [&](float u, float v) {
+#pragma clang fp contract(off)
+            const double d = (double)u - (double)v;
             dsum = dsum + d * d;
-        }
+        });
         s = s + (double)w.w[c] * (dsum / (double)m);
     }
     return s;
@@ -104,31 +152,18 @@ __device__ double exact_reference(const float* __restrict__ xw, int32_t num_chan
     for (int32_t c = 0; c < num_channels; ++c) {
         const float* __restrict__ xc = xw + (int64_t)c * channel_stride;
         double sum = 0.0;
-        for (int64_t i = 0; i < n; ++i) sum = sum + (double)xc[i];
+        for_pairs(xc, xc, n, [&](float u, float) { sum = sum + (double)u; });
         const double mean = sum / (double)n;
         double sq = 0.0;
-        for (int64_t i = 0; i < n; ++i) {
-            const double d = (double)xc[i] - mean;
+        for_pairs(xc, xc, n, [&](float u, float) {
+#pragma clang fp contract(off)
+            const double d = (double)u - mean;
             sq = sq + d * d;
-        }
+        });
         acc = acc + (double)w.w[c] * (sq / (double)n);
     }
     return 2.0 * acc;
 }
-
-struct Shared {
-    double red_d[kThreads];
-    double red_d2[kThreads];
-    int64_t red_i[kThreads];
-    int64_t red_j[kThreads];
-    int32_t need[kNeedCap];
-    int need_count;
-    int need_r;
-    int need_pk;
-    int rescored;
-    double r_lo, r_hi, r_v;
-    int r_exact;
-};
 
 __device__ double block_min_d(double v, double* red) {
     red[threadIdx.x] = v;
@@ -166,88 +201,180 @@ __device__ int64_t block_min_i(int64_t v, int64_t* red) {
     return r;
 }
 
-__global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a, Weights w) {
+
+// Tier-1 re-score: S(T) in fp64 by one wavefront.  Lane l accumulates the
+// terms i = l + 64 (4k + r) in four partial sums r = 0..3, which are combined
+// as (p0 + p1) + (p2 + p3) and then across lanes by a fixed shuffle tree; every
+// lane returns lane 0's value.  Each partial sum holds at most M/256 + 1 terms,
+// so the result is within (M/256 + 10) u of the exact sum (u = 2^-53).
+__device__ double wave_score(const float* __restrict__ xw, int32_t num_channels,
+                             int64_t channel_stride, int64_t n, int64_t t, const Weights& w,
+                             int lane) {
+    double s = 0.0;
+    for (int32_t c = 0; c < num_channels; ++c) {
+        const float* __restrict__ xc = xw + (int64_t)c * channel_stride;
+        const int64_t m = n - t;
+        double p[4] = {0.0, 0.0, 0.0, 0.0};
+        int64_t i = lane;
+        for (; i + 192 < m; i += 256) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const double d = (double)xc[i + 64 * r] - (double)xc[i + 64 * r + t];
+                p[r] = p[r] + d * d;
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int64_t k = i + 64 * r;
+            if (k < m) {
+                const double d = (double)xc[k] - (double)xc[k + t];
+                p[r] = p[r] + d * d;
+            }
+        }
+        double part = (p[0] + p[1]) + (p[2] + p[3]);
+        for (int off = 32; off > 0; off >>= 1) part = part + __shfl_down(part, off);
+        part = __shfl(part, 0);
+        s = s + (double)w.w[c] * (part / (double)m);
+    }
+    return s;
+}
+
+// Half-width of the interval around the two-pass fp64 R that contains the
+// plain sequential evaluation.  Any evaluation order of the mean of N samples
+// errs by at most (N+1) u A (A = mean |x|); the second pass then sums
+// Var + dmean^2 exactly, up to (N+4) u relative.  Two orders thus differ by at
+// most 4 (N+4) u Var + 4.02 ((N+1) u A)^2 per channel, weighted and doubled
+// for R, plus the rounding of the weighted channel sum.
+__device__ double reference_bound(const double* var2, int32_t num_channels, int64_t n,
+                                  const Weights& w, double r) {
+    const double u = 1.1102230246251565e-16;
+    const double nn = (double)n;
+    double e = 0.0;
+    for (int32_t c = 0; c < num_channels; ++c) {
+        const double v = var2[2 * c], am = var2[2 * c + 1];
+        const double dm = (nn + 1.0) * u * am;
+        e += (double)w.w[c] * (4.0 * (nn + 4.0) * u * v + 4.02 * dm * dm);
+    }
+    return 1.01 * (2.0 * e + (num_channels + 4.0) * u * r);
+}
+
+struct Shared {
+    double red_d[kThreads];
+    double red_d2[kThreads];
+    int64_t red_i[kThreads];
+    int64_t red_j[kThreads];
+    int done;
+    double r_approx;
+    double r_err;
+};
+
+__global__ __launch_bounds__(kThreads) void select_pass_kernel(SelectArgs a, Weights w) {
     __shared__ Shared sh;
     const int tid = threadIdx.x;
     const int64_t b = blockIdx.x;
     const int32_t tmin = a.tmin, tmax = a.tmax;
     double* __restrict__ s = a.s64 + b * (int64_t)a.lags;
-    uint32_t* __restrict__ bits = a.bits + b * (int64_t)a.words;
-    const float* __restrict__ xw = a.x + b * a.window_stride;
+    uint32_t* __restrict__ t1 = a.tier1 + b * (int64_t)a.words;
+    uint32_t* __restrict__ t2 = a.tier2 + b * (int64_t)a.words;
+    uint32_t* __restrict__ qd1 = a.queued1 + b * (int64_t)a.words;
+    uint32_t* __restrict__ qd2 = a.queued2 + b * (int64_t)a.words;
+    WinState* st = a.state + b;
     gpoeo_pd_result* res = a.results + b;
+    int32_t* count = a.q_count + 2 * a.pass;
 
-    for (int32_t k = tid; k < a.words; k += kThreads) bits[k] = 0u;
+    if (a.pass == 0) {
+        for (int32_t k = tid; k < a.words; k += kThreads) {
+            t1[k] = 0u;
+            t2[k] = 0u;
+            qd1[k] = 0u;
+            qd2[k] = 0u;
+        }
+        if (tid == 0) {
+            st->r_exact = 0.0;
+            st->done = 0;
+            st->r_queued = 0;
+            st->r_is_exact = 0;
+            st->rescored = 0;
+        }
+    }
     if (tid == 0) {
+        sh.done = a.pass == 0 ? 0 : st->done;
+        const double* v2 = a.var + 2 * b * a.num_channels;
         double acc = 0.0;
-        for (int32_t c = 0; c < a.num_channels; ++c)
-            acc += (double)w.w[c] * a.var[b * a.num_channels + c];
-        sh.r_v = 2.0 * acc;
-        sh.r_exact = 0;
-        sh.rescored = 0;
+        for (int32_t c = 0; c < a.num_channels; ++c) acc = acc + (double)w.w[c] * v2[2 * c];
+        sh.r_approx = 2.0 * acc;
+        sh.r_err = reference_bound(v2, a.num_channels, a.n, w, sh.r_approx);
     }
     __syncthreads();
-    const double r_approx = sh.r_v;
+    if (sh.done) return;
+    const double r_approx = sh.r_approx;
+    const double r_err = sh.r_err;
     if (r_approx == 0.0) {   // every weighted channel constant (exact: see window_stats)
         if (tid == 0) {
             gpoeo_pd_result o = {};
             o.verdict = GPOEO_PD_CONSTANT;
             *res = o;
+            st->done = 1;
         }
         return;
     }
-
-    const bool rescue = (a.flags & GPOEO_PD_NO_RESCUE) == 0;
-    bool unresolved = false;
+    const bool r_exact = a.pass > 0 && st->r_is_exact;
+    const double r_x = r_exact ? st->r_exact : 0.0;
     const double c_lag = a.c_lag;
 
-    for (int pass = 0;; ++pass) {
-        const bool last = !rescue || pass == kMaxPasses;
-        if (rescue && pass == kMaxPasses) unresolved = true;
-        const double tau = last ? 0.0 : kScoreRelBound;
-        const double tau_r = last ? 0.0 : kRefRelBound;
-        if (tid == 0) {
-            sh.need_count = 0;
-            sh.need_r = 0;
-            sh.need_pk = 0;
-            if (sh.r_exact) {
-                sh.r_lo = sh.r_hi = sh.r_v;
-            } else {
-                sh.r_lo = r_approx * (1.0 - tau_r);
-                sh.r_hi = r_approx * (1.0 + tau_r);
-                sh.r_v = r_approx;
-            }
-        }
-        __syncthreads();
-        const double r_lo = sh.r_lo, r_hi = sh.r_hi, r_v = sh.r_v;
+    // Queue (window b, lag t) for the next tier; lag -1 queues R.
+    auto enqueue = [&](int tier, int32_t t) {
+        const int k = atomicAdd(&count[tier - 1], 1);
+        if (k >= kQueueCap) return false;
+        a.q_win[(tier - 1) * kQueueCap + k] = (int32_t)b;
+        a.q_lag[(tier - 1) * kQueueCap + k] = t;
+        return true;
+    };
+    auto want_r = [&]() {
+        if (atomicExch(&st->r_queued, 1) == 0 && !enqueue(2, -1)) atomicExch(&st->r_queued, 0);
+    };
 
+    // One evaluation of the rule with tier-0 / tier-1 / reference half-widths.
+    // Returns true with `o` filled when every comparison was decided;
+    // otherwise queues what decides the open ones (when may_push).
+    auto rule = [&](double tau0, double tau1, double e_r, bool may_push,
+                    gpoeo_pd_result& o) -> bool {
+        const double r_lo = r_exact ? r_x : r_approx - e_r;
+        const double r_hi = r_exact ? r_x : r_approx + e_r;
+        const double r_v = r_exact ? r_x : r_approx;
         auto iv = [&](int64_t t) -> Iv {
             const int64_t j = t - tmin;
             const double v = s[j];
-            const bool ex = (bits[j >> 5] >> (j & 31)) & 1u;
+            const uint32_t bit = 1u << (j & 31);
             Iv r;
             r.v = v;
-            r.exact = ex;
-            if (ex) {
+            if (t2[j >> 5] & bit) {
+                r.exact = true;
                 r.lo = r.hi = v;
             } else {
-                r.lo = v * (1.0 - tau);
-                r.hi = v * (1.0 + tau);
+                const double e = (t1[j >> 5] & bit) ? tau1 : tau0;
+                r.exact = false;
+                r.lo = v * (1.0 - e);
+                r.hi = v * (1.0 + e);
             }
             return r;
         };
         auto push = [&](int64_t t, const Iv& z) {
-            if (z.exact || last) return;
-            const int k = atomicAdd(&sh.need_count, 1);
-            if (k < kNeedCap) sh.need[k] = (int32_t)t;
+            if (z.exact || !may_push) return;
+            const int64_t j = t - tmin;
+            const uint32_t bit = 1u << (j & 31);
+            const bool at1 = (t1[j >> 5] & bit) != 0;
+            uint32_t* qd = at1 ? qd2 : qd1;
+            if (atomicOr(&qd[j >> 5], bit) & bit) return;   // already queued
+            if (!enqueue(at1 ? 2 : 1, (int32_t)t)) atomicAnd(&qd[j >> 5], ~bit);   // full
         };
-        // peak status of T: kYes / kNo / kUnk (and pushes the lags of an open test)
         auto peak = [&](int64_t t, Iv& z, bool do_push) -> Tri {
             const Iv m = iv(t - 1);
             z = iv(t);
             const Iv p = iv(t + 1);
-            const Tri t1 = lt(z, m), t2 = le(z, p);
-            if (t1 == kNo || t2 == kNo) return kNo;
-            if (t1 == kYes && t2 == kYes) return kYes;
+            const Tri c1 = lt(z, m), c2 = le(z, p);
+            if (c1 == kNo || c2 == kNo) return kNo;
+            if (c1 == kYes && c2 == kYes) return kYes;
             if (do_push) {
                 push(t - 1, m);
                 push(t, z);
@@ -255,199 +382,240 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a, Weights 
             }
             return kUnk;
         };
+        const double ulp4 = 4.0 * 2.220446049250313e-16;
+        o = gpoeo_pd_result{};
 
-        gpoeo_pd_result o = {};
-        bool done = false;
-        do {
-            // 1. peaks.  An open local-minimum test only matters for a lag that
-            // could be a candidate (S < thr) or the smallest peak; thr is at most
-            // thr(R_hi, min hi over decided peaks), so open tests of lags whose
-            // lower bound lies above that (and above the smallest decided peak)
-            // are left open.
-            int64_t npk = 0, unk = 0;
-            double pk_lo = INFINITY, pk_hi = INFINITY, unk_lo = INFINITY;
-            for (int64_t t = tmin + 1 + tid; t < tmax; t += kThreads) {
-                Iv z;
-                const Tri q = peak(t, z, false);
-                if (q == kYes) {
-                    ++npk;
-                    pk_lo = fmin(pk_lo, z.lo);
-                    pk_hi = fmin(pk_hi, z.hi);
-                } else if (q == kUnk) {
-                    ++unk;
-                    unk_lo = fmin(unk_lo, z.lo);
+        // 1. peaks.  An open local-minimum test only matters for a lag that
+        // could be a candidate (S < thr) or the smallest peak; thr is at most
+        // thr(R_hi, min hi over decided peaks), so open tests of lags whose
+        // lower bound lies above that (and above the smallest decided peak)
+        // are left open.
+        int64_t npk = 0, unk = 0;
+        double pk_lo = INFINITY, pk_hi = INFINITY, unk_lo = INFINITY;
+        for (int64_t t = tmin + 1 + tid; t < tmax; t += kThreads) {
+            Iv z;
+            const Tri q = peak(t, z, false);
+            if (q == kYes) {
+                ++npk;
+                pk_lo = fmin(pk_lo, z.lo);
+                pk_hi = fmin(pk_hi, z.hi);
+            } else if (q == kUnk) {
+                ++unk;
+                unk_lo = fmin(unk_lo, z.lo);
+            }
+        }
+        unk = block_sum_i(unk, sh.red_i);
+        npk = block_sum_i(npk, sh.red_j);
+        pk_lo = block_min_d(pk_lo, sh.red_d);
+        pk_hi = block_min_d(pk_hi, sh.red_d2);
+        unk_lo = block_min_d(unk_lo, sh.red_d);
+        if (unk > 0) {
+            const double cut =
+                npk > 0 ? fmax(r_hi - c_lag * (r_hi - pk_hi) + ulp4 * r_hi, pk_hi) : INFINITY;
+            if (unk_lo < cut) {
+                for (int64_t t = tmin + 1 + tid; t < tmax; t += kThreads) {
+                    Iv z;
+                    if (peak(t, z, false) == kUnk && z.lo < cut) peak(t, z, true);
+                }
+                return false;
+            }
+        }
+        if (npk == 0) {
+            o.verdict = GPOEO_PD_APERIODIC;
+            return true;
+        }
+        // 2. threshold and candidates
+        Iv thr;
+        if (pk_lo == pk_hi && r_lo == r_hi) {
+            thr.lo = thr.hi = r_v - c_lag * (r_v - pk_lo);
+        } else {
+            thr.lo = r_lo - c_lag * (r_lo - pk_lo) - ulp4 * r_hi;
+            thr.hi = r_hi - c_lag * (r_hi - pk_hi) + ulp4 * r_hi;
+        }
+        thr.v = 0.5 * (thr.lo + thr.hi);
+        thr.exact = thr.lo == thr.hi;
+        int64_t ncand = 0, tc = INT64_MAX;
+        unk = 0;
+        for (int64_t t = tmin + 1 + tid; t < tmax; t += kThreads) {
+            Iv z;
+            if (peak(t, z, false) != kYes) continue;
+            const Tri q = lt(z, thr);
+            if (q == kYes) {
+                ++ncand;
+                tc = min(tc, t);
+            } else if (q == kUnk) {
+                ++unk;
+                push(t, z);
+            }
+        }
+        unk = block_sum_i(unk, sh.red_i);
+        ncand = block_sum_i(ncand, sh.red_j);
+        tc = block_min_i(tc, sh.red_i);
+        if (unk > 0) {
+            // the threshold must tighten too: R and every peak that can be
+            // the smallest one
+            if (r_lo != r_hi && tid == 0 && may_push) want_r();
+            if (pk_lo != pk_hi) {
+                for (int64_t t = tmin + 1 + tid; t < tmax; t += kThreads) {
+                    Iv z;
+                    if (peak(t, z, false) == kYes && z.lo <= pk_hi) push(t, z);
                 }
             }
-            unk = block_sum_i(unk, sh.red_i);
-            npk = block_sum_i(npk, sh.red_j);
-            pk_lo = block_min_d(pk_lo, sh.red_d);
-            pk_hi = block_min_d(pk_hi, sh.red_d2);
-            unk_lo = block_min_d(unk_lo, sh.red_d);
-            if (unk > 0) {
-                const double pad = 4.0 * 2.220446049250313e-16 * r_hi;
-                const double cut =
-                    npk > 0 ? fmax(r_hi - c_lag * (r_hi - pk_hi) + pad, pk_hi) : INFINITY;
-                if (unk_lo < cut) {
-                    for (int64_t t = tmin + 1 + tid; t < tmax; t += kThreads) {
-                        Iv z;
-                        if (peak(t, z, false) == kUnk && z.lo < cut) peak(t, z, true);
-                    }
-                    break;
-                }
+            return false;
+        }
+        o.n_candidates = (int32_t)ncand;
+        if (ncand == 0) {
+            o.verdict = GPOEO_PD_APERIODIC;
+            return true;
+        }
+        o.t_cand = (int32_t)tc;
+        // 3. local search window
+        const int64_t d = a.n - 1;
+        int64_t lo = (tc * d + (d + tc) - 1) / (d + tc);
+        int64_t hi = (tc * d) / (d - tc);
+        lo = max(lo, (int64_t)tmin);
+        hi = min(hi, (int64_t)tmax);
+        o.t_low = (int32_t)lo;
+        o.t_up = (int32_t)hi;
+        double m_hi = INFINITY;
+        for (int64_t t = lo + tid; t <= hi; t += kThreads) m_hi = fmin(m_hi, iv(t).hi);
+        m_hi = block_min_d(m_hi, sh.red_d);
+        int64_t ncont = 0, nopen = 0, tbest = INT64_MAX;
+        for (int64_t t = lo + tid; t <= hi; t += kThreads) {
+            const Iv z = iv(t);
+            if (z.lo <= m_hi) {
+                ++ncont;
+                if (!z.exact) ++nopen;
+                tbest = min(tbest, t);
             }
-            if (npk == 0) {
-                o.verdict = GPOEO_PD_APERIODIC;
-                done = true;
-                break;
-            }
-            // 2. threshold and candidates
-            double thr_lo, thr_hi;
-            if (pk_lo == pk_hi && r_lo == r_hi) {
-                thr_lo = thr_hi = r_v - c_lag * (r_v - pk_lo);
-            } else {
-                const double pad = 4.0 * 2.220446049250313e-16 * r_hi;
-                thr_lo = r_lo - c_lag * (r_lo - pk_lo) - pad;
-                thr_hi = r_hi - c_lag * (r_hi - pk_hi) + pad;
-            }
-            Iv thr;
-            thr.lo = thr_lo;
-            thr.hi = thr_hi;
-            thr.v = 0.5 * (thr_lo + thr_hi);
-            thr.exact = thr_lo == thr_hi;
-            int64_t ncand = 0, tc = INT64_MAX;
-            unk = 0;
-            for (int64_t t = tmin + 1 + tid; t < tmax; t += kThreads) {
-                Iv z;
-                if (peak(t, z, false) != kYes) continue;
-                const Tri q = lt(z, thr);
-                if (q == kYes) {
-                    ++ncand;
-                    tc = min(tc, t);
-                } else if (q == kUnk) {
-                    ++unk;
-                    push(t, z);
-                }
-            }
-            unk = block_sum_i(unk, sh.red_i);
-            ncand = block_sum_i(ncand, sh.red_j);
-            tc = block_min_i(tc, sh.red_i);
-            if (unk > 0) {
-                // the threshold itself must become exact: R and every peak that
-                // can be the smallest one
-                if (r_lo != r_hi && tid == 0) sh.need_r = 1;
-                if (pk_lo != pk_hi) {
-                    for (int64_t t = tmin + 1 + tid; t < tmax; t += kThreads) {
-                        Iv z;
-                        if (peak(t, z, false) == kYes && z.lo <= pk_hi) push(t, z);
-                    }
-                }
-                break;
-            }
-            o.n_candidates = (int32_t)ncand;
-            if (ncand == 0) {
-                o.verdict = GPOEO_PD_APERIODIC;
-                done = true;
-                break;
-            }
-            o.t_cand = (int32_t)tc;
-            // 3. local search window
-            const int64_t d = a.n - 1;
-            int64_t lo = (tc * d + (d + tc) - 1) / (d + tc);
-            int64_t hi = (tc * d) / (d - tc);
-            lo = max(lo, (int64_t)tmin);
-            hi = min(hi, (int64_t)tmax);
-            o.t_low = (int32_t)lo;
-            o.t_up = (int32_t)hi;
-            double m_hi = INFINITY;
-            for (int64_t t = lo + tid; t <= hi; t += kThreads) m_hi = fmin(m_hi, iv(t).hi);
-            m_hi = block_min_d(m_hi, sh.red_d);
-            int64_t ncont = 0, nopen = 0, tbest = INT64_MAX;
+        }
+        ncont = block_sum_i(ncont, sh.red_i);
+        nopen = block_sum_i(nopen, sh.red_j);
+        tbest = block_min_i(tbest, sh.red_i);
+        if (ncont > 1 && nopen > 0 && tau0 > 0.0) {
             for (int64_t t = lo + tid; t <= hi; t += kThreads) {
                 const Iv z = iv(t);
-                if (z.lo <= m_hi) {
-                    ++ncont;
-                    if (!z.exact) ++nopen;
-                    tbest = min(tbest, t);
-                }
+                if (z.lo <= m_hi) push(t, z);
             }
-            ncont = block_sum_i(ncont, sh.red_i);
-            nopen = block_sum_i(nopen, sh.red_j);
-            tbest = block_min_i(tbest, sh.red_i);
-            if (ncont > 1 && nopen > 0 && !last) {
-                for (int64_t t = lo + tid; t <= hi; t += kThreads) {
-                    const Iv z = iv(t);
-                    if (z.lo <= m_hi) push(t, z);
-                }
-                break;
-            }
-            // One contender is the strict argmin; several exact contenders all
-            // equal m_hi, so the smallest lag wins the tie.
-            o.period = (int32_t)tbest;
-            const Iv z = iv(tbest);
-            // 4. err and verdict
-            bool aper;
-            if ((z.exact && r_lo == r_hi) || last) {
-                const double e = z.v / r_v;
-                aper = e >= a.err_max;
-                o.err = (float)e;
+            return false;
+        }
+        // One contender is the strict argmin; several exact contenders all
+        // equal m_hi, so the smallest lag wins the tie.
+        o.period = (int32_t)tbest;
+        const Iv z = iv(tbest);
+        // 4. err and verdict
+        bool aper;
+        if ((z.exact && r_lo == r_hi) || tau0 == 0.0) {
+            aper = z.v / r_v >= a.err_max;
+        } else {
+            const double e_lo = z.lo / r_hi * (1.0 - ulp4);
+            const double e_hi = z.hi / r_lo * (1.0 + ulp4);
+            if (e_lo >= a.err_max) {
+                aper = true;
+            } else if (e_hi < a.err_max) {
+                aper = false;
             } else {
-                const double e_lo = z.lo / r_hi * (1.0 - 4.0 * 2.220446049250313e-16);
-                const double e_hi = z.hi / r_lo * (1.0 + 4.0 * 2.220446049250313e-16);
-                if (e_lo >= a.err_max) {
-                    aper = true;
-                } else if (e_hi < a.err_max) {
-                    aper = false;
-                } else {
-                    if (tid == 0) {
-                        push(tbest, z);
-                        sh.need_r = 1;
-                    }
-                    break;
+                if (tid == 0 && may_push) {
+                    push(tbest, z);
+                    want_r();
                 }
-                o.err = (float)(z.v / r_v);
+                return false;
             }
-            o.verdict = aper ? GPOEO_PD_APERIODIC : GPOEO_PD_PERIODIC;
-            done = true;
-        } while (false);
+        }
+        o.err = (float)(z.v / r_v);
+        o.verdict = aper ? GPOEO_PD_APERIODIC : GPOEO_PD_PERIODIC;
+        return true;
+    };
 
-        __syncthreads();
-        if (done) {
-            if (tid == 0) {
-                o.n_rescored = sh.rescored;
-                o.flags = unresolved ? GPOEO_PD_UNRESOLVED : 0u;
-                *res = o;
-            }
-            return;
+    const bool rescue = (a.flags & GPOEO_PD_NO_RESCUE) == 0;
+    gpoeo_pd_result o;
+    bool done, unresolved = false;
+    if (!rescue) {
+        done = rule(0.0, 0.0, 0.0, false, o);
+    } else {
+        done = rule(kScoreRelBound, a.tau1, r_err, !a.last, o);
+        if (!done && a.last) {
+            done = rule(0.0, 0.0, 0.0, false, o);
+            unresolved = true;
         }
-        // Re-score the open lags (and R) as exact points, then run the rule again.
-        const int cnt = min(sh.need_count, kNeedCap);
-        for (int k = tid; k < cnt; k += kThreads) {
-            const int64_t t = sh.need[k];
-            const int64_t j = t - tmin;
-            if ((bits[j >> 5] >> (j & 31)) & 1u) continue;
-            const double v = exact_score(xw, a.num_channels, a.channel_stride, a.n, t, w);
-            s[j] = v;
-            __threadfence_block();
-            const uint32_t old = atomicOr(&bits[j >> 5], 1u << (j & 31));
-            if (!((old >> (j & 31)) & 1u)) atomicAdd(&sh.rescored, 1);
-        }
-        if (sh.need_r && tid == kThreads - 1 && !sh.r_exact) {
-            sh.r_v = exact_reference(xw, a.num_channels, a.channel_stride, a.n, w);
-            sh.r_exact = 1;
-        }
-        __syncthreads();
     }
+    __syncthreads();
+    if (tid == 0 && done) {
+        o.n_rescored = st->rescored;
+        o.flags = unresolved ? GPOEO_PD_UNRESOLVED : 0u;
+        *res = o;
+        st->done = 1;
+    }
+}
+
+// One re-score round: every wavefront takes queued tier-1 requests (one lag
+// per wavefront), then every lane takes queued tier-2 requests (one lag, or
+// one window's R, per lane).
+__global__ __launch_bounds__(kThreads) void rescore_kernel(SelectArgs a, Weights w) {
+    const int32_t* count = a.q_count + 2 * a.pass;
+    const int n1 = min(count[0], kQueueCap), n2 = min(count[1], kQueueCap);
+    if (n1 == 0 && n2 == 0) return;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t waves = (int64_t)gridDim.x * (kThreads / kWave);
+    const int64_t wave = (int64_t)blockIdx.x * (kThreads / kWave) +
+                         __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    for (int64_t e = wave; e < n1; e += waves) {
+        const int64_t b = a.q_win[e];
+        const int64_t t = a.q_lag[e];
+        const int64_t j = t - a.tmin;
+        uint32_t* t1 = a.tier1 + b * (int64_t)a.words;
+        if ((t1[j >> 5] >> (j & 31)) & 1u) continue;
+        const float* __restrict__ xw = a.x + b * a.window_stride;
+        const double v = wave_score(xw, a.num_channels, a.channel_stride, a.n, t, w, lane);
+        if (lane == 0) {
+            a.s64[b * (int64_t)a.lags + j] = v;
+            __threadfence();
+            const uint32_t old = atomicOr(&t1[j >> 5], 1u << (j & 31));
+            if (!((old >> (j & 31)) & 1u)) atomicAdd(&a.state[b].rescored, 1);
+        }
+    }
+    const int64_t lanes = (int64_t)gridDim.x * kThreads;
+    for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < n2; e += lanes) {
+        const int64_t b = a.q_win[kQueueCap + e];
+        const int64_t t = a.q_lag[kQueueCap + e];
+        const float* __restrict__ xw = a.x + b * a.window_stride;
+        if (t < 0) {
+            WinState* st = a.state + b;
+            st->r_exact = exact_reference(xw, a.num_channels, a.channel_stride, a.n, w);
+            __threadfence();
+            st->r_is_exact = 1;
+            continue;
+        }
+        const int64_t j = t - a.tmin;
+        uint32_t* t2 = a.tier2 + b * (int64_t)a.words;
+        if ((t2[j >> 5] >> (j & 31)) & 1u) continue;
+        a.s64[b * (int64_t)a.lags + j] =
+            exact_score(xw, a.num_channels, a.channel_stride, a.n, t, w);
+        __threadfence();
+        atomicOr(&t2[j >> 5], 1u << (j & 31));
+    }
+}
+
+__global__ void zero_counts_kernel(int32_t* counts, int n) {
+    if ((int)threadIdx.x < n) counts[threadIdx.x] = 0;
 }
 
 }  // namespace
 
 hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const double* var,
-                         double* s64, uint32_t* bits, void* results, hipStream_t s) {
+                         double* s64, const SelectBuffers& sb, void* results, hipStream_t s) {
     SelectArgs a;
     a.x = x;
     a.var = var;
     a.s64 = s64;
-    a.bits = bits;
+    a.tier1 = sb.tier1;
+    a.tier2 = sb.tier2;
+    a.queued1 = sb.queued1;
+    a.queued2 = sb.queued2;
+    a.state = sb.state;
+    a.q_win = sb.q_win;
+    a.q_lag = sb.q_lag;
+    a.q_count = sb.q_count;
     a.results = static_cast<gpoeo_pd_result*>(results);
     a.n = p.n;
     a.window_stride = p.window_stride;
@@ -460,7 +628,22 @@ hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const 
     a.c_lag = p.c_lag;
     a.err_max = p.err_max;
     a.flags = p.flags;
-    hipLaunchKernelGGL(select_kernel, dim3((unsigned)p.num_windows), dim3(kThreads), 0, s, a, w);
+    // Tier-1 half-width: the sequential sum (at most n + C + 6 roundings of
+    // u = 2^-53 each, relative to the exact value) plus the wavefront sum
+    // (n/256 + C + 16 roundings), with 1% margin.
+    const double u = 1.1102230246251565e-16;
+    a.tau1 = 1.01 * u * ((double)p.n * (1.0 + 1.0 / 256.0) + 2.0 * p.num_channels + 22.0);
+    const bool rescue = (p.flags & GPOEO_PD_NO_RESCUE) == 0;
+    const int passes = rescue ? kPasses : 1;
+    hipLaunchKernelGGL(zero_counts_kernel, dim3(1), dim3(64), 0, s, sb.q_count, 2 * kPasses);
+    const dim3 grid_sel((unsigned)p.num_windows);
+    const dim3 grid_re(kRescoreGroups);
+    for (int pass = 0; pass < passes; ++pass) {
+        a.pass = pass;
+        a.last = pass == passes - 1;
+        hipLaunchKernelGGL(select_pass_kernel, grid_sel, dim3(kThreads), 0, s, a, w);
+        if (!a.last) hipLaunchKernelGGL(rescore_kernel, grid_re, dim3(kThreads), 0, s, a, w);
+    }
     return hipGetLastError();
 }
 

@@ -2,9 +2,11 @@
 //
 // window_stats: per (window, channel), the population variance in fp64 by two
 //   passes (mean, then mean squared deviation), each a fixed-order workgroup
-//   reduction.  The selection forms R = 2 * sum_c w_c * Var_c from it, the
-//   reference the relative-height candidate filter of Algorithm 1 is measured
-//   against in the lag domain.
+//   reduction, and the mean absolute sample (which bounds how far any fp64
+//   evaluation order of the mean, and so of the variance, can stray).  The
+//   selection forms R = 2 * sum_c w_c * Var_c from it, the reference the
+//   relative-height candidate filter of Algorithm 1 is measured against in
+//   the lag domain.
 // finalize: per (window, lag), combines the fp64 chunk partials of every
 //   channel in ascending chunk order, divides by the N-T pairs and forms the
 //   weighted channel sum S(T) (the composite detection feature of Sec. 4.2).
@@ -36,16 +38,24 @@ __global__ __launch_bounds__(kStatsThreads) void window_stats_kernel(
     const int64_t b = bc / num_channels;
     const int32_t c = (int32_t)(bc % num_channels);
     const float* __restrict__ xw = x + b * window_stride + (int64_t)c * channel_stride;
-    double s = 0.0;
-    for (int64_t i = threadIdx.x; i < n; i += kStatsThreads) s += (double)xw[i];
+    double s = 0.0, sa = 0.0;
+    for (int64_t i = threadIdx.x; i < n; i += kStatsThreads) {
+        const double v = (double)xw[i];
+        s += v;
+        sa += fabs(v);
+    }
     const double mean = block_sum(s, red) / (double)n;
+    const double absmean = block_sum(sa, red) / (double)n;
     double q = 0.0;
     for (int64_t i = threadIdx.x; i < n; i += kStatsThreads) {
         const double d = (double)xw[i] - mean;
         q += d * d;
     }
     const double sq = block_sum(q, red);
-    if (threadIdx.x == 0) var[bc] = sq / (double)n;
+    if (threadIdx.x == 0) {
+        var[2 * bc] = sq / (double)n;
+        var[2 * bc + 1] = absmean;
+    }
 }
 
 __global__ __launch_bounds__(256) void finalize_kernel(const double* __restrict__ part,
