@@ -27,7 +27,7 @@ sys.path.insert(0, ROOT)
 FP32_VECTOR_PEAK_TFLOPS = 157.3   # MI355X published FP32 vector peak
 FLOP_PER_PAIR = 3                 # one subtraction, one multiply, one add per (x[i], x[i+T])
 METRIC = "lag·samples/sec and traces/sec for batched period detection; % FP32 peak"
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "lag_score_w3_counters.json")
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "lag_score_w3_counters.txt")
 SCORE_SOURCE = os.path.join(ROOT, "paper_2201_01684_amd", "csrc", "lag_score.hip")
 
 
@@ -81,16 +81,25 @@ class HipEvents:
             self.hip.hipEventDestroy(h)
 
 
-def counters_traffic():
-    """HBM bytes per lag-score launch from the committed rocprofv3 counter summary,
-    or None if there is none or the kernel source changed since it was taken."""
+def counters_traffic(workload: str):
+    """HBM bytes per lag-score launch from the committed rocprofv3 counter summary
+    (FETCH_SIZE and WRITE_SIZE scaled by a copy kernel of known size), or None
+    if the summary is missing, covers another workload, or the kernel source
+    changed since the counters were taken."""
+    if workload != "w3":
+        return None
     try:
+        fields = {}
         with open(COUNTERS_FILE) as f:
-            c = json.load(f)
+            for line in f:
+                if line.startswith("#") or ":" not in line:
+                    continue
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
         src = hashlib.sha256(open(SCORE_SOURCE, "rb").read()).hexdigest()
-        if c.get("source_sha256") != src:
+        if fields.get("source_sha256") != src:
             return None
-        return float(c["hbm_bytes_per_launch"])
+        return float(fields["hbm_bytes_per_launch"])
     except (OSError, ValueError, KeyError):
         return None
 
@@ -182,7 +191,8 @@ def main():
                      "select": float(stage_ms[:, 3].mean())},
         "roofline": {"kernel": "lag_score_kernel", "bound": "alu", "achieved": achieved,
                      "peak": FP32_VECTOR_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / FP32_VECTOR_PEAK_TFLOPS, "traffic": counters_traffic()},
+                     "frac": achieved / FP32_VECTOR_PEAK_TFLOPS,
+                     "traffic": counters_traffic(wl.name)},
         "windows_flagged_unresolved": int(np.count_nonzero(res["flags"] & pkg.UNRESOLVED)),
         "windows_rescored": int(np.count_nonzero(res["n_rescored"])),
     }
