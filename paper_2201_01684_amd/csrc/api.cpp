@@ -12,10 +12,27 @@
 namespace gpoeo {
 namespace {
 
-constexpr int64_t kTargetWaves = 8192;   // about 8 waves per SIMD on 256 CUs x 4 SIMDs
+// Enough score wavefronts for about 8 rounds of 5 resident waves on each of
+// the 1024 SIMDs, so that the last, partly filled round costs little.
+constexpr int64_t kTargetWaves = 40960;
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+// Lags per lane of the score kernel.  16 lets each staged sample serve more
+// lags and suits long windows; 8 halves the masked stretch at the end of each
+// lag block (64 * 16 samples at 16 lags per lane) and doubles occupancy (59
+// instead of 92 VGPRs), which pays once that stretch exceeds about 1% of the
+// mean pair range N - T.  Measured on MI355X: 16 is best for 262144-sample
+// windows, 8 for 65536- and 16384-sample windows, equal at 131072.
+int32_t choose_lags_per_lane(int64_t n, int32_t tmin, int32_t tmax) {
+    const double mean_range = (double)n - 0.5 * ((double)tmin + (double)tmax);
+    return (64.0 * 16.0 > 0.01 * mean_range) ? 8 : 16;
+}
+
+// Wavefronts per score workgroup: with 8 lags per lane, single-wave groups
+// measured faster (no wave of a group waits on a longer sibling).
+int32_t choose_waves_per_group(int32_t lags_per_lane) { return lags_per_lane == 8 ? 1 : 4; }
 
 bool mul_ok(int64_t a, int64_t b, int64_t* out) {
     if (a < 0 || b < 0) return false;
@@ -60,22 +77,26 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
 
     // Lag blocks end exactly at tmax when possible, so that no block is mostly
     // outside [tmin, tmax]; lags below tmin are computed and discarded.
-    p->lag_blocks = (p->lags + kLagsPerWave - 1) / kLagsPerWave;
-    int64_t t0 = (int64_t)d->tmax + 1 - (int64_t)p->lag_blocks * kLagsPerWave;
+    p->lags_per_lane = choose_lags_per_lane(d->n, d->tmin, d->tmax);
+    p->waves_per_group = choose_waves_per_group(p->lags_per_lane);
+    const int32_t lags_per_block = kWave * p->lags_per_lane;
+    p->lag_blocks = (p->lags + lags_per_block - 1) / lags_per_block;
+    int64_t t0 = (int64_t)d->tmax + 1 - (int64_t)p->lag_blocks * lags_per_block;
     if (t0 < 0) t0 = 0;
     p->t0 = (int32_t)t0;
-    p->lags_padded = p->lag_blocks * kLagsPerWave;
+    p->lags_padded = p->lag_blocks * lags_per_block;
 
     int64_t bc, base;
     if (!mul_ok(d->num_windows, d->num_channels, &bc)) return GPOEO_PD_EINVAL;
     if (!mul_ok(bc, p->lag_blocks, &base)) return GPOEO_PD_EINVAL;
     const int64_t span = d->n - p->t0;             // longest sample range of any lag
-    const int64_t max_chunks = (span + kRunSamples - 1) / kRunSamples;
+    const int64_t kMinChunk = 128;
+    const int64_t max_chunks = (span + kMinChunk - 1) / kMinChunk;
     int64_t chunks = (kTargetWaves + base - 1) / base;
     if (chunks < 1) chunks = 1;
     if (chunks > max_chunks) chunks = max_chunks;
     int64_t chunk = (span + chunks - 1) / chunks;
-    chunk = (chunk + kRunSamples - 1) / kRunSamples * kRunSamples;
+    chunk = (chunk + kBlockSamples - 1) / kBlockSamples * kBlockSamples;
     chunks = (span + chunk - 1) / chunk;
     p->chunk = chunk;
     p->chunks = (int32_t)chunks;

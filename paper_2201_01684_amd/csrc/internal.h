@@ -7,8 +7,6 @@
 namespace gpoeo {
 
 constexpr int kWave = 64;            // CDNA wavefront width
-constexpr int kLagsPerLane = 16;     // consecutive lags held in one lane's accumulators
-constexpr int kLagsPerWave = kWave * kLagsPerLane;
 constexpr int kBlockSamples = 16;    // samples per register block of the score kernel
 constexpr int kRunSamples = 256;     // samples per fp32 run before the fp64 flush
 constexpr int kMaxChannels = 256;    // channel weights travel as a kernel argument
@@ -58,10 +56,12 @@ struct Plan {
     int32_t tmin, tmax;
     int32_t lags;            // tmax - tmin + 1
     int32_t t0;              // first lag of lag block 0 (tmin rounded down to a multiple of 4)
-    int32_t lag_blocks;      // blocks of kLagsPerWave lags covering [t0, tmax]
-    int32_t lags_padded;     // lag_blocks * kLagsPerWave
+    int32_t lags_per_lane;   // consecutive lags in one lane's accumulators (8 or 16)
+    int32_t waves_per_group; // score-kernel wavefronts per workgroup (1 or 4)
+    int32_t lag_blocks;      // blocks of 64 * lags_per_lane lags covering [t0, tmax]
+    int32_t lags_padded;     // lag_blocks * 64 * lags_per_lane
     int32_t chunks;          // sample chunks per (window, channel, lag block)
-    int64_t chunk;           // samples per chunk, a multiple of kRunSamples
+    int64_t chunk;           // samples per chunk, a multiple of kBlockSamples
     int64_t tasks;           // waves of the score kernel
     bool aligned;            // x and strides allow 16-byte vector loads
     double c_lag, err_max;

@@ -6,14 +6,14 @@
 //
 // Work decomposition (one wavefront per task):
 //   task = (window*C + channel, lag block, sample chunk), chunk index fastest.
-//   A lag block is 1024 consecutive lags: lane l owns lags T_l .. T_l+15 with
-//   T_l = t0 + 1024*block + 16*l, so the 64 lanes tile the block.
-//   The wave walks its sample chunk in blocks of 16 samples.  x[i..i+15] is the
-//   same for every lane and is read with scalar loads; lane l reads its 32-float
-//   window x[i+T_l .. i+T_l+31] with vector loads (consecutive lanes read
-//   consecutive 64-byte pieces), and every staged value serves up to 16 lags
-//   from registers: 256 pairs per lane per block for 16 + 32 loaded floats.
-//   Each pair costs one v_sub_f32 and one v_fmac_f32.
+//   A lag block is 64*BT consecutive lags (BT = 8 or 16 lags per lane): lane l
+//   owns lags T_l .. T_l+BT-1 with T_l = t0 + 64*BT*block + BT*l, so the 64
+//   lanes tile the block.  The wave walks its sample chunk in blocks of 16
+//   samples.  x[i..i+15] is the same for every lane and is read with scalar
+//   loads; lane l reads its (16+BT)-float window x[i+T_l ..] with vector loads
+//   (consecutive lanes read consecutive pieces), and every staged value serves
+//   up to BT lags from registers: 16*BT pairs per lane per block.  Each pair
+//   costs one v_sub_f32 and one v_fmac_f32.
 //
 // Precision: the 16 per-lane accumulators are fp32 and are flushed into fp64
 // every 256 samples, so a run sums at most 256 non-negative terms.
@@ -42,16 +42,25 @@ struct ScoreArgs {
     int32_t chunks;
 };
 
-// Lane window y[k] = x[i + T_l + k], k < 32 (y[31] is loaded but never used).
-// kShift in 0..3: the window start sits kShift floats past a 16-byte boundary and
-// nine aligned float4 loads cover it; kShift == 4: plain dword loads, any alignment.
-template <int kShift>
-__device__ __forceinline__ void load_window(const float* __restrict__ p, float (&y)[32]) {
+// Lane window y[k] = x[i + T_l + k], k < kW = 16 + kBT - 1 (rounded up to a
+// multiple of 4; the extra entries are loaded but never used).
+// kShift in 0..3: the window start sits kShift floats past a 16-byte boundary
+// and kNQ aligned float4 loads cover it; kShift == 4: dword loads, any alignment.
+template <int kBT>
+struct Geometry {
+    static constexpr int kW = 16 + kBT;               // y entries kept (last one unused)
+    static constexpr int kNQ = (kW + 6) / 4;          // float4 loads covering kW + shift
+};
+
+template <int kBT, int kShift>
+__device__ __forceinline__ void load_window(const float* __restrict__ p,
+                                            float (&y)[Geometry<kBT>::kW]) {
+    constexpr int kW = Geometry<kBT>::kW, kNQ = Geometry<kBT>::kNQ;
     if constexpr (kShift < 4) {
         const float4* q = reinterpret_cast<const float4*>(p - kShift);
-        float t[36];
+        float t[4 * kNQ];
 #pragma unroll
-        for (int k = 0; k < 9; ++k) {
+        for (int k = 0; k < kNQ; ++k) {
             float4 v = q[k];
             t[4 * k + 0] = v.x;
             t[4 * k + 1] = v.y;
@@ -59,42 +68,48 @@ __device__ __forceinline__ void load_window(const float* __restrict__ p, float (
             t[4 * k + 3] = v.w;
         }
 #pragma unroll
-        for (int k = 0; k < 32; ++k) y[k] = t[k + kShift];
+        for (int k = 0; k < kW; ++k) y[k] = t[k + kShift];
     } else {
 #pragma unroll
-        for (int k = 0; k < 31; ++k) y[k] = p[k];
-        y[31] = 0.0f;
+        for (int k = 0; k < kW - 1; ++k) y[k] = p[k];
+        y[kW - 1] = 0.0f;
     }
 }
 
-// 16 samples x 16 lags, every pair valid.
-__device__ __forceinline__ void block_full(const float (&xs)[16], const float (&y)[32],
-                                           float (&acc)[16]) {
+// 16 samples x kBT lags, every pair valid.
+template <int kBT>
+__device__ __forceinline__ void block_full(const float (&xs)[16],
+                                           const float (&y)[Geometry<kBT>::kW],
+                                           float (&acc)[kBT]) {
 #pragma unroll
     for (int s = 0; s < 16; ++s) {
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
+        for (int j = 0; j < kBT; ++j) {
             float d = xs[s] - y[s + j];
             acc[j] = __builtin_fmaf(d, d, acc[j]);
         }
     }
 }
 
-// 16 samples x 16 lags, pair (s, j) valid iff s + j < rem.
-__device__ __forceinline__ void block_masked(const float (&xs)[16], const float (&y)[32], int rem,
-                                             float (&acc)[16]) {
+// 16 samples x kBT lags, pair (s, j) valid iff s + j < rem.
+template <int kBT>
+__device__ __forceinline__ void block_masked(const float (&xs)[16],
+                                             const float (&y)[Geometry<kBT>::kW], int rem,
+                                             float (&acc)[kBT]) {
 #pragma unroll
     for (int s = 0; s < 16; ++s) {
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
+        for (int j = 0; j < kBT; ++j) {
             float d = (s + j < rem) ? xs[s] - y[s + j] : 0.0f;
             acc[j] = __builtin_fmaf(d, d, acc[j]);
         }
     }
 }
 
-template <int kShift>
-__global__ __launch_bounds__(256) void lag_score_kernel(ScoreArgs a) {
+template <int kBT, int kWavesPerGroup, int kShift>
+__global__ __launch_bounds__(kWave * kWavesPerGroup) void lag_score_kernel(ScoreArgs a) {
+    constexpr int kW = Geometry<kBT>::kW;
+    constexpr int kLagsPerBlock = kWave * kBT;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     // Workgroups are dispatched round-robin over the 8 XCDs; remap so that each
@@ -104,7 +119,7 @@ __global__ __launch_bounds__(256) void lag_score_kernel(ScoreArgs a) {
     int64_t g = blockIdx.x;
     const int64_t full = groups - groups % 8;
     if (g < full) g = (g % 8) * (full / 8) + g / 8;
-    const int64_t task = g * (blockDim.x / kWave) + wave;
+    const int64_t task = g * kWavesPerGroup + wave;
     if (task >= a.tasks) return;
 
     const int32_t k = (int32_t)(task % a.chunks);
@@ -115,26 +130,26 @@ __global__ __launch_bounds__(256) void lag_score_kernel(ScoreArgs a) {
     const int32_t c = (int32_t)(bc % a.num_channels);
 
     const float* __restrict__ xw = a.x + b * a.window_stride + (int64_t)c * a.channel_stride;
-    const int64_t t_wave = (int64_t)a.t0 + (int64_t)blk * kLagsPerWave;
-    const int64_t t_lane = t_wave + (int64_t)lane * kLagsPerLane;
+    const int64_t t_wave = (int64_t)a.t0 + (int64_t)blk * kLagsPerBlock;
+    const int64_t t_lane = t_wave + (int64_t)lane * kBT;
     const int64_t n = a.n;
 
     const int64_t i_begin = (int64_t)k * a.chunk;
     const int64_t chunk_end = i_begin + a.chunk;
     // A block starting at i runs unmasked iff i + 16 <= lim_full: then every pair
     // of every lane is valid and the aligned window loads (which reach at most
-    // x[i + t_wave_hi + 20]) stay below sample n.
-    const int64_t t_wave_hi = t_wave + kLagsPerWave - 1;
+    // x[i + t_wave_hi + 20] for both lane widths) stay below sample n.
+    const int64_t t_wave_hi = t_wave + kLagsPerBlock - 1;
     const int64_t lim_full = min(chunk_end, n - t_wave_hi - 5);
     const int64_t lim_any = min(chunk_end, n - t_wave);
     const int64_t nb_full = lim_full > i_begin ? (lim_full - i_begin) / kBlockSamples : 0;
     const int64_t nb_any =
         lim_any > i_begin ? (lim_any - i_begin + kBlockSamples - 1) / kBlockSamples : 0;
 
-    float acc[16];
-    double acc64[16];
+    float acc[kBT];
+    double acc64[kBT];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
+    for (int j = 0; j < kBT; ++j) {
         acc[j] = 0.0f;
         acc64[j] = 0.0;
     }
@@ -148,12 +163,12 @@ __global__ __launch_bounds__(256) void lag_score_kernel(ScoreArgs a) {
             float xs[16];
 #pragma unroll
             for (int s = 0; s < 16; ++s) xs[s] = xw[i + s];
-            float y[32];
-            load_window<kShift>(xw + i + t_lane, y);
-            block_full(xs, y, acc);
+            float y[kW];
+            load_window<kBT, kShift>(xw + i + t_lane, y);
+            block_full<kBT>(xs, y, acc);
         }
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
+        for (int j = 0; j < kBT; ++j) {
             acc64[j] += (double)acc[j];
             acc[j] = 0.0f;
         }
@@ -168,13 +183,13 @@ __global__ __launch_bounds__(256) void lag_score_kernel(ScoreArgs a) {
             for (int s = 0; s < 16; ++s) xs[s] = (i + s < n) ? xw[i + s] : 0.0f;
             const int64_t rem64 = n - i - t_lane;   // pair (s, j) valid iff s + j < rem
             const int rem = (int)max((int64_t)-1, min(rem64, (int64_t)64));
-            float y[32];
+            float y[kW];
 #pragma unroll
-            for (int kk = 0; kk < 32; ++kk) y[kk] = (kk < rem) ? xw[i + t_lane + kk] : 0.0f;
-            block_masked(xs, y, rem, acc);
+            for (int kk = 0; kk < kW; ++kk) y[kk] = (kk < rem) ? xw[i + t_lane + kk] : 0.0f;
+            block_masked<kBT>(xs, y, rem, acc);
         }
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
+        for (int j = 0; j < kBT; ++j) {
             acc64[j] += (double)acc[j];
             acc[j] = 0.0f;
         }
@@ -182,7 +197,20 @@ __global__ __launch_bounds__(256) void lag_score_kernel(ScoreArgs a) {
 
     double* out = a.part + (bc * a.chunks + k) * (int64_t)a.lags_padded + (t_lane - a.t0);
 #pragma unroll
-    for (int j = 0; j < 16; ++j) out[j] = acc64[j];
+    for (int j = 0; j < kBT; ++j) out[j] = acc64[j];
+}
+
+template <int kBT, int kWPG>
+void launch_shifted(const Plan& p, const ScoreArgs& a, hipStream_t s) {
+    const int64_t groups = (p.tasks + kWPG - 1) / kWPG;
+    const dim3 grid((unsigned)groups), block(kWave * kWPG);
+    switch (p.aligned ? (p.t0 & 3) : 4) {
+        case 0: hipLaunchKernelGGL((lag_score_kernel<kBT, kWPG, 0>), grid, block, 0, s, a); break;
+        case 1: hipLaunchKernelGGL((lag_score_kernel<kBT, kWPG, 1>), grid, block, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((lag_score_kernel<kBT, kWPG, 2>), grid, block, 0, s, a); break;
+        case 3: hipLaunchKernelGGL((lag_score_kernel<kBT, kWPG, 3>), grid, block, 0, s, a); break;
+        default: hipLaunchKernelGGL((lag_score_kernel<kBT, kWPG, 4>), grid, block, 0, s, a); break;
+    }
 }
 
 }  // namespace
@@ -201,15 +229,12 @@ hipError_t launch_lag_score(const Plan& p, const float* x, double* part, hipStre
     a.lag_blocks = p.lag_blocks;
     a.lags_padded = p.lags_padded;
     a.chunks = p.chunks;
-    const int waves_per_group = 4;
-    const int64_t groups = (p.tasks + waves_per_group - 1) / waves_per_group;
-    dim3 grid((unsigned)groups), block(kWave * waves_per_group);
-    switch (p.aligned ? (p.t0 & 3) : 4) {
-        case 0: hipLaunchKernelGGL(lag_score_kernel<0>, grid, block, 0, s, a); break;
-        case 1: hipLaunchKernelGGL(lag_score_kernel<1>, grid, block, 0, s, a); break;
-        case 2: hipLaunchKernelGGL(lag_score_kernel<2>, grid, block, 0, s, a); break;
-        case 3: hipLaunchKernelGGL(lag_score_kernel<3>, grid, block, 0, s, a); break;
-        default: hipLaunchKernelGGL(lag_score_kernel<4>, grid, block, 0, s, a); break;
+    if (p.lags_per_lane == 8) {
+        if (p.waves_per_group == 1) launch_shifted<8, 1>(p, a, s);
+        else launch_shifted<8, 4>(p, a, s);
+    } else {
+        if (p.waves_per_group == 1) launch_shifted<16, 1>(p, a, s);
+        else launch_shifted<16, 4>(p, a, s);
     }
     return hipGetLastError();
 }
