@@ -141,6 +141,8 @@ def main():
     desc, keep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
                                wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights)
     det = pkg.Detector(x, desc, keep, want_scores=True)
+    plan = pkg.describe_plan(desc)
+    scored = plan["pairs_scored"]
     print(f"# {wl.name}: {wl.num_windows} windows x {wl.num_channels} ch x {wl.n} samples, "
           f"T {wl.tmin}..{wl.tmax}, {pairs:.4e} pairs, generated in {t_gen:.1f}s, "
           f"workspace {det.ws_bytes / 2**20:.1f} MiB", file=sys.stderr, flush=True)
@@ -163,7 +165,9 @@ def main():
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = pairs / (ms_per_step / 1e3)
     score_ms = float(stage_ms[:, 1].mean())
-    achieved = FLOP_PER_PAIR * pairs / (score_ms / 1e3) / 1e12
+    # the roofline counts what the score kernels evaluate: with overlapping
+    # windows sharing block partials that is fewer pairs than the definition sums
+    achieved = FLOP_PER_PAIR * scored / (score_ms / 1e3) / 1e12
     res = det.results_numpy()
     scores = det.scores
 
@@ -172,7 +176,8 @@ def main():
         "value": value,
         "unit": "lag·samples/s",
         "traces_per_sec": wl.num_windows / (ms_per_step / 1e3),
-        "pct_fp32_peak": 100.0 * FLOP_PER_PAIR * value / 1e12 / FP32_VECTOR_PEAK_TFLOPS,
+        "pct_fp32_peak": 100.0 * FLOP_PER_PAIR * scored / (ms_per_step / 1e3) / 1e12
+                         / FP32_VECTOR_PEAK_TFLOPS,
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -184,7 +189,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "description": wl.meta["description"],
                    "windows": wl.num_windows, "channels": wl.num_channels, "n": wl.n,
-                   "tmin": wl.tmin, "tmax": wl.tmax, "pairs": pairs, "sha256": sha},
+                   "tmin": wl.tmin, "tmax": wl.tmax, "pairs": pairs, "sha256": sha,
+                   "scoring": "shared block partials" if plan["mode"] == 1 else "per window",
+                   "pairs_scored": scored, "lags_per_lane": plan["lags_per_lane"]},
         "stage_ms": {"window_stats": float(stage_ms[:, 0].mean()),
                      "lag_score": score_ms,
                      "finalize": float(stage_ms[:, 2].mean()),

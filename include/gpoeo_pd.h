@@ -105,6 +105,21 @@ typedef struct {
     uint32_t flags;          /* GPOEO_PD_UNRESOLVED                                          */
 } gpoeo_pd_result;
 
+/* How gpoeo_pd_detect will run a descriptor (for measurement tools). */
+typedef struct {
+    int32_t mode;             /* 0: every window scored on its own; 1: overlapping windows
+                                 at a stride dividing N share per-block partials          */
+    int32_t lags_per_lane;    /* consecutive lags per lane of the score kernel (8 or 16)  */
+    int64_t score_waves;      /* wavefronts the score stage launches                      */
+    double pairs_defined;     /* sum over windows, channels and T in [tmin, tmax] of N - T:
+                                 the (x[i], x[i+T]) pairs the definition of S(T) sums     */
+    double pairs_scored;      /* pairs with T in [tmin, tmax] the score stage evaluates   */
+    size_t workspace_bytes;   /* same as gpoeo_pd_workspace_bytes                          */
+} gpoeo_pd_plan_info;
+
+/* Describes the launch plan of `desc`.  Host-only; GPOEO_PD_OK or GPOEO_PD_EINVAL. */
+int gpoeo_pd_describe_plan(const gpoeo_pd_desc* desc, gpoeo_pd_plan_info* info);
+
 /* ABI version the library was built with (GPOEO_PD_ABI_VERSION). */
 int gpoeo_pd_abi_version(void);
 

@@ -22,6 +22,7 @@ from ._binding import (  # noqa: F401
     Desc,
     Detector,
     GpoeoError,
+    describe_plan,
     detect_period,
     load_library,
     make_desc,

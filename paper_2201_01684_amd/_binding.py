@@ -41,6 +41,12 @@ class Result(ctypes.Structure):
                 ("flags", ctypes.c_uint32)]
 
 
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int32), ("lags_per_lane", ctypes.c_int32),
+                ("score_waves", ctypes.c_int64), ("pairs_defined", ctypes.c_double),
+                ("pairs_scored", ctypes.c_double), ("workspace_bytes", ctypes.c_size_t)]
+
+
 RESULT_DTYPE = np.dtype([("period", np.int32), ("verdict", np.int32), ("err", np.float32),
                          ("n_candidates", np.int32), ("t_cand", np.int32), ("t_low", np.int32),
                          ("t_up", np.int32), ("n_rescored", np.int32), ("flags", np.uint32)])
@@ -48,7 +54,7 @@ RESULT_WORDS = ctypes.sizeof(Result) // 4
 assert RESULT_DTYPE.itemsize == ctypes.sizeof(Result)
 
 EXPORTS = ("gpoeo_pd_abi_version", "gpoeo_pd_strerror", "gpoeo_pd_workspace_bytes",
-           "gpoeo_pd_detect", "gpoeo_pd_detect_staged")
+           "gpoeo_pd_describe_plan", "gpoeo_pd_detect", "gpoeo_pd_detect_staged")
 
 _lib = None
 
@@ -68,6 +74,8 @@ def load_library():
         lib.gpoeo_pd_workspace_bytes.restype = ctypes.c_int
         lib.gpoeo_pd_workspace_bytes.argtypes = [ctypes.POINTER(Desc),
                                                  ctypes.POINTER(ctypes.c_size_t)]
+        lib.gpoeo_pd_describe_plan.restype = ctypes.c_int
+        lib.gpoeo_pd_describe_plan.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(PlanInfo)]
         lib.gpoeo_pd_detect.restype = ctypes.c_int
         lib.gpoeo_pd_detect.argtypes = [ctypes.POINTER(Desc), ctypes.c_void_p, ctypes.c_void_p,
                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
@@ -111,6 +119,15 @@ def workspace_bytes(desc: Desc) -> int:
     if rc != OK:
         raise GpoeoError(rc, "gpoeo_pd_workspace_bytes")
     return int(size.value)
+
+
+def describe_plan(desc: Desc) -> dict:
+    """The launch plan of a descriptor: mode, lags per lane, waves, pair counts."""
+    info = PlanInfo()
+    rc = load_library().gpoeo_pd_describe_plan(ctypes.byref(desc), ctypes.byref(info))
+    if rc != OK:
+        raise GpoeoError(rc, "gpoeo_pd_describe_plan")
+    return {name: getattr(info, name) for name, _ in PlanInfo._fields_}
 
 
 def _stream_handle(stream) -> int:

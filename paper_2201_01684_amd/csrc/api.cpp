@@ -4,6 +4,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <algorithm>
 #include <cstring>
 
 #include "gpoeo_pd.h"
@@ -75,33 +76,80 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
     p->err_max = d->err_max;
     p->flags = d->flags;
 
-    // Lag blocks end exactly at tmax when possible, so that no block is mostly
-    // outside [tmin, tmax]; lags below tmin are computed and discarded.
     p->lags_per_lane = choose_lags_per_lane(d->n, d->tmin, d->tmax);
     p->waves_per_group = choose_waves_per_group(p->lags_per_lane);
     const int32_t lags_per_block = kWave * p->lags_per_lane;
     p->lag_blocks = (p->lags + lags_per_block - 1) / lags_per_block;
-    int64_t t0 = (int64_t)d->tmax + 1 - (int64_t)p->lag_blocks * lags_per_block;
-    if (t0 < 0) t0 = 0;
-    p->t0 = (int32_t)t0;
-    p->lags_padded = p->lag_blocks * lags_per_block;
 
     int64_t bc, base;
     if (!mul_ok(d->num_windows, d->num_channels, &bc)) return GPOEO_PD_EINVAL;
+
+    // Overlapping windows whose stride divides N (and is a whole number of lag
+    // blocks) share block partials when that saves at least a third of the work.
+    const int64_t ws_ = d->window_stride;
+    if (d->num_windows >= 2 && ws_ > 0 && ws_ < d->n && d->n % ws_ == 0 &&
+        ws_ % lags_per_block == 0) {
+        const int64_t m = d->n / ws_;
+        const double direct =
+            (double)d->num_windows * ((double)d->n - 0.5 * ((double)d->tmin + (double)d->tmax));
+        const double shared = (double)(d->num_windows + m - 1) * 1.5 * (double)ws_;
+        if (direct > 1.5 * shared) {
+            p->sliding = true;
+            p->m = (int32_t)m;
+            p->blocks = d->num_windows + m - 1;
+            p->trace_len = (d->num_windows - 1) * ws_ + d->n;
+        }
+    }
+    int64_t t0;
+    if (p->sliding) {
+        // lag blocks start at 1 (mod 64 * lags_per_lane), so that no block
+        // straddles a multiple of the stride (the cut partials need one
+        // floor((T - 1) / s) per wavefront)
+        t0 = 1 + (int64_t)lags_per_block * ((d->tmin - 1) / lags_per_block);
+        p->lag_blocks = (int32_t)((d->tmax - t0 + lags_per_block) / lags_per_block);
+    } else {
+        // lag blocks end exactly at tmax when possible, so that no block is
+        // mostly outside [tmin, tmax]; lags below tmin are computed and discarded
+        t0 = (int64_t)d->tmax + 1 - (int64_t)p->lag_blocks * lags_per_block;
+        if (t0 < 0) t0 = 0;
+    }
+    p->t0 = (int32_t)t0;
+    p->lags_padded = p->lag_blocks * lags_per_block;
+
+    const int64_t kMinChunk = 128;
     if (!mul_ok(bc, p->lag_blocks, &base)) return GPOEO_PD_EINVAL;
     const int64_t span = d->n - p->t0;             // longest sample range of any lag
-    const int64_t kMinChunk = 128;
-    const int64_t max_chunks = (span + kMinChunk - 1) / kMinChunk;
-    int64_t chunks = (kTargetWaves + base - 1) / base;
-    if (chunks < 1) chunks = 1;
-    if (chunks > max_chunks) chunks = max_chunks;
-    int64_t chunk = (span + chunks - 1) / chunks;
-    chunk = (chunk + kBlockSamples - 1) / kBlockSamples * kBlockSamples;
-    chunks = (span + chunk - 1) / chunk;
-    p->chunk = chunk;
-    p->chunks = (int32_t)chunks;
-    if (!mul_ok(base, chunks, &p->tasks)) return GPOEO_PD_EINVAL;
-    if (p->tasks / 4 + 1 > INT32_MAX) return GPOEO_PD_EINVAL;
+    {
+        const int64_t max_chunks = (span + kMinChunk - 1) / kMinChunk;
+        int64_t chunks = (kTargetWaves + base - 1) / base;
+        if (chunks < 1) chunks = 1;
+        if (chunks > max_chunks) chunks = max_chunks;
+        int64_t chunk = (span + chunks - 1) / chunks;
+        chunk = (chunk + kBlockSamples - 1) / kBlockSamples * kBlockSamples;
+        chunks = (span + chunk - 1) / chunk;
+        p->chunk = chunk;
+        p->chunks = (int32_t)chunks;
+        if (!mul_ok(base, chunks, &p->tasks)) return GPOEO_PD_EINVAL;
+        if (p->tasks / p->waves_per_group + 1 > INT32_MAX) return GPOEO_PD_EINVAL;
+    }
+    if (p->sliding) {
+        int64_t bbase;
+        if (!mul_ok(p->blocks * d->num_channels, p->lag_blocks, &bbase)) return GPOEO_PD_EINVAL;
+        // Two launches (full and cut partials) share the target, and every
+        // extra chunk adds one partial per lag and block for the finalisation
+        // to read, so blocks are split only when there are few of them.
+        const int64_t max_chunks = (ws_ + kMinChunk - 1) / kMinChunk;
+        int64_t chunks = (kTargetWaves / 4 + bbase - 1) / bbase;
+        if (chunks < 1) chunks = 1;
+        if (chunks > max_chunks) chunks = max_chunks;
+        int64_t chunk = (ws_ + chunks - 1) / chunks;
+        chunk = (chunk + kBlockSamples - 1) / kBlockSamples * kBlockSamples;
+        chunks = (ws_ + chunk - 1) / chunk;
+        p->block_chunk = chunk;
+        p->block_chunks = (int32_t)chunks;
+        if (!mul_ok(bbase, chunks, &p->block_tasks)) return GPOEO_PD_EINVAL;
+        if (p->block_tasks / p->waves_per_group + 1 > INT32_MAX) return GPOEO_PD_EINVAL;
+    }
     p->bitmap_words = (p->lags + 31) / 32;
 
     int64_t n_var, n_s, n_bits, n_part;
@@ -109,7 +157,14 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
     if (!mul_ok(d->num_windows, p->lags, &n_s)) return GPOEO_PD_EINVAL;
     if (!mul_ok(d->num_windows, p->bitmap_words, &n_bits)) return GPOEO_PD_EINVAL;
     int64_t tmp;
-    if (!mul_ok(bc, chunks, &tmp) || !mul_ok(tmp, p->lags_padded, &n_part)) return GPOEO_PD_EINVAL;
+    if (p->sliding) {
+        if (!mul_ok(p->blocks * d->num_channels, p->block_chunks, &tmp) ||
+            !mul_ok(tmp, p->lags_padded, &n_part))
+            return GPOEO_PD_EINVAL;
+    } else {
+        if (!mul_ok(bc, p->chunks, &tmp) || !mul_ok(tmp, p->lags_padded, &n_part))
+            return GPOEO_PD_EINVAL;
+    }
     if (n_part > (INT64_MAX / 16)) return GPOEO_PD_EINVAL;
     size_t off = 0;
     p->off_var = off;
@@ -124,6 +179,8 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
     off = align_up(off + (4 * (size_t)kQueueCap + 2 * kPasses) * sizeof(int32_t));
     p->off_part = off;
     off = align_up(off + (size_t)n_part * sizeof(double));
+    p->off_cut = off;                             // cut-block partials (sliding mode)
+    if (p->sliding) off = align_up(off + (size_t)n_part * sizeof(double));
     p->bytes = off;
     return GPOEO_PD_OK;
 }
@@ -151,6 +208,40 @@ int gpoeo_pd_workspace_bytes(const gpoeo_pd_desc* desc, size_t* bytes) {
     const int rc = gpoeo::make_plan(desc, &p);
     if (rc != GPOEO_PD_OK) return rc;
     *bytes = p.bytes;
+    return GPOEO_PD_OK;
+}
+
+int gpoeo_pd_describe_plan(const gpoeo_pd_desc* desc, gpoeo_pd_plan_info* info) {
+    if (!info) return GPOEO_PD_EINVAL;
+    gpoeo::Plan p;
+    const int rc = gpoeo::make_plan(desc, &p);
+    if (rc != GPOEO_PD_OK) return rc;
+    info->mode = p.sliding ? 1 : 0;
+    info->lags_per_lane = p.lags_per_lane;
+    info->score_waves = p.sliding ? 2 * p.block_tasks : p.tasks;
+    info->workspace_bytes = p.bytes;
+    const double wc = (double)p.num_windows * p.num_channels;
+    double defined = 0.0, scored = 0.0;
+    for (int64_t t = p.tmin; t <= p.tmax; ++t) {
+        defined += wc * (double)(p.n - t);
+        if (!p.sliding) continue;
+        const int64_t s = p.window_stride;
+        const int64_t e = p.trace_len - t;          // positions whose partner exists
+        const int64_t q = (t - 1) / s;
+        const int64_t r = (q + 1) * s - t;          // pairs per cut block
+        double cut = 0.0;
+        if (e >= r) {
+            int64_t full = (e - r) / s + 1;
+            if (full > p.blocks) full = p.blocks;
+            cut = (double)full * (double)r;
+            if (full < p.blocks) cut += (double)std::max<int64_t>(0, e - full * s);
+        } else {
+            cut = (double)std::max<int64_t>(0, e);
+        }
+        scored += (double)p.num_channels * ((double)std::max<int64_t>(0, e) + cut);
+    }
+    info->pairs_defined = defined;
+    info->pairs_scored = p.sliding ? scored : defined;
     return GPOEO_PD_OK;
 }
 
@@ -195,10 +286,19 @@ static int detect_impl(const gpoeo_pd_desc* desc, const float* x, float* scores,
     if (!scores_only && gpoeo::launch_window_stats(p, x, var, stream) != hipSuccess)
         return GPOEO_PD_EHIP;
     if (!mark(1)) return GPOEO_PD_EHIP;
-    if (gpoeo::launch_lag_score(p, x, part, stream) != hipSuccess) return GPOEO_PD_EHIP;
-    if (!mark(2)) return GPOEO_PD_EHIP;
-    if (gpoeo::launch_finalize(p, w, part, s64, scores, stream) != hipSuccess)
-        return GPOEO_PD_EHIP;
+    if (p.sliding) {
+        double* cut = reinterpret_cast<double*>(ws + p.off_cut);
+        if (gpoeo::launch_lag_score_blocks(p, x, part, cut, stream) != hipSuccess)
+            return GPOEO_PD_EHIP;
+        if (!mark(2)) return GPOEO_PD_EHIP;
+        if (gpoeo::launch_finalize_blocks(p, w, part, cut, s64, scores, stream) != hipSuccess)
+            return GPOEO_PD_EHIP;
+    } else {
+        if (gpoeo::launch_lag_score(p, x, part, stream) != hipSuccess) return GPOEO_PD_EHIP;
+        if (!mark(2)) return GPOEO_PD_EHIP;
+        if (gpoeo::launch_finalize(p, w, part, s64, scores, stream) != hipSuccess)
+            return GPOEO_PD_EHIP;
+    }
     if (!mark(3)) return GPOEO_PD_EHIP;
     if (!scores_only &&
         gpoeo::launch_select(p, w, x, var, s64, sb, results, stream) != hipSuccess)

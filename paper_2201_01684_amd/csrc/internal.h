@@ -64,17 +64,35 @@ struct Plan {
     int64_t chunk;           // samples per chunk, a multiple of kBlockSamples
     int64_t tasks;           // waves of the score kernel
     bool aligned;            // x and strides allow 16-byte vector loads
+    // Overlapping windows at stride s with N = m * s share per-block partials:
+    // the trace (trace_len = (B-1) s + N samples per channel) is cut into
+    // blocks = B + m - 1 blocks of s samples, each scored for every lag as a
+    // full block (pairs up to the trace end) and as a cut block (pairs up to
+    // the end of the block the lag's range stops in).
+    bool sliding;
+    int32_t m;               // N / s
+    int64_t blocks;
+    int64_t trace_len;
+    int64_t block_chunk;     // samples per chunk of a block
+    int32_t block_chunks;
+    int64_t block_tasks;     // waves of each of the two block-partial launches
     double c_lag, err_max;
     uint32_t flags;
     int32_t bitmap_words;    // 32-bit words per window of the exactness bitmap
     // workspace layout (byte offsets, 256-byte aligned)
-    size_t off_var, off_s64, off_bits, off_state, off_queue, off_part, bytes;
+    size_t off_var, off_s64, off_bits, off_state, off_queue, off_part, off_cut, bytes;
 };
 
 // Kernel launchers; each returns hipGetLastError() after enqueueing.
 // var: [B][C][2] = population variance, mean |x| per window and channel.
 hipError_t launch_window_stats(const Plan& p, const float* x, double* var, hipStream_t s);
 hipError_t launch_lag_score(const Plan& p, const float* x, double* part, hipStream_t s);
+// Sliding mode: full-block partials into `full`, cut-block partials into `cut`,
+// each [blocks*C + channel][block_chunks][lags_padded].
+hipError_t launch_lag_score_blocks(const Plan& p, const float* x, double* full, double* cut,
+                                   hipStream_t s);
+hipError_t launch_finalize_blocks(const Plan& p, const Weights& w, const double* full,
+                                  const double* cut, double* s64, float* scores, hipStream_t s);
 hipError_t launch_finalize(const Plan& p, const Weights& w, const double* part, double* s64,
                            float* scores, hipStream_t s);
 hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const double* var,

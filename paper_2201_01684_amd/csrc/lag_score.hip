@@ -30,7 +30,10 @@ namespace {
 struct ScoreArgs {
     const float* x;
     double* part;          // [window*C + channel][chunk][lags_padded]
-    int64_t n;
+    int64_t n;             // pair bound: pair (i, i+T) counts iff i + T < n
+    int64_t range;         // samples scored per window: i < range
+    int64_t trace_len;     // > 0: also i + T < trace_len - window start
+    int64_t cut;           // > 0: also i + T < (floor((T_wave - 1) / cut) + 1) * cut
     int64_t window_stride;
     int64_t channel_stride;
     int64_t chunk;
@@ -132,10 +135,15 @@ __global__ __launch_bounds__(kWave * kWavesPerGroup) void lag_score_kernel(Score
     const float* __restrict__ xw = a.x + b * a.window_stride + (int64_t)c * a.channel_stride;
     const int64_t t_wave = (int64_t)a.t0 + (int64_t)blk * kLagsPerBlock;
     const int64_t t_lane = t_wave + (int64_t)lane * kBT;
-    const int64_t n = a.n;
+    // Pair bound of this wave (wave-uniform): the window length, or for the
+    // shared block partials of overlapping windows the trace end and, for the
+    // cut partials, the end of the block the lags' ranges stop in.
+    int64_t n = a.n;
+    if (a.trace_len > 0) n = min(n, a.trace_len - b * a.window_stride);
+    if (a.cut > 0) n = min(n, ((t_wave - 1) / a.cut + 1) * a.cut);
 
     const int64_t i_begin = (int64_t)k * a.chunk;
-    const int64_t chunk_end = i_begin + a.chunk;
+    const int64_t chunk_end = min(i_begin + a.chunk, a.range);
     // A block starting at i runs unmasked iff i + 16 <= lim_full: then every pair
     // of every lane is valid and the aligned window loads (which reach at most
     // x[i + t_wave_hi + 20] for both lane widths) stay below sample n.
@@ -202,7 +210,7 @@ __global__ __launch_bounds__(kWave * kWavesPerGroup) void lag_score_kernel(Score
 
 template <int kBT, int kWPG>
 void launch_shifted(const Plan& p, const ScoreArgs& a, hipStream_t s) {
-    const int64_t groups = (p.tasks + kWPG - 1) / kWPG;
+    const int64_t groups = (a.tasks + kWPG - 1) / kWPG;
     const dim3 grid((unsigned)groups), block(kWave * kWPG);
     switch (p.aligned ? (p.t0 & 3) : 4) {
         case 0: hipLaunchKernelGGL((lag_score_kernel<kBT, kWPG, 0>), grid, block, 0, s, a); break;
@@ -213,13 +221,24 @@ void launch_shifted(const Plan& p, const ScoreArgs& a, hipStream_t s) {
     }
 }
 
-}  // namespace
+void launch(const Plan& p, const ScoreArgs& a, hipStream_t s) {
+    if (p.lags_per_lane == 8) {
+        if (p.waves_per_group == 1) launch_shifted<8, 1>(p, a, s);
+        else launch_shifted<8, 4>(p, a, s);
+    } else {
+        if (p.waves_per_group == 1) launch_shifted<16, 1>(p, a, s);
+        else launch_shifted<16, 4>(p, a, s);
+    }
+}
 
-hipError_t launch_lag_score(const Plan& p, const float* x, double* part, hipStream_t s) {
+ScoreArgs common(const Plan& p, const float* x) {
     ScoreArgs a;
     a.x = x;
-    a.part = part;
+    a.part = nullptr;
     a.n = p.n;
+    a.range = p.n;
+    a.trace_len = 0;
+    a.cut = 0;
     a.window_stride = p.window_stride;
     a.channel_stride = p.channel_stride;
     a.chunk = p.chunk;
@@ -229,13 +248,35 @@ hipError_t launch_lag_score(const Plan& p, const float* x, double* part, hipStre
     a.lag_blocks = p.lag_blocks;
     a.lags_padded = p.lags_padded;
     a.chunks = p.chunks;
-    if (p.lags_per_lane == 8) {
-        if (p.waves_per_group == 1) launch_shifted<8, 1>(p, a, s);
-        else launch_shifted<8, 4>(p, a, s);
-    } else {
-        if (p.waves_per_group == 1) launch_shifted<16, 1>(p, a, s);
-        else launch_shifted<16, 4>(p, a, s);
-    }
+    return a;
+}
+
+}  // namespace
+
+hipError_t launch_lag_score(const Plan& p, const float* x, double* part, hipStream_t s) {
+    ScoreArgs a = common(p, x);
+    a.part = part;
+    launch(p, a, s);
+    return hipGetLastError();
+}
+
+hipError_t launch_lag_score_blocks(const Plan& p, const float* x, double* full, double* cut,
+                                   hipStream_t s) {
+    // Overlapping windows at stride B_s = p.window_stride with N = m * B_s: the
+    // trace is cut into G = num_windows + m - 1 blocks of B_s samples, scored
+    // as "windows" of B_s samples whose pairs may reach past the block.
+    ScoreArgs a = common(p, x);
+    a.range = p.window_stride;
+    a.n = p.window_stride + p.lags_padded + p.t0;   // no bound beyond the trace end
+    a.trace_len = p.trace_len;
+    a.tasks = p.block_tasks;
+    a.chunk = p.block_chunk;
+    a.chunks = p.block_chunks;
+    a.part = full;                                  // full-block partials F_g(T)
+    launch(p, a, s);
+    a.part = cut;                                   // cut-block partials C_g(T)
+    a.cut = p.window_stride;
+    launch(p, a, s);
     return hipGetLastError();
 }
 

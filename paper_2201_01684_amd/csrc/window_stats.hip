@@ -84,7 +84,53 @@ __global__ __launch_bounds__(256) void finalize_kernel(const double* __restrict_
     }
 }
 
+// Overlapping windows at stride s, N = m s: window b's pairs for lag T cover
+// its first m - 1 - q blocks in full (q = floor((T-1)/s): the lag's range ends
+// inside block m - 1 - q) and block m - 1 - q up to that end.  So
+//   D_b(T) = sum_{k < m-1-q} F_{b+k}(T) + C_{b+m-1-q}(T),
+// summed in this fixed order (blocks, then the chunks of each block).
+__global__ __launch_bounds__(256) void finalize_blocks_kernel(
+    const double* __restrict__ full, const double* __restrict__ cut, double* __restrict__ s64,
+    float* __restrict__ scores, Weights w, int64_t num_windows, int32_t num_channels, int64_t n,
+    int64_t stride, int32_t m, int32_t tmin, int32_t lags, int32_t t0, int32_t lags_padded,
+    int32_t chunks) {
+    const int64_t total = num_windows * (int64_t)lags;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t b = e / lags;
+        const int32_t j = (int32_t)(e % lags);
+        const int64_t t = (int64_t)tmin + j;
+        const int64_t q = (t - 1) / stride;
+        double s = 0.0;
+        for (int32_t c = 0; c < num_channels; ++c) {
+            double d = 0.0;
+            for (int64_t k = 0; k + 1 + q < m; ++k) {
+                const double* p = full + ((b + k) * num_channels + c) * chunks * (int64_t)lags_padded +
+                                  (t - t0);
+                for (int32_t h = 0; h < chunks; ++h) d += p[(int64_t)h * lags_padded];
+            }
+            const double* p = cut + ((b + m - 1 - q) * num_channels + c) * chunks *
+                                        (int64_t)lags_padded + (t - t0);
+            for (int32_t h = 0; h < chunks; ++h) d += p[(int64_t)h * lags_padded];
+            s += (double)w.w[c] * (d / (double)(n - t));
+        }
+        s64[e] = s;
+        if (scores) scores[e] = (float)s;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_finalize_blocks(const Plan& p, const Weights& w, const double* full,
+                                  const double* cut, double* s64, float* scores, hipStream_t s) {
+    const int64_t total = p.num_windows * (int64_t)p.lags;
+    int64_t groups = (total + 255) / 256;
+    if (groups > 65536) groups = 65536;
+    hipLaunchKernelGGL(finalize_blocks_kernel, dim3((unsigned)groups), dim3(256), 0, s, full, cut,
+                       s64, scores, w, p.num_windows, p.num_channels, p.n, p.window_stride, p.m,
+                       p.tmin, p.lags, p.t0, p.lags_padded, p.block_chunks);
+    return hipGetLastError();
+}
 
 hipError_t launch_window_stats(const Plan& p, const float* x, double* var, hipStream_t s) {
     const int64_t groups = p.num_windows * p.num_channels;

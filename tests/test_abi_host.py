@@ -140,3 +140,20 @@ def test_scores_only_needs_no_results_pointer_but_still_a_workspace(lib):
                                None) == B.EINVAL
     assert lib.gpoeo_pd_detect(ctypes.byref(d), 0x100000, None, None, 0x300000, need - 1,
                                None) == B.ENOMEM
+
+
+def test_plan_description(lib):
+    from gen import make_workload
+    wl = make_workload("w4", total=65536, n=16384, stride=2048, tmax=4096)
+    d, _ = B.make_desc(wl.num_windows, 1, wl.n, wl.window_stride, wl.channel_stride, wl.tmin,
+                       wl.tmax)
+    info = B.describe_plan(d)
+    assert info["mode"] == 1 and info["pairs_defined"] == wl.pairs()
+    assert 0 < info["pairs_scored"] < info["pairs_defined"]
+    assert info["workspace_bytes"] == B.workspace_bytes(d)
+    # non-overlapping windows: every window scored on its own
+    d, _ = good_desc()
+    info = B.describe_plan(d)
+    assert info["mode"] == 0 and info["pairs_scored"] == info["pairs_defined"]
+    assert info["pairs_defined"] == 4 * 2 * sum(4096 - t for t in range(2, 1025))
+    assert info["lags_per_lane"] in (8, 16)

@@ -129,6 +129,22 @@ def test_unaligned_strides_and_overlapping_windows():
         parity(x, lay, f"overlap tmin={tmin}")
 
 
+@pytest.mark.parametrize("channels,tmin,tmax,stride", [(1, 3, 3000, 1024), (2, 2, 2048, 1024),
+                                                        (1, 700, 4000, 512), (3, 1, 1500, 2048)])
+def test_sliding_windows_share_block_partials(channels, tmin, tmax, stride):
+    import paper_2201_01684_amd as pkg
+    total, n = 40960, 8192
+    rows = [planted_trace(total, 301 + 40 * c, 7, seed=11 + c, sigma=1.5) for c in range(channels)]
+    x = np.stack(rows).astype(np.float32)            # [C][total], channel stride = total
+    b = (total - n) // stride + 1
+    w = np.linspace(1.0, 0.5, channels).astype(np.float32)
+    lay = oracle.Layout(b, channels, n, stride, total, tmin, tmax, weights=w)
+    desc, _keep = pkg.make_desc(b, channels, n, stride, total, tmin, tmax, weights=w)
+    info = pkg.describe_plan(desc)
+    assert info["mode"] == 1 and info["pairs_scored"] < 0.7 * info["pairs_defined"]
+    parity(x, lay, f"sliding C={channels} T=[{tmin},{tmax}] stride={stride}")
+
+
 def test_weighted_channels():
     rng = np.random.default_rng(3)
     b, c, n = 3, 3, 6000
