@@ -54,6 +54,21 @@ class _Out(ctypes.Structure):
                 ("r", ctypes.c_double), ("s_pk", ctypes.c_double)]
 
 
+ROLLING_MAX = 32
+
+
+class _RollingParams(ctypes.Structure):
+    _fields_ = [("c_measure", ctypes.c_double), ("step", ctypes.c_double),
+                ("c_eval", ctypes.c_double), ("diff_threshold", ctypes.c_double)]
+
+
+ROLLING_DTYPE = np.dtype([("period", np.int32), ("verdict", np.int32), ("stable", np.int32),
+                          ("n_windows", np.int32), ("t_init", np.int32), ("best", np.int32),
+                          ("smpdur_next", np.float64), ("diff", np.float64), ("err", np.float64),
+                          ("starts", np.int64, ROLLING_MAX), ("periods", np.int32, ROLLING_MAX),
+                          ("verdicts", np.int32, ROLLING_MAX), ("errs", np.float64, ROLLING_MAX)],
+                         align=True)
+
 OUT_DTYPE = np.dtype([("period", np.int32), ("verdict", np.int32), ("err", np.float64),
                       ("n_candidates", np.int32), ("t_cand", np.int32), ("t_low", np.int32),
                       ("t_up", np.int32), ("n_peaks", np.int32), ("r", np.float64),
@@ -86,6 +101,13 @@ def _load():
         lib.oracle_pd_score_list.restype = ctypes.c_int
         lib.oracle_pd_score_list.argtypes = [P(_Params), ctypes.c_void_p, ctypes.c_void_p,
                                              ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+        lib.oracle_pd_rolling.restype = ctypes.c_int
+        lib.oracle_pd_rolling.argtypes = [P(_Params), P(_RollingParams), ctypes.c_void_p,
+                                          ctypes.c_void_p]
+        lib.oracle_pd_rolling_schedule.restype = ctypes.c_int32
+        lib.oracle_pd_rolling_schedule.argtypes = [ctypes.c_int64, ctypes.c_int32,
+                                                   P(_RollingParams), ctypes.c_void_p,
+                                                   ctypes.c_int32, P(ctypes.c_double)]
         lib.oracle_pd_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -208,3 +230,38 @@ def select(s: np.ndarray, n: int, tmin: int, tmax: int, r: float,
     _load().oracle_pd_select(s.ctypes.data, int(n), int(tmin), int(tmax), float(r),
                              float(c_lag), float(err_max), ctypes.byref(o))
     return {name: getattr(o, name) for name, _ in _Out._fields_}
+
+
+# Algorithm 3's constants as the paper sets them (Sec. 4.1.3); the stability
+# threshold on the relative period spread is not given there.
+C_MEASURE, STEP, C_EVAL = 2.0, 0.5, 6.5
+DEFAULT_DIFF_THRESHOLD = 0.05
+
+
+def rolling(x: np.ndarray, lay: Layout, c_measure: float = C_MEASURE, step: float = STEP,
+            c_eval: float = C_EVAL, diff_threshold: float = DEFAULT_DIFF_THRESHOLD) -> np.ndarray:
+    """Algorithm 3 on every window of the batch: one ROLLING_DTYPE record each."""
+    x = _as_f32(x)
+    _check_extent(x, lay)
+    keep: list = []
+    p = _params(lay, keep)
+    rp = _RollingParams(float(c_measure), float(step), float(c_eval), float(diff_threshold))
+    out = np.zeros(lay.num_windows, dtype=ROLLING_DTYPE)
+    rc = _load().oracle_pd_rolling(ctypes.byref(p), ctypes.byref(rp), x.ctypes.data,
+                                   out.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle rejected the parameters")
+    return out
+
+
+def rolling_schedule(n: int, t_init: int, c_measure: float = C_MEASURE, step: float = STEP,
+                     c_eval: float = C_EVAL):
+    """(suffix start samples, too-short next duration) of Algorithm 3's schedule."""
+    rp = _RollingParams(float(c_measure), float(step), float(c_eval), 0.0)
+    starts = np.zeros(ROLLING_MAX, dtype=np.int64)
+    nxt = ctypes.c_double()
+    k = _load().oracle_pd_rolling_schedule(int(n), int(t_init), ctypes.byref(rp),
+                                           starts.ctypes.data, ROLLING_MAX, ctypes.byref(nxt))
+    if k < 0:
+        raise ValueError("schedule longer than the oracle's limit")
+    return starts[:k].tolist(), nxt.value

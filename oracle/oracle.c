@@ -13,6 +13,7 @@
 #include <math.h>
 #include <stddef.h>
 #include <stdlib.h>
+#include <string.h>
 #include <omp.h>
 
 static double weight_of(const float* w, int32_t c) { return w ? (double)w[c] : 1.0; }
@@ -166,6 +167,120 @@ int oracle_pd_score_list(const oracle_pd_params* p, const float* x, const int64_
         scores_out[k] = oracle_pd_score(x + w[k] * p->window_stride, p->num_channels,
                                         p->channel_stride, p->n, t[k], p->channel_weights);
     return 0;
+}
+
+/* The rule on one window of n samples (channels at channel_stride), lags
+ * [tmin, tmax]; scores in the caller's buffer of tmax - tmin + 1 doubles. */
+static void detect_one(const oracle_pd_params* p, const float* xw, int64_t n, int32_t tmax,
+                       double* s, oracle_pd_out* o) {
+    const int64_t L = (int64_t)tmax - p->tmin + 1;
+    double r = oracle_pd_reference(xw, p->num_channels, p->channel_stride, n, p->channel_weights);
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t j = 0; j < L; ++j)
+        s[j] = oracle_pd_score(xw, p->num_channels, p->channel_stride, n, p->tmin + j,
+                               p->channel_weights);
+    oracle_pd_select(s, n, p->tmin, tmax, r, p->c_lag, p->err_max, o);
+}
+
+int32_t oracle_pd_rolling_schedule(int64_t n, int32_t t_init, const oracle_pd_rolling_params* rp,
+                                   int64_t* starts, int32_t cap, double* short_next) {
+    const double t = (double)t_init;
+    const double dur = (double)(n - 1);
+    *short_next = 0.0;
+    if (dur < rp->c_measure * t) {
+        *short_next = rp->c_measure * t - dur;
+        return 0;
+    }
+    double t_start = dur - (2.0 + rp->c_eval * rp->step) * t;
+    if (t_start < 0.0) t_start = 0.0;
+    int32_t j = 0;
+    while ((dur - t_start) / t >= rp->c_measure) {
+        if (j == cap) return -1;
+        starts[j++] = (int64_t)floor(t_start);
+        t_start += rp->step * t;
+    }
+    return j;
+}
+
+int oracle_pd_rolling(const oracle_pd_params* p, const oracle_pd_rolling_params* rp,
+                      const float* x, oracle_pd_rolling_out* out) {
+    if (check_params(p) || !rp || !x || !out) return -1;
+    if (!(rp->c_measure > 0.0) || !(rp->step > 0.0) || !(rp->c_eval >= 0.0)) return -1;
+    const int64_t L = (int64_t)p->tmax - p->tmin + 1;
+    double* s = (double*)malloc((size_t)L * sizeof(double));
+    if (!s) return -1;
+    int rc = 0;
+    for (int64_t b = 0; b < p->num_windows && rc == 0; ++b) {
+        const float* xw = x + b * p->window_stride;
+        oracle_pd_rolling_out* o = &out[b];
+        memset(o, 0, sizeof(*o));
+        o->best = -1;
+        oracle_pd_out first;
+        detect_one(p, xw, p->n, p->tmax, s, &first);
+        o->t_init = first.period;
+        if (first.verdict != ORACLE_PERIODIC) {
+            o->verdict = first.verdict;
+            continue;
+        }
+        const double dur = (double)(p->n - 1);
+        double short_next;
+        const int32_t j = oracle_pd_rolling_schedule(p->n, first.period, rp, o->starts,
+                                                     ORACLE_ROLLING_MAX, &short_next);
+        if (j < 0) {
+            rc = -1;
+            break;
+        }
+        if (j == 0) {   /* too short for a rolling evaluation (or no suffix fits) */
+            o->verdict = ORACLE_PERIODIC;
+            o->period = first.period;
+            o->err = first.err;
+            o->smpdur_next = short_next;
+            continue;
+        }
+        for (int32_t k = 0; k < j; ++k) {
+            const int64_t start = o->starts[k];
+            const int64_t nj = p->n - start;
+            int32_t tmax_j = p->tmax;
+            if ((int64_t)tmax_j > nj / 2) tmax_j = (int32_t)(nj / 2);
+            if (tmax_j >= p->tmin + 2) {
+                oracle_pd_out sub;
+                detect_one(p, xw + start, nj, tmax_j, s, &sub);
+                o->verdicts[k] = sub.verdict;
+                o->periods[k] = sub.verdict == ORACLE_PERIODIC ? sub.period : 0;
+                o->errs[k] = sub.err;
+            } else {
+                o->verdicts[k] = ORACLE_APERIODIC;
+            }
+        }
+        o->n_windows = j;
+        /* best window, spread and next sampling duration over the periodic suffixes */
+        int32_t cnt = 0, tmin_p = 0, tmax_p = 0;
+        double sum = 0.0;
+        for (int32_t k = 0; k < j; ++k) {
+            if (o->verdicts[k] != ORACLE_PERIODIC) continue;
+            if (o->best < 0 || o->errs[k] < o->errs[o->best]) o->best = k;
+            if (cnt == 0 || o->periods[k] < tmin_p) tmin_p = o->periods[k];
+            if (cnt == 0 || o->periods[k] > tmax_p) tmax_p = o->periods[k];
+            sum += (double)o->periods[k];
+            ++cnt;
+        }
+        if (cnt == 0) {
+            o->verdict = ORACLE_APERIODIC;
+            continue;
+        }
+        o->verdict = ORACLE_PERIODIC;
+        o->period = o->periods[o->best];
+        o->err = o->errs[o->best];
+        o->diff = fabs(((double)tmax_p - (double)tmin_p) / (sum / (double)cnt));
+        if (o->diff < rp->diff_threshold) {
+            o->stable = 1;
+            o->smpdur_next = -1.0;
+        } else {
+            o->smpdur_next = ceil(dur / (double)tmax_p) * (double)tmax_p - dur;
+        }
+    }
+    free(s);
+    return rc;
 }
 
 int oracle_pd_threads(void) { return omp_get_max_threads(); }

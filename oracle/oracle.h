@@ -96,6 +96,60 @@ int oracle_pd_detect(const oracle_pd_params* p, const float* x, double* scores,
 int oracle_pd_score_list(const oracle_pd_params* p, const float* x, const int64_t* w,
                          const int32_t* t, int64_t count, double* scores_out);
 
+/* Algorithm 3 (Sec. 4.1.3): rolling detection over suffix windows.
+ *
+ *   T_init  = period of the whole window (the rule above); if it is not
+ *             PERIODIC the result carries its verdict, period 0 and no windows.
+ *   D       = N - 1 (the sampling duration in samples, T_s = 1)
+ *   D < c_measure * T_init: too short; period T_init, next = c_measure T_init - D
+ *   t_start = max(0, D - (2 + c_eval * step) * T_init)
+ *   while (D - t_start) / T_init >= c_measure:
+ *       suffix x[floor(t_start) .. N-1] (N_j = N - floor(t_start) samples),
+ *       lags [tmin, min(tmax, N_j / 2)], same rule -> T_j, err_j
+ *       t_start += step * T_init
+ *   the suffixes with a PERIODIC verdict form T and Err (none -> APERIODIC)
+ *   period  = T_k with err_k = min Err (first such k)
+ *   diff    = |max T - min T| / mean T
+ *   next    = -1 (stable) if diff < diff_threshold,
+ *             else ceil(D / max T) * max T - D
+ */
+#define ORACLE_ROLLING_MAX 32
+
+typedef struct {
+    double c_measure;       /* 2 in the paper */
+    double step;            /* 0.5 */
+    double c_eval;          /* 6.5 */
+    double diff_threshold;  /* not given by the paper */
+} oracle_pd_rolling_params;
+
+typedef struct {
+    int32_t period;
+    int32_t verdict;
+    int32_t stable;
+    int32_t n_windows;
+    int32_t t_init;
+    int32_t best;                       /* index of the selected suffix window, -1 if none */
+    double smpdur_next;
+    double diff;
+    double err;
+    int64_t starts[ORACLE_ROLLING_MAX];  /* suffix start sample */
+    int32_t periods[ORACLE_ROLLING_MAX]; /* T_j (0: no period) */
+    int32_t verdicts[ORACLE_ROLLING_MAX];
+    double errs[ORACLE_ROLLING_MAX];
+} oracle_pd_rolling_out;
+
+/* The suffix-window schedule alone: for a window of n samples and T_init,
+ * writes the start sample of every suffix window and returns their number, or
+ * returns 0 and sets *short_next to c_measure T_init - D when the window is too
+ * short (otherwise *short_next = 0); -1 if more than `cap` windows. */
+int32_t oracle_pd_rolling_schedule(int64_t n, int32_t t_init, const oracle_pd_rolling_params* rp,
+                                   int64_t* starts, int32_t cap, double* short_next);
+
+/* One result per window of the batch; returns 0, or -1 on invalid parameters
+ * (including a schedule longer than ORACLE_ROLLING_MAX windows). */
+int oracle_pd_rolling(const oracle_pd_params* p, const oracle_pd_rolling_params* rp,
+                      const float* x, oracle_pd_rolling_out* out);
+
 /* Number of threads the parallel loops use. */
 int oracle_pd_threads(void);
 
