@@ -75,6 +75,8 @@ extern "C" {
 /* result->flags */
 #define GPOEO_PD_UNRESOLVED 1u   /* some comparison stayed undecided after the exact
                                     re-scoring limit; the result uses bounded scores       */
+#define GPOEO_PD_SHORT 2u        /* (rolling detection) a suffix window too short for
+                                    three lags starting at tmin; no period                 */
 
 typedef struct {
     int64_t num_windows;     /* B >= 1: traces, or sliding windows of one long trace        */
@@ -157,6 +159,56 @@ int gpoeo_pd_detect(const gpoeo_pd_desc* desc, const float* x, float* scores,
 int gpoeo_pd_detect_staged(const gpoeo_pd_desc* desc, const float* x, float* scores,
                            gpoeo_pd_result* results, void* workspace, size_t workspace_bytes,
                            hipStream_t stream, hipEvent_t stage_events[5]);
+
+/* ---------------------------------------------------------------------------
+ * Rolling detection (Algorithm 3, Sec. 4.1.3).  For every window of the batch
+ * (read as the samples gathered so far): T_init = the period of the whole
+ * window (the rule above); then, with D = N - 1 and T_s = 1 sample,
+ *   D < c_measure * T_init: too short, period T_init, smpdur_next = c_measure T_init - D;
+ *   otherwise suffix windows x[floor(t) .. N-1] for t = max(0, D - (2 + c_eval step) T_init),
+ *   t += step T_init while (D - t) / T_init >= c_measure, each scored and
+ *   selected with lags [tmin, min(tmax, N_j / 2)]; among the suffixes with a
+ *   PERIODIC verdict the smallest err gives the period (first on ties),
+ *   diff = |max T - min T| / mean T, and smpdur_next = -1 (stable) when
+ *   diff < diff_threshold, else ceil(D / max T) max T - D.
+ * The whole pipeline runs on `stream` (two detection passes, a schedule kernel
+ * and a combining kernel); the same precision rules as gpoeo_pd_detect apply.
+ * ------------------------------------------------------------------------- */
+#define GPOEO_PD_ROLLING_MAX 16   /* suffix windows per window, at most */
+
+typedef struct {
+    double c_measure;        /* periods a (suffix) window must span; the paper uses 2       */
+    double step;             /* advance of the suffix start, in periods; the paper uses 0.5 */
+    double c_eval;           /* the first suffix spans 2 + c_eval * step periods; paper 6.5 */
+    double diff_threshold;   /* stable iff diff < this; not given by the paper (0.05)        */
+} gpoeo_pd_rolling_params;
+
+typedef struct {
+    int32_t period;          /* T_iter in samples; 0 if none                                  */
+    int32_t verdict;         /* of the whole window's first pass                              */
+    int32_t stable;          /* 1 when smpdur_next == -1                                      */
+    int32_t n_windows;       /* suffix windows evaluated (0: too short or not periodic)       */
+    int32_t t_init;          /* period of the whole window                                    */
+    int32_t best;            /* index of the selected suffix window, -1 if none               */
+    double smpdur_next;      /* samples to keep sampling before the next call; -1 if stable   */
+    float diff;              /* relative period spread over the periodic suffix windows       */
+    float err;               /* err of the selected period                                    */
+    uint32_t flags;          /* GPOEO_PD_UNRESOLVED if any selection of this window was       */
+    int32_t reserved;
+    int32_t periods[GPOEO_PD_ROLLING_MAX];   /* T_j per suffix window (0: none)               */
+    int64_t starts[GPOEO_PD_ROLLING_MAX];    /* first sample of each suffix window            */
+} gpoeo_pd_rolling_result;
+
+/* Validates desc (flags may hold GPOEO_PD_NO_RESCUE only) and params and writes
+ * the device workspace size of gpoeo_pd_detect_rolling.  EINVAL if the schedule
+ * could exceed GPOEO_PD_ROLLING_MAX suffix windows. */
+int gpoeo_pd_rolling_workspace_bytes(const gpoeo_pd_desc* desc,
+                                     const gpoeo_pd_rolling_params* params, size_t* bytes);
+
+/* Rolling detection of every window; results: device, one record per window. */
+int gpoeo_pd_detect_rolling(const gpoeo_pd_desc* desc, const gpoeo_pd_rolling_params* params,
+                            const float* x, gpoeo_pd_rolling_result* results, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -19,11 +19,16 @@ from ._binding import (  # noqa: F401
     RESULT_DTYPE,
     SCORES_ONLY,
     UNRESOLVED,
+    ROLLING_DTYPE,
     Desc,
     Detector,
+    RollingDetector,
     GpoeoError,
     describe_plan,
     detect_period,
+    detect_rolling,
+    rolling_params,
+    rolling_workspace_bytes,
     load_library,
     make_desc,
     results_to_numpy,

@@ -47,6 +47,34 @@ class PlanInfo(ctypes.Structure):
                 ("pairs_scored", ctypes.c_double), ("workspace_bytes", ctypes.c_size_t)]
 
 
+ROLLING_MAX = 16
+
+
+class RollingParams(ctypes.Structure):
+    _fields_ = [("c_measure", ctypes.c_double), ("step", ctypes.c_double),
+                ("c_eval", ctypes.c_double), ("diff_threshold", ctypes.c_double)]
+
+
+class RollingResult(ctypes.Structure):
+    _fields_ = [("period", ctypes.c_int32), ("verdict", ctypes.c_int32),
+                ("stable", ctypes.c_int32), ("n_windows", ctypes.c_int32),
+                ("t_init", ctypes.c_int32), ("best", ctypes.c_int32),
+                ("smpdur_next", ctypes.c_double), ("diff", ctypes.c_float),
+                ("err", ctypes.c_float), ("flags", ctypes.c_uint32), ("reserved", ctypes.c_int32),
+                ("periods", ctypes.c_int32 * ROLLING_MAX), ("starts", ctypes.c_int64 * ROLLING_MAX)]
+
+
+ROLLING_DTYPE = np.dtype([("period", np.int32), ("verdict", np.int32), ("stable", np.int32),
+                          ("n_windows", np.int32), ("t_init", np.int32), ("best", np.int32),
+                          ("smpdur_next", np.float64), ("diff", np.float32), ("err", np.float32),
+                          ("flags", np.uint32), ("reserved", np.int32),
+                          ("periods", np.int32, ROLLING_MAX), ("starts", np.int64, ROLLING_MAX)])
+assert ROLLING_DTYPE.itemsize == ctypes.sizeof(RollingResult)
+
+# Algorithm 3's constants as the paper sets them (Sec. 4.1.3); the paper gives
+# no value for the stability threshold on the relative period spread.
+C_MEASURE, STEP, C_EVAL, DEFAULT_DIFF_THRESHOLD = 2.0, 0.5, 6.5, 0.05
+
 RESULT_DTYPE = np.dtype([("period", np.int32), ("verdict", np.int32), ("err", np.float32),
                          ("n_candidates", np.int32), ("t_cand", np.int32), ("t_low", np.int32),
                          ("t_up", np.int32), ("n_rescored", np.int32), ("flags", np.uint32)])
@@ -54,7 +82,8 @@ RESULT_WORDS = ctypes.sizeof(Result) // 4
 assert RESULT_DTYPE.itemsize == ctypes.sizeof(Result)
 
 EXPORTS = ("gpoeo_pd_abi_version", "gpoeo_pd_strerror", "gpoeo_pd_workspace_bytes",
-           "gpoeo_pd_describe_plan", "gpoeo_pd_detect", "gpoeo_pd_detect_staged")
+           "gpoeo_pd_describe_plan", "gpoeo_pd_detect", "gpoeo_pd_detect_staged",
+           "gpoeo_pd_rolling_workspace_bytes", "gpoeo_pd_detect_rolling")
 
 _lib = None
 
@@ -85,6 +114,14 @@ def load_library():
                                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                                ctypes.c_size_t, ctypes.c_void_p,
                                                ctypes.c_void_p]
+        lib.gpoeo_pd_rolling_workspace_bytes.restype = ctypes.c_int
+        lib.gpoeo_pd_rolling_workspace_bytes.argtypes = [ctypes.POINTER(Desc),
+                                                         ctypes.POINTER(RollingParams),
+                                                         ctypes.POINTER(ctypes.c_size_t)]
+        lib.gpoeo_pd_detect_rolling.restype = ctypes.c_int
+        lib.gpoeo_pd_detect_rolling.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(RollingParams),
+                                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                                ctypes.c_size_t, ctypes.c_void_p]
         _lib = lib
     return _lib
 
@@ -228,3 +265,71 @@ def detect_period(traces: torch.Tensor, tmin: int, tmax: int, *, n: int | None =
     torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
     res = None if (flags & SCORES_ONLY) else det.results_numpy()
     return det.scores, res
+
+
+def rolling_params(c_measure: float = C_MEASURE, step: float = STEP, c_eval: float = C_EVAL,
+                   diff_threshold: float = DEFAULT_DIFF_THRESHOLD) -> RollingParams:
+    return RollingParams(float(c_measure), float(step), float(c_eval), float(diff_threshold))
+
+
+def rolling_workspace_bytes(desc: Desc, params: RollingParams) -> int:
+    size = ctypes.c_size_t(0)
+    rc = load_library().gpoeo_pd_rolling_workspace_bytes(ctypes.byref(desc),
+                                                         ctypes.byref(params),
+                                                         ctypes.byref(size))
+    if rc != OK:
+        raise GpoeoError(rc, "gpoeo_pd_rolling_workspace_bytes")
+    return int(size.value)
+
+
+class RollingDetector:
+    """Reusable call site of gpoeo_pd_detect_rolling (buffers allocated once)."""
+
+    def __init__(self, x: torch.Tensor, desc: Desc, params: RollingParams,
+                 weights_keepalive=None):
+        if not isinstance(x, torch.Tensor) or x.dtype != torch.float32 or not x.is_cuda:
+            raise TypeError("x must be a float32 GPU tensor")
+        if not x.is_contiguous():
+            raise ValueError("x must be contiguous")
+        need = ((desc.num_windows - 1) * desc.window_stride
+                + (desc.num_channels - 1) * desc.channel_stride + desc.n)
+        if x.numel() < need:
+            raise ValueError(f"x has {x.numel()} samples, the layout addresses {need}")
+        self.x, self.desc, self.params, self._w = x, desc, params, weights_keepalive
+        self.results = torch.zeros((desc.num_windows, ROLLING_DTYPE.itemsize // 4),
+                                   dtype=torch.int32, device=x.device)
+        self.ws_bytes = rolling_workspace_bytes(desc, params)
+        self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=x.device)
+        self._lib = load_library()
+
+    def run(self, stream=None) -> None:
+        rc = self._lib.gpoeo_pd_detect_rolling(
+            ctypes.byref(self.desc), ctypes.byref(self.params), self.x.data_ptr(),
+            self.results.data_ptr(), self.workspace.data_ptr(), self.ws_bytes,
+            _stream_handle(stream))
+        if rc != OK:
+            raise GpoeoError(rc, "gpoeo_pd_detect_rolling")
+
+    def results_numpy(self) -> np.ndarray:
+        host = self.results.detach().to("cpu").contiguous().numpy()
+        return host.view(ROLLING_DTYPE).reshape(-1)
+
+
+def detect_rolling(traces: torch.Tensor, tmin: int, tmax: int, *, weights=None,
+                   c_lag: float = DEFAULT_C_LAG, err_max: float = DEFAULT_ERR_MAX,
+                   flags: int = 0, stream=None, **params):
+    """Algorithm 3 on every row of a [B, N] or [B, C, N] float32 GPU tensor; returns
+    one ROLLING_DTYPE record per row (params: c_measure, step, c_eval, diff_threshold)."""
+    if traces.dim() == 2:
+        b, n = traces.shape
+        c, ws, cs = 1, n, n
+    elif traces.dim() == 3:
+        b, c, n = traces.shape
+        ws, cs = c * n, n
+    else:
+        raise ValueError("traces must be 2-D or 3-D")
+    desc, w = make_desc(b, c, n, ws, cs, tmin, tmax, c_lag, err_max, weights, flags)
+    det = RollingDetector(traces.contiguous(), desc, rolling_params(**params), w)
+    det.run(stream)
+    (torch.cuda.current_stream() if stream is None else stream).synchronize()
+    return det.results_numpy()

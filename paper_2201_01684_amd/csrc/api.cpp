@@ -18,7 +18,11 @@ namespace {
 constexpr int64_t kTargetWaves = 40960;
 constexpr size_t kAlign = 256;
 
+}  // namespace
+
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+namespace {
 
 // Lags per lane of the score kernel.  16 lets each staged sample serve more
 // lags and suits long windows; 8 halves the masked stretch at the end of each
@@ -188,6 +192,153 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
 }  // namespace
 }  // namespace gpoeo
 
+namespace {
+
+struct Carved {
+    double* var;
+    double* s64;
+    gpoeo::SelectBuffers sb;
+    double* part;
+    double* cut;
+};
+
+Carved carve(const gpoeo::Plan& p, void* workspace) {
+    char* ws = static_cast<char*>(workspace);
+    Carved c;
+    c.var = reinterpret_cast<double*>(ws + p.off_var);
+    c.s64 = reinterpret_cast<double*>(ws + p.off_s64);
+    const size_t words = (size_t)p.num_windows * p.bitmap_words;
+    uint32_t* bits = reinterpret_cast<uint32_t*>(ws + p.off_bits);
+    int32_t* queue = reinterpret_cast<int32_t*>(ws + p.off_queue);
+    c.sb.tier1 = bits;
+    c.sb.tier2 = bits + words;
+    c.sb.queued1 = bits + 2 * words;
+    c.sb.queued2 = bits + 3 * words;
+    c.sb.state = reinterpret_cast<gpoeo::WinState*>(ws + p.off_state);
+    c.sb.q_win = queue;
+    c.sb.q_lag = queue + 2 * gpoeo::kQueueCap;
+    c.sb.q_count = queue + 4 * gpoeo::kQueueCap;
+    c.part = reinterpret_cast<double*>(ws + p.off_part);
+    c.cut = reinterpret_cast<double*>(ws + p.off_cut);
+    return c;
+}
+
+gpoeo::Weights weights_of(const gpoeo_pd_desc* d, int32_t num_channels) {
+    gpoeo::Weights w;
+    for (int c = 0; c < gpoeo::kMaxChannels; ++c)
+        w.w[c] = (d->channel_weights && c < num_channels) ? d->channel_weights[c] : 1.0f;
+    return w;
+}
+
+bool x_aligned(const float* x, const gpoeo::Plan& p) {
+    return (reinterpret_cast<uintptr_t>(x) % 16 == 0) &&
+           (p.num_windows == 1 || p.window_stride % 4 == 0) &&
+           (p.num_channels == 1 || p.channel_stride % 4 == 0);
+}
+
+// Enqueues the four stages of one plan (stats, scores, finalisation, selection).
+int run_plan(const gpoeo::Plan& p, const gpoeo::Weights& w, const float* x, float* scores,
+             gpoeo_pd_result* results, void* workspace, hipStream_t stream, hipEvent_t* ev) {
+    const bool scores_only = (p.flags & GPOEO_PD_SCORES_ONLY) != 0;
+    const Carved c = carve(p, workspace);
+    auto mark = [&](int k) { return !ev || hipEventRecord(ev[k], stream) == hipSuccess; };
+    if (!mark(0)) return GPOEO_PD_EHIP;
+    if (!scores_only && gpoeo::launch_window_stats(p, x, c.var, stream) != hipSuccess)
+        return GPOEO_PD_EHIP;
+    if (!mark(1)) return GPOEO_PD_EHIP;
+    if (p.sliding) {
+        if (gpoeo::launch_lag_score_blocks(p, x, c.part, c.cut, stream) != hipSuccess)
+            return GPOEO_PD_EHIP;
+        if (!mark(2)) return GPOEO_PD_EHIP;
+        if (gpoeo::launch_finalize_blocks(p, w, c.part, c.cut, c.s64, scores, stream) != hipSuccess)
+            return GPOEO_PD_EHIP;
+    } else {
+        if (gpoeo::launch_lag_score(p, x, c.part, stream) != hipSuccess) return GPOEO_PD_EHIP;
+        if (!mark(2)) return GPOEO_PD_EHIP;
+        if (gpoeo::launch_finalize(p, w, c.part, c.s64, scores, stream) != hipSuccess)
+            return GPOEO_PD_EHIP;
+    }
+    if (!mark(3)) return GPOEO_PD_EHIP;
+    if (!scores_only &&
+        gpoeo::launch_select(p, w, x, c.var, c.s64, c.sb, results, stream) != hipSuccess)
+        return GPOEO_PD_EHIP;
+    if (!mark(4)) return GPOEO_PD_EHIP;
+    return GPOEO_PD_OK;
+}
+
+int detect_impl(const gpoeo_pd_desc* desc, const float* x, float* scores,
+                gpoeo_pd_result* results, void* workspace, size_t workspace_bytes,
+                hipStream_t stream, hipEvent_t* ev) {
+    gpoeo::Plan p;
+    const int rc = gpoeo::make_plan(desc, &p);
+    if (rc != GPOEO_PD_OK) return rc;
+    const bool scores_only = (p.flags & GPOEO_PD_SCORES_ONLY) != 0;
+    if (!x || (!results && !scores_only) || !workspace) return GPOEO_PD_EINVAL;
+    if (reinterpret_cast<uintptr_t>(workspace) % gpoeo::kAlign) return GPOEO_PD_EINVAL;
+    if (reinterpret_cast<uintptr_t>(x) % sizeof(float)) return GPOEO_PD_EINVAL;
+    if (workspace_bytes < p.bytes) return GPOEO_PD_ENOMEM;
+    p.aligned = x_aligned(x, p);
+    return run_plan(p, weights_of(desc, p.num_channels), x, scores, results, workspace, stream,
+                    ev);
+}
+
+// Rolling detection: the whole-window plan, the suffix-window plan (a window
+// table of B * jmax slots) and the workspace around them.
+struct RollingPlan {
+    gpoeo::Plan a, c;
+    gpoeo::RollingConfig rc;
+    size_t off_res_a, off_tab_off, off_tab_n, off_tab_tmax, off_res_c, off_state, off_detect;
+    size_t bytes;
+};
+
+int make_rolling(const gpoeo_pd_desc* d, const gpoeo_pd_rolling_params* rp, RollingPlan* r) {
+    if (!d || !rp) return GPOEO_PD_EINVAL;
+    if (d->flags & GPOEO_PD_SCORES_ONLY) return GPOEO_PD_EINVAL;
+    if (!(rp->c_measure > 0.0) || !(rp->step > 0.0) || !(rp->c_eval >= 0.0) ||
+        !std::isfinite(rp->c_measure) || !std::isfinite(rp->step) ||
+        !std::isfinite(rp->c_eval) || std::isnan(rp->diff_threshold))
+        return GPOEO_PD_EINVAL;
+    // Suffix windows per window: durations 2 + c_eval * step, minus k * step,
+    // down to c_measure periods; one slot of margin for rounding.
+    const double span = (2.0 + rp->c_eval * rp->step - rp->c_measure) / rp->step;
+    if (!(span < GPOEO_PD_ROLLING_MAX)) return GPOEO_PD_EINVAL;
+    const int32_t jmax = span < 0.0 ? 1 : (int32_t)std::floor(span) + 2;
+    if (jmax > GPOEO_PD_ROLLING_MAX) return GPOEO_PD_EINVAL;
+    int rc = gpoeo::make_plan(d, &r->a);
+    if (rc != GPOEO_PD_OK) return rc;
+    gpoeo_pd_desc dc = *d;
+    if (d->num_windows > INT32_MAX / jmax) return GPOEO_PD_EINVAL;
+    dc.num_windows = d->num_windows * jmax;
+    dc.window_stride = d->n;     // placeholder: the window table gives every offset
+    rc = gpoeo::make_plan(&dc, &r->c);
+    if (rc != GPOEO_PD_OK) return rc;
+    r->rc.c_measure = rp->c_measure;
+    r->rc.step = rp->step;
+    r->rc.c_eval = rp->c_eval;
+    r->rc.diff_threshold = rp->diff_threshold;
+    r->rc.jmax = jmax;
+    const size_t b = (size_t)d->num_windows, bj = b * jmax;
+    size_t off = 0;
+    r->off_res_a = off;
+    off = gpoeo::align_up(off + b * sizeof(gpoeo_pd_result));
+    r->off_tab_off = off;
+    off = gpoeo::align_up(off + bj * sizeof(int64_t));
+    r->off_tab_n = off;
+    off = gpoeo::align_up(off + bj * sizeof(int64_t));
+    r->off_tab_tmax = off;
+    off = gpoeo::align_up(off + bj * sizeof(int32_t));
+    r->off_res_c = off;
+    off = gpoeo::align_up(off + bj * sizeof(gpoeo_pd_result));
+    r->off_state = off;
+    off = gpoeo::align_up(off + b * sizeof(gpoeo::RollState));
+    r->off_detect = off;           // shared by the two detection passes, one after the other
+    off = gpoeo::align_up(off + std::max(r->a.bytes, r->c.bytes));
+    r->bytes = off;
+    return GPOEO_PD_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 int gpoeo_pd_abi_version(void) { return GPOEO_PD_ABI_VERSION; }
@@ -245,68 +396,6 @@ int gpoeo_pd_describe_plan(const gpoeo_pd_desc* desc, gpoeo_pd_plan_info* info) 
     return GPOEO_PD_OK;
 }
 
-static int detect_impl(const gpoeo_pd_desc* desc, const float* x, float* scores,
-                       gpoeo_pd_result* results, void* workspace, size_t workspace_bytes,
-                       hipStream_t stream, hipEvent_t* ev) {
-    gpoeo::Plan p;
-    const int rc = gpoeo::make_plan(desc, &p);
-    if (rc != GPOEO_PD_OK) return rc;
-    const bool scores_only = (p.flags & GPOEO_PD_SCORES_ONLY) != 0;
-    if (!x || (!results && !scores_only) || !workspace) return GPOEO_PD_EINVAL;
-    if (reinterpret_cast<uintptr_t>(workspace) % gpoeo::kAlign) return GPOEO_PD_EINVAL;
-    if (reinterpret_cast<uintptr_t>(x) % sizeof(float)) return GPOEO_PD_EINVAL;
-    if (workspace_bytes < p.bytes) return GPOEO_PD_ENOMEM;
-    p.aligned = (reinterpret_cast<uintptr_t>(x) % 16 == 0) &&
-                (p.num_windows == 1 || p.window_stride % 4 == 0) &&
-                (p.num_channels == 1 || p.channel_stride % 4 == 0);
-
-    gpoeo::Weights w;
-    for (int c = 0; c < gpoeo::kMaxChannels; ++c)
-        w.w[c] = (desc->channel_weights && c < p.num_channels) ? desc->channel_weights[c] : 1.0f;
-
-    char* ws = static_cast<char*>(workspace);
-    double* var = reinterpret_cast<double*>(ws + p.off_var);
-    double* s64 = reinterpret_cast<double*>(ws + p.off_s64);
-    const size_t words = (size_t)p.num_windows * p.bitmap_words;
-    uint32_t* bits = reinterpret_cast<uint32_t*>(ws + p.off_bits);
-    int32_t* queue = reinterpret_cast<int32_t*>(ws + p.off_queue);
-    gpoeo::SelectBuffers sb;
-    sb.tier1 = bits;
-    sb.tier2 = bits + words;
-    sb.queued1 = bits + 2 * words;
-    sb.queued2 = bits + 3 * words;
-    sb.state = reinterpret_cast<gpoeo::WinState*>(ws + p.off_state);
-    sb.q_win = queue;
-    sb.q_lag = queue + 2 * gpoeo::kQueueCap;
-    sb.q_count = queue + 4 * gpoeo::kQueueCap;
-    double* part = reinterpret_cast<double*>(ws + p.off_part);
-
-    auto mark = [&](int k) { return !ev || hipEventRecord(ev[k], stream) == hipSuccess; };
-    if (!mark(0)) return GPOEO_PD_EHIP;
-    if (!scores_only && gpoeo::launch_window_stats(p, x, var, stream) != hipSuccess)
-        return GPOEO_PD_EHIP;
-    if (!mark(1)) return GPOEO_PD_EHIP;
-    if (p.sliding) {
-        double* cut = reinterpret_cast<double*>(ws + p.off_cut);
-        if (gpoeo::launch_lag_score_blocks(p, x, part, cut, stream) != hipSuccess)
-            return GPOEO_PD_EHIP;
-        if (!mark(2)) return GPOEO_PD_EHIP;
-        if (gpoeo::launch_finalize_blocks(p, w, part, cut, s64, scores, stream) != hipSuccess)
-            return GPOEO_PD_EHIP;
-    } else {
-        if (gpoeo::launch_lag_score(p, x, part, stream) != hipSuccess) return GPOEO_PD_EHIP;
-        if (!mark(2)) return GPOEO_PD_EHIP;
-        if (gpoeo::launch_finalize(p, w, part, s64, scores, stream) != hipSuccess)
-            return GPOEO_PD_EHIP;
-    }
-    if (!mark(3)) return GPOEO_PD_EHIP;
-    if (!scores_only &&
-        gpoeo::launch_select(p, w, x, var, s64, sb, results, stream) != hipSuccess)
-        return GPOEO_PD_EHIP;
-    if (!mark(4)) return GPOEO_PD_EHIP;
-    return GPOEO_PD_OK;
-}
-
 int gpoeo_pd_detect(const gpoeo_pd_desc* desc, const float* x, float* scores,
                     gpoeo_pd_result* results, void* workspace, size_t workspace_bytes,
                     hipStream_t stream) {
@@ -321,6 +410,81 @@ int gpoeo_pd_detect_staged(const gpoeo_pd_desc* desc, const float* x, float* sco
         if (!stage_events[k]) return GPOEO_PD_EINVAL;
     return detect_impl(desc, x, scores, results, workspace, workspace_bytes, stream,
                        stage_events);
+}
+
+}  // extern "C"
+
+extern "C" {
+
+int gpoeo_pd_rolling_workspace_bytes(const gpoeo_pd_desc* desc,
+                                     const gpoeo_pd_rolling_params* params, size_t* bytes) {
+    if (!bytes) return GPOEO_PD_EINVAL;
+    RollingPlan r;
+    const int rc = make_rolling(desc, params, &r);
+    if (rc != GPOEO_PD_OK) return rc;
+    *bytes = r.bytes;
+    return GPOEO_PD_OK;
+}
+
+int gpoeo_pd_detect_rolling(const gpoeo_pd_desc* desc, const gpoeo_pd_rolling_params* params,
+                            const float* x, gpoeo_pd_rolling_result* results, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+    RollingPlan r;
+    int rc = make_rolling(desc, params, &r);
+    if (rc != GPOEO_PD_OK) return rc;
+    if (!x || !results || !workspace) return GPOEO_PD_EINVAL;
+    if (reinterpret_cast<uintptr_t>(workspace) % gpoeo::kAlign) return GPOEO_PD_EINVAL;
+    if (reinterpret_cast<uintptr_t>(x) % sizeof(float)) return GPOEO_PD_EINVAL;
+    if (workspace_bytes < r.bytes) return GPOEO_PD_ENOMEM;
+    char* ws = static_cast<char*>(workspace);
+    auto* res_a = reinterpret_cast<gpoeo_pd_result*>(ws + r.off_res_a);
+    auto* tab_off = reinterpret_cast<int64_t*>(ws + r.off_tab_off);
+    auto* tab_n = reinterpret_cast<int64_t*>(ws + r.off_tab_n);
+    auto* tab_tmax = reinterpret_cast<int32_t*>(ws + r.off_tab_tmax);
+    auto* res_c = reinterpret_cast<gpoeo_pd_result*>(ws + r.off_res_c);
+    auto* state = reinterpret_cast<gpoeo::RollState*>(ws + r.off_state);
+    void* detect_ws = ws + r.off_detect;
+    const gpoeo::Weights w = weights_of(desc, r.a.num_channels);
+
+    r.a.aligned = x_aligned(x, r.a);
+    rc = run_plan(r.a, w, x, nullptr, res_a, detect_ws, stream, nullptr);
+    if (rc != GPOEO_PD_OK) return rc;
+    if (gpoeo::launch_rolling_schedule(r.a, r.rc, res_a, tab_off, tab_n, tab_tmax, state,
+                                       stream) != hipSuccess)
+        return GPOEO_PD_EHIP;
+    r.c.table.off = tab_off;
+    r.c.table.n = tab_n;
+    r.c.table.tmax = tab_tmax;
+    r.c.aligned = false;         // suffix windows start at any sample
+    rc = run_plan(r.c, w, x, nullptr, res_c, detect_ws, stream, nullptr);
+    if (rc != GPOEO_PD_OK) return rc;
+    const Carved cv = carve(r.c, detect_ws);
+    gpoeo::RollingCombineArgs ca;
+    ca.x = x;
+    ca.res_c = res_c;
+    ca.s64 = cv.s64;
+    ca.tier1 = cv.sb.tier1;
+    ca.tier2 = cv.sb.tier2;
+    ca.wstate = cv.sb.state;
+    ca.var = cv.var;
+    ca.state = state;
+    ca.out = results;
+    ca.tab_off = tab_off;
+    ca.tab_n = tab_n;
+    ca.lags = r.c.lags;
+    ca.words = r.c.bitmap_words;
+    ca.n = r.a.n;
+    ca.window_stride = r.a.window_stride;
+    ca.channel_stride = r.a.channel_stride;
+    ca.tmin = r.a.tmin;
+    ca.num_channels = r.a.num_channels;
+    ca.jmax = r.rc.jmax;
+    const double u = 1.1102230246251565e-16;
+    ca.tau1 = 1.01 * u * ((double)r.c.n * (1.0 + 1.0 / 256.0) + 2.0 * r.c.num_channels + 22.0);
+    ca.diff_threshold = r.rc.diff_threshold;
+    if (gpoeo::launch_rolling_combine(ca, w, r.a.num_windows, stream) != hipSuccess)
+        return GPOEO_PD_EHIP;
+    return GPOEO_PD_OK;
 }
 
 }  // extern "C"

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "gpoeo_pd.h"
+
 namespace gpoeo {
 
 constexpr int kWave = 64;            // CDNA wavefront width
@@ -19,6 +21,26 @@ constexpr double kScoreRelBound = 2.5e-5;
 struct Weights {
     float w[kMaxChannels];
 };
+
+// Optional per-window table (device arrays) for batches of windows of
+// different lengths: window b starts at off[b] (channel 0), has n[b] samples
+// (0: an empty slot) and lags up to tmax[b].  Null pointers: window b starts at
+// b * window_stride with the descriptor's N and Tmax.
+struct WindowTable {
+    const int64_t* off;
+    const int64_t* n;
+    const int32_t* tmax;
+};
+
+__device__ __forceinline__ int64_t table_off(const WindowTable& t, int64_t b, int64_t stride) {
+    return t.off ? t.off[b] : b * stride;
+}
+__device__ __forceinline__ int64_t table_n(const WindowTable& t, int64_t b, int64_t n) {
+    return t.n ? t.n[b] : n;
+}
+__device__ __forceinline__ int32_t table_tmax(const WindowTable& t, int64_t b, int32_t tmax) {
+    return t.tmax ? t.tmax[b] : tmax;
+}
 
 // Selection passes (with one re-score round between consecutive passes) and the
 // capacity of each re-score queue (per tier, per round, all windows together).
@@ -78,9 +100,49 @@ struct Plan {
     int64_t block_tasks;     // waves of each of the two block-partial launches
     double c_lag, err_max;
     uint32_t flags;
+    WindowTable table;       // per-window offsets / lengths / Tmax, or all null
     int32_t bitmap_words;    // 32-bit words per window of the exactness bitmap
     // workspace layout (byte offsets, 256-byte aligned)
     size_t off_var, off_s64, off_bits, off_state, off_queue, off_part, off_cut, bytes;
+};
+
+// Rolling detection (Algorithm 3).
+struct RollingConfig {
+    double c_measure, step, c_eval, diff_threshold;
+    int32_t jmax;            // suffix-window slots per window
+};
+
+struct RollState {           // per window, between the schedule and the combination
+    double err_a;            // err of the whole-window pass
+    double short_next;       // next sampling duration when too short
+    int32_t t_init;
+    int32_t verdict_a;
+    int32_t count;           // suffix windows scheduled
+    uint32_t flags;
+};
+
+struct RollingCombineArgs {
+    const float* x;
+    const gpoeo_pd_result* res_c;   // [B * jmax] results of the suffix pass
+    const double* s64;       // suffix pass workspace: scores, tiers, states, variances
+    const uint32_t* tier1;
+    const uint32_t* tier2;
+    const WinState* wstate;
+    const double* var;
+    const RollState* state;
+    gpoeo_pd_rolling_result* out;   // [B]
+    const int64_t* tab_off;
+    const int64_t* tab_n;
+    int64_t lags;
+    int64_t words;
+    int64_t n;
+    int64_t window_stride;
+    int64_t channel_stride;
+    int32_t tmin;
+    int32_t num_channels;
+    int32_t jmax;
+    double tau1;
+    double diff_threshold;
 };
 
 // Kernel launchers; each returns hipGetLastError() after enqueueing.
@@ -97,5 +159,10 @@ hipError_t launch_finalize(const Plan& p, const Weights& w, const double* part, 
                            float* scores, hipStream_t s);
 hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const double* var,
                          double* s64, const SelectBuffers& sb, void* results, hipStream_t s);
+hipError_t launch_rolling_schedule(const Plan& p, const RollingConfig& rc,
+                                   const gpoeo_pd_result* res_a, int64_t* tab_off, int64_t* tab_n,
+                                   int32_t* tab_tmax, RollState* state, hipStream_t s);
+hipError_t launch_rolling_combine(const RollingCombineArgs& a, const Weights& w,
+                                  int64_t num_windows, hipStream_t s);
 
 }  // namespace gpoeo

@@ -43,6 +43,7 @@ struct ScoreArgs {
     int32_t lag_blocks;
     int32_t lags_padded;
     int32_t chunks;
+    WindowTable tab;
 };
 
 // Lane window y[k] = x[i + T_l + k], k < kW = 16 + kBT - 1 (rounded up to a
@@ -132,13 +133,14 @@ __global__ __launch_bounds__(kWave * kWavesPerGroup) void lag_score_kernel(Score
     const int64_t b = bc / a.num_channels;
     const int32_t c = (int32_t)(bc % a.num_channels);
 
-    const float* __restrict__ xw = a.x + b * a.window_stride + (int64_t)c * a.channel_stride;
+    const float* __restrict__ xw =
+        a.x + table_off(a.tab, b, a.window_stride) + (int64_t)c * a.channel_stride;
     const int64_t t_wave = (int64_t)a.t0 + (int64_t)blk * kLagsPerBlock;
     const int64_t t_lane = t_wave + (int64_t)lane * kBT;
     // Pair bound of this wave (wave-uniform): the window length, or for the
     // shared block partials of overlapping windows the trace end and, for the
     // cut partials, the end of the block the lags' ranges stop in.
-    int64_t n = a.n;
+    int64_t n = table_n(a.tab, b, a.n);
     if (a.trace_len > 0) n = min(n, a.trace_len - b * a.window_stride);
     if (a.cut > 0) n = min(n, ((t_wave - 1) / a.cut + 1) * a.cut);
 
@@ -248,6 +250,7 @@ ScoreArgs common(const Plan& p, const float* x) {
     a.lag_blocks = p.lag_blocks;
     a.lags_padded = p.lags_padded;
     a.chunks = p.chunks;
+    a.tab = p.table;
     return a;
 }
 

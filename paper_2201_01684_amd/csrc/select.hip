@@ -33,10 +33,16 @@
 // between consecutive ones; a window still open in the last pass is decided
 // on the unwidened values and flagged GPOEO_PD_UNRESOLVED.
 #include "internal.h"
+#include "exact.h"
 #include "gpoeo_pd.h"
 
 namespace gpoeo {
 namespace {
+
+using exact::exact_reference;
+using exact::exact_score;
+using exact::reference_bound;
+using exact::wave_score;
 
 constexpr int kThreads = 256;
 constexpr int kRescoreGroups = 1024;   // workgroups of one re-score round
@@ -63,6 +69,7 @@ struct SelectArgs {
     uint32_t flags;
     int32_t pass;
     int32_t last;
+    WindowTable tab;
 };
 
 enum Tri : int { kNo = 0, kYes = 1, kUnk = 2 };
@@ -81,88 +88,6 @@ __device__ __forceinline__ Tri le(const Iv& a, const Iv& b) {
     if (a.hi <= b.lo) return kYes;
     if (a.lo > b.hi) return kNo;
     return kUnk;
-}
-
-// The exact re-scores below are plain sequential fp64 sums (ascending index,
-// one rounding per addition, no contraction).  Their cost is a chain of
-// dependent additions; to keep it from also waiting on memory at every step,
-// samples are staged through registers in chunks of kChunk and the loads of
-// the next chunk are issued before the additions of the current one.
-constexpr int kChunk = 32;
-
-template <typename F>
-__device__ __forceinline__ void for_pairs(const float* __restrict__ a, const float* __restrict__ b,
-                                          int64_t m, F&& step) {
-    float ca[kChunk], cb[kChunk], na[kChunk], nb[kChunk];
-    const int64_t full = m / kChunk;
-    if (full > 0) {
-#pragma unroll
-        for (int k = 0; k < kChunk; ++k) {
-            ca[k] = a[k];
-            cb[k] = b[k];
-        }
-    }
-    for (int64_t c = 0; c < full; ++c) {
-        const bool more = c + 1 < full;
-        if (more) {
-            const int64_t o = (c + 1) * kChunk;
-#pragma unroll
-            for (int k = 0; k < kChunk; ++k) {
-                na[k] = a[o + k];
-                nb[k] = b[o + k];
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < kChunk; ++k) step(ca[k], cb[k]);
-        if (more) {
-#pragma unroll
-            for (int k = 0; k < kChunk; ++k) {
-                ca[k] = na[k];
-                cb[k] = nb[k];
-            }
-        }
-    }
-    for (int64_t i = full * kChunk; i < m; ++i) step(a[i], b[i]);
-}
-
-// Plain sequential fp64 evaluation of S(T) = sum_c w_c * D_c(T) / (N - T).
-__device__ double exact_score(const float* __restrict__ xw, int32_t num_channels,
-                              int64_t channel_stride, int64_t n, int64_t t, const Weights& w) {
-#pragma clang fp contract(off)
-    double s = 0.0;
-    for (int32_t c = 0; c < num_channels; ++c) {
-        const float* __restrict__ xc = xw + (int64_t)c * channel_stride;
-        const int64_t m = n - t;
-        double dsum = 0.0;
-        for_pairs(xc, xc + t, m, [&](float u, float v) {
-#pragma clang fp contract(off)
-            const double d = (double)u - (double)v;
-            dsum = dsum + d * d;
-        });
-        s = s + (double)w.w[c] * (dsum / (double)m);
-    }
-    return s;
-}
-
-// Plain sequential fp64 evaluation of R = 2 * sum_c w_c * Var_c (two passes).
-__device__ double exact_reference(const float* __restrict__ xw, int32_t num_channels,
-                                  int64_t channel_stride, int64_t n, const Weights& w) {
-#pragma clang fp contract(off)
-    double acc = 0.0;
-    for (int32_t c = 0; c < num_channels; ++c) {
-        const float* __restrict__ xc = xw + (int64_t)c * channel_stride;
-        double sum = 0.0;
-        for_pairs(xc, xc, n, [&](float u, float) { sum = sum + (double)u; });
-        const double mean = sum / (double)n;
-        double sq = 0.0;
-        for_pairs(xc, xc, n, [&](float u, float) {
-#pragma clang fp contract(off)
-            const double d = (double)u - mean;
-            sq = sq + d * d;
-        });
-        acc = acc + (double)w.w[c] * (sq / (double)n);
-    }
-    return 2.0 * acc;
 }
 
 __device__ double block_min_d(double v, double* red) {
@@ -202,62 +127,6 @@ __device__ int64_t block_min_i(int64_t v, int64_t* red) {
 }
 
 
-// Tier-1 re-score: S(T) in fp64 by one wavefront.  Lane l accumulates the
-// terms i = l + 64 (4k + r) in four partial sums r = 0..3, which are combined
-// as (p0 + p1) + (p2 + p3) and then across lanes by a fixed shuffle tree; every
-// lane returns lane 0's value.  Each partial sum holds at most M/256 + 1 terms,
-// so the result is within (M/256 + 10) u of the exact sum (u = 2^-53).
-__device__ double wave_score(const float* __restrict__ xw, int32_t num_channels,
-                             int64_t channel_stride, int64_t n, int64_t t, const Weights& w,
-                             int lane) {
-    double s = 0.0;
-    for (int32_t c = 0; c < num_channels; ++c) {
-        const float* __restrict__ xc = xw + (int64_t)c * channel_stride;
-        const int64_t m = n - t;
-        double p[4] = {0.0, 0.0, 0.0, 0.0};
-        int64_t i = lane;
-        for (; i + 192 < m; i += 256) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const double d = (double)xc[i + 64 * r] - (double)xc[i + 64 * r + t];
-                p[r] = p[r] + d * d;
-            }
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int64_t k = i + 64 * r;
-            if (k < m) {
-                const double d = (double)xc[k] - (double)xc[k + t];
-                p[r] = p[r] + d * d;
-            }
-        }
-        double part = (p[0] + p[1]) + (p[2] + p[3]);
-        for (int off = 32; off > 0; off >>= 1) part = part + __shfl_down(part, off);
-        part = __shfl(part, 0);
-        s = s + (double)w.w[c] * (part / (double)m);
-    }
-    return s;
-}
-
-// Half-width of the interval around the two-pass fp64 R that contains the
-// plain sequential evaluation.  Any evaluation order of the mean of N samples
-// errs by at most (N+1) u A (A = mean |x|); the second pass then sums
-// Var + dmean^2 exactly, up to (N+4) u relative.  Two orders thus differ by at
-// most 4 (N+4) u Var + 4.02 ((N+1) u A)^2 per channel, weighted and doubled
-// for R, plus the rounding of the weighted channel sum.
-__device__ double reference_bound(const double* var2, int32_t num_channels, int64_t n,
-                                  const Weights& w, double r) {
-    const double u = 1.1102230246251565e-16;
-    const double nn = (double)n;
-    double e = 0.0;
-    for (int32_t c = 0; c < num_channels; ++c) {
-        const double v = var2[2 * c], am = var2[2 * c + 1];
-        const double dm = (nn + 1.0) * u * am;
-        e += (double)w.w[c] * (4.0 * (nn + 4.0) * u * v + 4.02 * dm * dm);
-    }
-    return 1.01 * (2.0 * e + (num_channels + 4.0) * u * r);
-}
-
 struct Shared {
     double red_d[kThreads];
     double red_d2[kThreads];
@@ -272,7 +141,9 @@ __global__ __launch_bounds__(kThreads) void select_pass_kernel(SelectArgs a, Wei
     __shared__ Shared sh;
     const int tid = threadIdx.x;
     const int64_t b = blockIdx.x;
-    const int32_t tmin = a.tmin, tmax = a.tmax;
+    const int32_t tmin = a.tmin;
+    const int32_t tmax = table_tmax(a.tab, b, a.tmax);   // this window's lag range and length
+    const int64_t n = table_n(a.tab, b, a.n);
     double* __restrict__ s = a.s64 + b * (int64_t)a.lags;
     uint32_t* __restrict__ t1 = a.tier1 + b * (int64_t)a.words;
     uint32_t* __restrict__ t2 = a.tier2 + b * (int64_t)a.words;
@@ -303,10 +174,20 @@ __global__ __launch_bounds__(kThreads) void select_pass_kernel(SelectArgs a, Wei
         double acc = 0.0;
         for (int32_t c = 0; c < a.num_channels; ++c) acc = acc + (double)w.w[c] * v2[2 * c];
         sh.r_approx = 2.0 * acc;
-        sh.r_err = reference_bound(v2, a.num_channels, a.n, w, sh.r_approx);
+        sh.r_err = reference_bound(v2, a.num_channels, n, w, sh.r_approx);
     }
     __syncthreads();
     if (sh.done) return;
+    if (n == 0 || tmax < tmin + 2) {   // empty or too short a slot of a window table
+        if (tid == 0) {
+            gpoeo_pd_result o = {};
+            o.verdict = GPOEO_PD_APERIODIC;
+            o.flags = GPOEO_PD_SHORT;
+            *res = o;
+            st->done = 1;
+        }
+        return;
+    }
     const double r_approx = sh.r_approx;
     const double r_err = sh.r_err;
     if (r_approx == 0.0) {   // every weighted channel constant (exact: see window_stats)
@@ -470,7 +351,7 @@ __global__ __launch_bounds__(kThreads) void select_pass_kernel(SelectArgs a, Wei
         }
         o.t_cand = (int32_t)tc;
         // 3. local search window
-        const int64_t d = a.n - 1;
+        const int64_t d = n - 1;
         int64_t lo = (tc * d + (d + tc) - 1) / (d + tc);
         int64_t hi = (tc * d) / (d - tc);
         lo = max(lo, (int64_t)tmin);
@@ -565,8 +446,9 @@ __global__ __launch_bounds__(kThreads) void rescore_kernel(SelectArgs a, Weights
         const int64_t j = t - a.tmin;
         uint32_t* t1 = a.tier1 + b * (int64_t)a.words;
         if ((t1[j >> 5] >> (j & 31)) & 1u) continue;
-        const float* __restrict__ xw = a.x + b * a.window_stride;
-        const double v = wave_score(xw, a.num_channels, a.channel_stride, a.n, t, w, lane);
+        const float* __restrict__ xw = a.x + table_off(a.tab, b, a.window_stride);
+        const double v =
+            wave_score(xw, a.num_channels, a.channel_stride, table_n(a.tab, b, a.n), t, w, lane);
         if (lane == 0) {
             a.s64[b * (int64_t)a.lags + j] = v;
             __threadfence();
@@ -578,10 +460,11 @@ __global__ __launch_bounds__(kThreads) void rescore_kernel(SelectArgs a, Weights
     for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < n2; e += lanes) {
         const int64_t b = a.q_win[kQueueCap + e];
         const int64_t t = a.q_lag[kQueueCap + e];
-        const float* __restrict__ xw = a.x + b * a.window_stride;
+        const float* __restrict__ xw = a.x + table_off(a.tab, b, a.window_stride);
+        const int64_t n = table_n(a.tab, b, a.n);
         if (t < 0) {
             WinState* st = a.state + b;
-            st->r_exact = exact_reference(xw, a.num_channels, a.channel_stride, a.n, w);
+            st->r_exact = exact_reference(xw, a.num_channels, a.channel_stride, n, w);
             __threadfence();
             st->r_is_exact = 1;
             continue;
@@ -589,8 +472,7 @@ __global__ __launch_bounds__(kThreads) void rescore_kernel(SelectArgs a, Weights
         const int64_t j = t - a.tmin;
         uint32_t* t2 = a.tier2 + b * (int64_t)a.words;
         if ((t2[j >> 5] >> (j & 31)) & 1u) continue;
-        a.s64[b * (int64_t)a.lags + j] =
-            exact_score(xw, a.num_channels, a.channel_stride, a.n, t, w);
+        a.s64[b * (int64_t)a.lags + j] = exact_score(xw, a.num_channels, a.channel_stride, n, t, w);
         __threadfence();
         atomicOr(&t2[j >> 5], 1u << (j & 31));
     }
@@ -628,6 +510,7 @@ hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const 
     a.c_lag = p.c_lag;
     a.err_max = p.err_max;
     a.flags = p.flags;
+    a.tab = p.table;
     // Tier-1 half-width: the sequential sum (at most n + C + 6 roundings of
     // u = 2^-53 each, relative to the exact value) plus the wavefront sum
     // (n/256 + C + 16 roundings), with 1% margin.

@@ -31,13 +31,19 @@ __device__ double block_sum(double v, double* red) {
 }
 
 __global__ __launch_bounds__(kStatsThreads) void window_stats_kernel(
-    const float* __restrict__ x, double* __restrict__ var, int64_t n, int64_t window_stride,
-    int64_t channel_stride, int32_t num_channels) {
+    const float* __restrict__ x, double* __restrict__ var, int64_t n_all, int64_t window_stride,
+    int64_t channel_stride, int32_t num_channels, WindowTable tab) {
     __shared__ double red[kStatsThreads];
     const int64_t bc = blockIdx.x;
     const int64_t b = bc / num_channels;
     const int32_t c = (int32_t)(bc % num_channels);
-    const float* __restrict__ xw = x + b * window_stride + (int64_t)c * channel_stride;
+    const int64_t n = table_n(tab, b, n_all);
+    if (n == 0) {   // empty slot of a window table
+        if (threadIdx.x == 0) var[2 * bc] = var[2 * bc + 1] = 0.0;
+        return;
+    }
+    const float* __restrict__ xw =
+        x + table_off(tab, b, window_stride) + (int64_t)c * channel_stride;
     double s = 0.0, sa = 0.0;
     for (int64_t i = threadIdx.x; i < n; i += kStatsThreads) {
         const double v = (double)xw[i];
@@ -62,15 +68,21 @@ __global__ __launch_bounds__(256) void finalize_kernel(const double* __restrict_
                                                        double* __restrict__ s64,
                                                        float* __restrict__ scores, Weights w,
                                                        int64_t num_windows, int32_t num_channels,
-                                                       int64_t n, int32_t tmin, int32_t lags,
+                                                       int64_t n_all, int32_t tmin, int32_t lags,
                                                        int32_t t0, int32_t lags_padded,
-                                                       int32_t chunks) {
+                                                       int32_t chunks, WindowTable tab) {
     const int64_t total = num_windows * (int64_t)lags;
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total;
          e += (int64_t)gridDim.x * blockDim.x) {
         const int64_t b = e / lags;
         const int32_t j = (int32_t)(e % lags);
         const int64_t t = (int64_t)tmin + j;
+        const int64_t n = table_n(tab, b, n_all);
+        if (t > table_tmax(tab, b, tmin + lags - 1) || n == 0) {   // outside this window's range
+            s64[e] = 0.0;
+            if (scores) scores[e] = 0.0f;
+            continue;
+        }
         double s = 0.0;
         for (int32_t c = 0; c < num_channels; ++c) {
             const double* p = part + ((b * num_channels + c) * chunks) * (int64_t)lags_padded +
@@ -135,7 +147,7 @@ hipError_t launch_finalize_blocks(const Plan& p, const Weights& w, const double*
 hipError_t launch_window_stats(const Plan& p, const float* x, double* var, hipStream_t s) {
     const int64_t groups = p.num_windows * p.num_channels;
     hipLaunchKernelGGL(window_stats_kernel, dim3((unsigned)groups), dim3(kStatsThreads), 0, s, x,
-                       var, p.n, p.window_stride, p.channel_stride, p.num_channels);
+                       var, p.n, p.window_stride, p.channel_stride, p.num_channels, p.table);
     return hipGetLastError();
 }
 
@@ -146,7 +158,7 @@ hipError_t launch_finalize(const Plan& p, const Weights& w, const double* part, 
     if (groups > 65536) groups = 65536;
     hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)groups), dim3(256), 0, s, part, s64,
                        scores, w, p.num_windows, p.num_channels, p.n, p.tmin, p.lags, p.t0,
-                       p.lags_padded, p.chunks);
+                       p.lags_padded, p.chunks, p.table);
     return hipGetLastError();
 }
 

@@ -53,9 +53,12 @@ def test_struct_layout_matches_header(tmp_path):
 #include <stddef.h>
 #include "gpoeo_pd.h"
 int main(void) {
-  printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(gpoeo_pd_desc), offsetof(gpoeo_pd_desc, c_lag),
-         offsetof(gpoeo_pd_desc, channel_weights), offsetof(gpoeo_pd_desc, flags),
-         sizeof(gpoeo_pd_result), offsetof(gpoeo_pd_result, n_rescored));
+  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(gpoeo_pd_desc),
+         offsetof(gpoeo_pd_desc, c_lag), offsetof(gpoeo_pd_desc, channel_weights),
+         offsetof(gpoeo_pd_desc, flags), sizeof(gpoeo_pd_result),
+         offsetof(gpoeo_pd_result, n_rescored), sizeof(gpoeo_pd_rolling_result),
+         offsetof(gpoeo_pd_rolling_result, smpdur_next), offsetof(gpoeo_pd_rolling_result, starts),
+         sizeof(gpoeo_pd_plan_info));
   return 0;
 }
 """)
@@ -65,7 +68,9 @@ int main(void) {
     got = list(map(int, subprocess.run([str(exe)], capture_output=True, text=True,
                                        check=True).stdout.split()))
     want = [ctypes.sizeof(B.Desc), B.Desc.c_lag.offset, B.Desc.channel_weights.offset,
-            B.Desc.flags.offset, ctypes.sizeof(B.Result), B.Result.n_rescored.offset]
+            B.Desc.flags.offset, ctypes.sizeof(B.Result), B.Result.n_rescored.offset,
+            ctypes.sizeof(B.RollingResult), B.RollingResult.smpdur_next.offset,
+            B.RollingResult.starts.offset, ctypes.sizeof(B.PlanInfo)]
     assert got == want
 
 
@@ -157,3 +162,30 @@ def test_plan_description(lib):
     assert info["mode"] == 0 and info["pairs_scored"] == info["pairs_defined"]
     assert info["pairs_defined"] == 4 * 2 * sum(4096 - t for t in range(2, 1025))
     assert info["lags_per_lane"] in (8, 16)
+
+
+@pytest.mark.parametrize("kw", [dict(c_measure=0.0), dict(step=0.0), dict(c_eval=-1.0),
+                                dict(diff_threshold=float("nan")), dict(c_eval=100.0),
+                                dict(step=float("inf"))])
+def test_rolling_parameters_validated(lib, kw):
+    d, _ = good_desc()
+    with pytest.raises(B.GpoeoError) as e:
+        B.rolling_workspace_bytes(d, B.rolling_params(**kw))
+    assert e.value.status == B.EINVAL
+
+
+def test_rolling_workspace_and_flags(lib):
+    d, _ = good_desc()
+    assert B.rolling_workspace_bytes(d, B.rolling_params()) > B.workspace_bytes(d)
+    d, _ = good_desc(flags=B.SCORES_ONLY)
+    with pytest.raises(B.GpoeoError):
+        B.rolling_workspace_bytes(d, B.rolling_params())
+    d, _ = good_desc()
+    p = B.rolling_params()
+    need = B.rolling_workspace_bytes(d, p)
+    call = lib.gpoeo_pd_detect_rolling
+    assert call(ctypes.byref(d), ctypes.byref(p), 0x100000, 0x200000, 0x300000, need - 1,
+                None) == B.ENOMEM
+    assert call(ctypes.byref(d), None, 0x100000, 0x200000, 0x300000, need, None) == B.EINVAL
+    assert call(ctypes.byref(d), ctypes.byref(p), 0x100000, None, 0x300000, need,
+                None) == B.EINVAL
