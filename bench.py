@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--mode", choices=("detect", "rolling"), default="detect",
+                    help="detect: gpoeo_pd_detect (the default measurement); rolling: "
+                         "Algorithm 3's rolling detection, gpoeo_pd_detect_rolling")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a device-to-device copy of this many MiB (the reference "
                          "kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -131,6 +134,9 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": nbytes, "launches": 3}), flush=True)
         return
+
+    if args.mode == "rolling":
+        return bench_rolling(args)
 
     t_gen = time.perf_counter()
     wl = make_workload(args.workload)
@@ -239,6 +245,68 @@ def main():
                                           f"{wl.lags} lags each, {t_cpu:.1f} s"}
         line["parity_sample"] = {"windows": done, "period_match": match,
                                  "max_score_rel_err": worst}
+    print(json.dumps(line), flush=True)
+
+
+def bench_rolling(args):
+    """Rolling detection (Algorithm 3) over the workload's windows: one step is one
+    gpoeo_pd_detect_rolling call (whole-window pass, suffix schedule, suffix pass,
+    combination)."""
+    import numpy as np
+    import torch
+
+    import paper_2201_01684_amd as pkg
+    from gen import make_workload
+
+    wl = make_workload(args.workload)
+    x = torch.from_numpy(wl.x).to("cuda:0")
+    desc, keep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
+                               wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights)
+    params = pkg.rolling_params()
+    det = pkg.RollingDetector(x, desc, params, keep)
+    for _ in range(args.warmup):
+        det.run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        det.run()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    res = det.results_numpy()
+    line = {
+        "metric": "rolling detections/sec (Algorithm 3 over every window of the batch)",
+        "value": wl.num_windows / (ms / 1e3), "unit": "windows/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "description": wl.meta["description"],
+                   "windows": wl.num_windows, "channels": wl.num_channels, "n": wl.n,
+                   "tmin": wl.tmin, "tmax": wl.tmax, "sha256": wl.sha256,
+                   "c_measure": params.c_measure, "step": params.step, "c_eval": params.c_eval,
+                   "diff_threshold": params.diff_threshold},
+        "stable_windows": int(np.count_nonzero(res["stable"])),
+        "mean_suffix_windows": float(res["n_windows"].mean()),
+        "windows_flagged_unresolved": int(np.count_nonzero(res["flags"])),
+        "roofline": None,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        lay1 = oracle.Layout.of(wl, num_windows=1)
+        span = (wl.num_channels - 1) * wl.channel_stride + wl.n
+        done, t_cpu, match = 0, 0.0, 0
+        while done < wl.num_windows and (done == 0 or t_cpu < args.cpu_seconds):
+            sub = wl.x[done * wl.window_stride: done * wl.window_stride + span]
+            t = time.perf_counter()
+            o = oracle.rolling(sub, lay1)[0]
+            t_cpu += time.perf_counter() - t
+            g = res[done]
+            match += int(o["period"] == g["period"] and o["stable"] == g["stable"]
+                         and o["smpdur_next"] == g["smpdur_next"])
+            done += 1
+        line["cpu_baseline"] = {"value": done / t_cpu, "unit": "windows/s",
+                                "cores": oracle.threads(), "kind": "oracle",
+                                "sample": f"first {done} of {wl.num_windows} windows, {t_cpu:.1f} s"}
+        line["parity_sample"] = {"windows": done, "period_stable_next_match": match}
     print(json.dumps(line), flush=True)
 
 
