@@ -57,6 +57,10 @@ class _Out(ctypes.Structure):
 ROLLING_MAX = 32
 
 
+class _SimilarityParams(ctypes.Structure):
+    _fields_ = [("num_groups", ctypes.c_int32), ("em_iters", ctypes.c_int32)]
+
+
 class _RollingParams(ctypes.Structure):
     _fields_ = [("c_measure", ctypes.c_double), ("step", ctypes.c_double),
                 ("c_eval", ctypes.c_double), ("diff_threshold", ctypes.c_double)]
@@ -108,6 +112,10 @@ def _load():
         lib.oracle_pd_rolling_schedule.argtypes = [ctypes.c_int64, ctypes.c_int32,
                                                    P(_RollingParams), ctypes.c_void_p,
                                                    ctypes.c_int32, P(ctypes.c_double)]
+        lib.oracle_pd_similarity.restype = ctypes.c_int
+        lib.oracle_pd_similarity.argtypes = [P(_Params), P(_SimilarityParams), ctypes.c_void_p,
+                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                             ctypes.c_void_p]
         lib.oracle_pd_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -265,3 +273,27 @@ def rolling_schedule(n: int, t_init: int, c_measure: float = C_MEASURE, step: fl
     if k < 0:
         raise ValueError("schedule longer than the oracle's limit")
     return starts[:k].tolist(), nxt.value
+
+
+# Algorithm 2's group count and EM iterations are not given by the paper.
+DEFAULT_GROUPS, DEFAULT_EM_ITERS = 3, 20
+
+
+def similarity(x: np.ndarray, lay: Layout, windows, lags, num_groups: int = DEFAULT_GROUPS,
+               em_iters: int = DEFAULT_EM_ITERS) -> np.ndarray:
+    """Algorithm 2's Err_T for the given (window, lag) pairs (-1: fewer than two sub-curves)."""
+    x = _as_f32(x)
+    _check_extent(x, lay)
+    w = np.ascontiguousarray(windows, dtype=np.int64)
+    t = np.ascontiguousarray(lags, dtype=np.int32)
+    if w.shape != t.shape:
+        raise ValueError("windows and lags differ in length")
+    keep: list = []
+    p = _params(lay, keep)
+    sp = _SimilarityParams(int(num_groups), int(em_iters))
+    out = np.empty(w.shape, dtype=np.float64)
+    rc = _load().oracle_pd_similarity(ctypes.byref(p), ctypes.byref(sp), x.ctypes.data,
+                                      w.ctypes.data, t.ctypes.data, int(w.size), out.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle rejected the parameters")
+    return out

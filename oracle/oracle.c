@@ -283,4 +283,157 @@ int oracle_pd_rolling(const oracle_pd_params* p, const oracle_pd_rolling_params*
     return rc;
 }
 
+/* SMAPE of two relative group values; 0 / 0 := 0. */
+static double smape(double a, double b) {
+    const double den = (fabs(a) + fabs(b)) / 2.0;
+    if (den == 0.0) return 0.0;
+    return fabs(a - b) / den;
+}
+
+/* Hard group index of every sample of v[0..m-1] (1-D GMM, EM, see oracle.h). */
+static void gmm_groups(const double* v, int64_t m, int32_t g, int32_t iters, int32_t* group,
+                       double* resp /* m * g scratch */) {
+    double lo = v[0], hi = v[0];
+    for (int64_t i = 1; i < m; ++i) {
+        if (v[i] < lo) lo = v[i];
+        if (v[i] > hi) hi = v[i];
+    }
+    if (hi == lo) {
+        for (int64_t i = 0; i < m; ++i) group[i] = 0;
+        return;
+    }
+    double mu[64], var[64], pi[64];
+    const double width = (hi - lo) / (double)g;
+    const double floor_var = 1e-6 * width * width;
+    for (int32_t k = 0; k < g; ++k) {
+        mu[k] = lo + ((double)k + 0.5) * width;
+        var[k] = width * width;
+        pi[k] = 1.0 / (double)g;
+    }
+    const double two_pi = 6.283185307179586;
+    for (int32_t it = 0; it < iters; ++it) {
+        /* E step: responsibilities from log densities, normalised per sample */
+        for (int64_t i = 0; i < m; ++i) {
+            double* r = resp + i * g;
+            double best = -INFINITY;
+            for (int32_t k = 0; k < g; ++k) {
+                const double d = v[i] - mu[k];
+                r[k] = log(pi[k]) - 0.5 * log(two_pi * var[k]) - d * d / (2.0 * var[k]);
+                if (r[k] > best) best = r[k];
+            }
+            double sum = 0.0;
+            for (int32_t k = 0; k < g; ++k) {
+                r[k] = exp(r[k] - best);
+                sum += r[k];
+            }
+            for (int32_t k = 0; k < g; ++k) r[k] /= sum;
+        }
+        /* M step */
+        for (int32_t k = 0; k < g; ++k) {
+            double nk = 0.0, s1 = 0.0;
+            for (int64_t i = 0; i < m; ++i) {
+                nk += resp[i * g + k];
+                s1 += resp[i * g + k] * v[i];
+            }
+            if (!(nk > 0.0)) continue;
+            const double mk = s1 / nk;
+            double s2 = 0.0;
+            for (int64_t i = 0; i < m; ++i) {
+                const double d = v[i] - mk;
+                s2 += resp[i * g + k] * d * d;
+            }
+            mu[k] = mk;
+            var[k] = s2 / nk;
+            if (var[k] < floor_var) var[k] = floor_var;
+            pi[k] = nk / (double)m;
+        }
+    }
+    /* hard assignment: the most responsible component (lower index on ties) */
+    for (int64_t i = 0; i < m; ++i) {
+        int32_t arg = 0;
+        double best = -INFINITY;
+        for (int32_t k = 0; k < g; ++k) {
+            const double d = v[i] - mu[k];
+            const double lk = log(pi[k]) - 0.5 * log(two_pi * var[k]) - d * d / (2.0 * var[k]);
+            if (lk > best) {
+                best = lk;
+                arg = k;
+            }
+        }
+        group[i] = arg;
+    }
+}
+
+/* Err_T of one channel of one window (Algorithm 2). */
+static double similarity_one(const float* xc, int64_t n, int64_t t, int32_t g, int32_t iters) {
+    const int64_t num_t = n / t;
+    if (num_t < 2) return -1.0;
+    double* a = (double*)malloc((size_t)t * sizeof(double));
+    double* b = (double*)malloc((size_t)t * sizeof(double));
+    int32_t* grp = (int32_t*)malloc((size_t)t * sizeof(int32_t));
+    double* resp = (double*)malloc((size_t)t * (size_t)g * sizeof(double));
+    if (!a || !b || !grp || !resp) {
+        free(a); free(b); free(grp); free(resp);
+        return -2.0;
+    }
+    double total = 0.0;
+    for (int64_t i = 0; i + 1 < num_t; ++i) {
+        double mean_prev = 0.0, mean_back = 0.0;
+        for (int64_t j = 0; j < t; ++j) {
+            a[j] = (double)xc[i * t + j];
+            b[j] = (double)xc[(i + 1) * t + j];
+            mean_prev += a[j];
+            mean_back += b[j];
+        }
+        mean_prev /= (double)t;
+        mean_back /= (double)t;
+        gmm_groups(a, t, g, iters, grp, resp);
+        double err = 0.0;
+        for (int32_t k = 0; k < g; ++k) {
+            double sa = 0.0, sb = 0.0;
+            int64_t cnt = 0;
+            for (int64_t j = 0; j < t; ++j) {
+                if (grp[j] != k) continue;
+                sa += a[j];
+                sb += b[j];
+                ++cnt;
+            }
+            if (cnt == 0) continue;
+            const double rel_prev = sa / (double)cnt - mean_prev;
+            const double rel_back = sb / (double)cnt - mean_back;
+            err += (double)cnt * smape(rel_prev, rel_back);
+        }
+        total += err / (double)t;
+    }
+    free(a); free(b); free(grp); free(resp);
+    return total / (double)(num_t - 1);
+}
+
+int oracle_pd_similarity(const oracle_pd_params* p, const oracle_pd_similarity_params* sp,
+                         const float* x, const int64_t* w, const int32_t* t, int64_t count,
+                         double* err_out) {
+    if (check_params(p) || !sp || !x || (count > 0 && (!w || !t || !err_out))) return -1;
+    if (sp->num_groups < 1 || sp->num_groups > 64 || sp->em_iters < 0) return -1;
+    for (int64_t k = 0; k < count; ++k)
+        if (w[k] < 0 || w[k] >= p->num_windows || t[k] < 1 || (int64_t)t[k] > p->n) return -1;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
+    for (int64_t k = 0; k < count; ++k) {
+        const float* xw = x + w[k] * p->window_stride;
+        double wsum = 0.0, acc = 0.0;
+        int undefined = 0;
+        for (int32_t c = 0; c < p->num_channels; ++c) {
+            const double e = similarity_one(xw + (int64_t)c * p->channel_stride, p->n, t[k],
+                                            sp->num_groups, sp->em_iters);
+            if (e == -2.0) bad = 1;
+            if (e < 0.0) undefined = 1;
+            const double wc = weight_of(p->channel_weights, c);
+            acc += wc * e;
+            wsum += wc;
+        }
+        err_out[k] = undefined ? -1.0 : acc / wsum;
+    }
+    return bad ? -1 : 0;
+}
+
 int oracle_pd_threads(void) { return omp_get_max_threads(); }

@@ -150,6 +150,35 @@ int32_t oracle_pd_rolling_schedule(int64_t n, int32_t t_init, const oracle_pd_ro
 int oracle_pd_rolling(const oracle_pd_params* p, const oracle_pd_rolling_params* rp,
                       const float* x, oracle_pd_rolling_out* out);
 
+/* Algorithm 2 (Sec. 4.1.2): feature sequence similarity error Err_T.
+ *
+ *   sub-curves  Smp_i = x[(i-1) T .. i T - 1], i = 1 .. Num_T = floor(N / T)
+ *   for each adjacent pair (Smp_i, Smp_{i+1}), per channel:
+ *     groups    a 1-D Gaussian mixture of num_groups components fitted to the
+ *               values of Smp_i by em_iters EM iterations (fp64), then every
+ *               sample assigned to its most responsible component (ties: the
+ *               lower index).  Initialisation: means evenly spaced at
+ *               min + (k + 1/2) (max - min) / G, variances ((max - min) / G)^2,
+ *               weights 1/G; variances never drop below 1e-6 ((max - min)/G)^2;
+ *               a component that loses all responsibility keeps its
+ *               parameters.  A constant Smp_i is a single group.
+ *     RelVal    group mean minus sub-curve mean, on Smp_i and on Smp_{i+1}
+ *               with the same sample indices
+ *     grperr    SMAPE(a, b) = |a - b| / ((|a| + |b|) / 2), 0 / 0 := 0
+ *     err_i     mean of grperr over groups weighted by group size
+ *   Err_T      mean over the Num_T - 1 pairs, then weighted sum over channels
+ *              (weights w_c / sum w_c); -1 when Num_T < 2.
+ */
+typedef struct {
+    int32_t num_groups;     /* NumG; the paper leaves it open */
+    int32_t em_iters;       /* EM iterations */
+} oracle_pd_similarity_params;
+
+/* err_out[k] = Err_T of window w[k] at lag t[k]; returns 0 or -1. */
+int oracle_pd_similarity(const oracle_pd_params* p, const oracle_pd_similarity_params* sp,
+                         const float* x, const int64_t* w, const int32_t* t, int64_t count,
+                         double* err_out);
+
 /* Number of threads the parallel loops use. */
 int oracle_pd_threads(void);
 
