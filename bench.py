@@ -40,9 +40,11 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=("detect", "rolling"), default="detect",
+    ap.add_argument("--mode", choices=("detect", "rolling", "similarity"), default="detect",
                     help="detect: gpoeo_pd_detect (the default measurement); rolling: "
-                         "Algorithm 3's rolling detection, gpoeo_pd_detect_rolling")
+                         "Algorithm 3's rolling detection, gpoeo_pd_detect_rolling; "
+                         "similarity: Algorithm 2's grouped similarity of 5 finalist periods "
+                         "per window (the selected one, its neighbours, its double and half)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a device-to-device copy of this many MiB (the reference "
                          "kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -137,6 +139,8 @@ def main():
 
     if args.mode == "rolling":
         return bench_rolling(args)
+    if args.mode == "similarity":
+        return bench_similarity(args)
 
     t_gen = time.perf_counter()
     wl = make_workload(args.workload)
@@ -245,6 +249,71 @@ def main():
                                           f"{wl.lags} lags each, {t_cpu:.1f} s"}
         line["parity_sample"] = {"windows": done, "period_match": match,
                                  "max_score_rel_err": worst}
+    print(json.dumps(line), flush=True)
+
+
+def bench_similarity(args):
+    """Algorithm 2 on finalist periods: one step is one gpoeo_pd_similarity call on
+    5 (window, period) queries per window, built from a detection run before timing."""
+    import numpy as np
+    import torch
+
+    import paper_2201_01684_amd as pkg
+    from gen import make_workload
+
+    wl = make_workload(args.workload)
+    x = torch.from_numpy(wl.x).to("cuda:0")
+    desc, keep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
+                               wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights)
+    det = pkg.Detector(x, desc, keep, want_scores=False)
+    det.run()
+    res = det.results_numpy()
+    ws, ts = [], []
+    for b in range(wl.num_windows):
+        p = max(int(res["period"][b]), 2)
+        for t in (p, p - 1, p + 1, 2 * p, max(1, p // 2)):
+            ws.append(b)
+            ts.append(t)
+    wt = torch.tensor(np.asarray(ws, dtype=np.int32), device="cuda:0")
+    tt = torch.tensor(np.asarray(ts, dtype=np.int32), device="cuda:0")
+    for _ in range(args.warmup):
+        pkg.similarity(x, desc, wt, tt)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        err = pkg.similarity(x, desc, wt, tt)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    g = err.cpu().numpy()
+    samples = sum(wl.num_channels * (wl.n // t) * t for t in ts if wl.n // t >= 2)
+    line = {
+        "metric": "grouped-similarity evaluations/sec (Algorithm 2, 5 finalist periods per window)",
+        "value": len(ts) / (ms / 1e3), "unit": "period evaluations/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "description": wl.meta["description"],
+                   "windows": wl.num_windows, "queries": len(ts), "num_groups": 3,
+                   "em_iters": 20, "sub_curve_samples": samples, "sha256": wl.sha256},
+        "roofline": None,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        lay = oracle.Layout.of(wl)
+        done, t_cpu, worst = 0, 0.0, 0.0
+        while done < len(ts) and (done == 0 or t_cpu < args.cpu_seconds):
+            k = min(len(ts), done + 5)
+            t = time.perf_counter()
+            o = oracle.similarity(wl.x, lay, ws[done:k], ts[done:k])
+            t_cpu += time.perf_counter() - t
+            nz = o > 0
+            if nz.any():
+                worst = max(worst, float(np.max(np.abs(g[done:k][nz] - o[nz]) / o[nz])))
+            done = k
+        line["cpu_baseline"] = {"value": done / t_cpu, "unit": "period evaluations/s",
+                                "cores": oracle.threads(), "kind": "oracle",
+                                "sample": f"first {done} of {len(ts)} queries, {t_cpu:.1f} s"}
+        line["parity_sample"] = {"queries": done, "max_rel_err": worst}
     print(json.dumps(line), flush=True)
 
 

@@ -210,6 +210,29 @@ int gpoeo_pd_detect_rolling(const gpoeo_pd_desc* desc, const gpoeo_pd_rolling_pa
                             const float* x, gpoeo_pd_rolling_result* results, void* workspace,
                             size_t workspace_bytes, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Feature sequence similarity (Algorithm 2, Sec. 4.1.2) of finalist periods.
+ * For query k, window windows[k] and candidate period T = lags[k]: whole
+ * sub-curves of T samples; each sub-curve's samples grouped by a 1-D Gaussian
+ * mixture (num_groups components, em_iters EM iterations in fp64, hard
+ * assignment to the most responsible component); per group, its mean minus the
+ * sub-curve mean, compared with the same sample indices of the next sub-curve
+ * by SMAPE(a, b) = |a - b| / ((|a| + |b|) / 2) (0/0 = 0), weighted by group
+ * size; err[k] = mean over adjacent pairs, weighted mean over channels.
+ * err[k] = -1 when floor(N / T) < 2, NaN for a window or lag out of range.
+ * windows, lags: device int32 [count]; err: device double [count].  The
+ * window layout (and the channel weights) come from desc, whose lag range is
+ * not used.  No workspace.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+    int32_t num_groups;      /* NumG, 1..8 (the paper leaves it open; 3 recommended)    */
+    int32_t em_iters;        /* EM iterations, >= 0 (20 recommended)                    */
+} gpoeo_pd_similarity_params;
+
+int gpoeo_pd_similarity(const gpoeo_pd_desc* desc, const gpoeo_pd_similarity_params* params,
+                        const float* x, const int32_t* windows, const int32_t* lags,
+                        int64_t count, double* err, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

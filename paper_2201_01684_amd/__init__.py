@@ -28,6 +28,7 @@ from ._binding import (  # noqa: F401
     detect_period,
     detect_rolling,
     rolling_params,
+    similarity,
     rolling_workspace_bytes,
     load_library,
     make_desc,

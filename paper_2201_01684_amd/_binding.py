@@ -75,6 +75,13 @@ assert ROLLING_DTYPE.itemsize == ctypes.sizeof(RollingResult)
 # no value for the stability threshold on the relative period spread.
 C_MEASURE, STEP, C_EVAL, DEFAULT_DIFF_THRESHOLD = 2.0, 0.5, 6.5, 0.05
 
+class SimilarityParams(ctypes.Structure):
+    _fields_ = [("num_groups", ctypes.c_int32), ("em_iters", ctypes.c_int32)]
+
+
+# Algorithm 2's group count and EM iterations are not given by the paper.
+DEFAULT_GROUPS, DEFAULT_EM_ITERS = 3, 20
+
 RESULT_DTYPE = np.dtype([("period", np.int32), ("verdict", np.int32), ("err", np.float32),
                          ("n_candidates", np.int32), ("t_cand", np.int32), ("t_low", np.int32),
                          ("t_up", np.int32), ("n_rescored", np.int32), ("flags", np.uint32)])
@@ -83,7 +90,7 @@ assert RESULT_DTYPE.itemsize == ctypes.sizeof(Result)
 
 EXPORTS = ("gpoeo_pd_abi_version", "gpoeo_pd_strerror", "gpoeo_pd_workspace_bytes",
            "gpoeo_pd_describe_plan", "gpoeo_pd_detect", "gpoeo_pd_detect_staged",
-           "gpoeo_pd_rolling_workspace_bytes", "gpoeo_pd_detect_rolling")
+           "gpoeo_pd_rolling_workspace_bytes", "gpoeo_pd_detect_rolling", "gpoeo_pd_similarity")
 
 _lib = None
 
@@ -122,6 +129,10 @@ def load_library():
         lib.gpoeo_pd_detect_rolling.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(RollingParams),
                                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                                 ctypes.c_size_t, ctypes.c_void_p]
+        lib.gpoeo_pd_similarity.restype = ctypes.c_int
+        lib.gpoeo_pd_similarity.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(SimilarityParams),
+                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
         _lib = lib
     return _lib
 
@@ -333,3 +344,24 @@ def detect_rolling(traces: torch.Tensor, tmin: int, tmax: int, *, weights=None,
     det.run(stream)
     (torch.cuda.current_stream() if stream is None else stream).synchronize()
     return det.results_numpy()
+
+
+def similarity(x: torch.Tensor, desc: Desc, windows: torch.Tensor, lags: torch.Tensor,
+               num_groups: int = DEFAULT_GROUPS, em_iters: int = DEFAULT_EM_ITERS,
+               stream=None) -> torch.Tensor:
+    """Algorithm 2's Err_T for (windows[k], lags[k]) (int32 GPU tensors); returns a
+    float64 GPU tensor (-1: fewer than two sub-curves, NaN: out of range)."""
+    if windows.dtype != torch.int32 or lags.dtype != torch.int32:
+        raise TypeError("windows and lags must be int32 tensors")
+    if windows.shape != lags.shape or windows.dim() != 1:
+        raise ValueError("windows and lags must be 1-D and of equal length")
+    windows, lags = windows.contiguous(), lags.contiguous()
+    err = torch.empty(windows.shape, dtype=torch.float64, device=x.device)
+    p = SimilarityParams(int(num_groups), int(em_iters))
+    rc = load_library().gpoeo_pd_similarity(ctypes.byref(desc), ctypes.byref(p), x.data_ptr(),
+                                            windows.data_ptr(), lags.data_ptr(),
+                                            int(windows.numel()), err.data_ptr(),
+                                            _stream_handle(stream))
+    if rc != OK:
+        raise GpoeoError(rc, "gpoeo_pd_similarity")
+    return err

@@ -488,3 +488,22 @@ int gpoeo_pd_detect_rolling(const gpoeo_pd_desc* desc, const gpoeo_pd_rolling_pa
 }
 
 }  // extern "C"
+
+extern "C" int gpoeo_pd_similarity(const gpoeo_pd_desc* desc,
+                                   const gpoeo_pd_similarity_params* params, const float* x,
+                                   const int32_t* windows, const int32_t* lags, int64_t count,
+                                   double* err, hipStream_t stream) {
+    gpoeo::Plan p;
+    const int rc = gpoeo::make_plan(desc, &p);
+    if (rc != GPOEO_PD_OK) return rc;
+    if (!params || params->num_groups < 1 || params->num_groups > 8 || params->em_iters < 0)
+        return GPOEO_PD_EINVAL;
+    if (count < 0 || count > INT32_MAX) return GPOEO_PD_EINVAL;
+    if (count == 0) return GPOEO_PD_OK;
+    if (!x || !windows || !lags || !err) return GPOEO_PD_EINVAL;
+    if (gpoeo::launch_similarity(p, weights_of(desc, p.num_channels), params->num_groups,
+                                 params->em_iters, x, windows, lags, count, err,
+                                 stream) != hipSuccess)
+        return GPOEO_PD_EHIP;
+    return GPOEO_PD_OK;
+}
