@@ -13,9 +13,11 @@
 // group-size weighted average is err_i, and Err_T is the mean of err_i over
 // the pairs, then the weighted mean over channels.  Err_T = -1 when Num_T < 2.
 //
-// One wavefront per (window, lag) query: its lanes stride over the samples of
-// a sub-curve, and every sum is a per-lane partial sum combined by a fixed
-// shuffle tree, so all lanes hold the same mixture parameters.
+// One workgroup of kWaves wavefronts per (window, lag) query: wavefront v takes
+// the pairs i = v, v + kWaves, ...; its lanes stride over the samples of a
+// sub-curve, and every sum is a per-lane partial sum combined by a fixed
+// shuffle tree, so all lanes hold the same mixture parameters.  The pair
+// errors of the wavefronts are added in wavefront order.
 #include <cmath>
 
 #include "internal.h"
@@ -24,6 +26,7 @@ namespace gpoeo {
 namespace {
 
 constexpr int kMaxGroups = 8;
+constexpr int kWaves = 4;
 
 __device__ __forceinline__ double wave_sum(double v) {
     for (int off = 32; off > 0; off >>= 1) v = v + __shfl_down(v, off);
@@ -196,36 +199,44 @@ __device__ double pair_error(const float* __restrict__ a, const float* __restric
 }
 
 template <int G>
-__global__ __launch_bounds__(kWave) void similarity_kernel(SimArgs a, Weights w) {
-    const int lane = threadIdx.x;
+__global__ __launch_bounds__(kWave * kWaves) void similarity_kernel(SimArgs a, Weights w) {
+    __shared__ double part[kWaves];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t q = blockIdx.x;
     const int64_t win = a.windows[q];
     const int64_t t = a.lags[q];
     if (win < 0 || win >= a.num_windows || t < 1 || t > a.n) {
-        if (lane == 0) a.err[q] = NAN;
+        if (threadIdx.x == 0) a.err[q] = NAN;
         return;
     }
     const int64_t num_t = a.n / t;
     if (num_t < 2) {
-        if (lane == 0) a.err[q] = -1.0;
+        if (threadIdx.x == 0) a.err[q] = -1.0;
         return;
     }
     double acc = 0.0, wsum = 0.0;
     for (int32_t c = 0; c < a.num_channels; ++c) {
         const float* xc = a.x + win * a.window_stride + (int64_t)c * a.channel_stride;
+        double mine = 0.0;
+        for (int64_t i = wave; i + 1 < num_t; i += kWaves)
+            mine += pair_error<G>(xc + i * t, xc + (i + 1) * t, t, a.iters, lane);
+        if (lane == 0) part[wave] = mine;
+        __syncthreads();
         double total = 0.0;
-        for (int64_t i = 0; i + 1 < num_t; ++i)
-            total += pair_error<G>(xc + i * t, xc + (i + 1) * t, t, a.iters, lane);
+        for (int v = 0; v < kWaves; ++v) total += part[v];
+        __syncthreads();
         const double wc = (double)w.w[c];
         acc += wc * (total / (double)(num_t - 1));
         wsum += wc;
     }
-    if (lane == 0) a.err[q] = acc / wsum;
+    if (threadIdx.x == 0) a.err[q] = acc / wsum;
 }
 
 template <int G>
 void launch_g(const SimArgs& a, const Weights& w, hipStream_t s) {
-    hipLaunchKernelGGL(similarity_kernel<G>, dim3((unsigned)a.count), dim3(kWave), 0, s, a, w);
+    hipLaunchKernelGGL(similarity_kernel<G>, dim3((unsigned)a.count), dim3(kWave * kWaves), 0, s,
+                       a, w);
 }
 
 }  // namespace
