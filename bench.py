@@ -25,6 +25,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 FP32_VECTOR_PEAK_TFLOPS = 157.3   # MI355X published FP32 vector peak
+HBM_PEAK_GBS = 8000.0              # MI355X published HBM3E bandwidth
 FLOP_PER_PAIR = 3                 # one subtraction, one multiply, one add per (x[i], x[i+T])
 METRIC = "lag·samples/sec and traces/sec for batched period detection; % FP32 peak"
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "lag_score_w3_counters.txt")
@@ -40,8 +41,11 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=("detect", "rolling", "similarity"), default="detect",
-                    help="detect: gpoeo_pd_detect (the default measurement); rolling: "
+    ap.add_argument("--mode", choices=("detect", "fft", "rolling", "similarity"),
+                    default="detect",
+                    help="detect: gpoeo_pd_detect (the default measurement); fft: the same "
+                         "call with GPOEO_PD_FFT_SCORES (fp64 FFT autocorrelation scores); "
+                         "rolling: "
                          "Algorithm 3's rolling detection, gpoeo_pd_detect_rolling; "
                          "similarity: Algorithm 2's grouped similarity of 5 finalist periods "
                          "per window (the selected one, its neighbours, its double and half)")
@@ -109,6 +113,23 @@ def counters_traffic(workload: str):
         return None
 
 
+def fft_stage_bytes(wl) -> float:
+    """HBM bytes the FFT score stage moves per call: the samples read three times
+    (mean, sums, and the column transforms), the head and tail sums written and
+    read, each pair's complex fp64 transform written by the column kernel, read
+    and written by the row kernel and read by the inverse column kernel, and the
+    per-channel D(T) written."""
+    s = wl.num_windows * wl.num_channels
+    pairs = (s + 1) // 2
+    length = 64
+    while length < wl.n + wl.tmax:
+        length *= 2
+    lags = wl.tmax - wl.tmin + 1
+    sweeps = 0 if length <= 4096 else 4      # up to 4096 points a pair stays in LDS
+    return float(3 * 4 * s * wl.n + 2 * 2 * 8 * s * (wl.tmax + 1)
+                 + sweeps * 16 * pairs * length + 8 * s * lags)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -148,8 +169,10 @@ def main():
     t_gen = time.perf_counter() - t_gen
     pairs = wl.pairs()
     x = torch.from_numpy(wl.x).to(dev)
+    fft = args.mode == "fft"
     desc, keep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
-                               wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights)
+                               wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights,
+                               flags=pkg.FFT_SCORES if fft else 0)
     det = pkg.Detector(x, desc, keep, want_scores=True)
     plan = pkg.describe_plan(desc)
     scored = plan["pairs_scored"]
@@ -180,14 +203,27 @@ def main():
     achieved = FLOP_PER_PAIR * scored / (score_ms / 1e3) / 1e12
     res = det.results_numpy()
     scores = det.scores
+    if fft:
+        fft_bytes = fft_stage_bytes(wl)
+        roofline = {"kernel": "FFT score stage (prep, column, row and inverse-column "
+                              "transform kernels)", "bound": "hbm",
+                    "achieved": fft_bytes / (score_ms / 1e3) / 1e9,
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": fft_bytes / (score_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+                    "traffic": None, "bytes_per_launch": fft_bytes}
+    else:
+        roofline = {"kernel": "lag_score_kernel", "bound": "alu", "achieved": achieved,
+                    "peak": FP32_VECTOR_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": achieved / FP32_VECTOR_PEAK_TFLOPS,
+                    "traffic": counters_traffic(wl.name)}
 
     line = {
         "metric": METRIC,
         "value": value,
         "unit": "lag·samples/s",
         "traces_per_sec": wl.num_windows / (ms_per_step / 1e3),
-        "pct_fp32_peak": 100.0 * FLOP_PER_PAIR * scored / (ms_per_step / 1e3) / 1e12
-                         / FP32_VECTOR_PEAK_TFLOPS,
+        "pct_fp32_peak": None if fft else 100.0 * FLOP_PER_PAIR * scored
+                         / (ms_per_step / 1e3) / 1e12 / FP32_VECTOR_PEAK_TFLOPS,
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -195,21 +231,19 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f64" if fft else "f32",
         "data": "synthetic",
         "config": {"workload": wl.name, "description": wl.meta["description"],
                    "windows": wl.num_windows, "channels": wl.num_channels, "n": wl.n,
                    "tmin": wl.tmin, "tmax": wl.tmax, "pairs": pairs, "sha256": sha,
-                   "scoring": "shared block partials" if plan["mode"] == 1 else "per window",
+                   "scoring": {0: "per window", 1: "shared block partials",
+                               2: "fp64 FFT autocorrelation"}[plan["mode"]],
                    "pairs_scored": scored, "lags_per_lane": plan["lags_per_lane"]},
         "stage_ms": {"window_stats": float(stage_ms[:, 0].mean()),
                      "lag_score": score_ms,
                      "finalize": float(stage_ms[:, 2].mean()),
                      "select": float(stage_ms[:, 3].mean())},
-        "roofline": {"kernel": "lag_score_kernel", "bound": "alu", "achieved": achieved,
-                     "peak": FP32_VECTOR_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / FP32_VECTOR_PEAK_TFLOPS,
-                     "traffic": counters_traffic(wl.name)},
+        "roofline": roofline,
         "windows_flagged_unresolved": int(np.count_nonzero(res["flags"] & pkg.UNRESOLVED)),
         "windows_rescored": int(np.count_nonzero(res["n_rescored"])),
     }

@@ -35,6 +35,18 @@
  * multiply-add, i.e. on the same values a straightforward fp64 evaluation of
  * the definitions gives.
  *
+ * FFT scores (GPOEO_PD_FFT_SCORES).  The spectrum that Sec. 4.1.1 starts
+ * from, used in the lag domain: each channel is centred by its fp64 mean,
+ * zero-padded to L = 2^k >= N + Tmax points and transformed in fp64, and
+ *   D_c(T) = sum_{i<N-T} y_i^2 + sum_{i>=T} y_i^2 - 2 r(T),
+ * with the autocorrelation r the inverse transform of the power spectrum
+ * (O(L log L) per channel instead of O(N (Tmax - Tmin))).  A rigorous
+ * absolute error bound of each D_c(T), from the channel norms, decides which
+ * scores are within 1e-6 relative of the exact value; every other lag
+ * (exact zeros included) is recomputed as an fp64 sum before the selection,
+ * which then proceeds as above.  Selections equal those of the direct scores.
+ * Requires N + Tmax <= 2^22.  Sliding-window block sharing does not apply.
+ *
  * Threading and ownership.  All buffers except `desc` and `desc->channel_weights`
  * are DEVICE memory owned by the caller.  The library never allocates or frees
  * memory and keeps no mutable global state: calls on different streams with
@@ -70,7 +82,9 @@ extern "C" {
 
 /* desc->flags */
 #define GPOEO_PD_SCORES_ONLY 1u  /* compute scores only; `results` is not written           */
-#define GPOEO_PD_NO_RESCUE 2u    /* decide on the bounded fp32-accumulated scores only       */
+#define GPOEO_PD_NO_RESCUE 2u    /* decide on the bounded tier-0 scores only                */
+#define GPOEO_PD_FFT_SCORES 4u   /* scores from an fp64 FFT autocorrelation instead of the
+                                    direct sums (see below); needs N + Tmax <= 2^22        */
 
 /* result->flags */
 #define GPOEO_PD_UNRESOLVED 1u   /* some comparison stayed undecided after the exact
@@ -92,7 +106,7 @@ typedef struct {
     double err_max;          /* APERIODIC if S(period)/R >= err_max (1.0: never for a
                                 selected period)                                            */
     const float* channel_weights; /* HOST array of C weights > 0, or NULL for all 1          */
-    uint32_t flags;          /* GPOEO_PD_SCORES_ONLY | GPOEO_PD_NO_RESCUE                   */
+    uint32_t flags;          /* GPOEO_PD_SCORES_ONLY | GPOEO_PD_NO_RESCUE | _FFT_SCORES     */
     uint32_t reserved1;      /* must be 0                                                   */
 } gpoeo_pd_desc;
 
@@ -110,7 +124,8 @@ typedef struct {
 /* How gpoeo_pd_detect will run a descriptor (for measurement tools). */
 typedef struct {
     int32_t mode;             /* 0: every window scored on its own; 1: overlapping windows
-                                 at a stride dividing N share per-block partials          */
+                                 at a stride dividing N share per-block partials; 2: FFT
+                                 scores (score_waves and pairs_scored are then 0)         */
     int32_t lags_per_lane;    /* consecutive lags per lane of the score kernel (8 or 16)  */
     int64_t score_waves;      /* wavefronts the score stage launches                      */
     double pairs_defined;     /* sum over windows, channels and T in [tmin, tmax] of N - T:
@@ -199,7 +214,7 @@ typedef struct {
     int64_t starts[GPOEO_PD_ROLLING_MAX];    /* first sample of each suffix window            */
 } gpoeo_pd_rolling_result;
 
-/* Validates desc (flags may hold GPOEO_PD_NO_RESCUE only) and params and writes
+/* Validates desc (flags may hold GPOEO_PD_NO_RESCUE and GPOEO_PD_FFT_SCORES) and params and writes
  * the device workspace size of gpoeo_pd_detect_rolling.  EINVAL if the schedule
  * could exceed GPOEO_PD_ROLLING_MAX suffix windows. */
 int gpoeo_pd_rolling_workspace_bytes(const gpoeo_pd_desc* desc,

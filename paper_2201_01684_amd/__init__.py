@@ -13,6 +13,7 @@ from ._binding import (  # noqa: F401
     DEFAULT_C_LAG,
     DEFAULT_ERR_MAX,
     EXPORTS,
+    FFT_SCORES,
     LIB_PATH,
     NO_RESCUE,
     PERIODIC,

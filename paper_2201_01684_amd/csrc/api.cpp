@@ -49,7 +49,8 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
 int make_plan(const gpoeo_pd_desc* d, Plan* p) {
     if (!d) return GPOEO_PD_EINVAL;
     if (d->reserved0 != 0 || d->reserved1 != 0) return GPOEO_PD_EINVAL;
-    if (d->flags & ~(GPOEO_PD_SCORES_ONLY | GPOEO_PD_NO_RESCUE)) return GPOEO_PD_EINVAL;
+    if (d->flags & ~(GPOEO_PD_SCORES_ONLY | GPOEO_PD_NO_RESCUE | GPOEO_PD_FFT_SCORES))
+        return GPOEO_PD_EINVAL;
     if (d->num_windows < 1 || d->num_windows > INT32_MAX) return GPOEO_PD_EINVAL;
     if (d->num_channels < 1 || d->num_channels > kMaxChannels) return GPOEO_PD_EINVAL;
     if (d->n < 8 || d->n > (int64_t(1) << 40)) return GPOEO_PD_EINVAL;
@@ -80,6 +81,26 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
     p->err_max = d->err_max;
     p->flags = d->flags;
 
+    p->fft = (d->flags & GPOEO_PD_FFT_SCORES) != 0;
+    if (p->fft) {
+        // smallest power of two (at least 64) holding N + Tmax points
+        int32_t lg = 6;
+        while ((int64_t(1) << lg) < d->n + d->tmax) ++lg;
+        if (lg > kFftMaxLog2) return GPOEO_PD_EINVAL;
+        p->fft_log2 = lg;
+        p->fft_len = int64_t(1) << lg;
+        if (lg <= 12) {
+            p->fft_m1 = (int32_t)p->fft_len;
+            p->fft_m2 = 1;
+            p->fft_cols = 1;
+        } else {
+            const int32_t lg1 = lg / 2, lg2 = lg - lg1;   // row transforms of at most 2^11
+            p->fft_m1 = 1 << lg1;
+            p->fft_m2 = 1 << lg2;
+            p->fft_cols = std::min<int32_t>(p->fft_m2, 1 << (12 - lg1));
+        }
+    }
+
     p->lags_per_lane = choose_lags_per_lane(d->n, d->tmin, d->tmax);
     p->waves_per_group = choose_waves_per_group(p->lags_per_lane);
     const int32_t lags_per_block = kWave * p->lags_per_lane;
@@ -91,7 +112,7 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
     // Overlapping windows whose stride divides N (and is a whole number of lag
     // blocks) share block partials when that saves at least a third of the work.
     const int64_t ws_ = d->window_stride;
-    if (d->num_windows >= 2 && ws_ > 0 && ws_ < d->n && d->n % ws_ == 0 &&
+    if (!p->fft && d->num_windows >= 2 && ws_ > 0 && ws_ < d->n && d->n % ws_ == 0 &&
         ws_ % lags_per_block == 0) {
         const int64_t m = d->n / ws_;
         const double direct =
@@ -154,6 +175,12 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
         if (!mul_ok(bbase, chunks, &p->block_tasks)) return GPOEO_PD_EINVAL;
         if (p->block_tasks / p->waves_per_group + 1 > INT32_MAX) return GPOEO_PD_EINVAL;
     }
+    if (p->fft) {   // one D(T) per (window, channel, lag), lags from tmin
+        p->t0 = d->tmin;
+        p->lags_padded = p->lags;
+        p->chunks = 1;
+        p->fft_pairs = (bc + 1) / 2;
+    }
     p->bitmap_words = (p->lags + 31) / 32;
 
     int64_t n_var, n_s, n_bits, n_part;
@@ -170,6 +197,13 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
             return GPOEO_PD_EINVAL;
     }
     if (n_part > (INT64_MAX / 16)) return GPOEO_PD_EINVAL;
+    int64_t n_fstat = 0, n_edge = 0, n_tw = 0, n_z = 0;
+    if (p->fft) {
+        if (!mul_ok(bc, 4, &n_fstat) || !mul_ok(bc, 2 * ((int64_t)d->tmax + 1), &n_edge) ||
+            !mul_ok(p->fft_pairs, p->fft_len, &n_z) || n_z > (INT64_MAX / 64))
+            return GPOEO_PD_EINVAL;
+        n_tw = fft_twiddle_count(*p);
+    }
     size_t off = 0;
     p->off_var = off;
     off = align_up(off + (size_t)n_var * sizeof(double));
@@ -185,6 +219,14 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
     off = align_up(off + (size_t)n_part * sizeof(double));
     p->off_cut = off;                             // cut-block partials (sliding mode)
     if (p->sliding) off = align_up(off + (size_t)n_part * sizeof(double));
+    p->off_fstat = off;                           // FFT mode: per-sequence sums
+    off = align_up(off + (size_t)n_fstat * sizeof(double));
+    p->off_edge = off;                            // head and tail sums of squares
+    off = align_up(off + (size_t)n_edge * sizeof(double));
+    p->off_tw = off;                              // twiddle tables (complex fp64)
+    off = align_up(off + (size_t)n_tw * 2 * sizeof(double));
+    p->off_z = off;                               // transforms (complex fp64)
+    off = align_up(off + (size_t)n_z * 2 * sizeof(double));
     p->bytes = off;
     return GPOEO_PD_OK;
 }
@@ -246,7 +288,20 @@ int run_plan(const gpoeo::Plan& p, const gpoeo::Weights& w, const float* x, floa
     if (!scores_only && gpoeo::launch_window_stats(p, x, c.var, stream) != hipSuccess)
         return GPOEO_PD_EHIP;
     if (!mark(1)) return GPOEO_PD_EHIP;
-    if (p.sliding) {
+    if (p.fft) {
+        char* ws = static_cast<char*>(workspace);
+        double* fstat = reinterpret_cast<double*>(ws + p.off_fstat);
+        if (gpoeo::launch_fft_scores(p, x, fstat, reinterpret_cast<double*>(ws + p.off_edge),
+                                     reinterpret_cast<double*>(ws + p.off_tw),
+                                     reinterpret_cast<double*>(ws + p.off_z), c.part,
+                                     stream) != hipSuccess)
+            return GPOEO_PD_EHIP;
+        if (!mark(2)) return GPOEO_PD_EHIP;
+        if (gpoeo::launch_finalize(p, w, c.part, c.s64, scores, stream) != hipSuccess ||
+            gpoeo::launch_select_init(p, c.sb, stream) != hipSuccess ||
+            gpoeo::launch_fft_fixup(p, w, x, fstat, c.s64, scores, c.sb, stream) != hipSuccess)
+            return GPOEO_PD_EHIP;
+    } else if (p.sliding) {
         if (gpoeo::launch_lag_score_blocks(p, x, c.part, c.cut, stream) != hipSuccess)
             return GPOEO_PD_EHIP;
         if (!mark(2)) return GPOEO_PD_EHIP;
@@ -259,9 +314,12 @@ int run_plan(const gpoeo::Plan& p, const gpoeo::Weights& w, const float* x, floa
             return GPOEO_PD_EHIP;
     }
     if (!mark(3)) return GPOEO_PD_EHIP;
-    if (!scores_only &&
-        gpoeo::launch_select(p, w, x, c.var, c.s64, c.sb, results, stream) != hipSuccess)
-        return GPOEO_PD_EHIP;
+    if (!scores_only) {
+        if (!p.fft && gpoeo::launch_select_init(p, c.sb, stream) != hipSuccess)
+            return GPOEO_PD_EHIP;
+        if (gpoeo::launch_select(p, w, x, c.var, c.s64, c.sb, results, stream) != hipSuccess)
+            return GPOEO_PD_EHIP;
+    }
     if (!mark(4)) return GPOEO_PD_EHIP;
     return GPOEO_PD_OK;
 }
@@ -367,9 +425,9 @@ int gpoeo_pd_describe_plan(const gpoeo_pd_desc* desc, gpoeo_pd_plan_info* info) 
     gpoeo::Plan p;
     const int rc = gpoeo::make_plan(desc, &p);
     if (rc != GPOEO_PD_OK) return rc;
-    info->mode = p.sliding ? 1 : 0;
+    info->mode = p.fft ? 2 : (p.sliding ? 1 : 0);
     info->lags_per_lane = p.lags_per_lane;
-    info->score_waves = p.sliding ? 2 * p.block_tasks : p.tasks;
+    info->score_waves = p.fft ? 0 : (p.sliding ? 2 * p.block_tasks : p.tasks);
     info->workspace_bytes = p.bytes;
     const double wc = (double)p.num_windows * p.num_channels;
     double defined = 0.0, scored = 0.0;
@@ -392,7 +450,7 @@ int gpoeo_pd_describe_plan(const gpoeo_pd_desc* desc, gpoeo_pd_plan_info* info) 
         scored += (double)p.num_channels * ((double)std::max<int64_t>(0, e) + cut);
     }
     info->pairs_defined = defined;
-    info->pairs_scored = p.sliding ? scored : defined;
+    info->pairs_scored = p.fft ? 0.0 : (p.sliding ? scored : defined);
     return GPOEO_PD_OK;
 }
 
@@ -480,6 +538,7 @@ int gpoeo_pd_detect_rolling(const gpoeo_pd_desc* desc, const gpoeo_pd_rolling_pa
     ca.num_channels = r.a.num_channels;
     ca.jmax = r.rc.jmax;
     const double u = 1.1102230246251565e-16;
+    ca.tau0 = r.c.fft ? gpoeo::kFftRelBound : gpoeo::kScoreRelBound;
     ca.tau1 = 1.01 * u * ((double)r.c.n * (1.0 + 1.0 / 256.0) + 2.0 * r.c.num_channels + 22.0);
     ca.diff_threshold = r.rc.diff_threshold;
     if (gpoeo::launch_rolling_combine(ca, w, r.a.num_windows, stream) != hipSuccess)

@@ -18,6 +18,14 @@ constexpr int kMaxChannels = 256;    // channel weights travel as a kernel argum
 // difference, about 258 * 2^-24 = 1.54e-5) and combined in fp64; rounded up.
 constexpr double kScoreRelBound = 2.5e-5;
 
+// Relative half-width of a tier-0 score from the fp64 FFT path: a lag whose
+// rigorous FFT error bound exceeds half of this (times the score) is re-scored
+// in fp64 before the selection.
+constexpr double kFftRelBound = 1e-6;
+
+// Largest transform of the FFT path (complex fp64 points per pair of sequences).
+constexpr int kFftMaxLog2 = 22;
+
 struct Weights {
     float w[kMaxChannels];
 };
@@ -98,12 +106,22 @@ struct Plan {
     int64_t block_chunk;     // samples per chunk of a block
     int32_t block_chunks;
     int64_t block_tasks;     // waves of each of the two block-partial launches
+    // FFT scores: every (window, channel) sequence, centred and zero-padded to
+    // fft_len = 2^fft_log2 >= N + Tmax, is paired with the next one as the real
+    // and imaginary parts of one complex transform.  Up to 2^12 points one
+    // workgroup transforms a pair in LDS; beyond that the transform is split
+    // as fft_len = fft_m1 * fft_m2 (columns of fft_m1 points, rows of fft_m2).
+    bool fft;
+    int32_t fft_log2, fft_m1, fft_m2, fft_cols;
+    int64_t fft_len;
+    int64_t fft_pairs;
     double c_lag, err_max;
     uint32_t flags;
     WindowTable table;       // per-window offsets / lengths / Tmax, or all null
     int32_t bitmap_words;    // 32-bit words per window of the exactness bitmap
     // workspace layout (byte offsets, 256-byte aligned)
-    size_t off_var, off_s64, off_bits, off_state, off_queue, off_part, off_cut, bytes;
+    size_t off_var, off_s64, off_bits, off_state, off_queue, off_part, off_cut;
+    size_t off_fstat, off_edge, off_tw, off_z, bytes;
 };
 
 // Rolling detection (Algorithm 3).
@@ -141,6 +159,7 @@ struct RollingCombineArgs {
     int32_t tmin;
     int32_t num_channels;
     int32_t jmax;
+    double tau0;
     double tau1;
     double diff_threshold;
 };
@@ -157,6 +176,18 @@ hipError_t launch_finalize_blocks(const Plan& p, const Weights& w, const double*
                                   const double* cut, double* s64, float* scores, hipStream_t s);
 hipError_t launch_finalize(const Plan& p, const Weights& w, const double* part, double* s64,
                            float* scores, hipStream_t s);
+// FFT scores.  fstat: [B*C][4] = mean, sum of squares and sum of |.| of the
+// centred sequence, and its absolute error bound on D(T); edge: [B*C][2][Tmax+1]
+// prefix sums of squares from the head and from the tail; tw: twiddle tables;
+// z: [pairs][fft_len] complex fp64.  Writes D_c(T) into part ([B*C][lags]).
+int64_t fft_twiddle_count(const Plan& p);
+hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, double* edge,
+                             double* tw, double* z, double* part, hipStream_t s);
+// After the finalisation: every lag whose FFT bound does not give the tier-0
+// guarantee is re-scored in fp64 (score, fp32 score and tier-1 bit).
+hipError_t launch_fft_fixup(const Plan& p, const Weights& w, const float* x, const double* fstat,
+                            double* s64, float* scores, const SelectBuffers& sb, hipStream_t s);
+hipError_t launch_select_init(const Plan& p, const SelectBuffers& sb, hipStream_t s);
 hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const double* var,
                          double* s64, const SelectBuffers& sb, void* results, hipStream_t s);
 hipError_t launch_rolling_schedule(const Plan& p, const RollingConfig& rc,

@@ -119,7 +119,7 @@ __global__ __launch_bounds__(kWave) void rolling_combine_kernel(RollingCombineAr
                 s_lo = s_hi = s_v;
             } else {
                 const double e =
-                    (a.tier1[win * a.words + (j >> 5)] & bit) ? a.tau1 : kScoreRelBound;
+                    (a.tier1[win * a.words + (j >> 5)] & bit) ? a.tau1 : a.tau0;
                 s_lo = s_v * (1.0 - e);
                 s_hi = s_v * (1.0 + e);
             }

@@ -18,7 +18,9 @@
 // Every score carries a tier and is handled as an interval [v(1-e), v(1+e)]
 // that contains the value a plain sequential fp64 evaluation of the definition
 // gives:
-//   tier 0  from the score kernels (fp32 runs, fp64 combine): e = kScoreRelBound
+//   tier 0  from the score kernels: e = kScoreRelBound for fp32 runs combined
+//           in fp64, kFftRelBound for the fp64 FFT scores (whose lags without
+//           that guarantee were raised to tier 1 before the first pass)
 //   tier 1  re-scored in fp64 by one wavefront (64 strided partial sums and a
 //           fixed-order tree): e = tau1, derived from N (about 3e-11 at
 //           N = 262144) - it covers the rounding of both evaluation orders
@@ -32,6 +34,8 @@
 // again.  The launcher runs kPasses selection passes with a re-score round
 // between consecutive ones; a window still open in the last pass is decided
 // on the unwidened values and flagged GPOEO_PD_UNRESOLVED.
+#include <algorithm>
+
 #include "internal.h"
 #include "exact.h"
 #include "gpoeo_pd.h"
@@ -65,7 +69,7 @@ struct SelectArgs {
     int64_t channel_stride;
     int32_t num_channels;
     int32_t tmin, tmax, lags, words;
-    double c_lag, err_max, tau1;
+    double c_lag, err_max, tau0, tau1;
     uint32_t flags;
     int32_t pass;
     int32_t last;
@@ -153,21 +157,6 @@ __global__ __launch_bounds__(kThreads) void select_pass_kernel(SelectArgs a, Wei
     gpoeo_pd_result* res = a.results + b;
     int32_t* count = a.q_count + 2 * a.pass;
 
-    if (a.pass == 0) {
-        for (int32_t k = tid; k < a.words; k += kThreads) {
-            t1[k] = 0u;
-            t2[k] = 0u;
-            qd1[k] = 0u;
-            qd2[k] = 0u;
-        }
-        if (tid == 0) {
-            st->r_exact = 0.0;
-            st->done = 0;
-            st->r_queued = 0;
-            st->r_is_exact = 0;
-            st->rescored = 0;
-        }
-    }
     if (tid == 0) {
         sh.done = a.pass == 0 ? 0 : st->done;
         const double* v2 = a.var + 2 * b * a.num_channels;
@@ -414,7 +403,7 @@ __global__ __launch_bounds__(kThreads) void select_pass_kernel(SelectArgs a, Wei
     if (!rescue) {
         done = rule(0.0, 0.0, 0.0, false, o);
     } else {
-        done = rule(kScoreRelBound, a.tau1, r_err, !a.last, o);
+        done = rule(a.tau0, a.tau1, r_err, !a.last, o);
         if (!done && a.last) {
             done = rule(0.0, 0.0, 0.0, false, o);
             unresolved = true;
@@ -478,11 +467,40 @@ __global__ __launch_bounds__(kThreads) void rescore_kernel(SelectArgs a, Weights
     }
 }
 
-__global__ void zero_counts_kernel(int32_t* counts, int n) {
-    if ((int)threadIdx.x < n) counts[threadIdx.x] = 0;
+// Clears the tier and queue bitmaps and the state of every window (a fill
+// kernel rather than a memset, so that the sequence stays capturable).
+__global__ __launch_bounds__(kThreads) void select_init_kernel(SelectBuffers sb, int64_t words,
+                                                               int64_t num_windows) {
+    const int64_t total = words * num_windows;
+    const int64_t step = (int64_t)gridDim.x * kThreads;
+    for (int64_t k = (int64_t)blockIdx.x * kThreads + threadIdx.x; k < total; k += step) {
+        sb.tier1[k] = 0u;
+        sb.tier2[k] = 0u;
+        sb.queued1[k] = 0u;
+        sb.queued2[k] = 0u;
+    }
+    for (int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x; b < num_windows; b += step) {
+        WinState z;
+        z.r_exact = 0.0;
+        z.done = 0;
+        z.r_queued = 0;
+        z.r_is_exact = 0;
+        z.rescored = 0;
+        sb.state[b] = z;
+    }
+    if (blockIdx.x == 0 && (int)threadIdx.x < 2 * kPasses) sb.q_count[threadIdx.x] = 0;
 }
 
 }  // namespace
+
+hipError_t launch_select_init(const Plan& p, const SelectBuffers& sb, hipStream_t s) {
+    const int64_t total = std::max<int64_t>((int64_t)p.bitmap_words * p.num_windows, p.num_windows);
+    int64_t groups = (total + kThreads - 1) / kThreads;
+    if (groups > 4096) groups = 4096;
+    hipLaunchKernelGGL(select_init_kernel, dim3((unsigned)groups), dim3(kThreads), 0, s, sb,
+                       (int64_t)p.bitmap_words, p.num_windows);
+    return hipGetLastError();
+}
 
 hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const double* var,
                          double* s64, const SelectBuffers& sb, void* results, hipStream_t s) {
@@ -511,6 +529,7 @@ hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const 
     a.err_max = p.err_max;
     a.flags = p.flags;
     a.tab = p.table;
+    a.tau0 = p.fft ? kFftRelBound : kScoreRelBound;
     // Tier-1 half-width: the sequential sum (at most n + C + 6 roundings of
     // u = 2^-53 each, relative to the exact value) plus the wavefront sum
     // (n/256 + C + 16 roundings), with 1% margin.
@@ -518,7 +537,6 @@ hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const 
     a.tau1 = 1.01 * u * ((double)p.n * (1.0 + 1.0 / 256.0) + 2.0 * p.num_channels + 22.0);
     const bool rescue = (p.flags & GPOEO_PD_NO_RESCUE) == 0;
     const int passes = rescue ? kPasses : 1;
-    hipLaunchKernelGGL(zero_counts_kernel, dim3(1), dim3(64), 0, s, sb.q_count, 2 * kPasses);
     const dim3 grid_sel((unsigned)p.num_windows);
     const dim3 grid_re(kRescoreGroups);
     for (int pass = 0; pass < passes; ++pass) {

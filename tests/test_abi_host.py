@@ -94,7 +94,7 @@ def test_workspace_size_valid_and_monotone(lib):
     dict(n=7, tmin=1, tmax=3), dict(tmin=0), dict(tmin=5, tmax=6), dict(tmax=2049),
     dict(window_stride=0), dict(channel_stride=4095), dict(window_stride=-1),
     dict(c_lag=0.0), dict(c_lag=1.0), dict(c_lag=float("nan")), dict(err_max=float("nan")),
-    dict(flags=4),
+    dict(flags=8), dict(flags=4, n=4 << 20, tmax=2 << 20),
 ])
 def test_invalid_descriptors_rejected(lib, kw):
     d, _ = good_desc(**kw)
@@ -189,3 +189,26 @@ def test_rolling_workspace_and_flags(lib):
     assert call(ctypes.byref(d), None, 0x100000, 0x200000, 0x300000, need, None) == B.EINVAL
     assert call(ctypes.byref(d), ctypes.byref(p), 0x100000, None, 0x300000, need,
                 None) == B.EINVAL
+
+
+def test_fft_plan(lib):
+    d, _ = good_desc()
+    direct = B.workspace_bytes(d)
+    d, _ = good_desc(flags=B.FFT_SCORES)
+    info = B.describe_plan(d)
+    assert info["mode"] == 2 and info["score_waves"] == 0 and info["pairs_scored"] == 0
+    assert info["pairs_defined"] == 4 * 2 * sum(4096 - t for t in range(2, 1025))
+    # 8 complex fp64 transforms of 8192 points (4096 + 1024 <= 2^13) at least
+    assert info["workspace_bytes"] >= 4 * 8192 * 16
+    assert info["workspace_bytes"] != direct
+    # the largest transform: N + Tmax <= 2^22
+    d, _ = good_desc(flags=B.FFT_SCORES, num_windows=1, n=(1 << 22) - 1000, tmax=1000,
+                     channel_stride=1 << 22)
+    assert B.describe_plan(d)["mode"] == 2
+    d, _ = good_desc(flags=B.FFT_SCORES, num_windows=1, n=(1 << 22) - 1000, tmax=1001,
+                     channel_stride=1 << 22)
+    with pytest.raises(B.GpoeoError):
+        B.workspace_bytes(d)
+    # rolling accepts the FFT flag
+    d, _ = good_desc(flags=B.FFT_SCORES)
+    assert B.rolling_workspace_bytes(d, B.rolling_params()) > 0
