@@ -114,20 +114,22 @@ def counters_traffic(workload: str):
 
 
 def fft_stage_bytes(wl) -> float:
-    """HBM bytes the FFT score stage moves per call: the samples read three times
-    (mean, sums, and the column transforms), the head and tail sums written and
-    read, each pair's complex fp64 transform written by the column kernel, read
-    and written by the row kernel and read by the inverse column kernel, and the
-    per-channel D(T) written."""
+    """HBM bytes the FFT score stage moves per call: the samples read once by the
+    column transforms (the centring sums come with the window statistics), the
+    first and last Tmax samples of each sequence read and their head and tail
+    sums written and read back, each pair's complex fp64 transform written by
+    the column kernel, read and written by the row kernel and read by the
+    inverse column kernel (none of that up to 4096 points, where a pair stays
+    in LDS), and the per-channel D(T) written."""
     s = wl.num_windows * wl.num_channels
     pairs = (s + 1) // 2
     length = 64
     while length < wl.n + wl.tmax:
         length *= 2
     lags = wl.tmax - wl.tmin + 1
-    sweeps = 0 if length <= 4096 else 4      # up to 4096 points a pair stays in LDS
-    return float(3 * 4 * s * wl.n + 2 * 2 * 8 * s * (wl.tmax + 1)
-                 + sweeps * 16 * pairs * length + 8 * s * lags)
+    sweeps = 0 if length <= 4096 else 4
+    edges = 2 * 4 * s * wl.tmax + 2 * 8 * s * (wl.tmax + 1) + 2 * 8 * s * lags
+    return float(4 * s * wl.n + edges + sweeps * 16 * pairs * length + 8 * s * lags)
 
 
 def main():

@@ -285,12 +285,14 @@ int run_plan(const gpoeo::Plan& p, const gpoeo::Weights& w, const float* x, floa
     const Carved c = carve(p, workspace);
     auto mark = [&](int k) { return !ev || hipEventRecord(ev[k], stream) == hipSuccess; };
     if (!mark(0)) return GPOEO_PD_EHIP;
-    if (!scores_only && gpoeo::launch_window_stats(p, x, c.var, stream) != hipSuccess)
+    double* fstat = p.fft ? reinterpret_cast<double*>(static_cast<char*>(workspace) + p.off_fstat)
+                          : nullptr;
+    if ((!scores_only || p.fft) &&
+        gpoeo::launch_window_stats(p, x, c.var, fstat, stream) != hipSuccess)
         return GPOEO_PD_EHIP;
     if (!mark(1)) return GPOEO_PD_EHIP;
     if (p.fft) {
         char* ws = static_cast<char*>(workspace);
-        double* fstat = reinterpret_cast<double*>(ws + p.off_fstat);
         if (gpoeo::launch_fft_scores(p, x, fstat, reinterpret_cast<double*>(ws + p.off_edge),
                                      reinterpret_cast<double*>(ws + p.off_tw),
                                      reinterpret_cast<double*>(ws + p.off_z), c.part,

@@ -40,7 +40,7 @@ constexpr int kRegPoints = kLdsPoints / kThreads;
 
 struct FftArgs {
     const float* x;
-    double* fstat;             // [S][4]: mean, sum y^2, sum |y|, unused
+    const double* fstat;       // [S][4]: mean, sum y^2, sum |y|, unused (window statistics)
     double* edge;              // [S][2][tmax + 1]: head and tail sums of y^2
     const double2* tw;         // twiddle tables
     double2* z;                // [pairs][len]
@@ -51,7 +51,7 @@ struct FftArgs {
     int64_t tw_a, tw_b, tw_lo, tw_hi;
     int32_t num_channels;
     int32_t tmin, tmax, lags;
-    int32_t lg, lg1, lg2, lgc;
+    int32_t lg, lg1, lg2, lgc, lgr;
     WindowTable tab;
 };
 
@@ -79,49 +79,84 @@ __device__ __forceinline__ int64_t xcd_remap(int64_t bid, int64_t nblk) {
     return (bid & 7) * (nblk >> 3) + (bid >> 3);
 }
 
-// Forward transform (exp(-2 pi i kn/L), L = 2^lg) of `cols` interleaved
-// sequences s[i * cols + q], by decimation in frequency: natural order in,
-// bit-reversed out.  tw[m] = exp(-2 pi i m / L), m < L/2.
-__device__ void lds_fft_fwd(double2* s, int lg, int lgc, const double2* __restrict__ tw) {
+// Transforms of `cols` interleaved sequences of L = 2^lg points, s[i * cols + q],
+// as radix-2 butterflies: forward by decimation in frequency (natural order
+// in, bit-reversed out), at stage h = 2^st the pair (i, i + h) becomes
+// (a + b, (a - b) W_2h^j), j = i mod h; inverse by decimation in time
+// (bit-reversed in, natural out), (a + b conj(W_2h^j), a - b conj(W_2h^j)).
+// tw[m] = exp(-2 pi i m / L), m < L/2, so W_2h^j = tw[j L / 2h].
+//
+// A pass runs 2^R-point groups through R consecutive stages in registers (the
+// same butterflies, so the same roundings as stage-by-stage): the points of a
+// group share every index bit outside the pass's stages.  Passes hold up to 4
+// stages, with at least 256 groups when the LDS tile allows (all threads busy).
+template <int R, bool kInverse>
+__device__ __forceinline__ void fft_pass(double2* s, int lg, int lgc, int st_lo,
+                                         const double2* __restrict__ tw) {
+    constexpr int kR = 1 << R;
     const int cols = 1 << lgc;
-    const int nb = 1 << (lg - 1 + lgc);
-    for (int st = lg - 1; st >= 0; --st) {
-        const int h = 1 << st;
-        for (int f = threadIdx.x; f < nb; f += kThreads) {
-            const int q = f & (cols - 1);
-            const int bf = f >> lgc;
-            const int j = bf & (h - 1);
-            const int i0 = ((bf >> st) << (st + 1)) + j;
-            const int i1 = i0 + h;
-            const double2 a = s[i0 * cols + q], b = s[i1 * cols + q];
-            const double2 w = tw[j << (lg - 1 - st)];
-            s[i0 * cols + q] = cadd(a, b);
-            s[i1 * cols + q] = cmul(csub(a, b), w);
+    const int groups = 1 << (lg - R + lgc);
+    const int lo_mask = (1 << st_lo) - 1;
+    for (int gi = threadIdx.x; gi < groups; gi += kThreads) {
+        const int q = gi & (cols - 1);
+        const int g = gi >> lgc;
+        const int blo = g & lo_mask;
+        const int base = ((g >> st_lo) << (st_lo + R)) | blo;
+        double2 v[kR];
+#pragma unroll
+        for (int m = 0; m < kR; ++m) v[m] = s[(base + (m << st_lo)) * cols + q];
+#pragma unroll
+        for (int kk = 0; kk < R; ++kk) {
+            const int k = kInverse ? kk : R - 1 - kk;   // stage st_lo + k
+            const int st = st_lo + k;
+#pragma unroll
+            for (int m = 0; m < kR; ++m) {
+                if (m & (1 << k)) continue;
+                const int j = blo + ((m & ((1 << k) - 1)) << st_lo);
+                const double2 w = tw[j << (lg - 1 - st)];
+                const double2 a = v[m];
+                if (kInverse) {
+                    const double2 b = cmul_conj(v[m + (1 << k)], w);
+                    v[m] = cadd(a, b);
+                    v[m + (1 << k)] = csub(a, b);
+                } else {
+                    const double2 b = v[m + (1 << k)];
+                    v[m] = cadd(a, b);
+                    v[m + (1 << k)] = cmul(csub(a, b), w);
+                }
+            }
         }
-        __syncthreads();
+#pragma unroll
+        for (int m = 0; m < kR; ++m) s[(base + (m << st_lo)) * cols + q] = v[m];
     }
 }
 
-// Inverse transform (exp(+2 pi i kn/L), no 1/L) by decimation in time:
-// bit-reversed order in, natural out.
-__device__ void lds_fft_inv(double2* s, int lg, int lgc, const double2* __restrict__ tw) {
-    const int cols = 1 << lgc;
-    const int nb = 1 << (lg - 1 + lgc);
-    for (int st = 0; st < lg; ++st) {
-        const int h = 1 << st;
-        for (int f = threadIdx.x; f < nb; f += kThreads) {
-            const int q = f & (cols - 1);
-            const int bf = f >> lgc;
-            const int j = bf & (h - 1);
-            const int i0 = ((bf >> st) << (st + 1)) + j;
-            const int i1 = i0 + h;
-            const double2 a = s[i0 * cols + q];
-            const double2 b = cmul_conj(s[i1 * cols + q], tw[j << (lg - 1 - st)]);
-            s[i0 * cols + q] = cadd(a, b);
-            s[i1 * cols + q] = csub(a, b);
+template <bool kInverse>
+__device__ void lds_fft(double2* s, int lg, int lgc, const double2* __restrict__ tw) {
+    int rmax = lg + lgc - 8;   // log2 of the points per thread
+    rmax = rmax < 1 ? 1 : (rmax > 4 ? 4 : rmax);
+    const int np = (lg + rmax - 1) / rmax;
+    const int base = lg / np, extra = lg % np;
+    int st = kInverse ? 0 : lg;
+    for (int p = 0; p < np; ++p) {
+        const int r = base + (p < extra ? 1 : 0);
+        const int st_lo = kInverse ? st : st - r;
+        switch (r) {
+            case 1: fft_pass<1, kInverse>(s, lg, lgc, st_lo, tw); break;
+            case 2: fft_pass<2, kInverse>(s, lg, lgc, st_lo, tw); break;
+            case 3: fft_pass<3, kInverse>(s, lg, lgc, st_lo, tw); break;
+            default: fft_pass<4, kInverse>(s, lg, lgc, st_lo, tw); break;
         }
         __syncthreads();
+        st = kInverse ? st + r : st_lo;
     }
+}
+
+__device__ __forceinline__ void lds_fft_fwd(double2* s, int lg, int lgc, const double2* tw) {
+    lds_fft<false>(s, lg, lgc, tw);
+}
+__device__ __forceinline__ void lds_fft_inv(double2* s, int lg, int lgc, const double2* tw) {
+    lds_fft<true>(s, lg, lgc, tw);
 }
 
 // W_L^e = exp(-2 pi i e / L) for e < L from two tables split at bit lg2.
@@ -177,81 +212,71 @@ __device__ __forceinline__ void write_d(const FftArgs& a, int64_t s, int64_t t, 
     a.part[s * a.lags + (t - a.tmin)] = d;
 }
 
-__device__ double block_sum(double v, double* red) {
-    red[threadIdx.x] = v;
-    __syncthreads();
-    for (int w = kThreads / 2; w > 0; w >>= 1) {
-        if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-        __syncthreads();
-    }
-    const double r = red[0];
-    __syncthreads();
-    return r;
-}
+// Sums of y^2 over the first T samples (head) and the last T samples (tail)
+// of a sequence, T = 0..Tmax; one workgroup per (sequence, side).  Tiles of
+// 4096 terms are staged in LDS with coalesced loads; each thread adds 16
+// consecutive terms, the thread totals are added in thread order, and the
+// running sums go back through LDS for coalesced stores.  (The mean, sum y^2
+// and sum |y| come from the window statistics, computed with the same mean.)
+constexpr int kEdgeTile = 4096;
+constexpr int kEdgePer = kEdgeTile / kThreads;   // 16 terms per thread
 
-// Per sequence: the fp64 mean (the centring constant), sum y^2 and sum |y| of
-// the centred samples, and the sums of y^2 over the first and the last T
-// samples for T = 0..Tmax (each thread sums a contiguous stretch, then the
-// stretch totals are added in thread order).
-__global__ __launch_bounds__(kThreads) void fft_prep_kernel(FftArgs a) {
-    __shared__ double red[kThreads];
-    __shared__ double base[kThreads];
-    const int64_t s = blockIdx.x;
+__device__ __forceinline__ int edge_slot(int k) { return k + (k >> 4); }   // padded: no bank clash
+
+__global__ __launch_bounds__(kThreads) void fft_edge_kernel(FftArgs a) {
+    __shared__ double tile[kEdgeTile + kEdgeTile / 16];
+    __shared__ double excl[kThreads];
+    const int64_t s = blockIdx.x >> 1;
+    const int side = blockIdx.x & 1;
     const int64_t b = s / a.num_channels;
     const int64_t c = s % a.num_channels;
     const int64_t n = table_n(a.tab, b, a.n_all);
     const float* __restrict__ p = a.x + table_off(a.tab, b, a.window_stride) + c * a.channel_stride;
-    double sum = 0.0;
-    for (int64_t i = threadIdx.x; i < n; i += kThreads) sum += (double)p[i];
-    const double mu = n > 0 ? block_sum(sum, red) / (double)n : 0.0;
-    double e = 0.0, l1 = 0.0;
-    for (int64_t i = threadIdx.x; i < n; i += kThreads) {
-        const double y = (double)p[i] - mu;
-        e += y * y;
-        l1 += fabs(y);
-    }
-    e = block_sum(e, red);
-    l1 = block_sum(l1, red);
-    if (threadIdx.x == 0) {
-        a.fstat[4 * s] = mu;
-        a.fstat[4 * s + 1] = e;
-        a.fstat[4 * s + 2] = l1;
-        a.fstat[4 * s + 3] = 0.0;
-    }
+    const double mu = a.fstat[4 * s];
     const int64_t span = (int64_t)a.tmax + 1;
-    double* __restrict__ head = a.edge + s * 2 * span;
-    double* __restrict__ tail = head + span;
-    const int64_t per = (span + kThreads - 1) / kThreads;
-    const int64_t lo = threadIdx.x * per;
-    const int64_t hi = lo + per < span ? lo + per : span;
-    for (int side = 0; side < 2; ++side) {
-        // term k (k = 0..Tmax-1) of the running sum: y_k (head) or y_{n-1-k} (tail)
-        auto term = [&](int64_t k) -> double {
-            const int64_t i = side == 0 ? k : n - 1 - k;
-            if (k >= n || i < 0) return 0.0;
-            const double y = (double)p[i] - mu;
-            return y * y;
-        };
-        double t = 0.0;
-        for (int64_t k = lo; k < hi; ++k)
-            if (k >= 1) t += term(k - 1);
-        base[threadIdx.x] = t;
+    double* __restrict__ out = a.edge + (s * 2 + side) * span;   // out[T], T = 0..Tmax
+    if (threadIdx.x == 0) out[0] = 0.0;
+    double carry = 0.0;
+    for (int64_t k0 = 0; k0 < span - 1; k0 += kEdgeTile) {   // terms k0 .. k0 + 4095
+        for (int r = 0; r < kEdgePer; ++r) {
+            const int k = (int)threadIdx.x + r * kThreads;
+            const int64_t kk = k0 + k;
+            double t = 0.0;
+            if (kk < n && kk < span - 1) {
+                const int64_t i = side == 0 ? kk : n - 1 - kk;
+                const double y = (double)p[i] - mu;
+                t = y * y;
+            }
+            tile[edge_slot(k)] = t;
+        }
+        __syncthreads();
+        double part = 0.0;
+        for (int r = 0; r < kEdgePer; ++r) part += tile[edge_slot((int)threadIdx.x * kEdgePer + r)];
+        excl[threadIdx.x] = part;
         __syncthreads();
         if (threadIdx.x == 0) {
-            double run = 0.0;
+            double run = carry;
             for (int k = 0; k < kThreads; ++k) {
-                const double v = base[k];
-                base[k] = run;
+                const double v = excl[k];
+                excl[k] = run;
                 run += v;
             }
+            tile[kEdgeTile + kEdgeTile / 16 - 1] = run;   // carry for the next tile
         }
         __syncthreads();
-        double* __restrict__ out = side == 0 ? head : tail;
-        double run = base[threadIdx.x];
-        for (int64_t k = lo; k < hi; ++k) {
-            if (k >= 1) run += term(k - 1);
-            out[k] = run;
+        double run = excl[threadIdx.x];
+        for (int r = 0; r < kEdgePer; ++r) {
+            const int k = (int)threadIdx.x * kEdgePer + r;
+            run += tile[edge_slot(k)];
+            tile[edge_slot(k)] = run;   // sum of terms 0 .. k0 + k: the value at T = k0 + k + 1
         }
+        __syncthreads();
+        for (int r = 0; r < kEdgePer; ++r) {
+            const int k = (int)threadIdx.x + r * kThreads;
+            const int64_t t = k0 + k + 1;
+            if (t < span) out[t] = tile[edge_slot(k)];
+        }
+        carry = tile[kEdgeTile + kEdgeTile / 16 - 1];
         __syncthreads();
     }
 }
@@ -352,51 +377,64 @@ __global__ __launch_bounds__(kThreads) void fft_cols_fwd_kernel(FftArgs a) {
 // Split transform, step 2: row k1 and its mirror row L1 - k1 (frequencies k
 // and L - k pair up between them): forward row transforms, separation into
 // the two sequences' power spectra, inverse row transforms, inverse twiddles.
+// A workgroup takes 2^lgr consecutive row pairs (4096 points in LDS).
 __global__ __launch_bounds__(kThreads) void fft_rows_kernel(FftArgs a) {
-    extern __shared__ double2 lds[];   // [L2][2], slot q of point i at 2 i + q
-    const int64_t per = (int64_t(1) << (a.lg1 - 1)) + 1;
+    extern __shared__ double2 lds[];   // point i of slot q at i * 2^(lgr+1) + q
+    const int64_t per = (int64_t(1) << (a.lg1 - 1)) + 1;   // row pairs per transform
+    const int64_t wgs = (per + (1 << a.lgr) - 1) >> a.lgr;
     const int64_t id = xcd_remap(blockIdx.x, gridDim.x);
-    const int64_t pair = id / per;
+    const int64_t pair = id / wgs;
+    const int64_t g0 = (id % wgs) << a.lgr;
     const uint32_t l1 = 1u << a.lg1;
-    const uint32_t k1a = (uint32_t)(id % per);
-    const uint32_t k1b = (l1 - k1a) & (l1 - 1);
-    const bool self = k1a == k1b;
-    const int64_t ra = bitrev(k1a, a.lg1), rb = bitrev(k1b, a.lg1);
+    const int lgs = a.lgr + 1;                 // log2 of the slots
+    const int slots = 1 << lgs;
     const int l2 = 1 << a.lg2;
+    const int npts = l2 << lgs;
     double2* __restrict__ zp = a.z + pair * a.len;
-    for (int f = threadIdx.x; f < 2 * l2; f += kThreads) {
-        const int64_t row = (f & 1) ? rb : ra;
-        lds[f] = zp[row * l2 + (f >> 1)];
+    // slot q: row pair g0 + (q >> 1), side q & 1 (0: k1 = g, 1: k1 = L1 - g)
+    auto k1_of = [&](int q, bool& valid, bool& self) -> uint32_t {
+        const int64_t g = g0 + (q >> 1);
+        valid = g < per;
+        const uint32_t ka = (uint32_t)g, kb = (l1 - (uint32_t)g) & (l1 - 1);
+        self = ka == kb;
+        return (q & 1) ? kb : ka;
+    };
+    for (int f = threadIdx.x; f < npts; f += kThreads) {
+        bool valid, self;
+        const uint32_t k1 = k1_of(f & (slots - 1), valid, self);
+        lds[f] = valid ? zp[(int64_t)bitrev(k1, a.lg1) * l2 + (f >> lgs)] : make_double2(0.0, 0.0);
     }
     __syncthreads();
-    lds_fft_fwd(lds, a.lg2, 1, a.tw + a.tw_b);
+    lds_fft_fwd(lds, a.lg2, lgs, a.tw + a.tw_b);
     double2 wv[kRegPoints];
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {
         const int f = threadIdx.x + r * kThreads;
-        if (f < 2 * l2) {
-            const int q = f & 1;
-            const uint32_t k1 = q ? k1b : k1a;
-            const uint32_t k2 = bitrev(f >> 1, a.lg2);
+        if (f < npts) {
+            const int q = f & (slots - 1);
+            bool valid, self;
+            const uint32_t k1 = k1_of(q, valid, self);
+            const uint32_t k2 = bitrev(f >> lgs, a.lg2);
             const uint32_t k2m = k1 == 0 ? ((l2 - k2) & (l2 - 1)) : (l2 - 1 - k2);
-            const int qm = self ? q : 1 - q;
-            wv[r] = power_pair(lds[f], lds[2 * bitrev(k2m, a.lg2) + qm]);
+            const int qm = self ? q : (q ^ 1);
+            wv[r] = power_pair(lds[f], lds[(bitrev(k2m, a.lg2) << lgs) + qm]);
         }
     }
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {
         const int f = threadIdx.x + r * kThreads;
-        if (f < 2 * l2) lds[f] = wv[r];
+        if (f < npts) lds[f] = wv[r];
     }
     __syncthreads();
-    lds_fft_inv(lds, a.lg2, 1, a.tw + a.tw_b);
-    for (int f = threadIdx.x; f < 2 * l2; f += kThreads) {
-        const int q = f & 1;
-        if (q && self) continue;
-        const int64_t n2 = f >> 1;
-        const int64_t k1 = q ? k1b : k1a;
-        zp[(q ? rb : ra) * l2 + n2] = cmul_conj(lds[f], twiddle(a, k1 * n2));
+    lds_fft_inv(lds, a.lg2, lgs, a.tw + a.tw_b);
+    for (int f = threadIdx.x; f < npts; f += kThreads) {
+        const int q = f & (slots - 1);
+        bool valid, self;
+        const uint32_t k1 = k1_of(q, valid, self);
+        if (!valid || ((q & 1) && self)) continue;
+        const int64_t n2 = f >> lgs;
+        zp[(int64_t)bitrev(k1, a.lg1) * l2 + n2] = cmul_conj(lds[f], twiddle(a, (int64_t)k1 * n2));
     }
 }
 
@@ -551,12 +589,14 @@ FftArgs args_of(const Plan& p, const float* x, double* fstat, double* edge, doub
         a.lg1 = p.fft_log2;
         a.lg2 = 0;
         a.lgc = 0;
+        a.lgr = 0;
         a.tw_a = 0;
         a.tw_b = a.tw_lo = a.tw_hi = 0;
     } else {
         a.lg1 = __builtin_ctz((unsigned)p.fft_m1);
         a.lg2 = __builtin_ctz((unsigned)p.fft_m2);
         a.lgc = __builtin_ctz((unsigned)p.fft_cols);
+        a.lgr = a.lg2 >= 11 ? 0 : 11 - a.lg2;   // row pairs per workgroup: 4096 points
         a.tw_a = 0;
         a.tw_b = p.fft_m1 / 2;
         a.tw_lo = a.tw_b + p.fft_m2 / 2;
@@ -588,7 +628,7 @@ hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, doubl
                            reinterpret_cast<double2*>(tw), a.lg1, a.lg2, a.lg, a.lg2,
                            (int64_t)(p.fft_m2 / 2), (int64_t)p.fft_m2, (int64_t)p.fft_m1);
     }
-    hipLaunchKernelGGL(fft_prep_kernel, dim3((unsigned)a.seqs), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(fft_edge_kernel, dim3((unsigned)(2 * a.seqs)), dim3(kThreads), 0, s, a);
     if (p.fft_m2 == 1) {
         const size_t lds = sizeof(double2) * (size_t)p.fft_len;
         hipLaunchKernelGGL(fft_single_kernel, dim3((unsigned)p.fft_pairs), dim3(kThreads), lds, s,
@@ -597,8 +637,9 @@ hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, doubl
     }
     const int64_t col_groups = p.fft_pairs * (p.fft_m2 / p.fft_cols);
     const size_t lds_cols = sizeof(double2) * (size_t)p.fft_m1 * p.fft_cols;
-    const size_t lds_rows = sizeof(double2) * 2 * (size_t)p.fft_m2;
-    const int64_t row_groups = p.fft_pairs * (p.fft_m1 / 2 + 1);
+    const int64_t rp = int64_t(1) << a.lgr;
+    const size_t lds_rows = sizeof(double2) * 2 * rp * (size_t)p.fft_m2;
+    const int64_t row_groups = p.fft_pairs * ((p.fft_m1 / 2 + 1 + rp - 1) / rp);
     hipLaunchKernelGGL(fft_cols_fwd_kernel, dim3((unsigned)col_groups), dim3(kThreads), lds_cols,
                        s, a);
     hipLaunchKernelGGL(fft_rows_kernel, dim3((unsigned)row_groups), dim3(kThreads), lds_rows, s, a);

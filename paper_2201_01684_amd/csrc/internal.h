@@ -166,7 +166,9 @@ struct RollingCombineArgs {
 
 // Kernel launchers; each returns hipGetLastError() after enqueueing.
 // var: [B][C][2] = population variance, mean |x| per window and channel.
-hipError_t launch_window_stats(const Plan& p, const float* x, double* var, hipStream_t s);
+// fstat (nullable): [B*C][4] = mean, sum (x - mean)^2, sum |x - mean|, 0.
+hipError_t launch_window_stats(const Plan& p, const float* x, double* var, double* fstat,
+                               hipStream_t s);
 hipError_t launch_lag_score(const Plan& p, const float* x, double* part, hipStream_t s);
 // Sliding mode: full-block partials into `full`, cut-block partials into `cut`,
 // each [blocks*C + channel][block_chunks][lags_padded].

@@ -6,7 +6,8 @@
 //   evaluation order of the mean, and so of the variance, can stray).  The
 //   selection forms R = 2 * sum_c w_c * Var_c from it, the reference the
 //   relative-height candidate filter of Algorithm 1 is measured against in
-//   the lag domain.
+//   the lag domain.  For the FFT scores it also keeps the mean, the sum of
+//   squared deviations and the sum of absolute deviations.
 // finalize: per (window, lag), combines the fp64 chunk partials of every
 //   channel in ascending chunk order, divides by the N-T pairs and forms the
 //   weighted channel sum S(T) (the composite detection feature of Sec. 4.2).
@@ -32,14 +33,17 @@ __device__ double block_sum(double v, double* red) {
 
 __global__ __launch_bounds__(kStatsThreads) void window_stats_kernel(
     const float* __restrict__ x, double* __restrict__ var, int64_t n_all, int64_t window_stride,
-    int64_t channel_stride, int32_t num_channels, WindowTable tab) {
+    int64_t channel_stride, int32_t num_channels, WindowTable tab, double* __restrict__ fstat) {
     __shared__ double red[kStatsThreads];
     const int64_t bc = blockIdx.x;
     const int64_t b = bc / num_channels;
     const int32_t c = (int32_t)(bc % num_channels);
     const int64_t n = table_n(tab, b, n_all);
     if (n == 0) {   // empty slot of a window table
-        if (threadIdx.x == 0) var[2 * bc] = var[2 * bc + 1] = 0.0;
+        if (threadIdx.x == 0) {
+            var[2 * bc] = var[2 * bc + 1] = 0.0;
+            if (fstat) fstat[4 * bc] = fstat[4 * bc + 1] = fstat[4 * bc + 2] = fstat[4 * bc + 3] = 0.0;
+        }
         return;
     }
     const float* __restrict__ xw =
@@ -52,15 +56,23 @@ __global__ __launch_bounds__(kStatsThreads) void window_stats_kernel(
     }
     const double mean = block_sum(s, red) / (double)n;
     const double absmean = block_sum(sa, red) / (double)n;
-    double q = 0.0;
+    double q = 0.0, qa = 0.0;
     for (int64_t i = threadIdx.x; i < n; i += kStatsThreads) {
         const double d = (double)xw[i] - mean;
         q += d * d;
+        qa += fabs(d);
     }
     const double sq = block_sum(q, red);
+    const double sabs = fstat ? block_sum(qa, red) : 0.0;
     if (threadIdx.x == 0) {
         var[2 * bc] = sq / (double)n;
         var[2 * bc + 1] = absmean;
+        if (fstat) {   // the FFT scores centre each sequence by this same mean
+            fstat[4 * bc] = mean;
+            fstat[4 * bc + 1] = sq;
+            fstat[4 * bc + 2] = sabs;
+            fstat[4 * bc + 3] = 0.0;
+        }
     }
 }
 
@@ -144,10 +156,11 @@ hipError_t launch_finalize_blocks(const Plan& p, const Weights& w, const double*
     return hipGetLastError();
 }
 
-hipError_t launch_window_stats(const Plan& p, const float* x, double* var, hipStream_t s) {
+hipError_t launch_window_stats(const Plan& p, const float* x, double* var, double* fstat,
+                               hipStream_t s) {
     const int64_t groups = p.num_windows * p.num_channels;
     hipLaunchKernelGGL(window_stats_kernel, dim3((unsigned)groups), dim3(kStatsThreads), 0, s, x,
-                       var, p.n, p.window_stride, p.channel_stride, p.num_channels, p.table);
+                       var, p.n, p.window_stride, p.channel_stride, p.num_channels, p.table, fstat);
     return hipGetLastError();
 }
 
