@@ -44,7 +44,8 @@ class _Params(ctypes.Structure):
                 ("n", ctypes.c_int64), ("window_stride", ctypes.c_int64),
                 ("channel_stride", ctypes.c_int64), ("tmin", ctypes.c_int32),
                 ("tmax", ctypes.c_int32), ("c_lag", ctypes.c_double),
-                ("err_max", ctypes.c_double), ("channel_weights", ctypes.c_void_p)]
+                ("err_max", ctypes.c_double), ("channel_weights", ctypes.c_void_p),
+                ("centred", ctypes.c_int32)]
 
 
 class _Out(ctypes.Structure):
@@ -95,6 +96,8 @@ def _load():
         lib.oracle_pd_score.restype = ctypes.c_double
         lib.oracle_pd_score.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
                                         ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
+        lib.oracle_pd_score_centred.restype = ctypes.c_double
+        lib.oracle_pd_score_centred.argtypes = lib.oracle_pd_score.argtypes
         lib.oracle_pd_select.restype = None
         lib.oracle_pd_select.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
                                          ctypes.c_int32, ctypes.c_double, ctypes.c_double,
@@ -137,6 +140,7 @@ class Layout:
     c_lag: float = DEFAULT_C_LAG
     err_max: float = DEFAULT_ERR_MAX
     weights: np.ndarray | None = None
+    centred: bool = False      # score with Algorithm 2's per-sub-curve mean removal
 
     @classmethod
     def of(cls, wl, **kw) -> "Layout":
@@ -159,7 +163,7 @@ def _params(lay: Layout, keep: list) -> _Params:
         keep.append(w)
     return _Params(lay.num_windows, lay.num_channels, lay.n, lay.window_stride,
                    lay.channel_stride, lay.tmin, lay.tmax, float(lay.c_lag), float(lay.err_max),
-                   None if w is None else w.ctypes.data)
+                   None if w is None else w.ctypes.data, 1 if lay.centred else 0)
 
 
 def _as_f32(x: np.ndarray) -> np.ndarray:
@@ -217,6 +221,15 @@ def score(xw: np.ndarray, t: int, weights=None) -> float:
     w = None if weights is None else np.ascontiguousarray(weights, dtype=np.float32)
     return float(_load().oracle_pd_score(xw.ctypes.data, c, n, n, int(t),
                                          None if w is None else w.ctypes.data))
+
+
+def score_centred(xw: np.ndarray, t: int, weights=None) -> float:
+    """S_c(T), the mean-removed score, of one window given as [C][N] (or [N]) float32."""
+    xw = np.ascontiguousarray(np.atleast_2d(xw), dtype=np.float32)
+    c, n = xw.shape
+    w = None if weights is None else np.ascontiguousarray(weights, dtype=np.float32)
+    return float(_load().oracle_pd_score_centred(xw.ctypes.data, c, n, n, int(t),
+                                                 None if w is None else w.ctypes.data))
 
 
 def reference(xw: np.ndarray, weights=None) -> float:

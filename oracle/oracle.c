@@ -55,6 +55,41 @@ double oracle_pd_score(const float* x, int32_t num_channels, int64_t channel_str
     return s;
 }
 
+double oracle_pd_score_centred(const float* x, int32_t num_channels, int64_t channel_stride,
+                               int64_t n, int64_t t, const float* channel_weights) {
+    /* Algorithm 2's relative values with one group per sample: whole
+     * sub-curves of T samples, each pair of neighbours compared point by point
+     * after removing each sub-curve's own mean. */
+    double s = 0.0;
+    const int64_t pairs = n / t - 1;
+    for (int32_t c = 0; c < num_channels; ++c) {
+        const float* xc = x + (int64_t)c * channel_stride;
+        double dsum = 0.0;
+        for (int64_t i = 0; i < pairs; ++i) {
+            const float* a = xc + i * t;
+            const float* b = a + t;
+            double sa = 0.0, sb = 0.0;
+            for (int64_t j = 0; j < t; ++j) sa += (double)a[j];
+            for (int64_t j = 0; j < t; ++j) sb += (double)b[j];
+            const double mu_a = sa / (double)t, mu_b = sb / (double)t;
+            for (int64_t j = 0; j < t; ++j) {
+                const double d = ((double)a[j] - mu_a) - ((double)b[j] - mu_b);
+                dsum += d * d;
+            }
+        }
+        s += weight_of(channel_weights, c) * (dsum / (double)(pairs * t));
+    }
+    return s;
+}
+
+static double score_of(const oracle_pd_params* p, const float* xw, int64_t n, int64_t t) {
+    return p->centred
+               ? oracle_pd_score_centred(xw, p->num_channels, p->channel_stride, n, t,
+                                         p->channel_weights)
+               : oracle_pd_score(xw, p->num_channels, p->channel_stride, n, t,
+                                 p->channel_weights);
+}
+
 static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }   /* a >= 0, b > 0 */
 
 void oracle_pd_select(const double* s, int64_t n, int32_t tmin, int32_t tmax, double r,
@@ -148,9 +183,7 @@ int oracle_pd_detect(const oracle_pd_params* p, const float* x, double* scores,
             sw = s_local;
         }
 #pragma omp parallel for schedule(dynamic, 16)
-        for (int64_t j = 0; j < L; ++j)
-            sw[j] = oracle_pd_score(xw, p->num_channels, p->channel_stride, p->n, p->tmin + j,
-                                    p->channel_weights);
+        for (int64_t j = 0; j < L; ++j) sw[j] = score_of(p, xw, p->n, p->tmin + j);
         oracle_pd_select(sw, p->n, p->tmin, p->tmax, r, p->c_lag, p->err_max, &out[b]);
     }
     free(s_local);
@@ -161,11 +194,12 @@ int oracle_pd_score_list(const oracle_pd_params* p, const float* x, const int64_
                          const int32_t* t, int64_t count, double* scores_out) {
     if (check_params(p) || !x || (count > 0 && (!w || !t || !scores_out))) return -1;
     for (int64_t k = 0; k < count; ++k)
-        if (w[k] < 0 || w[k] >= p->num_windows || t[k] < 0 || (int64_t)t[k] >= p->n) return -1;
+        if (w[k] < 0 || w[k] >= p->num_windows || t[k] < 0 || (int64_t)t[k] >= p->n ||
+            (p->centred && (t[k] < 1 || 2 * (int64_t)t[k] > p->n)))
+            return -1;
 #pragma omp parallel for schedule(dynamic, 1)
     for (int64_t k = 0; k < count; ++k)
-        scores_out[k] = oracle_pd_score(x + w[k] * p->window_stride, p->num_channels,
-                                        p->channel_stride, p->n, t[k], p->channel_weights);
+        scores_out[k] = score_of(p, x + w[k] * p->window_stride, p->n, t[k]);
     return 0;
 }
 
@@ -176,9 +210,7 @@ static void detect_one(const oracle_pd_params* p, const float* xw, int64_t n, in
     const int64_t L = (int64_t)tmax - p->tmin + 1;
     double r = oracle_pd_reference(xw, p->num_channels, p->channel_stride, n, p->channel_weights);
 #pragma omp parallel for schedule(dynamic, 16)
-    for (int64_t j = 0; j < L; ++j)
-        s[j] = oracle_pd_score(xw, p->num_channels, p->channel_stride, n, p->tmin + j,
-                               p->channel_weights);
+    for (int64_t j = 0; j < L; ++j) s[j] = score_of(p, xw, n, p->tmin + j);
     oracle_pd_select(s, n, p->tmin, tmax, r, p->c_lag, p->err_max, o);
 }
 

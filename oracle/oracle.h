@@ -21,6 +21,9 @@
  *     corresponding points of adjacent sub-curves of length T (Sec. 4.1.2,
  *     Algorithm 2), taken over all N-T overlapping pairs.
  *
+ *   (with params.centred = 1 every S below is the mean-removed S_c instead;
+ *   see oracle_pd_score_centred)
+ *
  *   selection   (Algorithm 1: peak finding, relative-height candidate filter,
  *               choice of the candidate, local search around it)
  *     peaks     interior local minima Tmin < T < Tmax with
@@ -60,6 +63,7 @@ typedef struct {
     double c_lag;
     double err_max;
     const float* channel_weights;   /* C weights, or NULL for all 1 */
+    int32_t centred;                /* 1: the mean-removed score S_c below instead of S */
 } oracle_pd_params;
 
 typedef struct {
@@ -82,6 +86,21 @@ double oracle_pd_reference(const float* x, int32_t num_channels, int64_t channel
 /* S(T) of one window at one lag. */
 double oracle_pd_score(const float* x, int32_t num_channels, int64_t channel_stride,
                        int64_t n, int64_t t, const float* channel_weights);
+
+/* Mean-removed score S_c(T) of one window at one lag (Sec. 4.1.2, Algorithm 2
+ * with one group per sample: every value is taken relative to the mean of its
+ * own sub-curve before corresponding points of adjacent sub-curves are compared):
+ *
+ *   Num_T = floor(N / T) whole sub-curves; K = Num_T - 1 adjacent pairs
+ *   mu_i  = (sum_{j<T} x_c[iT + j]) / T
+ *   D_c   = sum_{i<K} sum_{j<T} ((x_c[iT+j] - mu_i) - (x_c[(i+1)T+j] - mu_{i+1}))^2
+ *   S_c(T) = sum_c w_c * (D_c / (K T))
+ *
+ * Unlike S it is unchanged by adding a linear ramp to a channel, so a drifting
+ * periodic trace still scores exactly zero at its period.  Each mean is a
+ * sequential sum divided by T, recomputed for every pair that uses it. */
+double oracle_pd_score_centred(const float* x, int32_t num_channels, int64_t channel_stride,
+                               int64_t n, int64_t t, const float* channel_weights);
 
 /* Selection rule on one window's scores s[0..L-1] (s[j] = S(tmin + j)). */
 void oracle_pd_select(const double* s, int64_t n, int32_t tmin, int32_t tmax, double r,
