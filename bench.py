@@ -41,14 +41,15 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=("detect", "fft", "rolling", "similarity"),
+    ap.add_argument("--mode", choices=("detect", "fft", "rolling", "similarity", "centred"),
                     default="detect",
                     help="detect: gpoeo_pd_detect (the default measurement); fft: the same "
                          "call with GPOEO_PD_FFT_SCORES (fp64 FFT autocorrelation scores); "
                          "rolling: "
                          "Algorithm 3's rolling detection, gpoeo_pd_detect_rolling; "
                          "similarity: Algorithm 2's grouped similarity of 5 finalist periods "
-                         "per window (the selected one, its neighbours, its double and half)")
+                         "per window (the selected one, its neighbours, its double and half); "
+                         "centred: the mean-removed score of the same 5 finalists")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a device-to-device copy of this many MiB (the reference "
                          "kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -162,7 +163,7 @@ def main():
 
     if args.mode == "rolling":
         return bench_rolling(args)
-    if args.mode == "similarity":
+    if args.mode in ("similarity", "centred"):
         return bench_similarity(args)
 
     t_gen = time.perf_counter()
@@ -289,8 +290,9 @@ def main():
 
 
 def bench_similarity(args):
-    """Algorithm 2 on finalist periods: one step is one gpoeo_pd_similarity call on
-    5 (window, period) queries per window, built from a detection run before timing."""
+    """Algorithm 2 on finalist periods: one step is one gpoeo_pd_similarity call
+    (or, with --mode centred, one gpoeo_pd_score_centred call) on 5 (window,
+    period) queries per window, built from a detection run before timing."""
     import numpy as np
     import torch
 
@@ -312,35 +314,44 @@ def bench_similarity(args):
             ts.append(t)
     wt = torch.tensor(np.asarray(ws, dtype=np.int32), device="cuda:0")
     tt = torch.tensor(np.asarray(ts, dtype=np.int32), device="cuda:0")
+    centred = args.mode == "centred"
+    call = pkg.score_centred if centred else pkg.similarity
     for _ in range(args.warmup):
-        pkg.similarity(x, desc, wt, tt)
+        call(x, desc, wt, tt)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        err = pkg.similarity(x, desc, wt, tt)
+        err = call(x, desc, wt, tt)
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / args.steps
     g = err.cpu().numpy()
     samples = sum(wl.num_channels * (wl.n // t) * t for t in ts if wl.n // t >= 2)
+    metric = ("mean-removed score evaluations/sec (Algorithm 2 relative values, 5 finalist "
+              "periods per window)" if centred else
+              "grouped-similarity evaluations/sec (Algorithm 2, 5 finalist periods per window)")
     line = {
-        "metric": "grouped-similarity evaluations/sec (Algorithm 2, 5 finalist periods per window)",
+        "metric": metric,
         "value": len(ts) / (ms / 1e3), "unit": "period evaluations/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
         "data": "synthetic",
         "config": {"workload": wl.name, "description": wl.meta["description"],
-                   "windows": wl.num_windows, "queries": len(ts), "num_groups": 3,
-                   "em_iters": 20, "sub_curve_samples": samples, "sha256": wl.sha256},
+                   "windows": wl.num_windows, "queries": len(ts),
+                   "sub_curve_samples": samples, "sha256": wl.sha256,
+                   **({} if centred else {"num_groups": 3, "em_iters": 20})},
         "roofline": None,
     }
     if not args.no_cpu_baseline:
         import oracle
-        lay = oracle.Layout.of(wl)
+        lay = oracle.Layout.of(wl, centred=centred)
         done, t_cpu, worst = 0, 0.0, 0.0
         while done < len(ts) and (done == 0 or t_cpu < args.cpu_seconds):
             k = min(len(ts), done + 5)
             t = time.perf_counter()
-            o = oracle.similarity(wl.x, lay, ws[done:k], ts[done:k])
+            if centred:
+                o = oracle.score_list(wl.x, lay, ws[done:k], ts[done:k])
+            else:
+                o = oracle.similarity(wl.x, lay, ws[done:k], ts[done:k])
             t_cpu += time.perf_counter() - t
             nz = o > 0
             if nz.any():

@@ -248,6 +248,26 @@ int gpoeo_pd_similarity(const gpoeo_pd_desc* desc, const gpoeo_pd_similarity_par
                         const float* x, const int32_t* windows, const int32_t* lags,
                         int64_t count, double* err, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Mean-removed score of finalist periods (Algorithm 2's relative values, Sec.
+ * 4.1.2, with one group per sample).  For query k, window windows[k] and
+ * candidate period T = lags[k]: floor(N / T) whole sub-curves of T samples;
+ * every adjacent pair compared point by point after removing each
+ * sub-curve's own mean,
+ *   S_c(T) = sum_c w_c * sum_{i,j} ((x[iT+j] - mu_i) - (x[(i+1)T+j] - mu_{i+1}))^2
+ *            / ((floor(N/T) - 1) T),
+ * i.e. the whole-sub-curve pair sum minus T sum_i (mu_i - mu_{i+1})^2: adding
+ * a linear drift to a channel changes no S_c.  Short lags lose most of their
+ * differences to the means, so this re-scores candidates rather than scanning
+ * every T.  score[k] = -1 when floor(N / T) < 2, NaN for a window or lag out of
+ * range.  windows, lags: device int32 [count]; score: device double [count];
+ * layout and weights from desc (its lag range is not used).  fp64 throughout.
+ * No workspace.
+ * ------------------------------------------------------------------------- */
+int gpoeo_pd_score_centred(const gpoeo_pd_desc* desc, const float* x, const int32_t* windows,
+                           const int32_t* lags, int64_t count, double* score,
+                           hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -30,6 +30,7 @@ from ._binding import (  # noqa: F401
     detect_rolling,
     rolling_params,
     similarity,
+    score_centred,
     rolling_workspace_bytes,
     load_library,
     make_desc,

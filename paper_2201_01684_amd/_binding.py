@@ -90,7 +90,8 @@ assert RESULT_DTYPE.itemsize == ctypes.sizeof(Result)
 
 EXPORTS = ("gpoeo_pd_abi_version", "gpoeo_pd_strerror", "gpoeo_pd_workspace_bytes",
            "gpoeo_pd_describe_plan", "gpoeo_pd_detect", "gpoeo_pd_detect_staged",
-           "gpoeo_pd_rolling_workspace_bytes", "gpoeo_pd_detect_rolling", "gpoeo_pd_similarity")
+           "gpoeo_pd_rolling_workspace_bytes", "gpoeo_pd_detect_rolling", "gpoeo_pd_similarity",
+           "gpoeo_pd_score_centred")
 
 _lib = None
 
@@ -129,6 +130,10 @@ def load_library():
         lib.gpoeo_pd_detect_rolling.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(RollingParams),
                                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                                 ctypes.c_size_t, ctypes.c_void_p]
+        lib.gpoeo_pd_score_centred.restype = ctypes.c_int
+        lib.gpoeo_pd_score_centred.argtypes = [ctypes.POINTER(Desc), ctypes.c_void_p,
+                                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                               ctypes.c_void_p, ctypes.c_void_p]
         lib.gpoeo_pd_similarity.restype = ctypes.c_int
         lib.gpoeo_pd_similarity.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(SimilarityParams),
                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -365,3 +370,22 @@ def similarity(x: torch.Tensor, desc: Desc, windows: torch.Tensor, lags: torch.T
     if rc != OK:
         raise GpoeoError(rc, "gpoeo_pd_similarity")
     return err
+
+
+def score_centred(x: torch.Tensor, desc: Desc, windows: torch.Tensor, lags: torch.Tensor,
+                  stream=None) -> torch.Tensor:
+    """Mean-removed score S_c(T) for (windows[k], lags[k]) (int32 GPU tensors); returns a
+    float64 GPU tensor (-1: fewer than two sub-curves, NaN: out of range)."""
+    if windows.dtype != torch.int32 or lags.dtype != torch.int32:
+        raise TypeError("windows and lags must be int32 tensors")
+    if windows.shape != lags.shape or windows.dim() != 1:
+        raise ValueError("windows and lags must be 1-D and of equal length")
+    windows, lags = windows.contiguous(), lags.contiguous()
+    out = torch.empty(windows.shape, dtype=torch.float64, device=x.device)
+    rc = load_library().gpoeo_pd_score_centred(ctypes.byref(desc), x.data_ptr(),
+                                               windows.data_ptr(), lags.data_ptr(),
+                                               int(windows.numel()), out.data_ptr(),
+                                               _stream_handle(stream))
+    if rc != OK:
+        raise GpoeoError(rc, "gpoeo_pd_score_centred")
+    return out

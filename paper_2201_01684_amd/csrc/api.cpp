@@ -568,3 +568,18 @@ extern "C" int gpoeo_pd_similarity(const gpoeo_pd_desc* desc,
         return GPOEO_PD_EHIP;
     return GPOEO_PD_OK;
 }
+
+extern "C" int gpoeo_pd_score_centred(const gpoeo_pd_desc* desc, const float* x,
+                                      const int32_t* windows, const int32_t* lags, int64_t count,
+                                      double* score, hipStream_t stream) {
+    gpoeo::Plan p;
+    const int rc = gpoeo::make_plan(desc, &p);
+    if (rc != GPOEO_PD_OK) return rc;
+    if (count < 0 || count > INT32_MAX) return GPOEO_PD_EINVAL;
+    if (count == 0) return GPOEO_PD_OK;
+    if (!x || !windows || !lags || !score) return GPOEO_PD_EINVAL;
+    if (gpoeo::launch_centred(p, weights_of(desc, p.num_channels), x, windows, lags, count, score,
+                              stream) != hipSuccess)
+        return GPOEO_PD_EHIP;
+    return GPOEO_PD_OK;
+}

@@ -197,6 +197,8 @@ hipError_t launch_rolling_schedule(const Plan& p, const RollingConfig& rc,
                                    int32_t* tab_tmax, RollState* state, hipStream_t s);
 hipError_t launch_rolling_combine(const RollingCombineArgs& a, const Weights& w,
                                   int64_t num_windows, hipStream_t s);
+hipError_t launch_centred(const Plan& p, const Weights& w, const float* x, const int32_t* windows,
+                          const int32_t* lags, int64_t count, double* out, hipStream_t s);
 hipError_t launch_similarity(const Plan& p, const Weights& w, int32_t groups, int32_t iters,
                              const float* x, const int32_t* windows, const int32_t* lags,
                              int64_t count, double* err, hipStream_t s);
