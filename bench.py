@@ -120,7 +120,7 @@ def fft_stage_bytes(wl) -> float:
     first and last Tmax samples of each sequence read and their head and tail
     sums written and read back, each pair's complex fp64 transform written by
     the column kernel, read and written by the row kernel and read by the
-    inverse column kernel (none of that up to 4096 points, where a pair stays
+    inverse column kernel (none of that up to 2048 points, where a pair stays
     in LDS), and the per-channel D(T) written."""
     s = wl.num_windows * wl.num_channels
     pairs = (s + 1) // 2
@@ -128,7 +128,7 @@ def fft_stage_bytes(wl) -> float:
     while length < wl.n + wl.tmax:
         length *= 2
     lags = wl.tmax - wl.tmin + 1
-    sweeps = 0 if length <= 4096 else 4
+    sweeps = 0 if length <= 2048 else 4
     edges = 2 * 4 * s * wl.tmax + 2 * 8 * s * (wl.tmax + 1) + 2 * 8 * s * lags
     return float(4 * s * wl.n + edges + sweeps * 16 * pairs * length + 8 * s * lags)
 

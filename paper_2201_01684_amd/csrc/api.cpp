@@ -89,15 +89,16 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
         if (lg > kFftMaxLog2) return GPOEO_PD_EINVAL;
         p->fft_log2 = lg;
         p->fft_len = int64_t(1) << lg;
-        if (lg <= 12) {
+        const int tile = fft_tile_log2(lg);
+        if (lg <= tile) {
             p->fft_m1 = (int32_t)p->fft_len;
             p->fft_m2 = 1;
             p->fft_cols = 1;
         } else {
-            const int32_t lg1 = lg / 2, lg2 = lg - lg1;   // row transforms of at most 2^11
+            const int32_t lg1 = lg / 2, lg2 = lg - lg1;   // a row pair fits one tile
             p->fft_m1 = 1 << lg1;
             p->fft_m2 = 1 << lg2;
-            p->fft_cols = std::min<int32_t>(p->fft_m2, 1 << (12 - lg1));
+            p->fft_cols = std::min<int32_t>(p->fft_m2, 1 << (tile - lg1));
         }
     }
 

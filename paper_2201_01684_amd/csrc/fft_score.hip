@@ -34,9 +34,9 @@
 namespace gpoeo {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kLdsPoints = 4096;           // complex fp64 points per workgroup: 64 KiB
-constexpr int kRegPoints = kLdsPoints / kThreads;
+constexpr int kThreads = 256;                          // edge and fix-up kernels
+constexpr int kTThreads = 1 << kFftThreadsLog2;        // transform kernels
+
 
 struct FftArgs {
     const float* x;
@@ -97,7 +97,7 @@ __device__ __forceinline__ void fft_pass(double2* s, int lg, int lgc, int st_lo,
     const int cols = 1 << lgc;
     const int groups = 1 << (lg - R + lgc);
     const int lo_mask = (1 << st_lo) - 1;
-    for (int gi = threadIdx.x; gi < groups; gi += kThreads) {
+    for (int gi = threadIdx.x; gi < groups; gi += kTThreads) {
         const int q = gi & (cols - 1);
         const int g = gi >> lgc;
         const int blo = g & lo_mask;
@@ -133,7 +133,7 @@ __device__ __forceinline__ void fft_pass(double2* s, int lg, int lgc, int st_lo,
 
 template <bool kInverse>
 __device__ void lds_fft(double2* s, int lg, int lgc, const double2* __restrict__ tw) {
-    int rmax = lg + lgc - 8;   // log2 of the points per thread
+    int rmax = lg + lgc - kFftThreadsLog2;   // log2 of the points per thread
     rmax = rmax < 1 ? 1 : (rmax > 4 ? 4 : rmax);
     const int np = (lg + rmax - 1) / rmax;
     const int base = lg / np, extra = lg % np;
@@ -311,21 +311,23 @@ __global__ void fft_twiddle_kernel(double2* tw, int lga, int lgb, int lg, int lg
 }
 
 // Whole transform of one pair in one workgroup (L <= 2^12).
-__global__ __launch_bounds__(kThreads) void fft_single_kernel(FftArgs a) {
+template <int kTile>
+__global__ __launch_bounds__(kTThreads) void fft_single_kernel(FftArgs a) {
+    constexpr int kRegPoints = (1 << kTile) / kTThreads;
     extern __shared__ double2 lds[];
     const int64_t pair = blockIdx.x;
     const Seq qa = seq_of(a, 2 * pair), qb = seq_of(a, 2 * pair + 1);
     const int lg = a.lg;
     const int len = 1 << lg;
     const double2* tw = a.tw + a.tw_a;
-    for (int i = threadIdx.x; i < len; i += kThreads)
+    for (int i = threadIdx.x; i < len; i += kTThreads)
         lds[i] = make_double2(centred(qa, i), centred(qb, i));
     __syncthreads();
     lds_fft_fwd(lds, lg, 0, tw);
     double2 wv[kRegPoints];
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {
-        const int pos = threadIdx.x + r * kThreads;
+        const int pos = threadIdx.x + r * kTThreads;
         if (pos < len) {
             const uint32_t k = bitrev(pos, lg);
             const uint32_t km = (len - k) & (len - 1);
@@ -335,12 +337,12 @@ __global__ __launch_bounds__(kThreads) void fft_single_kernel(FftArgs a) {
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {
-        const int pos = threadIdx.x + r * kThreads;
+        const int pos = threadIdx.x + r * kTThreads;
         if (pos < len) lds[pos] = wv[r];
     }
     __syncthreads();
     lds_fft_inv(lds, lg, 0, tw);
-    for (int64_t t = a.tmin + threadIdx.x; t <= a.tmax; t += kThreads) {
+    for (int64_t t = a.tmin + threadIdx.x; t <= a.tmax; t += kTThreads) {
         write_d(a, 2 * pair, t, lds[t].x);
         write_d(a, 2 * pair + 1, t, lds[t].y);
     }
@@ -349,7 +351,9 @@ __global__ __launch_bounds__(kThreads) void fft_single_kernel(FftArgs a) {
 // Split transform, step 1: column transforms (L1 points, stride L2) of
 // 2^lgc neighbouring columns, then the twiddles W_L^(k1 n2).  Row p of the
 // output holds frequency k1 = bitrev(p).
-__global__ __launch_bounds__(kThreads) void fft_cols_fwd_kernel(FftArgs a) {
+template <int kTile>
+__global__ __launch_bounds__(kTThreads) void fft_cols_fwd_kernel(FftArgs a) {
+    constexpr int kRegPoints = (1 << kTile) / kTThreads;
     extern __shared__ double2 lds[];
     const int64_t groups = int64_t(1) << (a.lg2 - a.lgc);
     const int64_t id = xcd_remap(blockIdx.x, gridDim.x);
@@ -359,14 +363,14 @@ __global__ __launch_bounds__(kThreads) void fft_cols_fwd_kernel(FftArgs a) {
     const int npts = (1 << a.lg1) * cols;
     const int64_t l2 = int64_t(1) << a.lg2;
     const Seq qa = seq_of(a, 2 * pair), qb = seq_of(a, 2 * pair + 1);
-    for (int f = threadIdx.x; f < npts; f += kThreads) {
+    for (int f = threadIdx.x; f < npts; f += kTThreads) {
         const int64_t i = (int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1));
         lds[f] = make_double2(centred(qa, i), centred(qb, i));
     }
     __syncthreads();
     lds_fft_fwd(lds, a.lg1, a.lgc, a.tw + a.tw_a);
     double2* __restrict__ zp = a.z + pair * a.len;
-    for (int f = threadIdx.x; f < npts; f += kThreads) {
+    for (int f = threadIdx.x; f < npts; f += kTThreads) {
         const int pos = f >> a.lgc;
         const int64_t n2 = c0 + (f & (cols - 1));
         const int64_t k1 = bitrev(pos, a.lg1);
@@ -378,7 +382,9 @@ __global__ __launch_bounds__(kThreads) void fft_cols_fwd_kernel(FftArgs a) {
 // and L - k pair up between them): forward row transforms, separation into
 // the two sequences' power spectra, inverse row transforms, inverse twiddles.
 // A workgroup takes 2^lgr consecutive row pairs (4096 points in LDS).
-__global__ __launch_bounds__(kThreads) void fft_rows_kernel(FftArgs a) {
+template <int kTile>
+__global__ __launch_bounds__(kTThreads) void fft_rows_kernel(FftArgs a) {
+    constexpr int kRegPoints = (1 << kTile) / kTThreads;
     extern __shared__ double2 lds[];   // point i of slot q at i * 2^(lgr+1) + q
     const int64_t per = (int64_t(1) << (a.lg1 - 1)) + 1;   // row pairs per transform
     const int64_t wgs = (per + (1 << a.lgr) - 1) >> a.lgr;
@@ -399,7 +405,7 @@ __global__ __launch_bounds__(kThreads) void fft_rows_kernel(FftArgs a) {
         self = ka == kb;
         return (q & 1) ? kb : ka;
     };
-    for (int f = threadIdx.x; f < npts; f += kThreads) {
+    for (int f = threadIdx.x; f < npts; f += kTThreads) {
         bool valid, self;
         const uint32_t k1 = k1_of(f & (slots - 1), valid, self);
         lds[f] = valid ? zp[(int64_t)bitrev(k1, a.lg1) * l2 + (f >> lgs)] : make_double2(0.0, 0.0);
@@ -409,7 +415,7 @@ __global__ __launch_bounds__(kThreads) void fft_rows_kernel(FftArgs a) {
     double2 wv[kRegPoints];
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {
-        const int f = threadIdx.x + r * kThreads;
+        const int f = threadIdx.x + r * kTThreads;
         if (f < npts) {
             const int q = f & (slots - 1);
             bool valid, self;
@@ -423,12 +429,12 @@ __global__ __launch_bounds__(kThreads) void fft_rows_kernel(FftArgs a) {
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {
-        const int f = threadIdx.x + r * kThreads;
+        const int f = threadIdx.x + r * kTThreads;
         if (f < npts) lds[f] = wv[r];
     }
     __syncthreads();
     lds_fft_inv(lds, a.lg2, lgs, a.tw + a.tw_b);
-    for (int f = threadIdx.x; f < npts; f += kThreads) {
+    for (int f = threadIdx.x; f < npts; f += kTThreads) {
         const int q = f & (slots - 1);
         bool valid, self;
         const uint32_t k1 = k1_of(q, valid, self);
@@ -441,7 +447,9 @@ __global__ __launch_bounds__(kThreads) void fft_rows_kernel(FftArgs a) {
 // Split transform, step 3: inverse column transforms (row p holds k1 =
 // bitrev(p): the bit-reversed input order of the decimation in time), and
 // D(T) for the lags T = n1 L2 + n2 in [tmin, tmax].
-__global__ __launch_bounds__(kThreads) void fft_cols_inv_kernel(FftArgs a) {
+template <int kTile>
+__global__ __launch_bounds__(kTThreads) void fft_cols_inv_kernel(FftArgs a) {
+    constexpr int kRegPoints = (1 << kTile) / kTThreads;
     extern __shared__ double2 lds[];
     const int64_t groups = int64_t(1) << (a.lg2 - a.lgc);
     const int64_t id = xcd_remap(blockIdx.x, gridDim.x);
@@ -451,12 +459,12 @@ __global__ __launch_bounds__(kThreads) void fft_cols_inv_kernel(FftArgs a) {
     const int npts = (1 << a.lg1) * cols;
     const int64_t l2 = int64_t(1) << a.lg2;
     const double2* __restrict__ zp = a.z + pair * a.len;
-    for (int f = threadIdx.x; f < npts; f += kThreads)
+    for (int f = threadIdx.x; f < npts; f += kTThreads)
         lds[f] = zp[(int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1))];
     __syncthreads();
     lds_fft_inv(lds, a.lg1, a.lgc, a.tw + a.tw_a);
     const int rows = (int)(a.tmax / l2) + 1;
-    for (int f = threadIdx.x; f < rows * cols; f += kThreads) {
+    for (int f = threadIdx.x; f < rows * cols; f += kTThreads) {
         const int64_t t = (int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1));
         write_d(a, 2 * pair, t, lds[f].x);
         write_d(a, 2 * pair + 1, t, lds[f].y);
@@ -596,13 +604,35 @@ FftArgs args_of(const Plan& p, const float* x, double* fstat, double* edge, doub
         a.lg1 = __builtin_ctz((unsigned)p.fft_m1);
         a.lg2 = __builtin_ctz((unsigned)p.fft_m2);
         a.lgc = __builtin_ctz((unsigned)p.fft_cols);
-        a.lgr = a.lg2 >= 11 ? 0 : 11 - a.lg2;   // row pairs per workgroup: 4096 points
+        const int tile = fft_tile_log2(a.lg);
+        a.lgr = a.lg2 >= tile - 1 ? 0 : tile - 1 - a.lg2;   // row pairs per tile
         a.tw_a = 0;
         a.tw_b = p.fft_m1 / 2;
         a.tw_lo = a.tw_b + p.fft_m2 / 2;
         a.tw_hi = a.tw_lo + p.fft_m2;
     }
     return a;
+}
+
+template <int kTile>
+void launch_transforms(const Plan& p, const FftArgs& a, hipStream_t s) {
+    if (p.fft_m2 == 1) {
+        const size_t lds = sizeof(double2) * (size_t)p.fft_len;
+        hipLaunchKernelGGL(fft_single_kernel<kTile>, dim3((unsigned)p.fft_pairs), dim3(kTThreads),
+                           lds, s, a);
+        return;
+    }
+    const int64_t col_groups = p.fft_pairs * (p.fft_m2 / p.fft_cols);
+    const size_t lds_cols = sizeof(double2) * (size_t)p.fft_m1 * p.fft_cols;
+    const int64_t rp = int64_t(1) << a.lgr;
+    const size_t lds_rows = sizeof(double2) * 2 * rp * (size_t)p.fft_m2;
+    const int64_t row_groups = p.fft_pairs * ((p.fft_m1 / 2 + 1 + rp - 1) / rp);
+    hipLaunchKernelGGL(fft_cols_fwd_kernel<kTile>, dim3((unsigned)col_groups), dim3(kTThreads),
+                       lds_cols, s, a);
+    hipLaunchKernelGGL(fft_rows_kernel<kTile>, dim3((unsigned)row_groups), dim3(kTThreads),
+                       lds_rows, s, a);
+    hipLaunchKernelGGL(fft_cols_inv_kernel<kTile>, dim3((unsigned)col_groups), dim3(kTThreads),
+                       lds_cols, s, a);
 }
 
 }  // namespace
@@ -629,22 +659,10 @@ hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, doubl
                            (int64_t)(p.fft_m2 / 2), (int64_t)p.fft_m2, (int64_t)p.fft_m1);
     }
     hipLaunchKernelGGL(fft_edge_kernel, dim3((unsigned)(2 * a.seqs)), dim3(kThreads), 0, s, a);
-    if (p.fft_m2 == 1) {
-        const size_t lds = sizeof(double2) * (size_t)p.fft_len;
-        hipLaunchKernelGGL(fft_single_kernel, dim3((unsigned)p.fft_pairs), dim3(kThreads), lds, s,
-                           a);
-        return hipGetLastError();
-    }
-    const int64_t col_groups = p.fft_pairs * (p.fft_m2 / p.fft_cols);
-    const size_t lds_cols = sizeof(double2) * (size_t)p.fft_m1 * p.fft_cols;
-    const int64_t rp = int64_t(1) << a.lgr;
-    const size_t lds_rows = sizeof(double2) * 2 * rp * (size_t)p.fft_m2;
-    const int64_t row_groups = p.fft_pairs * ((p.fft_m1 / 2 + 1 + rp - 1) / rp);
-    hipLaunchKernelGGL(fft_cols_fwd_kernel, dim3((unsigned)col_groups), dim3(kThreads), lds_cols,
-                       s, a);
-    hipLaunchKernelGGL(fft_rows_kernel, dim3((unsigned)row_groups), dim3(kThreads), lds_rows, s, a);
-    hipLaunchKernelGGL(fft_cols_inv_kernel, dim3((unsigned)col_groups), dim3(kThreads), lds_cols,
-                       s, a);
+    if (fft_tile_log2(a.lg) == kFftSmallTileLog2)
+        launch_transforms<kFftSmallTileLog2>(p, a, s);
+    else
+        launch_transforms<kFftTileLog2>(p, a, s);
     return hipGetLastError();
 }
 

@@ -23,8 +23,15 @@ constexpr double kScoreRelBound = 2.5e-5;
 // in fp64 before the selection.
 constexpr double kFftRelBound = 1e-6;
 
-// Largest transform of the FFT path (complex fp64 points per pair of sequences).
-constexpr int kFftMaxLog2 = 22;
+// FFT path: complex fp64 points per transform workgroup (held in LDS): 2^11
+// (32 KiB, four workgroups per CU) for transforms up to 2^20 points, 2^12
+// beyond (a row pair must fit one tile); threads per transform workgroup;
+// the largest transform.
+constexpr int kFftSmallTileLog2 = 11;
+constexpr int kFftTileLog2 = 12;
+constexpr int kFftThreadsLog2 = 8;
+constexpr int kFftMaxLog2 = 2 * (kFftTileLog2 - 1);
+inline int fft_tile_log2(int lg) { return lg <= 2 * (kFftSmallTileLog2 - 1) ? kFftSmallTileLog2 : kFftTileLog2; }
 
 struct Weights {
     float w[kMaxChannels];
