@@ -3,7 +3,8 @@
 The FFT path promises every score within 1e-6 relative of the exact value
 (lags its error bound cannot certify are re-scored in fp64 first), exact
 zeros where the oracle has them, and selections identical to the oracle's.
-Covered: the one-workgroup transform (up to 4096 points) and the split one,
+Covered: the one-workgroup transform (up to 2048 points), the split one with
+2048-point tiles and, beyond 2^20 points, with 4096-point tiles,
 an odd number of sequences (one transform carries a single sequence),
 weighted channels, exactly periodic windows (every multiple of the period
 re-scored), a window table (rolling detection), scores only, determinism, and
@@ -50,15 +51,16 @@ def fft_parity(x, lay, where="", flags=0):
 
 def test_plan_modes():
     import paper_2201_01684_amd as pkg
-    for n, tmax, mode in [(2000, 1000, "single"), (4096, 1024, "split")]:
+    for n, tmax, mode in [(1500, 500, "single"), (4096, 1024, "split")]:
         desc, _ = pkg.make_desc(1, 1, n, n, n, 2, tmax, flags=fft_flag())
         assert pkg.describe_plan(desc)["mode"] == 2, mode
 
 
 @pytest.mark.parametrize("n,tmin,tmax", [
     (8, 1, 4),            # smallest window: 64-point transform
-    (2000, 2, 1000),      # 4096 points, one workgroup
-    (4096, 1, 2048),      # 8192 points: the split transform
+    (1500, 2, 500),       # 2048 points: the largest one-workgroup transform
+    (2000, 2, 1000),      # 4096 points: the smallest split transform
+    (4096, 1, 2048),      # 8192 points
     (4099, 3, 2049),      # ragged N
     (3000, 1021, 1500),   # lag range far from zero
     (20000, 6, 3333),
@@ -181,3 +183,21 @@ def test_full_size(name):
         o_scores, o_out = oracle.detect(sub, lay1)
         check_fft_scores(gf[b:b + 1].astype(np.float64), o_scores, f"fft {name} window {b}")
         check_results(rf[b:b + 1], o_out, f"fft {name} window {b}")
+
+
+def test_transform_beyond_2_20_points_uses_the_large_tile():
+    # N + Tmax = 1,100,000 > 2^20: a 2^21-point transform, row pairs of 2^11
+    # points in 4096-point tiles
+    import paper_2201_01684_amd as pkg
+    n, tmax = 1_000_000, 100_000
+    x = planted_trace(n, 3001, 9, seed=21, sigma=2.0)
+    lay = oracle.Layout(1, 1, n, n, n, 2, tmax)
+    g, res = gpu_run(x, lay, flags=fft_flag())
+    gd, rd = gpu_run(x, lay)
+    for f in ("period", "verdict", "t_cand", "t_low", "t_up", "n_candidates"):
+        assert np.array_equal(res[f], rd[f]), f
+    assert res["period"][0] == 3001
+    rng = np.random.default_rng(2)
+    ts = np.concatenate([rng.integers(2, tmax + 1, size=48), [2, 3001, 6002, tmax]])
+    o = oracle.score_list(x, lay, np.zeros(ts.size, dtype=np.int64), ts)
+    check_fft_scores(g[0, ts - 2], o, "2^21-point transform")
