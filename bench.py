@@ -50,6 +50,8 @@ def parse():
                          "similarity: Algorithm 2's grouped similarity of 5 finalist periods "
                          "per window (the selected one, its neighbours, its double and half); "
                          "centred: the mean-removed score of the same 5 finalists")
+    ap.add_argument("--fft-scores", action="store_true",
+                    help="rolling mode: score with GPOEO_PD_FFT_SCORES")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a device-to-device copy of this many MiB (the reference "
                          "kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -377,7 +379,8 @@ def bench_rolling(args):
     wl = make_workload(args.workload)
     x = torch.from_numpy(wl.x).to("cuda:0")
     desc, keep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
-                               wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights)
+                               wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights,
+                               flags=pkg.FFT_SCORES if args.fft_scores else 0)
     params = pkg.rolling_params()
     det = pkg.RollingDetector(x, desc, params, keep)
     for _ in range(args.warmup):
@@ -399,7 +402,8 @@ def bench_rolling(args):
                    "windows": wl.num_windows, "channels": wl.num_channels, "n": wl.n,
                    "tmin": wl.tmin, "tmax": wl.tmax, "sha256": wl.sha256,
                    "c_measure": params.c_measure, "step": params.step, "c_eval": params.c_eval,
-                   "diff_threshold": params.diff_threshold},
+                   "diff_threshold": params.diff_threshold,
+                   "scoring": "fp64 FFT autocorrelation" if args.fft_scores else "direct"},
         "stable_windows": int(np.count_nonzero(res["stable"])),
         "mean_suffix_windows": float(res["n_windows"].mean()),
         "windows_flagged_unresolved": int(np.count_nonzero(res["flags"])),
