@@ -31,6 +31,32 @@ __device__ double block_sum(double v, double* red) {
     return r;
 }
 
+// Visits x[0..n) once in a fixed order per thread: a scalar head up to 16-byte
+// alignment, then 16-byte groups (thread t takes groups t, t + 256, ..., four
+// loads in flight), then a scalar tail.
+template <typename F>
+__device__ __forceinline__ void visit(const float* __restrict__ xw, int64_t n, F&& f) {
+    const int64_t mis = (int64_t)((reinterpret_cast<uintptr_t>(xw) >> 2) & 3);
+    const int64_t head = ((4 - mis) & 3) < n ? ((4 - mis) & 3) : n;
+    for (int64_t i = threadIdx.x; i < head; i += kStatsThreads) f(xw[i]);
+    const float4* __restrict__ v = reinterpret_cast<const float4*>(xw + head);
+    const int64_t groups = (n - head) >> 2;
+    int64_t g = threadIdx.x;
+    for (; g + 3 * kStatsThreads < groups; g += 4 * kStatsThreads) {
+        const float4 a = v[g], b = v[g + kStatsThreads], c = v[g + 2 * kStatsThreads],
+                     d = v[g + 3 * kStatsThreads];
+        f(a.x); f(a.y); f(a.z); f(a.w);
+        f(b.x); f(b.y); f(b.z); f(b.w);
+        f(c.x); f(c.y); f(c.z); f(c.w);
+        f(d.x); f(d.y); f(d.z); f(d.w);
+    }
+    for (; g < groups; g += kStatsThreads) {
+        const float4 a = v[g];
+        f(a.x); f(a.y); f(a.z); f(a.w);
+    }
+    for (int64_t i = head + (groups << 2) + threadIdx.x; i < n; i += kStatsThreads) f(xw[i]);
+}
+
 __global__ __launch_bounds__(kStatsThreads) void window_stats_kernel(
     const float* __restrict__ x, double* __restrict__ var, int64_t n_all, int64_t window_stride,
     int64_t channel_stride, int32_t num_channels, WindowTable tab, double* __restrict__ fstat) {
@@ -49,19 +75,19 @@ __global__ __launch_bounds__(kStatsThreads) void window_stats_kernel(
     const float* __restrict__ xw =
         x + table_off(tab, b, window_stride) + (int64_t)c * channel_stride;
     double s = 0.0, sa = 0.0;
-    for (int64_t i = threadIdx.x; i < n; i += kStatsThreads) {
-        const double v = (double)xw[i];
+    visit(xw, n, [&](float x) {
+        const double v = (double)x;
         s += v;
         sa += fabs(v);
-    }
+    });
     const double mean = block_sum(s, red) / (double)n;
     const double absmean = block_sum(sa, red) / (double)n;
     double q = 0.0, qa = 0.0;
-    for (int64_t i = threadIdx.x; i < n; i += kStatsThreads) {
-        const double d = (double)xw[i] - mean;
+    visit(xw, n, [&](float x) {
+        const double d = (double)x - mean;
         q += d * d;
         qa += fabs(d);
-    }
+    });
     const double sq = block_sum(q, red);
     const double sabs = fstat ? block_sum(qa, red) : 0.0;
     if (threadIdx.x == 0) {
