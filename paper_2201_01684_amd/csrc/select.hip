@@ -48,7 +48,10 @@ using exact::exact_score;
 using exact::reference_bound;
 using exact::wave_score;
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 256;       // re-score and initialisation kernels and short windows
+// Selection passes run one workgroup per window; from this many lags on, four
+// times as many threads keep more of a window's scores in flight.
+constexpr int kWideLags = 4096;
 constexpr int kRescoreGroups = 1024;   // workgroups of one re-score round
 
 struct SelectArgs {
@@ -94,10 +97,11 @@ __device__ __forceinline__ Tri le(const Iv& a, const Iv& b) {
     return kUnk;
 }
 
+template <int kT>
 __device__ double block_min_d(double v, double* red) {
     red[threadIdx.x] = v;
     __syncthreads();
-    for (int w = kThreads / 2; w > 0; w >>= 1) {
+    for (int w = kT / 2; w > 0; w >>= 1) {
         if ((int)threadIdx.x < w) red[threadIdx.x] = fmin(red[threadIdx.x], red[threadIdx.x + w]);
         __syncthreads();
     }
@@ -106,10 +110,11 @@ __device__ double block_min_d(double v, double* red) {
     return r;
 }
 
+template <int kT>
 __device__ int64_t block_sum_i(int64_t v, int64_t* red) {
     red[threadIdx.x] = v;
     __syncthreads();
-    for (int w = kThreads / 2; w > 0; w >>= 1) {
+    for (int w = kT / 2; w > 0; w >>= 1) {
         if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
         __syncthreads();
     }
@@ -118,10 +123,11 @@ __device__ int64_t block_sum_i(int64_t v, int64_t* red) {
     return r;
 }
 
+template <int kT>
 __device__ int64_t block_min_i(int64_t v, int64_t* red) {
     red[threadIdx.x] = v;
     __syncthreads();
-    for (int w = kThreads / 2; w > 0; w >>= 1) {
+    for (int w = kT / 2; w > 0; w >>= 1) {
         if ((int)threadIdx.x < w) red[threadIdx.x] = min(red[threadIdx.x], red[threadIdx.x + w]);
         __syncthreads();
     }
@@ -131,18 +137,20 @@ __device__ int64_t block_min_i(int64_t v, int64_t* red) {
 }
 
 
+template <int kT>
 struct Shared {
-    double red_d[kThreads];
-    double red_d2[kThreads];
-    int64_t red_i[kThreads];
-    int64_t red_j[kThreads];
+    double red_d[kT];
+    double red_d2[kT];
+    int64_t red_i[kT];
+    int64_t red_j[kT];
     int done;
     double r_approx;
     double r_err;
 };
 
-__global__ __launch_bounds__(kThreads) void select_pass_kernel(SelectArgs a, Weights w) {
-    __shared__ Shared sh;
+template <int kSelThreads>
+__global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, Weights w) {
+    __shared__ Shared<kSelThreads> sh;
     const int tid = threadIdx.x;
     const int64_t b = blockIdx.x;
     const int32_t tmin = a.tmin;
@@ -262,7 +270,7 @@ __global__ __launch_bounds__(kThreads) void select_pass_kernel(SelectArgs a, Wei
         // are left open.
         int64_t npk = 0, unk = 0;
         double pk_lo = INFINITY, pk_hi = INFINITY, unk_lo = INFINITY;
-        for (int64_t t = tmin + 1 + tid; t < tmax; t += kThreads) {
+        for (int64_t t = tmin + 1 + tid; t < tmax; t += kSelThreads) {
             Iv z;
             const Tri q = peak(t, z, false);
             if (q == kYes) {
@@ -274,16 +282,16 @@ __global__ __launch_bounds__(kThreads) void select_pass_kernel(SelectArgs a, Wei
                 unk_lo = fmin(unk_lo, z.lo);
             }
         }
-        unk = block_sum_i(unk, sh.red_i);
-        npk = block_sum_i(npk, sh.red_j);
-        pk_lo = block_min_d(pk_lo, sh.red_d);
-        pk_hi = block_min_d(pk_hi, sh.red_d2);
-        unk_lo = block_min_d(unk_lo, sh.red_d);
+        unk = block_sum_i<kSelThreads>(unk, sh.red_i);
+        npk = block_sum_i<kSelThreads>(npk, sh.red_j);
+        pk_lo = block_min_d<kSelThreads>(pk_lo, sh.red_d);
+        pk_hi = block_min_d<kSelThreads>(pk_hi, sh.red_d2);
+        unk_lo = block_min_d<kSelThreads>(unk_lo, sh.red_d);
         if (unk > 0) {
             const double cut =
                 npk > 0 ? fmax(r_hi - c_lag * (r_hi - pk_hi) + ulp4 * r_hi, pk_hi) : INFINITY;
             if (unk_lo < cut) {
-                for (int64_t t = tmin + 1 + tid; t < tmax; t += kThreads) {
+                for (int64_t t = tmin + 1 + tid; t < tmax; t += kSelThreads) {
                     Iv z;
                     if (peak(t, z, false) == kUnk && z.lo < cut) peak(t, z, true);
                 }
@@ -306,7 +314,7 @@ __global__ __launch_bounds__(kThreads) void select_pass_kernel(SelectArgs a, Wei
         thr.exact = thr.lo == thr.hi;
         int64_t ncand = 0, tc = INT64_MAX;
         unk = 0;
-        for (int64_t t = tmin + 1 + tid; t < tmax; t += kThreads) {
+        for (int64_t t = tmin + 1 + tid; t < tmax; t += kSelThreads) {
             Iv z;
             if (peak(t, z, false) != kYes) continue;
             const Tri q = lt(z, thr);
@@ -318,15 +326,15 @@ __global__ __launch_bounds__(kThreads) void select_pass_kernel(SelectArgs a, Wei
                 push(t, z);
             }
         }
-        unk = block_sum_i(unk, sh.red_i);
-        ncand = block_sum_i(ncand, sh.red_j);
-        tc = block_min_i(tc, sh.red_i);
+        unk = block_sum_i<kSelThreads>(unk, sh.red_i);
+        ncand = block_sum_i<kSelThreads>(ncand, sh.red_j);
+        tc = block_min_i<kSelThreads>(tc, sh.red_i);
         if (unk > 0) {
             // the threshold must tighten too: R and every peak that can be
             // the smallest one
             if (r_lo != r_hi && tid == 0 && may_push) want_r();
             if (pk_lo != pk_hi) {
-                for (int64_t t = tmin + 1 + tid; t < tmax; t += kThreads) {
+                for (int64_t t = tmin + 1 + tid; t < tmax; t += kSelThreads) {
                     Iv z;
                     if (peak(t, z, false) == kYes && z.lo <= pk_hi) push(t, z);
                 }
@@ -348,10 +356,10 @@ __global__ __launch_bounds__(kThreads) void select_pass_kernel(SelectArgs a, Wei
         o.t_low = (int32_t)lo;
         o.t_up = (int32_t)hi;
         double m_hi = INFINITY;
-        for (int64_t t = lo + tid; t <= hi; t += kThreads) m_hi = fmin(m_hi, iv(t).hi);
-        m_hi = block_min_d(m_hi, sh.red_d);
+        for (int64_t t = lo + tid; t <= hi; t += kSelThreads) m_hi = fmin(m_hi, iv(t).hi);
+        m_hi = block_min_d<kSelThreads>(m_hi, sh.red_d);
         int64_t ncont = 0, nopen = 0, tbest = INT64_MAX;
-        for (int64_t t = lo + tid; t <= hi; t += kThreads) {
+        for (int64_t t = lo + tid; t <= hi; t += kSelThreads) {
             const Iv z = iv(t);
             if (z.lo <= m_hi) {
                 ++ncont;
@@ -359,11 +367,11 @@ __global__ __launch_bounds__(kThreads) void select_pass_kernel(SelectArgs a, Wei
                 tbest = min(tbest, t);
             }
         }
-        ncont = block_sum_i(ncont, sh.red_i);
-        nopen = block_sum_i(nopen, sh.red_j);
-        tbest = block_min_i(tbest, sh.red_i);
+        ncont = block_sum_i<kSelThreads>(ncont, sh.red_i);
+        nopen = block_sum_i<kSelThreads>(nopen, sh.red_j);
+        tbest = block_min_i<kSelThreads>(tbest, sh.red_i);
         if (ncont > 1 && nopen > 0 && tau0 > 0.0) {
-            for (int64_t t = lo + tid; t <= hi; t += kThreads) {
+            for (int64_t t = lo + tid; t <= hi; t += kSelThreads) {
                 const Iv z = iv(t);
                 if (z.lo <= m_hi) push(t, z);
             }
@@ -542,7 +550,10 @@ hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const 
     for (int pass = 0; pass < passes; ++pass) {
         a.pass = pass;
         a.last = pass == passes - 1;
-        hipLaunchKernelGGL(select_pass_kernel, grid_sel, dim3(kThreads), 0, s, a, w);
+        if (p.lags >= kWideLags)
+            hipLaunchKernelGGL(select_pass_kernel<1024>, grid_sel, dim3(1024), 0, s, a, w);
+        else
+            hipLaunchKernelGGL(select_pass_kernel<kThreads>, grid_sel, dim3(kThreads), 0, s, a, w);
         if (!a.last) hipLaunchKernelGGL(rescore_kernel, grid_re, dim3(kThreads), 0, s, a, w);
     }
     return hipGetLastError();
