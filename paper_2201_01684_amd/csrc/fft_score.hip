@@ -102,18 +102,24 @@ __device__ __forceinline__ void fft_pass(double2* s, int lg, int lgc, int st_lo,
         const int g = gi >> lgc;
         const int blo = g & lo_mask;
         const int base = ((g >> st_lo) << (st_lo + R)) | blo;
+        // the twiddles of all R stages first: stage k uses 2^k of them,
+        // W_2h^(blo + u 2^st_lo) for u < 2^k, at wt[2^k - 1 + u]
+        double2 wt[kR - 1];
+#pragma unroll
+        for (int k = 0; k < R; ++k)
+#pragma unroll
+            for (int u = 0; u < (1 << k); ++u)
+                wt[(1 << k) - 1 + u] = tw[(blo + (u << st_lo)) << (lg - 1 - (st_lo + k))];
         double2 v[kR];
 #pragma unroll
         for (int m = 0; m < kR; ++m) v[m] = s[(base + (m << st_lo)) * cols + q];
 #pragma unroll
         for (int kk = 0; kk < R; ++kk) {
             const int k = kInverse ? kk : R - 1 - kk;   // stage st_lo + k
-            const int st = st_lo + k;
 #pragma unroll
             for (int m = 0; m < kR; ++m) {
                 if (m & (1 << k)) continue;
-                const int j = blo + ((m & ((1 << k) - 1)) << st_lo);
-                const double2 w = tw[j << (lg - 1 - st)];
+                const double2 w = wt[(1 << k) - 1 + (m & ((1 << k) - 1))];
                 const double2 a = v[m];
                 if (kInverse) {
                     const double2 b = cmul_conj(v[m + (1 << k)], w);
@@ -131,32 +137,34 @@ __device__ __forceinline__ void fft_pass(double2* s, int lg, int lgc, int st_lo,
     }
 }
 
-template <bool kInverse>
+template <bool kInverse, int kMaxR>
 __device__ void lds_fft(double2* s, int lg, int lgc, const double2* __restrict__ tw) {
     int rmax = lg + lgc - kFftThreadsLog2;   // log2 of the points per thread
-    rmax = rmax < 1 ? 1 : (rmax > 4 ? 4 : rmax);
+    rmax = rmax < 1 ? 1 : (rmax > kMaxR ? kMaxR : rmax);
     const int np = (lg + rmax - 1) / rmax;
     const int base = lg / np, extra = lg % np;
     int st = kInverse ? 0 : lg;
     for (int p = 0; p < np; ++p) {
         const int r = base + (p < extra ? 1 : 0);
         const int st_lo = kInverse ? st : st - r;
-        switch (r) {
-            case 1: fft_pass<1, kInverse>(s, lg, lgc, st_lo, tw); break;
-            case 2: fft_pass<2, kInverse>(s, lg, lgc, st_lo, tw); break;
-            case 3: fft_pass<3, kInverse>(s, lg, lgc, st_lo, tw); break;
-            default: fft_pass<4, kInverse>(s, lg, lgc, st_lo, tw); break;
-        }
+        if (r == 1) fft_pass<1, kInverse>(s, lg, lgc, st_lo, tw);
+        else if (r == 2 || kMaxR < 3) fft_pass<(kMaxR < 2 ? 1 : 2), kInverse>(s, lg, lgc, st_lo, tw);
+        else if (r == 3 || kMaxR < 4) fft_pass<(kMaxR < 3 ? 1 : 3), kInverse>(s, lg, lgc, st_lo, tw);
+        else fft_pass<(kMaxR < 4 ? 1 : 4), kInverse>(s, lg, lgc, st_lo, tw);
         __syncthreads();
         st = kInverse ? st + r : st_lo;
     }
 }
 
+// A workgroup of 2^kFftThreadsLog2 threads on a tile of 2^kTile points holds
+// 2^(kTile - kFftThreadsLog2) points per thread: the largest useful pass radix.
+template <int kTile>
 __device__ __forceinline__ void lds_fft_fwd(double2* s, int lg, int lgc, const double2* tw) {
-    lds_fft<false>(s, lg, lgc, tw);
+    lds_fft<false, kTile - kFftThreadsLog2>(s, lg, lgc, tw);
 }
+template <int kTile>
 __device__ __forceinline__ void lds_fft_inv(double2* s, int lg, int lgc, const double2* tw) {
-    lds_fft<true>(s, lg, lgc, tw);
+    lds_fft<true, kTile - kFftThreadsLog2>(s, lg, lgc, tw);
 }
 
 // W_L^e = exp(-2 pi i e / L) for e < L from two tables split at bit lg2.
@@ -320,10 +328,21 @@ __global__ __launch_bounds__(kTThreads) void fft_single_kernel(FftArgs a) {
     const int lg = a.lg;
     const int len = 1 << lg;
     const double2* tw = a.tw + a.tw_a;
-    for (int i = threadIdx.x; i < len; i += kTThreads)
-        lds[i] = make_double2(centred(qa, i), centred(qb, i));
+    {   // all loads of a thread in flight before its LDS writes
+        double2 v[kRegPoints];
+#pragma unroll
+        for (int r = 0; r < kRegPoints; ++r) {
+            const int i = threadIdx.x + r * kTThreads;
+            v[r] = make_double2(centred(qa, i), centred(qb, i));
+        }
+#pragma unroll
+        for (int r = 0; r < kRegPoints; ++r) {
+            const int i = threadIdx.x + r * kTThreads;
+            if (i < len) lds[i] = v[r];
+        }
+    }
     __syncthreads();
-    lds_fft_fwd(lds, lg, 0, tw);
+    lds_fft_fwd<kTile>(lds, lg, 0, tw);
     double2 wv[kRegPoints];
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {
@@ -341,7 +360,7 @@ __global__ __launch_bounds__(kTThreads) void fft_single_kernel(FftArgs a) {
         if (pos < len) lds[pos] = wv[r];
     }
     __syncthreads();
-    lds_fft_inv(lds, lg, 0, tw);
+    lds_fft_inv<kTile>(lds, lg, 0, tw);
     for (int64_t t = a.tmin + threadIdx.x; t <= a.tmax; t += kTThreads) {
         write_d(a, 2 * pair, t, lds[t].x);
         write_d(a, 2 * pair + 1, t, lds[t].y);
@@ -363,18 +382,34 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_fwd_kernel(FftArgs a) {
     const int npts = (1 << a.lg1) * cols;
     const int64_t l2 = int64_t(1) << a.lg2;
     const Seq qa = seq_of(a, 2 * pair), qb = seq_of(a, 2 * pair + 1);
-    for (int f = threadIdx.x; f < npts; f += kTThreads) {
-        const int64_t i = (int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1));
-        lds[f] = make_double2(centred(qa, i), centred(qb, i));
+    {   // all loads of a thread in flight before its LDS writes
+        double2 v[kRegPoints];
+#pragma unroll
+        for (int r = 0; r < kRegPoints; ++r) {
+            const int f = threadIdx.x + r * kTThreads;
+            const int64_t i = f < npts ? (int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1)) : a.len;
+            v[r] = make_double2(centred(qa, i), centred(qb, i));
+        }
+#pragma unroll
+        for (int r = 0; r < kRegPoints; ++r) {
+            const int f = threadIdx.x + r * kTThreads;
+            if (f < npts) lds[f] = v[r];
+        }
     }
     __syncthreads();
-    lds_fft_fwd(lds, a.lg1, a.lgc, a.tw + a.tw_a);
+    lds_fft_fwd<kTile>(lds, a.lg1, a.lgc, a.tw + a.tw_a);
     double2* __restrict__ zp = a.z + pair * a.len;
-    for (int f = threadIdx.x; f < npts; f += kTThreads) {
-        const int pos = f >> a.lgc;
-        const int64_t n2 = c0 + (f & (cols - 1));
-        const int64_t k1 = bitrev(pos, a.lg1);
-        zp[pos * l2 + n2] = cmul(lds[f], twiddle(a, k1 * n2));
+    double2 w[kRegPoints];
+#pragma unroll
+    for (int r = 0; r < kRegPoints; ++r) {   // twiddle loads first
+        const int f = threadIdx.x + r * kTThreads;
+        const int64_t k1 = bitrev(f >> a.lgc, a.lg1);
+        w[r] = f < npts ? twiddle(a, k1 * (c0 + (f & (cols - 1)))) : make_double2(1.0, 0.0);
+    }
+#pragma unroll
+    for (int r = 0; r < kRegPoints; ++r) {
+        const int f = threadIdx.x + r * kTThreads;
+        if (f < npts) zp[(int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1))] = cmul(lds[f], w[r]);
     }
 }
 
@@ -405,13 +440,24 @@ __global__ __launch_bounds__(kTThreads) void fft_rows_kernel(FftArgs a) {
         self = ka == kb;
         return (q & 1) ? kb : ka;
     };
-    for (int f = threadIdx.x; f < npts; f += kTThreads) {
-        bool valid, self;
-        const uint32_t k1 = k1_of(f & (slots - 1), valid, self);
-        lds[f] = valid ? zp[(int64_t)bitrev(k1, a.lg1) * l2 + (f >> lgs)] : make_double2(0.0, 0.0);
+    {   // all loads of a thread in flight before its LDS writes
+        double2 v[kRegPoints];
+#pragma unroll
+        for (int r = 0; r < kRegPoints; ++r) {
+            const int f = threadIdx.x + r * kTThreads;
+            bool valid, self;
+            const uint32_t k1 = k1_of(f & (slots - 1), valid, self);
+            v[r] = (valid && f < npts) ? zp[(int64_t)bitrev(k1, a.lg1) * l2 + (f >> lgs)]
+                                       : make_double2(0.0, 0.0);
+        }
+#pragma unroll
+        for (int r = 0; r < kRegPoints; ++r) {
+            const int f = threadIdx.x + r * kTThreads;
+            if (f < npts) lds[f] = v[r];
+        }
     }
     __syncthreads();
-    lds_fft_fwd(lds, a.lg2, lgs, a.tw + a.tw_b);
+    lds_fft_fwd<kTile>(lds, a.lg2, lgs, a.tw + a.tw_b);
     double2 wv[kRegPoints];
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {
@@ -433,14 +479,22 @@ __global__ __launch_bounds__(kTThreads) void fft_rows_kernel(FftArgs a) {
         if (f < npts) lds[f] = wv[r];
     }
     __syncthreads();
-    lds_fft_inv(lds, a.lg2, lgs, a.tw + a.tw_b);
-    for (int f = threadIdx.x; f < npts; f += kTThreads) {
+    lds_fft_inv<kTile>(lds, a.lg2, lgs, a.tw + a.tw_b);
+#pragma unroll
+    for (int r = 0; r < kRegPoints; ++r) {   // twiddle loads first (wv is free again)
+        const int f = threadIdx.x + r * kTThreads;
+        bool valid, self;
+        const uint32_t k1 = k1_of(f & (slots - 1), valid, self);
+        wv[r] = (f < npts && valid) ? twiddle(a, (int64_t)k1 * (f >> lgs)) : make_double2(1.0, 0.0);
+    }
+#pragma unroll
+    for (int r = 0; r < kRegPoints; ++r) {
+        const int f = threadIdx.x + r * kTThreads;
         const int q = f & (slots - 1);
         bool valid, self;
         const uint32_t k1 = k1_of(q, valid, self);
-        if (!valid || ((q & 1) && self)) continue;
-        const int64_t n2 = f >> lgs;
-        zp[(int64_t)bitrev(k1, a.lg1) * l2 + n2] = cmul_conj(lds[f], twiddle(a, (int64_t)k1 * n2));
+        if (f >= npts || !valid || ((q & 1) && self)) continue;
+        zp[(int64_t)bitrev(k1, a.lg1) * l2 + (f >> lgs)] = cmul_conj(lds[f], wv[r]);
     }
 }
 
@@ -459,10 +513,22 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_inv_kernel(FftArgs a) {
     const int npts = (1 << a.lg1) * cols;
     const int64_t l2 = int64_t(1) << a.lg2;
     const double2* __restrict__ zp = a.z + pair * a.len;
-    for (int f = threadIdx.x; f < npts; f += kTThreads)
-        lds[f] = zp[(int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1))];
+    {   // all loads of a thread in flight before its LDS writes
+        double2 v[kRegPoints];
+#pragma unroll
+        for (int r = 0; r < kRegPoints; ++r) {
+            const int f = threadIdx.x + r * kTThreads;
+            v[r] = f < npts ? zp[(int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1))]
+                            : make_double2(0.0, 0.0);
+        }
+#pragma unroll
+        for (int r = 0; r < kRegPoints; ++r) {
+            const int f = threadIdx.x + r * kTThreads;
+            if (f < npts) lds[f] = v[r];
+        }
+    }
     __syncthreads();
-    lds_fft_inv(lds, a.lg1, a.lgc, a.tw + a.tw_a);
+    lds_fft_inv<kTile>(lds, a.lg1, a.lgc, a.tw + a.tw_a);
     const int rows = (int)(a.tmax / l2) + 1;
     for (int f = threadIdx.x; f < rows * cols; f += kTThreads) {
         const int64_t t = (int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1));
