@@ -50,6 +50,8 @@ def parse():
                          "similarity: Algorithm 2's grouped similarity of 5 finalist periods "
                          "per window (the selected one, its neighbours, its double and half); "
                          "centred: the mean-removed score of the same 5 finalists")
+    ap.add_argument("--no-fft-compare", action="store_true",
+                    help="detect mode: skip the untimed FFT-scores run of the same batch")
     ap.add_argument("--fft-scores", action="store_true",
                     help="rolling mode: score with GPOEO_PD_FFT_SCORES")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -252,6 +254,30 @@ def main():
         "windows_flagged_unresolved": int(np.count_nonzero(res["flags"] & pkg.UNRESOLVED)),
         "windows_rescored": int(np.count_nonzero(res["n_rescored"])),
     }
+    if not fft and not args.no_fft_compare:
+        # the same batch with FFT scores (GPOEO_PD_FFT_SCORES), after and outside
+        # the timed region: its time per call and whether every selection matches
+        fdesc, fkeep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
+                                     wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights,
+                                     flags=pkg.FFT_SCORES)
+        del det
+        torch.cuda.empty_cache()
+        fdet = pkg.Detector(x, fdesc, fkeep, want_scores=False)
+        fdet.run()
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for _ in range(args.steps):
+            fdet.run()
+        torch.cuda.synchronize()
+        f_ms = (time.perf_counter() - t) * 1e3 / args.steps
+        fres = fdet.results_numpy()
+        same = all(np.array_equal(fres[k], res[k]) for k in
+                   ("period", "verdict", "t_cand", "t_low", "t_up", "n_candidates"))
+        line["fft_scores"] = {"ms_per_step": f_ms, "value": pairs / (f_ms / 1e3),
+                              "traces_per_sec": wl.num_windows / (f_ms / 1e3),
+                              "selections_equal_direct": bool(same)}
+        del fdet
+        torch.cuda.empty_cache()
     if wl.truth is not None:
         d = wl.truth > 0
         if wl.jitter:
