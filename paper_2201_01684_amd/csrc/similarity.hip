@@ -111,45 +111,34 @@ __device__ double pair_error(const float* __restrict__ a, const float* __restric
 #pragma unroll
                 for (int k = 0; k < G; ++k) r[k] /= sum;
             };
-            double nk[G], s1[G];
+            // One pass: responsibility-weighted count, first and second moment
+            // about the sub-curve mean c; the M-step's variance about the new
+            // mean m_k is then sum r (x-c)^2 / n_k - (m_k - c)^2 (the same value
+            // as a second pass about m_k, up to rounding).
+            double nk[G], s1[G], s2[G];
 #pragma unroll
-            for (int k = 0; k < G; ++k) nk[k] = s1[k] = 0.0;
+            for (int k = 0; k < G; ++k) nk[k] = s1[k] = s2[k] = 0.0;
             for (int64_t j = lane; j < t; j += kWave) {
                 const double v = (double)a[j];
+                const double d = v - mean_prev;
                 double r[G];
                 resp(v, r);
 #pragma unroll
                 for (int k = 0; k < G; ++k) {
                     nk[k] += r[k];
-                    s1[k] += r[k] * v;
-                }
-            }
-            double mk[G];
-#pragma unroll
-            for (int k = 0; k < G; ++k) {
-                nk[k] = wave_sum(nk[k]);
-                s1[k] = wave_sum(s1[k]);
-                mk[k] = nk[k] > 0.0 ? s1[k] / nk[k] : mu[k];
-            }
-            double s2[G];
-#pragma unroll
-            for (int k = 0; k < G; ++k) s2[k] = 0.0;
-            for (int64_t j = lane; j < t; j += kWave) {
-                const double v = (double)a[j];
-                double r[G];
-                resp(v, r);
-#pragma unroll
-                for (int k = 0; k < G; ++k) {
-                    const double d = v - mk[k];
+                    s1[k] += r[k] * d;
                     s2[k] += r[k] * d * d;
                 }
             }
 #pragma unroll
             for (int k = 0; k < G; ++k) {
+                nk[k] = wave_sum(nk[k]);
+                s1[k] = wave_sum(s1[k]);
                 s2[k] = wave_sum(s2[k]);
                 if (!(nk[k] > 0.0)) continue;
-                mu[k] = mk[k];
-                var[k] = s2[k] / nk[k];
+                const double dm = s1[k] / nk[k];
+                mu[k] = mean_prev + dm;
+                var[k] = s2[k] / nk[k] - dm * dm;
                 if (var[k] < floor_var) var[k] = floor_var;
                 pi[k] = nk[k] / (double)t;
             }
