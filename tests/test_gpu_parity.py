@@ -188,3 +188,11 @@ def test_deterministic_bitwise():
     a, ra = gpu_run(wl.x, lay)
     b, rb = gpu_run(wl.x, lay)
     assert np.array_equal(a, b) and np.array_equal(ra, rb)
+
+
+@pytest.mark.parametrize("n,tmin,tmax", [(1 << 24, 2, 66), (3_000_001, 1000, 1500)])
+def test_very_long_windows(n, tmin, tmax):
+    # one window of up to 16,777,216 samples: hundreds of sample chunks per lag
+    # block, combined in fp64 in chunk order; every lag against the oracle
+    x = planted_trace(n, 61 if tmax < 100 else 1234, 6, seed=n % 97, sigma=1.0)
+    parity(x, oracle.Layout(1, 1, n, n, n, tmin, tmax), f"n={n}")
