@@ -50,6 +50,8 @@ def parse():
                          "similarity: Algorithm 2's grouped similarity of 5 finalist periods "
                          "per window (the selected one, its neighbours, its double and half); "
                          "centred: the mean-removed score of the same 5 finalists")
+    ap.add_argument("--graph", action="store_true",
+                    help="detect/fft mode: also time replays of one call captured in a HIP graph")
     ap.add_argument("--no-fft-compare", action="store_true",
                     help="detect mode: skip the untimed FFT-scores run of the same batch")
     ap.add_argument("--fft-scores", action="store_true",
@@ -254,6 +256,20 @@ def main():
         "windows_flagged_unresolved": int(np.count_nonzero(res["flags"] & pkg.UNRESOLVED)),
         "windows_rescored": int(np.count_nonzero(res["n_rescored"])),
     }
+    if args.graph:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            det.run()
+        g.replay()
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for _ in range(args.steps):
+            g.replay()
+        torch.cuda.synchronize()
+        g_ms = (time.perf_counter() - t) * 1e3 / args.steps
+        line["graph_replay"] = {"ms_per_step": g_ms, "value": pairs / (g_ms / 1e3),
+                                "traces_per_sec": wl.num_windows / (g_ms / 1e3)}
+        del g
     if not fft and not args.no_fft_compare:
         # the same batch with FFT scores (GPOEO_PD_FFT_SCORES), after and outside
         # the timed region: its time per call and whether every selection matches
