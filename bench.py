@@ -202,6 +202,7 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     stage_ms = np.array([[ev.elapsed_ms(s[j], s[j + 1]) for j in range(4)] for s in sets])
+    call_ms = np.array([ev.elapsed_ms(s[0], s[4]) for s in sets])   # each whole call
     for s in sets:
         ev.destroy(s)
     ms_per_step = (t1 - t0) * 1e3 / args.steps
@@ -248,6 +249,7 @@ def main():
                    "scoring": {0: "per window", 1: "shared block partials",
                                2: "fp64 FFT autocorrelation"}[plan["mode"]],
                    "pairs_scored": scored, "lags_per_lane": plan["lags_per_lane"]},
+        "call_ms": {"median": float(np.median(call_ms)), "min": float(call_ms.min())},
         "stage_ms": {"window_stats": float(stage_ms[:, 0].mean()),
                      "lag_score": score_ms,
                      "finalize": float(stage_ms[:, 2].mean()),
