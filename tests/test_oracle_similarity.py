@@ -1,10 +1,11 @@
 """Pins of the oracle's Algorithm 2 similarity error (GMM groups + SMAPE).
 
 The paper prints no worked example, and the EM details of the Gaussian mixture
-(initialisation, iterations) are this build's reading, so the values below are
-cases whose answer does not depend on those details: well-separated clusters
-(any mixture fit recovers them), a single group, exact periods, and the
-invariances of the definition.
+(initialisation, iterations) are this build's reading.  Pinned: cases whose
+answer does not depend on those details (well-separated clusters, which any
+mixture fit recovers; a single group; exact periods; the invariances of the
+definition), and the EM trajectory itself on overlapping clusters against
+scikit-learn's GaussianMixture started from the same parameters.
 """
 from fractions import Fraction
 
@@ -83,3 +84,47 @@ def test_paper_reason_for_groups_noise_robustness():
     # so the true period still scores far better than a wrong one.
     x = planted_trace(8000, 200, 6, seed=9, sigma=8.0)
     assert err(x, 200) < 0.5 * err(x, 230)
+
+
+def _err_via_sklearn(x, t, groups=3, iters=20):
+    """Algorithm 2's Err_T with the mixture fitted by scikit-learn's EM from the
+    same initial parameters (means evenly spread over [min, max], variances
+    ((max-min)/G)^2, weights 1/G; no regularisation, no early stop), then hard
+    labels, relative group means and SMAPE written out here."""
+    from sklearn.mixture import GaussianMixture
+    v = x.astype(np.float64)
+    pairs = v.size // t - 1
+    total = 0.0
+    for i in range(pairs):
+        a, b = v[i * t:(i + 1) * t], v[(i + 1) * t:(i + 2) * t]
+        lo, hi = a.min(), a.max()
+        width = (hi - lo) / groups
+        gm = GaussianMixture(n_components=groups, covariance_type="full", max_iter=iters, tol=0.0,
+                             reg_covar=0.0, weights_init=np.full(groups, 1.0 / groups),
+                             means_init=(lo + (np.arange(groups) + 0.5) * width).reshape(-1, 1),
+                             precisions_init=np.full((groups, 1, 1), 1.0 / width ** 2))
+        gm.fit(a.reshape(-1, 1))
+        labels = gm.predict(a.reshape(-1, 1))
+        err = 0.0
+        for k in range(groups):
+            sel = labels == k
+            if not sel.any():
+                continue
+            ra, rb = a[sel].mean() - a.mean(), b[sel].mean() - b.mean()
+            den = (abs(ra) + abs(rb)) / 2
+            err += sel.sum() * (0.0 if den == 0 else abs(ra - rb) / den)
+        total += err / t
+    return total / pairs
+
+
+@pytest.mark.filterwarnings("ignore::sklearn.exceptions.ConvergenceWarning")
+@pytest.mark.parametrize("t,seed", [(40, 1), (75, 2), (150, 3)])
+def test_em_trajectory_matches_scikit_learn(t, seed):
+    # overlapping clusters (levels 0, 3, 7 with sigma 1.2): twenty EM iterations
+    # that move the mixture far from its initialisation; the variance floor
+    # (1e-6 of the initial variance) never binds here
+    rng = np.random.default_rng(seed)
+    levels = np.repeat([0.0, 3.0, 7.0], [t // 3, t // 3, t - 2 * (t // 3)])
+    x = (np.tile(levels, 12) + rng.normal(0, 1.2, size=12 * t)).astype(np.float32)
+    want = _err_via_sklearn(x, t)
+    assert err(x, t) == pytest.approx(want, rel=1e-9)
