@@ -310,3 +310,72 @@ def similarity(x: np.ndarray, lay: Layout, windows, lags, num_groups: int = DEFA
     if rc != 0:
         raise ValueError("oracle rejected the parameters")
     return out
+
+
+# Algorithm 1, lines 1-5 (Sec. 4.1.1-4.1.2): the FFT front end.  c_peak is
+# 0.6-0.7 in the paper; the mid value is the default.
+DEFAULT_C_PEAK = 0.65
+SPECTRAL_MAX = 16
+
+
+def spectral_length(n: int) -> int:
+    """Transform length: the smallest power of two (at least 64) holding the window."""
+    length = 64
+    while length < n:
+        length *= 2
+    return length
+
+
+def amplitude_spectrum(xw: np.ndarray, weights=None) -> np.ndarray:
+    """A(k) = sum_c w_c |X_c(k)|, k = 0..L/2, of one window [C][N] (or [N]).
+
+    Each channel is centred by its mean (the transform of the constant part is
+    a peak at k = 0 only) and zero-padded to L = spectral_length(N); X_c is its
+    fp64 discrete Fourier transform (numpy's FFT, a library primitive)."""
+    xw = np.atleast_2d(np.asarray(xw, dtype=np.float32)).astype(np.float64)
+    c_count, n = xw.shape
+    length = spectral_length(n)
+    w = np.ones(c_count) if weights is None else np.asarray(weights, dtype=np.float32).astype(np.float64)
+    amp = np.zeros(length // 2 + 1)
+    for c in range(c_count):
+        y = xw[c] - xw[c].sum() / n
+        amp += w[c] * np.abs(np.fft.rfft(y, n=length))
+    return amp
+
+
+def spectral_candidates(xw: np.ndarray, tmin: int, tmax: int, c_peak: float = DEFAULT_C_PEAK,
+                        k_max: int = SPECTRAL_MAX, weights=None) -> dict:
+    """Candidate periods of one window from its amplitude spectrum (Algorithm 1,
+    lines 1-5, with T_s = 1 sample):
+
+      peaks   bins 2 <= k <= L/2 - 1 with A(k) > A(k-1) and A(k) >= A(k+1)
+              (strict on the left, as the lag-domain rule)
+      cands   peaks with A(k) > c_peak * max over peaks
+      period  round(L / k) (halves up), kept if in [tmin, tmax]; candidates in
+              order of decreasing A (ties: smaller k), a period already taken
+              by a stronger bin skipped, at most k_max of them
+    """
+    amp = amplitude_spectrum(xw, weights)
+    half = amp.size - 1
+    k = np.arange(2, half)
+    peak = (amp[k] > amp[k - 1]) & (amp[k] >= amp[k + 1])
+    pk = k[peak]
+    out = {"periods": [], "bins": [], "amplitudes": [], "n_peaks": int(pk.size)}
+    if pk.size == 0:
+        return out
+    top = amp[pk].max()
+    cand = pk[amp[pk] > c_peak * top]
+    order = sorted(cand.tolist(), key=lambda b: (-amp[b], b))
+    length = 2 * half
+    seen = set()
+    for b in order:
+        t = (2 * length + b) // (2 * b)          # round(L / b), halves up
+        if t < tmin or t > tmax or t in seen:
+            continue
+        seen.add(t)
+        out["periods"].append(int(t))
+        out["bins"].append(int(b))
+        out["amplitudes"].append(float(amp[b]))
+        if len(out["periods"]) == k_max:
+            break
+    return out
