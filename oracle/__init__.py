@@ -350,29 +350,29 @@ def spectral_candidates(xw: np.ndarray, tmin: int, tmax: int, c_peak: float = DE
 
       peaks   bins 2 <= k <= L/2 - 1 with A(k) > A(k-1) and A(k) >= A(k+1)
               (strict on the left, as the lag-domain rule)
-      cands   peaks with A(k) > c_peak * max over peaks
-      period  round(L / k) (halves up), kept if in [tmin, tmax]; candidates in
-              order of decreasing A (ties: smaller k), a period already taken
-              by a stronger bin skipped, at most k_max of them
+      cands   peaks with A(k) > c_peak * max over peaks whose period
+              round(L / k) (halves up) lies in [tmin, tmax]
+      order   decreasing A (ties: smaller k), at most k_max of them; two bins
+              may round to the same period (the paper's TCand is a list of
+              peak periods, not a set)
     """
     amp = amplitude_spectrum(xw, weights)
     half = amp.size - 1
     k = np.arange(2, half)
     peak = (amp[k] > amp[k - 1]) & (amp[k] >= amp[k + 1])
     pk = k[peak]
-    out = {"periods": [], "bins": [], "amplitudes": [], "n_peaks": int(pk.size)}
+    out = {"periods": [], "bins": [], "amplitudes": [], "n_peaks": int(pk.size), "max_peak": 0.0}
     if pk.size == 0:
         return out
     top = amp[pk].max()
+    out["max_peak"] = float(top)
     cand = pk[amp[pk] > c_peak * top]
     order = sorted(cand.tolist(), key=lambda b: (-amp[b], b))
     length = 2 * half
-    seen = set()
     for b in order:
         t = (2 * length + b) // (2 * b)          # round(L / b), halves up
-        if t < tmin or t > tmax or t in seen:
+        if t < tmin or t > tmax:
             continue
-        seen.add(t)
         out["periods"].append(int(t))
         out["bins"].append(int(b))
         out["amplitudes"].append(float(amp[b]))

@@ -3,8 +3,8 @@ spectrum and the candidate periods drawn from its peaks.
 
 Pinned against: the discrete Fourier transform written out as a direct sum on
 small windows, pure tones on integer bins (known amplitude A L / 2 and
-period), two-tone inputs on each side of the c_peak threshold, neighbouring
-bins that round to one period, the lag range and the candidate limit, channel
+period), two-tone inputs on each side of the c_peak threshold, two bins
+that round to one period (both listed), the lag range and the candidate limit, channel
 weighting (amplitudes add), and a constant offset (removed by the centring).
 """
 import math
@@ -60,12 +60,16 @@ def test_relative_height_threshold(ratio, count):
         assert c["periods"][1] == round(4096 / 48)
 
 
-def test_neighbouring_bins_rounding_to_one_period():
-    # bins 100 and 101 of 4096 points: periods 40.96 and 40.55 both round to 41
+def test_two_bins_rounding_to_one_period():
+    # bins 200 and 202 of 4096 points: periods 20.48 and 20.28 both round to
+    # 20; both are peaks above the threshold, listed strongest first.  (Of two
+    # adjacent bins only the stronger can be a peak.)
     length = 4096
-    x = tone(length, [(length / 100, 5.0), (length / 101, 4.5)])
+    x = tone(length, [(length / 200, 5.0), (length / 202, 4.5)])
     c = oracle.spectral_candidates(x, 2, 2048)
-    assert c["periods"] == [41] and c["bins"] == [100]
+    assert c["periods"] == [20, 20] and c["bins"] == [200, 202]
+    y = tone(length, [(length / 100, 5.0), (length / 101, 4.5)])
+    assert oracle.spectral_candidates(y, 2, 2048)["bins"] == [100]
 
 
 def test_lag_range_and_candidate_limit():
