@@ -41,7 +41,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=("detect", "fft", "rolling", "similarity", "centred"),
+    ap.add_argument("--mode", choices=("detect", "fft", "rolling", "similarity", "centred",
+                                       "spectral"),
                     default="detect",
                     help="detect: gpoeo_pd_detect (the default measurement); fft: the same "
                          "call with GPOEO_PD_FFT_SCORES (fp64 FFT autocorrelation scores); "
@@ -49,7 +50,8 @@ def parse():
                          "Algorithm 3's rolling detection, gpoeo_pd_detect_rolling; "
                          "similarity: Algorithm 2's grouped similarity of 5 finalist periods "
                          "per window (the selected one, its neighbours, its double and half); "
-                         "centred: the mean-removed score of the same 5 finalists")
+                         "centred: the mean-removed score of the same 5 finalists; "
+                         "spectral: Algorithm 1's FFT front end (candidate periods)")
     ap.add_argument("--graph", action="store_true",
                     help="detect/fft mode: also time replays of one call captured in a HIP graph")
     ap.add_argument("--no-fft-compare", action="store_true",
@@ -171,6 +173,8 @@ def main():
         return bench_rolling(args)
     if args.mode in ("similarity", "centred"):
         return bench_similarity(args)
+    if args.mode == "spectral":
+        return bench_spectral(args)
 
     t_gen = time.perf_counter()
     wl = make_workload(args.workload)
@@ -407,6 +411,73 @@ def bench_similarity(args):
                                 "cores": oracle.threads(), "kind": "oracle",
                                 "sample": f"first {done} of {len(ts)} queries, {t_cpu:.1f} s"}
         line["parity_sample"] = {"queries": done, "max_rel_err": worst}
+    print(json.dumps(line), flush=True)
+
+
+def bench_spectral(args):
+    """Algorithm 1's FFT front end over the workload's windows: one step is one
+    gpoeo_pd_spectral_candidates call (amplitude spectra, peaks, candidates)."""
+    import numpy as np
+    import torch
+
+    import paper_2201_01684_amd as pkg
+    from gen import make_workload
+
+    wl = make_workload(args.workload)
+    x = torch.from_numpy(wl.x).to("cuda:0")
+    desc, keep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
+                               wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights)
+    params = pkg.spectral_params()
+    det = pkg.SpectralDetector(x, desc, params, keep)
+    for _ in range(args.warmup):
+        det.run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        det.run()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    res = det.results_numpy()
+    line = {
+        "metric": "spectral candidate lists/sec (Algorithm 1's FFT front end over every window)",
+        "value": wl.num_windows / (ms / 1e3), "unit": "windows/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "description": wl.meta["description"],
+                   "windows": wl.num_windows, "channels": wl.num_channels, "n": wl.n,
+                   "tmin": wl.tmin, "tmax": wl.tmax, "sha256": wl.sha256,
+                   "c_peak": params.c_peak, "max_candidates": params.max_candidates},
+        "mean_candidates": float(res["count"].mean()),
+        "windows_flagged_unresolved": int(np.count_nonzero(res["flags"])),
+        "roofline": None,
+    }
+    if wl.truth is not None:
+        d = wl.truth > 0
+        hit = [any(abs(int(t) - int(wl.truth[b])) <= max(1, int(wl.truth[b]) // 50)
+                   for t in res["periods"][b][:res["count"][b]]) for b in np.nonzero(d)[0]]
+        line["planted_period_among_candidates"] = f"{int(sum(hit))}/{int(d.sum())}"
+    if not args.no_cpu_baseline:
+        import oracle
+        span = (wl.num_channels - 1) * wl.channel_stride + wl.n
+        done, t_cpu, match = 0, 0.0, 0
+        while done < wl.num_windows and (done == 0 or t_cpu < args.cpu_seconds):
+            base = done * wl.window_stride
+            xw = np.stack([wl.x.reshape(-1)[base + c * wl.channel_stride:
+                                            base + c * wl.channel_stride + wl.n]
+                           for c in range(wl.num_channels)])
+            t = time.perf_counter()
+            o = oracle.spectral_candidates(xw, wl.tmin, wl.tmax, params.c_peak,
+                                           params.max_candidates, wl.weights)
+            t_cpu += time.perf_counter() - t
+            r = res[done]
+            match += int(list(r["bins"][:r["count"]]) == o["bins"])
+            done += 1
+        line["cpu_baseline"] = {"value": done / t_cpu, "unit": "windows/s", "cores": 1,
+                                "kind": "oracle",
+                                "sample": f"first {done} of {wl.num_windows} windows, "
+                                          f"{t_cpu:.1f} s (numpy FFT, one thread)"}
+        line["parity_sample"] = {"windows": done, "candidate_lists_equal": match}
     print(json.dumps(line), flush=True)
 
 

@@ -268,6 +268,51 @@ int gpoeo_pd_score_centred(const gpoeo_pd_desc* desc, const float* x, const int3
                            const int32_t* lags, int64_t count, double* score,
                            hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Spectral candidates: Algorithm 1's FFT front end (lines 1-5; Sec. 4.1.1-4.1.2,
+ * with T_s = 1 sample).  Per window:
+ *   every channel centred by its fp64 mean and zero-padded to L = 2^k >= N
+ *   (at least 64) points; A(k) = sum_c w_c |X_c(k)|, k = 0..L/2, from an fp64
+ *   FFT ("Ampl");
+ *   peaks = bins 2 <= k <= L/2 - 1 with A(k) > A(k-1) and A(k) >= A(k+1);
+ *   candidates = peaks with A(k) > c_peak * (largest peak) whose period
+ *   round(L / k) (halves up) lies in [tmin, tmax], strongest first (ties: the
+ *   smaller k), at most max_candidates; two bins may give the same period.
+ * A window whose list could change within the rounding error bound of the
+ * amplitudes (a peak test, the threshold or the order of the listed
+ * candidates within that margin), or with more than 1024 qualifying peaks, is
+ * flagged GPOEO_PD_UNRESOLVED; its list is still written.  The candidates are
+ * what Algorithm 1 evaluates with Algorithm 2 (gpoeo_pd_similarity,
+ * gpoeo_pd_score_centred).  desc gives the window layout, channel weights and
+ * lag range (its flags are not used); L <= 2^22.  results: device, one record
+ * per window; workspace: caller-owned, gpoeo_pd_spectral_workspace_bytes.
+ * ------------------------------------------------------------------------- */
+#define GPOEO_PD_SPECTRAL_MAX 16
+
+typedef struct {
+    double c_peak;           /* relative peak height in (0, 1); the paper uses 0.6-0.7   */
+    int32_t max_candidates;  /* 1..GPOEO_PD_SPECTRAL_MAX                                 */
+    int32_t reserved;        /* must be 0                                                */
+} gpoeo_pd_spectral_params;
+
+typedef struct {
+    int32_t count;           /* candidates written                                       */
+    uint32_t flags;          /* GPOEO_PD_UNRESOLVED                                      */
+    int32_t n_peaks;         /* peaks of A                                               */
+    int32_t reserved;
+    double max_peak;         /* the largest peak of A; 0 if none                         */
+    int32_t periods[GPOEO_PD_SPECTRAL_MAX];   /* round(L / bin)                          */
+    int32_t bins[GPOEO_PD_SPECTRAL_MAX];      /* k                                       */
+    double amplitudes[GPOEO_PD_SPECTRAL_MAX]; /* A(k)                                    */
+} gpoeo_pd_spectral_result;
+
+int gpoeo_pd_spectral_workspace_bytes(const gpoeo_pd_desc* desc,
+                                      const gpoeo_pd_spectral_params* params, size_t* bytes);
+
+int gpoeo_pd_spectral_candidates(const gpoeo_pd_desc* desc, const gpoeo_pd_spectral_params* params,
+                                 const float* x, gpoeo_pd_spectral_result* results,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -31,6 +31,10 @@ from ._binding import (  # noqa: F401
     rolling_params,
     similarity,
     score_centred,
+    spectral_params,
+    spectral_workspace_bytes,
+    SpectralDetector,
+    SPECTRAL_DTYPE,
     rolling_workspace_bytes,
     load_library,
     make_desc,

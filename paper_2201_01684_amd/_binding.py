@@ -79,6 +79,22 @@ class SimilarityParams(ctypes.Structure):
     _fields_ = [("num_groups", ctypes.c_int32), ("em_iters", ctypes.c_int32)]
 
 
+SPECTRAL_MAX = 16
+DEFAULT_C_PEAK = 0.65          # the paper sets c_peak to 0.6-0.7
+
+
+class SpectralParams(ctypes.Structure):
+    _fields_ = [("c_peak", ctypes.c_double), ("max_candidates", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+SPECTRAL_DTYPE = np.dtype([("count", np.int32), ("flags", np.uint32), ("n_peaks", np.int32),
+                           ("reserved", np.int32), ("max_peak", np.float64),
+                           ("periods", np.int32, SPECTRAL_MAX), ("bins", np.int32, SPECTRAL_MAX),
+                           ("amplitudes", np.float64, SPECTRAL_MAX)])
+assert SPECTRAL_DTYPE.itemsize == 280
+
+
 # Algorithm 2's group count and EM iterations are not given by the paper.
 DEFAULT_GROUPS, DEFAULT_EM_ITERS = 3, 20
 
@@ -91,7 +107,8 @@ assert RESULT_DTYPE.itemsize == ctypes.sizeof(Result)
 EXPORTS = ("gpoeo_pd_abi_version", "gpoeo_pd_strerror", "gpoeo_pd_workspace_bytes",
            "gpoeo_pd_describe_plan", "gpoeo_pd_detect", "gpoeo_pd_detect_staged",
            "gpoeo_pd_rolling_workspace_bytes", "gpoeo_pd_detect_rolling", "gpoeo_pd_similarity",
-           "gpoeo_pd_score_centred")
+           "gpoeo_pd_score_centred", "gpoeo_pd_spectral_workspace_bytes",
+           "gpoeo_pd_spectral_candidates")
 
 _lib = None
 
@@ -138,6 +155,16 @@ def load_library():
         lib.gpoeo_pd_similarity.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(SimilarityParams),
                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                             ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+        lib.gpoeo_pd_spectral_workspace_bytes.restype = ctypes.c_int
+        lib.gpoeo_pd_spectral_workspace_bytes.argtypes = [ctypes.POINTER(Desc),
+                                                          ctypes.POINTER(SpectralParams),
+                                                          ctypes.POINTER(ctypes.c_size_t)]
+        lib.gpoeo_pd_spectral_candidates.restype = ctypes.c_int
+        lib.gpoeo_pd_spectral_candidates.argtypes = [ctypes.POINTER(Desc),
+                                                     ctypes.POINTER(SpectralParams),
+                                                     ctypes.c_void_p, ctypes.c_void_p,
+                                                     ctypes.c_void_p, ctypes.c_size_t,
+                                                     ctypes.c_void_p]
         _lib = lib
     return _lib
 
@@ -389,3 +416,49 @@ def score_centred(x: torch.Tensor, desc: Desc, windows: torch.Tensor, lags: torc
     if rc != OK:
         raise GpoeoError(rc, "gpoeo_pd_score_centred")
     return out
+
+
+def spectral_params(c_peak: float = DEFAULT_C_PEAK, max_candidates: int = SPECTRAL_MAX) -> SpectralParams:
+    return SpectralParams(float(c_peak), int(max_candidates), 0)
+
+
+def spectral_workspace_bytes(desc: Desc, params: SpectralParams) -> int:
+    size = ctypes.c_size_t()
+    rc = load_library().gpoeo_pd_spectral_workspace_bytes(ctypes.byref(desc), ctypes.byref(params),
+                                                          ctypes.byref(size))
+    if rc != OK:
+        raise GpoeoError(rc, "gpoeo_pd_spectral_workspace_bytes")
+    return int(size.value)
+
+
+class SpectralDetector:
+    """Reusable call site of gpoeo_pd_spectral_candidates (buffers allocated once)."""
+
+    def __init__(self, x: torch.Tensor, desc: Desc, params: SpectralParams,
+                 weights_keepalive=None):
+        if not isinstance(x, torch.Tensor) or x.dtype != torch.float32 or not x.is_cuda:
+            raise TypeError("x must be a float32 GPU tensor")
+        if not x.is_contiguous():
+            raise ValueError("x must be contiguous")
+        need = ((desc.num_windows - 1) * desc.window_stride
+                + (desc.num_channels - 1) * desc.channel_stride + desc.n)
+        if x.numel() < need:
+            raise ValueError(f"x has {x.numel()} samples, the layout addresses {need}")
+        self.x, self.desc, self.params, self._w = x, desc, params, weights_keepalive
+        self.results = torch.zeros((desc.num_windows, SPECTRAL_DTYPE.itemsize // 4),
+                                   dtype=torch.int32, device=x.device)
+        self.ws_bytes = spectral_workspace_bytes(desc, params)
+        self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=x.device)
+        self._lib = load_library()
+
+    def run(self, stream=None) -> None:
+        rc = self._lib.gpoeo_pd_spectral_candidates(
+            ctypes.byref(self.desc), ctypes.byref(self.params), self.x.data_ptr(),
+            self.results.data_ptr(), self.workspace.data_ptr(), self.ws_bytes,
+            _stream_handle(stream))
+        if rc != OK:
+            raise GpoeoError(rc, "gpoeo_pd_spectral_candidates")
+
+    def results_numpy(self) -> np.ndarray:
+        host = self.results.detach().to("cpu").contiguous().numpy()
+        return host.view(SPECTRAL_DTYPE).reshape(-1)

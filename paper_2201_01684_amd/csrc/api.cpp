@@ -46,6 +46,28 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
     return true;
 }
 
+}  // namespace
+
+bool set_fft_geometry(Plan* p, int32_t lg) {
+    if (lg > kFftMaxLog2) return false;
+    p->fft_log2 = lg;
+    p->fft_len = int64_t(1) << lg;
+    const int tile = fft_tile_log2(lg);
+    if (lg <= tile) {
+        p->fft_m1 = (int32_t)p->fft_len;
+        p->fft_m2 = 1;
+        p->fft_cols = 1;
+    } else {
+        const int32_t lg1 = lg / 2, lg2 = lg - lg1;   // a row pair fits one tile
+        p->fft_m1 = 1 << lg1;
+        p->fft_m2 = 1 << lg2;
+        p->fft_cols = std::min<int32_t>(p->fft_m2, 1 << (tile - lg1));
+    }
+    return true;
+}
+
+namespace {
+
 int make_plan(const gpoeo_pd_desc* d, Plan* p) {
     if (!d) return GPOEO_PD_EINVAL;
     if (d->reserved0 != 0 || d->reserved1 != 0) return GPOEO_PD_EINVAL;
@@ -86,20 +108,7 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
         // smallest power of two (at least 64) holding N + Tmax points
         int32_t lg = 6;
         while ((int64_t(1) << lg) < d->n + d->tmax) ++lg;
-        if (lg > kFftMaxLog2) return GPOEO_PD_EINVAL;
-        p->fft_log2 = lg;
-        p->fft_len = int64_t(1) << lg;
-        const int tile = fft_tile_log2(lg);
-        if (lg <= tile) {
-            p->fft_m1 = (int32_t)p->fft_len;
-            p->fft_m2 = 1;
-            p->fft_cols = 1;
-        } else {
-            const int32_t lg1 = lg / 2, lg2 = lg - lg1;   // a row pair fits one tile
-            p->fft_m1 = 1 << lg1;
-            p->fft_m2 = 1 << lg2;
-            p->fft_cols = std::min<int32_t>(p->fft_m2, 1 << (tile - lg1));
-        }
+        if (!set_fft_geometry(p, lg)) return GPOEO_PD_EINVAL;
     }
 
     p->lags_per_lane = choose_lags_per_lane(d->n, d->tmin, d->tmax);
@@ -584,3 +593,88 @@ extern "C" int gpoeo_pd_score_centred(const gpoeo_pd_desc* desc, const float* x,
         return GPOEO_PD_EHIP;
     return GPOEO_PD_OK;
 }
+
+namespace {
+
+// Spectral candidates: the descriptor's window layout and lag range, an FFT
+// geometry for L = 2^k >= N, and the workspace (window statistics, twiddles,
+// transforms, amplitudes).
+struct SpectralPlan {
+    gpoeo::Plan p;
+    size_t off_var, off_fstat, off_tw, off_z, off_amp, bytes;
+};
+
+int make_spectral(const gpoeo_pd_desc* d, const gpoeo_pd_spectral_params* sp, SpectralPlan* r) {
+    if (!d || !sp) return GPOEO_PD_EINVAL;
+    if (!(sp->c_peak > 0.0 && sp->c_peak < 1.0) || sp->reserved != 0 || sp->max_candidates < 1 ||
+        sp->max_candidates > GPOEO_PD_SPECTRAL_MAX)
+        return GPOEO_PD_EINVAL;
+    gpoeo_pd_desc dd = *d;
+    dd.flags = 0;
+    const int rc = gpoeo::make_plan(&dd, &r->p);
+    if (rc != GPOEO_PD_OK) return rc;
+    int32_t lg = 6;
+    while ((int64_t(1) << lg) < d->n) ++lg;
+    if (!gpoeo::set_fft_geometry(&r->p, lg)) return GPOEO_PD_EINVAL;
+    r->p.fft = true;
+    r->p.table = gpoeo::WindowTable{nullptr, nullptr, nullptr};
+    const int64_t seqs = d->num_windows * (int64_t)d->num_channels;
+    r->p.fft_pairs = (seqs + 1) / 2;
+    int64_t n_z = 0, n_amp = 0;
+    if (!gpoeo::mul_ok(r->p.fft_pairs, r->p.fft_len, &n_z) || n_z > (INT64_MAX / 64) ||
+        !gpoeo::mul_ok(seqs, r->p.fft_len / 2 + 1, &n_amp) || n_amp > (INT64_MAX / 16))
+        return GPOEO_PD_EINVAL;
+    if (r->p.fft_m2 == 1) n_z = 0;                 // one workgroup per pair: no transform buffer
+    size_t off = 0;
+    r->off_var = off;
+    off = gpoeo::align_up(off + (size_t)seqs * 2 * sizeof(double));
+    r->off_fstat = off;
+    off = gpoeo::align_up(off + (size_t)seqs * 4 * sizeof(double));
+    r->off_tw = off;
+    off = gpoeo::align_up(off + (size_t)gpoeo::fft_twiddle_count(r->p) * 2 * sizeof(double));
+    r->off_z = off;
+    off = gpoeo::align_up(off + (size_t)n_z * 2 * sizeof(double));
+    r->off_amp = off;
+    off = gpoeo::align_up(off + (size_t)n_amp * sizeof(double));
+    r->bytes = off;
+    return GPOEO_PD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int gpoeo_pd_spectral_workspace_bytes(const gpoeo_pd_desc* desc,
+                                      const gpoeo_pd_spectral_params* params, size_t* bytes) {
+    if (!bytes) return GPOEO_PD_EINVAL;
+    SpectralPlan r;
+    const int rc = make_spectral(desc, params, &r);
+    if (rc != GPOEO_PD_OK) return rc;
+    *bytes = r.bytes;
+    return GPOEO_PD_OK;
+}
+
+int gpoeo_pd_spectral_candidates(const gpoeo_pd_desc* desc, const gpoeo_pd_spectral_params* params,
+                                 const float* x, gpoeo_pd_spectral_result* results,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    SpectralPlan r;
+    const int rc = make_spectral(desc, params, &r);
+    if (rc != GPOEO_PD_OK) return rc;
+    if (!x || !results || !workspace) return GPOEO_PD_EINVAL;
+    if (reinterpret_cast<uintptr_t>(workspace) % gpoeo::kAlign) return GPOEO_PD_EINVAL;
+    if (reinterpret_cast<uintptr_t>(x) % sizeof(float)) return GPOEO_PD_EINVAL;
+    if (workspace_bytes < r.bytes) return GPOEO_PD_ENOMEM;
+    char* ws = static_cast<char*>(workspace);
+    double* var = reinterpret_cast<double*>(ws + r.off_var);
+    double* fstat = reinterpret_cast<double*>(ws + r.off_fstat);
+    const gpoeo::Weights w = weights_of(desc, r.p.num_channels);
+    if (gpoeo::launch_window_stats(r.p, x, var, fstat, stream) != hipSuccess) return GPOEO_PD_EHIP;
+    if (gpoeo::launch_spectral(r.p, w, x, fstat, reinterpret_cast<double*>(ws + r.off_tw),
+                               reinterpret_cast<double*>(ws + r.off_z),
+                               reinterpret_cast<double*>(ws + r.off_amp), params->c_peak,
+                               params->max_candidates, results, stream) != hipSuccess)
+        return GPOEO_PD_EHIP;
+    return GPOEO_PD_OK;
+}
+
+}  // extern "C"

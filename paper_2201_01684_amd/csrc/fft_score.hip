@@ -45,6 +45,7 @@ struct FftArgs {
     const double2* tw;         // twiddle tables
     double2* z;                // [pairs][len]
     double* part;              // [S][lags]: D(T)
+    double* amp;               // spectra: [S][len/2 + 1] amplitudes |X_s(k)|
     int64_t seqs;              // S = B * C
     int64_t n_all, window_stride, channel_stride;
     int64_t len;
@@ -537,6 +538,110 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_inv_kernel(FftArgs a) {
     }
 }
 
+// Amplitudes |X_a(k)| and |X_b(k)| of the two sequences of a pair at
+// frequency k <= L/2, from Z(k) and Z(L - k): |Z(k) + conj Z(L-k)| / 2 and
+// |Z(k) - conj Z(L-k)| / 2.
+__device__ __forceinline__ void write_amplitudes(const FftArgs& a, int64_t pair, int64_t k,
+                                                 double2 zk, double2 zm) {
+    const double ux = zk.x + zm.x, uy = zk.y - zm.y;
+    const double vx = zk.x - zm.x, vy = zk.y + zm.y;
+    const int64_t half = a.len / 2 + 1;
+    const int64_t sa = 2 * pair, sb = sa + 1;
+    a.amp[sa * half + k] = 0.5 * sqrt(ux * ux + uy * uy);
+    if (sb < a.seqs) a.amp[sb * half + k] = 0.5 * sqrt(vx * vx + vy * vy);
+}
+
+// Spectrum of one pair in one workgroup (L up to one tile).
+template <int kTile>
+__global__ __launch_bounds__(kTThreads) void spec_single_kernel(FftArgs a) {
+    constexpr int kRegPoints = (1 << kTile) / kTThreads;
+    extern __shared__ double2 lds[];
+    const int64_t pair = blockIdx.x;
+    const Seq qa = seq_of(a, 2 * pair), qb = seq_of(a, 2 * pair + 1);
+    const int lg = a.lg;
+    const int len = 1 << lg;
+    {
+        double2 v[kRegPoints];
+#pragma unroll
+        for (int r = 0; r < kRegPoints; ++r) {
+            const int i = threadIdx.x + r * kTThreads;
+            v[r] = make_double2(centred(qa, i), centred(qb, i));
+        }
+#pragma unroll
+        for (int r = 0; r < kRegPoints; ++r) {
+            const int i = threadIdx.x + r * kTThreads;
+            if (i < len) lds[i] = v[r];
+        }
+    }
+    __syncthreads();
+    lds_fft_fwd<kTile>(lds, lg, 0, a.tw + a.tw_a);
+    for (int pos = threadIdx.x; pos < len; pos += kTThreads) {
+        const uint32_t k = bitrev(pos, lg);
+        if (k > (uint32_t)(len / 2)) continue;
+        const uint32_t km = (len - k) & (len - 1);
+        write_amplitudes(a, pair, k, lds[pos], lds[bitrev(km, lg)]);
+    }
+}
+
+// Spectrum of a split transform: after the column kernel, forward row
+// transforms of row pairs (k1, L1 - k1), then the amplitudes at every
+// frequency k = k1 + L1 k2 <= L/2 (each written once: a self-paired row only
+// from its first slot).
+template <int kTile>
+__global__ __launch_bounds__(kTThreads) void spec_rows_kernel(FftArgs a) {
+    constexpr int kRegPoints = (1 << kTile) / kTThreads;
+    extern __shared__ double2 lds[];
+    const int64_t per = (int64_t(1) << (a.lg1 - 1)) + 1;
+    const int64_t wgs = (per + (1 << a.lgr) - 1) >> a.lgr;
+    const int64_t id = xcd_remap(blockIdx.x, gridDim.x);
+    const int64_t pair = id / wgs;
+    const int64_t g0 = (id % wgs) << a.lgr;
+    const uint32_t l1 = 1u << a.lg1;
+    const int lgs = a.lgr + 1;
+    const int slots = 1 << lgs;
+    const int l2 = 1 << a.lg2;
+    const int npts = l2 << lgs;
+    const double2* __restrict__ zp = a.z + pair * a.len;
+    auto k1_of = [&](int q, bool& valid, bool& self) -> uint32_t {
+        const int64_t g = g0 + (q >> 1);
+        valid = g < per;
+        const uint32_t ka = (uint32_t)g, kb = (l1 - (uint32_t)g) & (l1 - 1);
+        self = ka == kb;
+        return (q & 1) ? kb : ka;
+    };
+    {
+        double2 v[kRegPoints];
+#pragma unroll
+        for (int r = 0; r < kRegPoints; ++r) {
+            const int f = threadIdx.x + r * kTThreads;
+            bool valid, self;
+            const uint32_t k1 = k1_of(f & (slots - 1), valid, self);
+            v[r] = (valid && f < npts) ? zp[(int64_t)bitrev(k1, a.lg1) * l2 + (f >> lgs)]
+                                       : make_double2(0.0, 0.0);
+        }
+#pragma unroll
+        for (int r = 0; r < kRegPoints; ++r) {
+            const int f = threadIdx.x + r * kTThreads;
+            if (f < npts) lds[f] = v[r];
+        }
+    }
+    __syncthreads();
+    lds_fft_fwd<kTile>(lds, a.lg2, lgs, a.tw + a.tw_b);
+    const int64_t half_len = a.len / 2;
+    for (int f = threadIdx.x; f < npts; f += kTThreads) {
+        const int q = f & (slots - 1);
+        bool valid, self;
+        const uint32_t k1 = k1_of(q, valid, self);
+        if (!valid || ((q & 1) && self)) continue;
+        const uint32_t k2 = bitrev(f >> lgs, a.lg2);
+        const int64_t k = (int64_t)k1 + (int64_t)l1 * k2;
+        if (k > half_len) continue;
+        const uint32_t k2m = k1 == 0 ? ((l2 - k2) & (l2 - 1)) : (l2 - 1 - k2);
+        const int qm = self ? q : (q ^ 1);
+        write_amplitudes(a, pair, k, lds[f], lds[(bitrev(k2m, a.lg2) << lgs) + qm]);
+    }
+}
+
 // Absolute error bound of the computed D(T) of sequence s (any T), from the
 // norms of s and of the sequence it shares the transform with.
 //
@@ -639,6 +744,163 @@ __global__ __launch_bounds__(kThreads) void fft_fixup_kernel(FixArgs a, Weights 
     }
 }
 
+struct SpecSelArgs {
+    double* amp;               // [S][half]: per-channel amplitudes, channel 0 overwritten by A
+    const double* fstat;       // [S][4]
+    gpoeo_pd_spectral_result* out;
+    int64_t seqs, half, len;
+    int32_t num_channels, tmin, tmax, k_max, lg;
+    double c_peak;
+};
+
+constexpr int kCandCap = 1024;   // candidates collected per window
+
+// Candidates of one window from its amplitude spectrum A(k) = sum_c w_c |X_c(k)|:
+// peaks (2 <= k <= L/2 - 1, A(k) > A(k-1), A(k) >= A(k+1)), the largest peak,
+// then the peaks above c_peak times it whose period round(L/k) is in
+// [tmin, tmax], strongest first (ties: smaller k).  The window is flagged
+// UNRESOLVED when a peak test, the threshold, or the order of the reported
+// candidates lies within four times the amplitude error bound (the list a
+// correctly rounded spectrum gives could then differ), or when more than
+// kCandCap candidates qualify.
+__global__ __launch_bounds__(kThreads) void spec_select_kernel(SpecSelArgs a, Weights w) {
+    __shared__ double red[kThreads];
+    __shared__ int32_t redi[kThreads];
+    __shared__ double cand_a[kCandCap];
+    __shared__ int32_t cand_k[kCandCap];
+    __shared__ int32_t ncand;
+    __shared__ int32_t flag;
+    const int64_t b = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int64_t half = a.half;               // L/2 + 1 bins
+    double* __restrict__ amp = a.amp + b * a.num_channels * half;
+    // 1. channel sum in channel order (into channel 0)
+    for (int64_t k = tid; k < half; k += kThreads) {
+        double acc = 0.0;
+        for (int32_t c = 0; c < a.num_channels; ++c) acc += (double)w.w[c] * amp[c * half + k];
+        amp[k] = acc;
+    }
+    if (tid == 0) {
+        ncand = 0;
+        flag = 0;
+    }
+    __syncthreads();
+    // 2. peaks and the largest one
+    double mx = 0.0;
+    int32_t npk = 0;
+    for (int64_t k = 2 + tid; k <= half - 2; k += kThreads) {
+        const double v = amp[k];
+        if (v > amp[k - 1] && v >= amp[k + 1]) {
+            ++npk;
+            mx = fmax(mx, v);
+        }
+    }
+    red[tid] = mx;
+    redi[tid] = npk;
+    __syncthreads();
+    for (int st = kThreads / 2; st > 0; st >>= 1) {
+        if (tid < st) {
+            red[tid] = fmax(red[tid], red[tid + st]);
+            redi[tid] += redi[tid + st];
+        }
+        __syncthreads();
+    }
+    const double top = red[0];
+    const int32_t n_peaks = redi[0];
+    __syncthreads();
+    // 3. error bound of A (any k): the transform bound of each channel's pair
+    // (as for the FFT scores: phi sqrt(L) zeta, plus the separation), summed
+    // with the weights, plus the rounding of the amplitude and the channel sum
+    const double u = 1.1102230246251565e-16;
+    const double mu = 16.0 * u;
+    const double g4 = 4.0 * u / (1.0 - 4.0 * u);
+    const double keta = (double)(a.lg + 1) * (mu + g4 * (1.4142135623730951 + mu));
+    const double phi = keta / (1.0 - keta);
+    double eps = 0.0;
+    for (int32_t c = 0; c < a.num_channels; ++c) {
+        const int64_t sq = b * a.num_channels + c, o = sq ^ 1;
+        const double z2 = a.fstat[4 * sq + 1] + (o < a.seqs ? a.fstat[4 * o + 1] : 0.0);
+        eps += (double)w.w[c] * (phi + 4.0 * u) * sqrt((double)a.len) * sqrt(z2);
+    }
+    eps = 2.0 * (eps + ((double)a.num_channels + 6.0) * u * top);
+    const double m = 4.0 * eps;
+    const double thr = a.c_peak * top;
+    // 4. candidates, and decisions too close to call
+    for (int64_t k = 2 + tid; k <= half - 2; k += kThreads) {
+        const double v = amp[k];
+        if (v + m < a.c_peak * (top - m)) continue;       // cannot matter
+        const double l = amp[k - 1], r = amp[k + 1];
+        const bool peak = v > l && v >= r;
+        if (fabs(v - l) <= m || fabs(v - r) <= m) atomicOr(&flag, 1);
+        if (!peak) continue;
+        const int64_t t = (2 * a.len + k) / (2 * k);       // round(L / k), halves up
+        if (t < a.tmin || t > a.tmax) continue;
+        if (fabs(v - thr) <= m * (1.0 + a.c_peak)) atomicOr(&flag, 1);
+        if (!(v > thr)) continue;
+        const int slot = atomicAdd(&ncand, 1);
+        if (slot < kCandCap) {
+            cand_a[slot] = v;
+            cand_k[slot] = (int32_t)k;
+        } else {
+            atomicOr(&flag, 2);
+        }
+    }
+    __syncthreads();
+    const int nc = min(ncand, kCandCap);
+    // 5. the strongest first: rounds of a block-wide arg-max (larger A, then smaller k)
+    gpoeo_pd_spectral_result res = {};
+    double prev = 0.0;
+    int rounds = min(nc, a.k_max + 1);                     // one more to check the order
+    for (int r = 0; r < rounds; ++r) {
+        double bv = -1.0;
+        int32_t bk = INT32_MAX, bi = -1;
+        for (int i = tid; i < nc; i += kThreads) {
+            const double v = cand_a[i];
+            if (v > bv || (v == bv && cand_k[i] < bk)) {
+                bv = v;
+                bk = cand_k[i];
+                bi = i;
+            }
+        }
+        red[tid] = bv;
+        redi[tid] = bi;
+        __syncthreads();
+        for (int st = kThreads / 2; st > 0; st >>= 1) {
+            if (tid < st) {
+                const int i1 = redi[tid + st], i0 = redi[tid];
+                const double v1 = red[tid + st], v0 = red[tid];
+                if (i1 >= 0 && (i0 < 0 || v1 > v0 || (v1 == v0 && cand_k[i1] < cand_k[i0]))) {
+                    red[tid] = v1;
+                    redi[tid] = i1;
+                }
+            }
+            __syncthreads();
+        }
+        const int best = redi[0];
+        const double bvv = red[0];
+        __syncthreads();
+        if (tid == 0) {
+            if (r > 0 && prev - bvv <= m) flag |= 1;
+            if (r < a.k_max) {
+                const int32_t k = cand_k[best];
+                res.periods[r] = (int32_t)((2 * a.len + k) / (2 * (int64_t)k));
+                res.bins[r] = k;
+                res.amplitudes[r] = bvv;
+                res.count = r + 1;
+            }
+            cand_a[best] = -1.0;                           // taken
+        }
+        prev = bvv;
+        __syncthreads();
+    }
+    if (tid == 0) {
+        res.n_peaks = n_peaks;
+        res.max_peak = top;
+        res.flags = flag ? GPOEO_PD_UNRESOLVED : 0u;
+        a.out[b] = res;
+    }
+}
+
 FftArgs args_of(const Plan& p, const float* x, double* fstat, double* edge, double* tw, double* z,
                 double* part) {
     FftArgs a;
@@ -648,6 +910,7 @@ FftArgs args_of(const Plan& p, const float* x, double* fstat, double* edge, doub
     a.tw = reinterpret_cast<const double2*>(tw);
     a.z = reinterpret_cast<double2*>(z);
     a.part = part;
+    a.amp = nullptr;
     a.seqs = p.num_windows * (int64_t)p.num_channels;
     a.n_all = p.n;
     a.window_stride = p.window_stride;
@@ -709,9 +972,9 @@ int64_t fft_twiddle_count(const Plan& p) {
     return p.fft_m1 / 2 + p.fft_m2 / 2 + p.fft_m2 + p.fft_m1;
 }
 
-hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, double* edge,
-                             double* tw, double* z, double* part, hipStream_t s) {
-    const FftArgs a = args_of(p, x, fstat, edge, tw, z, part);
+namespace {
+
+void launch_twiddles(const Plan& p, const FftArgs& a, double* tw, hipStream_t s) {
     const int64_t count = fft_twiddle_count(p);
     int64_t tg = (count + 255) / 256;
     if (tg > 1024) tg = 1024;
@@ -724,6 +987,61 @@ hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, doubl
                            reinterpret_cast<double2*>(tw), a.lg1, a.lg2, a.lg, a.lg2,
                            (int64_t)(p.fft_m2 / 2), (int64_t)p.fft_m2, (int64_t)p.fft_m1);
     }
+}
+
+template <int kTile>
+void launch_spectrum(const Plan& p, const FftArgs& a, hipStream_t s) {
+    if (p.fft_m2 == 1) {
+        const size_t lds = sizeof(double2) * (size_t)p.fft_len;
+        hipLaunchKernelGGL(spec_single_kernel<kTile>, dim3((unsigned)p.fft_pairs), dim3(kTThreads),
+                           lds, s, a);
+        return;
+    }
+    const int64_t col_groups = p.fft_pairs * (p.fft_m2 / p.fft_cols);
+    const size_t lds_cols = sizeof(double2) * (size_t)p.fft_m1 * p.fft_cols;
+    const int64_t rp = int64_t(1) << a.lgr;
+    const size_t lds_rows = sizeof(double2) * 2 * rp * (size_t)p.fft_m2;
+    const int64_t row_groups = p.fft_pairs * ((p.fft_m1 / 2 + 1 + rp - 1) / rp);
+    hipLaunchKernelGGL(fft_cols_fwd_kernel<kTile>, dim3((unsigned)col_groups), dim3(kTThreads),
+                       lds_cols, s, a);
+    hipLaunchKernelGGL(spec_rows_kernel<kTile>, dim3((unsigned)row_groups), dim3(kTThreads),
+                       lds_rows, s, a);
+}
+
+}  // namespace
+
+hipError_t launch_spectral(const Plan& p, const Weights& w, const float* x, const double* fstat,
+                           double* tw, double* z, double* amp, double c_peak, int32_t k_max,
+                           gpoeo_pd_spectral_result* out, hipStream_t s) {
+    FftArgs a = args_of(p, x, const_cast<double*>(fstat), nullptr, tw, z, nullptr);
+    a.amp = amp;
+    launch_twiddles(p, a, tw, s);
+    if (fft_tile_log2(a.lg) == kFftSmallTileLog2)
+        launch_spectrum<kFftSmallTileLog2>(p, a, s);
+    else
+        launch_spectrum<kFftTileLog2>(p, a, s);
+    SpecSelArgs sa;
+    sa.amp = amp;
+    sa.fstat = fstat;
+    sa.out = out;
+    sa.seqs = a.seqs;
+    sa.half = p.fft_len / 2 + 1;
+    sa.len = p.fft_len;
+    sa.num_channels = p.num_channels;
+    sa.tmin = p.tmin;
+    sa.tmax = p.tmax;
+    sa.k_max = k_max;
+    sa.lg = p.fft_log2;
+    sa.c_peak = c_peak;
+    hipLaunchKernelGGL(spec_select_kernel, dim3((unsigned)p.num_windows), dim3(kThreads), 0, s, sa,
+                       w);
+    return hipGetLastError();
+}
+
+hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, double* edge,
+                             double* tw, double* z, double* part, hipStream_t s) {
+    const FftArgs a = args_of(p, x, fstat, edge, tw, z, part);
+    launch_twiddles(p, a, tw, s);
     hipLaunchKernelGGL(fft_edge_kernel, dim3((unsigned)(2 * a.seqs)), dim3(kThreads), 0, s, a);
     if (fft_tile_log2(a.lg) == kFftSmallTileLog2)
         launch_transforms<kFftSmallTileLog2>(p, a, s);

@@ -197,6 +197,13 @@ hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, doubl
 hipError_t launch_fft_fixup(const Plan& p, const Weights& w, const float* x, const double* fstat,
                             double* s64, float* scores, const SelectBuffers& sb, hipStream_t s);
 hipError_t launch_select_init(const Plan& p, const SelectBuffers& sb, hipStream_t s);
+// Spectral candidates (Algorithm 1's FFT front end) of every window: a plan
+// whose FFT geometry is that of L = 2^k >= N; amp: [B*C][L/2 + 1] fp64.
+hipError_t launch_spectral(const Plan& p, const Weights& w, const float* x, const double* fstat,
+                           double* tw, double* z, double* amp, double c_peak, int32_t k_max,
+                           gpoeo_pd_spectral_result* out, hipStream_t s);
+// Sets the transform geometry of a plan for 2^lg points; false if too large.
+bool set_fft_geometry(Plan* p, int32_t lg);
 hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const double* var,
                          double* s64, const SelectBuffers& sb, void* results, hipStream_t s);
 hipError_t launch_rolling_schedule(const Plan& p, const RollingConfig& rc,

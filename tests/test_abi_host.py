@@ -53,12 +53,14 @@ def test_struct_layout_matches_header(tmp_path):
 #include <stddef.h>
 #include "gpoeo_pd.h"
 int main(void) {
-  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(gpoeo_pd_desc),
+  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(gpoeo_pd_desc),
          offsetof(gpoeo_pd_desc, c_lag), offsetof(gpoeo_pd_desc, channel_weights),
          offsetof(gpoeo_pd_desc, flags), sizeof(gpoeo_pd_result),
          offsetof(gpoeo_pd_result, n_rescored), sizeof(gpoeo_pd_rolling_result),
          offsetof(gpoeo_pd_rolling_result, smpdur_next), offsetof(gpoeo_pd_rolling_result, starts),
-         sizeof(gpoeo_pd_plan_info));
+         sizeof(gpoeo_pd_plan_info), sizeof(gpoeo_pd_spectral_params),
+         sizeof(gpoeo_pd_spectral_result), offsetof(gpoeo_pd_spectral_result, max_peak),
+         offsetof(gpoeo_pd_spectral_result, amplitudes));
   return 0;
 }
 """)
@@ -70,7 +72,9 @@ int main(void) {
     want = [ctypes.sizeof(B.Desc), B.Desc.c_lag.offset, B.Desc.channel_weights.offset,
             B.Desc.flags.offset, ctypes.sizeof(B.Result), B.Result.n_rescored.offset,
             ctypes.sizeof(B.RollingResult), B.RollingResult.smpdur_next.offset,
-            B.RollingResult.starts.offset, ctypes.sizeof(B.PlanInfo)]
+            B.RollingResult.starts.offset, ctypes.sizeof(B.PlanInfo),
+            ctypes.sizeof(B.SpectralParams), B.SPECTRAL_DTYPE.itemsize,
+            B.SPECTRAL_DTYPE.fields["max_peak"][1], B.SPECTRAL_DTYPE.fields["amplitudes"][1]]
     assert got == want
 
 
@@ -212,3 +216,26 @@ def test_fft_plan(lib):
     # rolling accepts the FFT flag
     d, _ = good_desc(flags=B.FFT_SCORES)
     assert B.rolling_workspace_bytes(d, B.rolling_params()) > 0
+
+
+@pytest.mark.parametrize("kw", [dict(c_peak=0.0), dict(c_peak=1.0), dict(max_candidates=0),
+                                dict(max_candidates=17)])
+def test_spectral_parameters_validated(lib, kw):
+    d, _ = good_desc()
+    with pytest.raises(B.GpoeoError) as e:
+        B.spectral_workspace_bytes(d, B.spectral_params(**kw))
+    assert e.value.status == B.EINVAL
+
+
+def test_spectral_workspace_and_pointers(lib):
+    d, _ = good_desc()
+    p = B.spectral_params()
+    need = B.spectral_workspace_bytes(d, p)
+    # 8 sequences of 4096 points: amplitudes of 2049 bins each at least
+    assert need >= 8 * 2049 * 8
+    call = lib.gpoeo_pd_spectral_candidates
+    assert call(ctypes.byref(d), ctypes.byref(p), 0x100000, 0x200000, 0x300000, need - 1,
+                None) == B.ENOMEM
+    assert call(ctypes.byref(d), None, 0x100000, 0x200000, 0x300000, need, None) == B.EINVAL
+    assert call(ctypes.byref(d), ctypes.byref(p), 0x100000, None, 0x300000, need,
+                None) == B.EINVAL
