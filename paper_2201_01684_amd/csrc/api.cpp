@@ -380,6 +380,11 @@ int make_rolling(const gpoeo_pd_desc* d, const gpoeo_pd_rolling_params* rp, Roll
     if (d->num_windows > INT32_MAX / jmax) return GPOEO_PD_EINVAL;
     dc.num_windows = d->num_windows * jmax;
     dc.window_stride = d->n;     // placeholder: the window table gives every offset
+    // The longest suffix starts at floor(D - (2 + c_eval step) T_init) (or 0), so
+    // it holds at most (2 + c_eval step) Tmax + 2 samples: the suffix plan is
+    // sized for that (its Tmax stays within half of it, as 2 + c_eval step >= 2).
+    const double longest = std::ceil((2.0 + rp->c_eval * rp->step) * (double)d->tmax) + 2.0;
+    if (longest < (double)d->n) dc.n = (int64_t)longest;
     rc = gpoeo::make_plan(&dc, &r->c);
     if (rc != GPOEO_PD_OK) return rc;
     r->rc.c_measure = rp->c_measure;

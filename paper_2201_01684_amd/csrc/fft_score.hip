@@ -763,6 +763,7 @@ constexpr int kCandCap = 1024;   // candidates collected per window
 // candidates lies within four times the amplitude error bound (the list a
 // correctly rounded spectrum gives could then differ), or when more than
 // kCandCap candidates qualify.
+template <int kThreads>
 __global__ __launch_bounds__(kThreads) void spec_select_kernel(SpecSelArgs a, Weights w) {
     __shared__ double red[kThreads];
     __shared__ int32_t redi[kThreads];
@@ -1033,8 +1034,12 @@ hipError_t launch_spectral(const Plan& p, const Weights& w, const float* x, cons
     sa.k_max = k_max;
     sa.lg = p.fft_log2;
     sa.c_peak = c_peak;
-    hipLaunchKernelGGL(spec_select_kernel, dim3((unsigned)p.num_windows), dim3(kThreads), 0, s, sa,
-                       w);
+    if (sa.half > 16384)   // long spectra: more of each window's bins in flight
+        hipLaunchKernelGGL(spec_select_kernel<1024>, dim3((unsigned)p.num_windows), dim3(1024), 0,
+                           s, sa, w);
+    else
+        hipLaunchKernelGGL(spec_select_kernel<kThreads>, dim3((unsigned)p.num_windows),
+                           dim3(kThreads), 0, s, sa, w);
     return hipGetLastError();
 }
 
