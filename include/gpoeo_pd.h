@@ -92,8 +92,10 @@ extern "C" {
 #define GPOEO_PD_SHORT 2u        /* (rolling detection) a suffix window too short for
                                     three lags starting at tmin; no period                 */
 
+#define GPOEO_PD_MAX_WINDOWS (1 << 21)   /* windows per call (rolling: B * suffix slots) */
+
 typedef struct {
-    int64_t num_windows;     /* B >= 1: traces, or sliding windows of one long trace        */
+    int64_t num_windows;     /* 1 <= B <= GPOEO_PD_MAX_WINDOWS: traces, or sliding windows  */
     int32_t num_channels;    /* C >= 1: per-lag channel scores are summed with weights      */
     int32_t reserved0;       /* must be 0                                                   */
     int64_t n;               /* N >= 8 samples per window                                   */
@@ -216,7 +218,9 @@ typedef struct {
 
 /* Validates desc (flags may hold GPOEO_PD_NO_RESCUE and GPOEO_PD_FFT_SCORES) and params and writes
  * the device workspace size of gpoeo_pd_detect_rolling.  EINVAL if the schedule
- * could exceed GPOEO_PD_ROLLING_MAX suffix windows. */
+ * could exceed GPOEO_PD_ROLLING_MAX suffix windows, or if B times the suffix
+ * slots per window (floor((2 + c_eval step - c_measure) / step) + 2) exceeds
+ * GPOEO_PD_MAX_WINDOWS. */
 int gpoeo_pd_rolling_workspace_bytes(const gpoeo_pd_desc* desc,
                                      const gpoeo_pd_rolling_params* params, size_t* bytes);
 

@@ -48,32 +48,38 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
 
 }  // namespace
 
+void fft_geometry(int32_t lg, int32_t* m1, int32_t* m2, int32_t* cols) {
+    const int tile = fft_tile_log2(lg);
+    if (lg <= tile) {
+        *m1 = 1 << lg;
+        *m2 = 1;
+        *cols = 1;
+    } else {
+        const int32_t lg1 = lg / 2, lg2 = lg - lg1;   // a row pair fits one tile
+        *m1 = 1 << lg1;
+        *m2 = 1 << lg2;
+        *cols = std::min<int32_t>(*m2, 1 << (tile - lg1));
+    }
+}
+
 bool set_fft_geometry(Plan* p, int32_t lg) {
     if (lg > kFftMaxLog2) return false;
     p->fft_log2 = lg;
     p->fft_len = int64_t(1) << lg;
-    const int tile = fft_tile_log2(lg);
-    if (lg <= tile) {
-        p->fft_m1 = (int32_t)p->fft_len;
-        p->fft_m2 = 1;
-        p->fft_cols = 1;
-    } else {
-        const int32_t lg1 = lg / 2, lg2 = lg - lg1;   // a row pair fits one tile
-        p->fft_m1 = 1 << lg1;
-        p->fft_m2 = 1 << lg2;
-        p->fft_cols = std::min<int32_t>(p->fft_m2, 1 << (tile - lg1));
-    }
+    fft_geometry(lg, &p->fft_m1, &p->fft_m2, &p->fft_cols);
     return true;
 }
 
 namespace {
 
-int make_plan(const gpoeo_pd_desc* d, Plan* p) {
+// ragged: the windows will come from a table (lengths up to d->n, Tmax up to
+// d->tmax); an FFT plan then sizes its transforms per pair (length classes).
+int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
     if (!d) return GPOEO_PD_EINVAL;
     if (d->reserved0 != 0 || d->reserved1 != 0) return GPOEO_PD_EINVAL;
     if (d->flags & ~(GPOEO_PD_SCORES_ONLY | GPOEO_PD_NO_RESCUE | GPOEO_PD_FFT_SCORES))
         return GPOEO_PD_EINVAL;
-    if (d->num_windows < 1 || d->num_windows > INT32_MAX) return GPOEO_PD_EINVAL;
+    if (d->num_windows < 1 || d->num_windows > GPOEO_PD_MAX_WINDOWS) return GPOEO_PD_EINVAL;
     if (d->num_channels < 1 || d->num_channels > kMaxChannels) return GPOEO_PD_EINVAL;
     if (d->n < 8 || d->n > (int64_t(1) << 40)) return GPOEO_PD_EINVAL;
     if (d->tmin < 1 || (int64_t)d->tmin + 2 > (int64_t)d->tmax || (int64_t)d->tmax > d->n / 2)
@@ -104,6 +110,7 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
     p->flags = d->flags;
 
     p->fft = (d->flags & GPOEO_PD_FFT_SCORES) != 0;
+    p->fft_ragged = p->fft && ragged;
     if (p->fft) {
         // smallest power of two (at least 64) holding N + Tmax points
         int32_t lg = 6;
@@ -207,12 +214,13 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
             return GPOEO_PD_EINVAL;
     }
     if (n_part > (INT64_MAX / 16)) return GPOEO_PD_EINVAL;
-    int64_t n_fstat = 0, n_edge = 0, n_tw = 0, n_z = 0;
+    int64_t n_fstat = 0, n_edge = 0, n_tw = 0, n_z = 0, n_cls = 0;
     if (p->fft) {
         if (!mul_ok(bc, 4, &n_fstat) || !mul_ok(bc, 2 * ((int64_t)d->tmax + 1), &n_edge) ||
             !mul_ok(p->fft_pairs, p->fft_len, &n_z) || n_z > (INT64_MAX / 64))
             return GPOEO_PD_EINVAL;
         n_tw = fft_twiddle_count(*p);
+        n_cls = fft_class_ints(*p);
     }
     size_t off = 0;
     p->off_var = off;
@@ -237,6 +245,8 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p) {
     off = align_up(off + (size_t)n_tw * 2 * sizeof(double));
     p->off_z = off;                               // transforms (complex fp64)
     off = align_up(off + (size_t)n_z * 2 * sizeof(double));
+    p->off_cls = off;                             // length classes (ragged FFT plans)
+    off = align_up(off + (size_t)n_cls * sizeof(int32_t));
     p->bytes = off;
     return GPOEO_PD_OK;
 }
@@ -303,15 +313,17 @@ int run_plan(const gpoeo::Plan& p, const gpoeo::Weights& w, const float* x, floa
     if (!mark(1)) return GPOEO_PD_EHIP;
     if (p.fft) {
         char* ws = static_cast<char*>(workspace);
+        int32_t* cls = p.fft_ragged ? reinterpret_cast<int32_t*>(ws + p.off_cls) : nullptr;
         if (gpoeo::launch_fft_scores(p, x, fstat, reinterpret_cast<double*>(ws + p.off_edge),
                                      reinterpret_cast<double*>(ws + p.off_tw),
-                                     reinterpret_cast<double*>(ws + p.off_z), c.part,
+                                     reinterpret_cast<double*>(ws + p.off_z), c.part, cls,
                                      stream) != hipSuccess)
             return GPOEO_PD_EHIP;
         if (!mark(2)) return GPOEO_PD_EHIP;
         if (gpoeo::launch_finalize(p, w, c.part, c.s64, scores, stream) != hipSuccess ||
             gpoeo::launch_select_init(p, c.sb, stream) != hipSuccess ||
-            gpoeo::launch_fft_fixup(p, w, x, fstat, c.s64, scores, c.sb, stream) != hipSuccess)
+            gpoeo::launch_fft_fixup(p, w, x, fstat, cls, c.s64, scores, c.sb, stream) !=
+                hipSuccess)
             return GPOEO_PD_EHIP;
     } else if (p.sliding) {
         if (gpoeo::launch_lag_score_blocks(p, x, c.part, c.cut, stream) != hipSuccess)
@@ -385,7 +397,7 @@ int make_rolling(const gpoeo_pd_desc* d, const gpoeo_pd_rolling_params* rp, Roll
     // sized for that (its Tmax stays within half of it, as 2 + c_eval step >= 2).
     const double longest = std::ceil((2.0 + rp->c_eval * rp->step) * (double)d->tmax) + 2.0;
     if (longest < (double)d->n) dc.n = (int64_t)longest;
-    rc = gpoeo::make_plan(&dc, &r->c);
+    rc = gpoeo::make_plan(&dc, &r->c, true);
     if (rc != GPOEO_PD_OK) return rc;
     r->rc.c_measure = rp->c_measure;
     r->rc.step = rp->step;

@@ -26,6 +26,7 @@
 // Accuracy: every lag's D(T) is within an absolute bound derived from the
 // sequence norms (fft_bound below); the lags for which that bound is not a
 // small fraction of the score are re-scored in fp64 before any decision.
+#include <algorithm>
 #include <cmath>
 
 #include "internal.h"
@@ -54,7 +55,27 @@ struct FftArgs {
     int32_t tmin, tmax, lags;
     int32_t lg, lg1, lg2, lgc, lgr;
     WindowTable tab;
+    // Ragged launches (windows of different lengths) transform the pairs of
+    // one length class, list[bounds[cls] .. bounds[cls + 1]) (class = log2 of
+    // the transform length).  Transform z of pair p sits at z + p * zstride.
+    const int32_t* list;
+    const int32_t* bounds;
+    int64_t zstride;
+    int32_t cls;
 };
+
+// Transform kernels come in two forms: uniform (kRagged false: one workgroup
+// per item, grid = items, the loop below runs once) and ragged (a capped grid
+// whose workgroups loop over the items of one length class).
+template <bool kRagged>
+__device__ __forceinline__ int64_t work_items(const FftArgs& a, int64_t per_pair) {
+    return kRagged ? (int64_t)(a.bounds[a.cls + 1] - a.bounds[a.cls]) * per_pair
+                   : (int64_t)gridDim.x;
+}
+template <bool kRagged>
+__device__ __forceinline__ int64_t pair_at(const FftArgs& a, int64_t k) {
+    return kRagged ? (int64_t)a.list[a.bounds[a.cls] + k] : k;
+}
 
 __device__ __forceinline__ double2 cadd(double2 a, double2 b) {
     return make_double2(a.x + b.x, a.y + b.y);
@@ -222,19 +243,22 @@ __device__ __forceinline__ void write_d(const FftArgs& a, int64_t s, int64_t t, 
 }
 
 // Sums of y^2 over the first T samples (head) and the last T samples (tail)
-// of a sequence, T = 0..Tmax; one workgroup per (sequence, side).  Tiles of
-// 4096 terms are staged in LDS with coalesced loads; each thread adds 16
-// consecutive terms, the thread totals are added in thread order, and the
+// of a sequence, T = 0..Tmax of its window; one workgroup per (sequence,
+// side).  Tiles of 4096 terms are loaded (all of a thread's loads in flight at
+// once) and staged in LDS; each thread adds 16 consecutive terms, an
+// exclusive scan of the thread totals (lane shuffles within each wavefront,
+// then the wavefront totals in order) gives each thread its offset, and the
 // running sums go back through LDS for coalesced stores.  (The mean, sum y^2
 // and sum |y| come from the window statistics, computed with the same mean.)
 constexpr int kEdgeTile = 4096;
 constexpr int kEdgePer = kEdgeTile / kThreads;   // 16 terms per thread
+constexpr int kEdgeWaves = kThreads / kWave;
 
 __device__ __forceinline__ int edge_slot(int k) { return k + (k >> 4); }   // padded: no bank clash
 
 __global__ __launch_bounds__(kThreads) void fft_edge_kernel(FftArgs a) {
     __shared__ double tile[kEdgeTile + kEdgeTile / 16];
-    __shared__ double excl[kThreads];
+    __shared__ double wsum[kEdgeWaves];
     const int64_t s = blockIdx.x >> 1;
     const int side = blockIdx.x & 1;
     const int64_t b = s / a.num_channels;
@@ -242,38 +266,45 @@ __global__ __launch_bounds__(kThreads) void fft_edge_kernel(FftArgs a) {
     const int64_t n = table_n(a.tab, b, a.n_all);
     const float* __restrict__ p = a.x + table_off(a.tab, b, a.window_stride) + c * a.channel_stride;
     const double mu = a.fstat[4 * s];
-    const int64_t span = (int64_t)a.tmax + 1;
-    double* __restrict__ out = a.edge + (s * 2 + side) * span;   // out[T], T = 0..Tmax
+    double* __restrict__ out = a.edge + (s * 2 + side) * ((int64_t)a.tmax + 1);   // out[T]
+    // T = 0 .. this window's largest lag (nothing for an empty slot)
+    const int64_t span = n > 0 ? (int64_t)min(table_tmax(a.tab, b, a.tmax), a.tmax) + 1 : 1;
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     if (threadIdx.x == 0) out[0] = 0.0;
     double carry = 0.0;
     for (int64_t k0 = 0; k0 < span - 1; k0 += kEdgeTile) {   // terms k0 .. k0 + 4095
-        for (int r = 0; r < kEdgePer; ++r) {
-            const int k = (int)threadIdx.x + r * kThreads;
-            const int64_t kk = k0 + k;
-            double t = 0.0;
-            if (kk < n && kk < span - 1) {
-                const int64_t i = side == 0 ? kk : n - 1 - kk;
-                const double y = (double)p[i] - mu;
-                t = y * y;
+        {
+            float v[kEdgePer];
+#pragma unroll
+            for (int r = 0; r < kEdgePer; ++r) {
+                const int64_t kk = k0 + (int)threadIdx.x + r * kThreads;
+                const bool in = kk < n && kk < span - 1;
+                v[r] = in ? p[side == 0 ? kk : n - 1 - kk] : 0.0f;
             }
-            tile[edge_slot(k)] = t;
+#pragma unroll
+            for (int r = 0; r < kEdgePer; ++r) {
+                const int k = (int)threadIdx.x + r * kThreads;
+                const int64_t kk = k0 + k;
+                const double y = (kk < n && kk < span - 1) ? (double)v[r] - mu : 0.0;
+                tile[edge_slot(k)] = y * y;
+            }
         }
         __syncthreads();
         double part = 0.0;
         for (int r = 0; r < kEdgePer; ++r) part += tile[edge_slot((int)threadIdx.x * kEdgePer + r)];
-        excl[threadIdx.x] = part;
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            double run = carry;
-            for (int k = 0; k < kThreads; ++k) {
-                const double v = excl[k];
-                excl[k] = run;
-                run += v;
-            }
-            tile[kEdgeTile + kEdgeTile / 16 - 1] = run;   // carry for the next tile
+        double inc = part;   // inclusive scan within the wavefront
+        for (int o = 1; o < kWave; o <<= 1) {
+            const double u = __shfl_up(inc, o);
+            if (lane >= o) inc += u;
         }
+        if (lane == kWave - 1) wsum[wave] = inc;
         __syncthreads();
-        double run = excl[threadIdx.x];
+        double run = carry, total = carry;
+        for (int w = 0; w < kEdgeWaves; ++w) {
+            if (w < wave) run += wsum[w];
+            total += wsum[w];
+        }
+        run += inc - part;   // this thread's exclusive offset
         for (int r = 0; r < kEdgePer; ++r) {
             const int k = (int)threadIdx.x * kEdgePer + r;
             run += tile[edge_slot(k)];
@@ -285,7 +316,7 @@ __global__ __launch_bounds__(kThreads) void fft_edge_kernel(FftArgs a) {
             const int64_t t = k0 + k + 1;
             if (t < span) out[t] = tile[edge_slot(k)];
         }
-        carry = tile[kEdgeTile + kEdgeTile / 16 - 1];
+        carry = total;
         __syncthreads();
     }
 }
@@ -320,11 +351,15 @@ __global__ void fft_twiddle_kernel(double2* tw, int lga, int lgb, int lg, int lg
 }
 
 // Whole transform of one pair in one workgroup (L <= 2^12).
-template <int kTile>
+template <int kTile, bool kRagged>
 __global__ __launch_bounds__(kTThreads) void fft_single_kernel(FftArgs a) {
     constexpr int kRegPoints = (1 << kTile) / kTThreads;
     extern __shared__ double2 lds[];
-    const int64_t pair = blockIdx.x;
+    const int64_t items = work_items<kRagged>(a, 1);
+    for (int64_t base = 0; base < items; base += gridDim.x) {
+    const int64_t item = base + blockIdx.x;
+    if (item >= items) break;
+    const int64_t pair = pair_at<kRagged>(a, item);
     const Seq qa = seq_of(a, 2 * pair), qb = seq_of(a, 2 * pair + 1);
     const int lg = a.lg;
     const int len = 1 << lg;
@@ -362,22 +397,29 @@ __global__ __launch_bounds__(kTThreads) void fft_single_kernel(FftArgs a) {
     }
     __syncthreads();
     lds_fft_inv<kTile>(lds, lg, 0, tw);
-    for (int64_t t = a.tmin + threadIdx.x; t <= a.tmax; t += kTThreads) {
+    const int64_t tend = min((int64_t)a.tmax, (int64_t)len - 1);
+    for (int64_t t = a.tmin + threadIdx.x; t <= tend; t += kTThreads) {
         write_d(a, 2 * pair, t, lds[t].x);
         write_d(a, 2 * pair + 1, t, lds[t].y);
+    }
+    if (!kRagged) break;
+    __syncthreads();   // the next pair reuses the LDS
     }
 }
 
 // Split transform, step 1: column transforms (L1 points, stride L2) of
 // 2^lgc neighbouring columns, then the twiddles W_L^(k1 n2).  Row p of the
 // output holds frequency k1 = bitrev(p).
-template <int kTile>
+template <int kTile, bool kRagged>
 __global__ __launch_bounds__(kTThreads) void fft_cols_fwd_kernel(FftArgs a) {
     constexpr int kRegPoints = (1 << kTile) / kTThreads;
     extern __shared__ double2 lds[];
     const int64_t groups = int64_t(1) << (a.lg2 - a.lgc);
-    const int64_t id = xcd_remap(blockIdx.x, gridDim.x);
-    const int64_t pair = id / groups;
+    const int64_t items = work_items<kRagged>(a, groups);
+    for (int64_t base = 0; base < items; base += gridDim.x) {
+    const int64_t id = base + xcd_remap(blockIdx.x, gridDim.x);
+    if (id >= items) break;
+    const int64_t pair = pair_at<kRagged>(a, id / groups);
     const int64_t c0 = (id % groups) << a.lgc;
     const int cols = 1 << a.lgc;
     const int npts = (1 << a.lg1) * cols;
@@ -399,7 +441,7 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_fwd_kernel(FftArgs a) {
     }
     __syncthreads();
     lds_fft_fwd<kTile>(lds, a.lg1, a.lgc, a.tw + a.tw_a);
-    double2* __restrict__ zp = a.z + pair * a.len;
+    double2* __restrict__ zp = a.z + pair * a.zstride;
     double2 w[kRegPoints];
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {   // twiddle loads first
@@ -412,27 +454,33 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_fwd_kernel(FftArgs a) {
         const int f = threadIdx.x + r * kTThreads;
         if (f < npts) zp[(int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1))] = cmul(lds[f], w[r]);
     }
+    if (!kRagged) break;
+    __syncthreads();   // the next item reuses the LDS
+    }
 }
 
 // Split transform, step 2: row k1 and its mirror row L1 - k1 (frequencies k
 // and L - k pair up between them): forward row transforms, separation into
 // the two sequences' power spectra, inverse row transforms, inverse twiddles.
 // A workgroup takes 2^lgr consecutive row pairs (4096 points in LDS).
-template <int kTile>
+template <int kTile, bool kRagged>
 __global__ __launch_bounds__(kTThreads) void fft_rows_kernel(FftArgs a) {
     constexpr int kRegPoints = (1 << kTile) / kTThreads;
     extern __shared__ double2 lds[];   // point i of slot q at i * 2^(lgr+1) + q
     const int64_t per = (int64_t(1) << (a.lg1 - 1)) + 1;   // row pairs per transform
     const int64_t wgs = (per + (1 << a.lgr) - 1) >> a.lgr;
-    const int64_t id = xcd_remap(blockIdx.x, gridDim.x);
-    const int64_t pair = id / wgs;
+    const int64_t items = work_items<kRagged>(a, wgs);
+    for (int64_t base = 0; base < items; base += gridDim.x) {
+    const int64_t id = base + xcd_remap(blockIdx.x, gridDim.x);
+    if (id >= items) break;
+    const int64_t pair = pair_at<kRagged>(a, id / wgs);
     const int64_t g0 = (id % wgs) << a.lgr;
     const uint32_t l1 = 1u << a.lg1;
     const int lgs = a.lgr + 1;                 // log2 of the slots
     const int slots = 1 << lgs;
     const int l2 = 1 << a.lg2;
     const int npts = l2 << lgs;
-    double2* __restrict__ zp = a.z + pair * a.len;
+    double2* __restrict__ zp = a.z + pair * a.zstride;
     // slot q: row pair g0 + (q >> 1), side q & 1 (0: k1 = g, 1: k1 = L1 - g)
     auto k1_of = [&](int q, bool& valid, bool& self) -> uint32_t {
         const int64_t g = g0 + (q >> 1);
@@ -497,23 +545,29 @@ __global__ __launch_bounds__(kTThreads) void fft_rows_kernel(FftArgs a) {
         if (f >= npts || !valid || ((q & 1) && self)) continue;
         zp[(int64_t)bitrev(k1, a.lg1) * l2 + (f >> lgs)] = cmul_conj(lds[f], wv[r]);
     }
+    if (!kRagged) break;
+    __syncthreads();   // the next item reuses the LDS
+    }
 }
 
 // Split transform, step 3: inverse column transforms (row p holds k1 =
 // bitrev(p): the bit-reversed input order of the decimation in time), and
 // D(T) for the lags T = n1 L2 + n2 in [tmin, tmax].
-template <int kTile>
+template <int kTile, bool kRagged>
 __global__ __launch_bounds__(kTThreads) void fft_cols_inv_kernel(FftArgs a) {
     constexpr int kRegPoints = (1 << kTile) / kTThreads;
     extern __shared__ double2 lds[];
     const int64_t groups = int64_t(1) << (a.lg2 - a.lgc);
-    const int64_t id = xcd_remap(blockIdx.x, gridDim.x);
-    const int64_t pair = id / groups;
+    const int64_t items = work_items<kRagged>(a, groups);
+    for (int64_t base = 0; base < items; base += gridDim.x) {
+    const int64_t id = base + xcd_remap(blockIdx.x, gridDim.x);
+    if (id >= items) break;
+    const int64_t pair = pair_at<kRagged>(a, id / groups);
     const int64_t c0 = (id % groups) << a.lgc;
     const int cols = 1 << a.lgc;
     const int npts = (1 << a.lg1) * cols;
     const int64_t l2 = int64_t(1) << a.lg2;
-    const double2* __restrict__ zp = a.z + pair * a.len;
+    const double2* __restrict__ zp = a.z + pair * a.zstride;
     {   // all loads of a thread in flight before its LDS writes
         double2 v[kRegPoints];
 #pragma unroll
@@ -530,11 +584,14 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_inv_kernel(FftArgs a) {
     }
     __syncthreads();
     lds_fft_inv<kTile>(lds, a.lg1, a.lgc, a.tw + a.tw_a);
-    const int rows = (int)(a.tmax / l2) + 1;
+    const int rows = (int)min((int64_t)(a.tmax / l2) + 1, int64_t(1) << a.lg1);
     for (int f = threadIdx.x; f < rows * cols; f += kTThreads) {
         const int64_t t = (int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1));
         write_d(a, 2 * pair, t, lds[f].x);
         write_d(a, 2 * pair + 1, t, lds[f].y);
+    }
+    if (!kRagged) break;
+    __syncthreads();   // the next item reuses the LDS
     }
 }
 
@@ -601,7 +658,7 @@ __global__ __launch_bounds__(kTThreads) void spec_rows_kernel(FftArgs a) {
     const int slots = 1 << lgs;
     const int l2 = 1 << a.lg2;
     const int npts = l2 << lgs;
-    const double2* __restrict__ zp = a.z + pair * a.len;
+    const double2* __restrict__ zp = a.z + pair * a.zstride;
     auto k1_of = [&](int q, bool& valid, bool& self) -> uint32_t {
         const int64_t g = g0 + (q >> 1);
         valid = g < per;
@@ -694,6 +751,7 @@ struct FixArgs {
     int32_t num_channels, tmin, tmax, lags, words, lg;
     double tau0;
     WindowTable tab;
+    const int32_t* pair_lg;    // per pair: log2 of its transform length, or null (all lg)
 };
 
 // One workgroup per window: lags whose score the FFT bound cannot place within
@@ -708,8 +766,11 @@ __global__ __launch_bounds__(kThreads) void fft_fixup_kernel(FixArgs a, Weights 
     const int32_t tm = table_tmax(a.tab, b, a.tmax);
     if (threadIdx.x == 0) {
         double acc = 0.0;
-        for (int32_t c = 0; c < a.num_channels; ++c)
-            acc += (double)w.w[c] * fft_bound(a.fstat, b * a.num_channels + c, a.seqs, n, a.lg);
+        for (int32_t c = 0; c < a.num_channels; ++c) {
+            const int64_t sq = b * a.num_channels + c;
+            const int lg = a.pair_lg ? a.pair_lg[sq >> 1] : a.lg;
+            acc += (double)w.w[c] * fft_bound(a.fstat, sq, a.seqs, n, lg);
+        }
         abound = acc * (1.0 + 1e-12);
     }
     __syncthreads();
@@ -902,6 +963,117 @@ __global__ __launch_bounds__(kThreads) void spec_select_kernel(SpecSelArgs a, We
     }
 }
 
+// Length classes of a batch of windows of different lengths (a window table):
+// the class of a pair is the log2 of the smallest power of two (at least 64)
+// holding N + Tmax of each non-empty sequence of the pair, -1 if both are
+// empty.  Writes every pair's class, then the pairs sorted by class (ascending
+// pair index within a class: a stable counting sort in one workgroup) and the
+// start of each class in that list.
+constexpr int kClassThreads = 1024;
+constexpr int kClassWaves = kClassThreads / kWave;
+
+struct ClassArgs {
+    int32_t* pair_lg;          // [pairs]
+    int32_t* list;             // [pairs]
+    int32_t* bounds;           // [kFftClasses + 1]
+    int64_t pairs, seqs, n_all;
+    int32_t num_channels, tmax, lg_max;
+    WindowTable tab;
+};
+
+__device__ int class_of(const ClassArgs& a, int64_t pair) {
+    int lg = -1;
+    for (int64_t s = 2 * pair; s < 2 * pair + 2 && s < a.seqs; ++s) {
+        const int64_t b = s / a.num_channels;
+        const int64_t n = table_n(a.tab, b, a.n_all);
+        if (n <= 0) continue;
+        const int64_t need = n + (int64_t)min(table_tmax(a.tab, b, a.tmax), a.tmax);
+        int l = kFftMinLog2;
+        while (l < a.lg_max && (int64_t(1) << l) < need) ++l;
+        lg = max(lg, l);
+    }
+    return lg;
+}
+
+__global__ __launch_bounds__(kClassThreads) void fft_classify_kernel(ClassArgs a) {
+    __shared__ int32_t run[kFftClasses];
+    __shared__ int32_t wcount[kClassWaves][kFftClasses];
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    if (tid < kFftClasses) run[tid] = 0;
+    __syncthreads();
+    for (int64_t p = tid; p < a.pairs; p += kClassThreads) {
+        const int lg = class_of(a, p);
+        a.pair_lg[p] = lg;
+        if (lg >= 0) atomicAdd(&run[lg], 1);
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int32_t acc = 0;
+        for (int c = 0; c < kFftClasses; ++c) {
+            const int32_t k = run[c];
+            run[c] = acc;
+            a.bounds[c] = acc;
+            acc += k;
+        }
+        a.bounds[kFftClasses] = acc;
+    }
+    for (int64_t p0 = 0; p0 < a.pairs; p0 += kClassThreads) {
+        for (int i = tid; i < kClassWaves * kFftClasses; i += kClassThreads)
+            wcount[i / kFftClasses][i % kFftClasses] = 0;
+        __syncthreads();
+        const int64_t p = p0 + tid;
+        const int lg = p < a.pairs ? a.pair_lg[p] : -1;   // written by this thread above
+        int rank = 0;
+        uint64_t todo = __ballot(lg >= 0);
+        while (todo) {                                     // one round per class in the wave
+            const int c = __shfl(lg, __builtin_ctzll(todo));
+            const uint64_t same = __ballot(lg == c);
+            if (lg == c) rank = __popcll(same & ((uint64_t(1) << lane) - 1));
+            if (lane == 0) wcount[wave][c] = __popcll(same);
+            todo &= ~same;
+        }
+        __syncthreads();
+        if (lg >= 0) {
+            int32_t off = run[lg] + rank;
+            for (int w = 0; w < wave; ++w) off += wcount[w][lg];
+            a.list[off] = (int32_t)p;
+        }
+        __syncthreads();
+        if (tid < kFftClasses) {
+            int32_t add = 0;
+            for (int w = 0; w < kClassWaves; ++w) add += wcount[w][tid];
+            run[tid] += add;
+        }
+        __syncthreads();
+    }
+}
+
+// Transform geometry of 2^lg points in the launch arguments.
+void set_geometry(FftArgs& a, int lg) {
+    int32_t m1, m2, cols;
+    fft_geometry(lg, &m1, &m2, &cols);
+    a.lg = lg;
+    a.len = int64_t(1) << lg;
+    if (m2 == 1) {   // one workgroup per pair
+        a.lg1 = lg;
+        a.lg2 = 0;
+        a.lgc = 0;
+        a.lgr = 0;
+        a.tw_a = 0;
+        a.tw_b = a.tw_lo = a.tw_hi = 0;
+    } else {
+        a.lg1 = __builtin_ctz((unsigned)m1);
+        a.lg2 = __builtin_ctz((unsigned)m2);
+        a.lgc = __builtin_ctz((unsigned)cols);
+        const int tile = fft_tile_log2(lg);
+        a.lgr = a.lg2 >= tile - 1 ? 0 : tile - 1 - a.lg2;   // row pairs per tile
+        a.tw_a = 0;
+        a.tw_b = m1 / 2;
+        a.tw_lo = a.tw_b + m2 / 2;
+        a.tw_hi = a.tw_lo + m2;
+    }
+}
+
 FftArgs args_of(const Plan& p, const float* x, double* fstat, double* edge, double* tw, double* z,
                 double* part) {
     FftArgs a;
@@ -916,77 +1088,89 @@ FftArgs args_of(const Plan& p, const float* x, double* fstat, double* edge, doub
     a.n_all = p.n;
     a.window_stride = p.window_stride;
     a.channel_stride = p.channel_stride;
-    a.len = p.fft_len;
     a.num_channels = p.num_channels;
     a.tmin = p.tmin;
     a.tmax = p.tmax;
     a.lags = p.lags;
-    a.lg = p.fft_log2;
     a.tab = p.table;
-    if (p.fft_m2 == 1) {   // one workgroup per pair
-        a.lg1 = p.fft_log2;
-        a.lg2 = 0;
-        a.lgc = 0;
-        a.lgr = 0;
-        a.tw_a = 0;
-        a.tw_b = a.tw_lo = a.tw_hi = 0;
-    } else {
-        a.lg1 = __builtin_ctz((unsigned)p.fft_m1);
-        a.lg2 = __builtin_ctz((unsigned)p.fft_m2);
-        a.lgc = __builtin_ctz((unsigned)p.fft_cols);
-        const int tile = fft_tile_log2(a.lg);
-        a.lgr = a.lg2 >= tile - 1 ? 0 : tile - 1 - a.lg2;   // row pairs per tile
-        a.tw_a = 0;
-        a.tw_b = p.fft_m1 / 2;
-        a.tw_lo = a.tw_b + p.fft_m2 / 2;
-        a.tw_hi = a.tw_lo + p.fft_m2;
-    }
+    a.list = nullptr;
+    a.bounds = nullptr;
+    a.zstride = p.fft_len;
+    a.cls = 0;
+    set_geometry(a, p.fft_log2);
     return a;
 }
 
-template <int kTile>
-void launch_transforms(const Plan& p, const FftArgs& a, hipStream_t s) {
-    if (p.fft_m2 == 1) {
-        const size_t lds = sizeof(double2) * (size_t)p.fft_len;
-        hipLaunchKernelGGL(fft_single_kernel<kTile>, dim3((unsigned)p.fft_pairs), dim3(kTThreads),
-                           lds, s, a);
+// Workgroups of a ragged launch: the pairs of a class are known only on the
+// GPU, so each launch gets a fixed grid whose workgroups loop over the class.
+constexpr int64_t kRaggedGrid = 4096;
+
+// The transform kernels for the geometry in `a`, over `pairs` pairs (a
+// uniform batch: one workgroup per item), or over at most `pairs` pairs of one
+// length class (ragged: a capped grid).
+template <int kTile, bool kRagged>
+void launch_transforms(const FftArgs& a, int64_t pairs, hipStream_t s) {
+    auto grid = [&](int64_t items) {
+        return dim3((unsigned)(kRagged ? std::min(items, kRaggedGrid) : items));
+    };
+    if (a.lg2 == 0) {
+        const size_t lds = sizeof(double2) * (size_t)a.len;
+        hipLaunchKernelGGL((fft_single_kernel<kTile, kRagged>), grid(pairs), dim3(kTThreads), lds,
+                           s, a);
         return;
     }
-    const int64_t col_groups = p.fft_pairs * (p.fft_m2 / p.fft_cols);
-    const size_t lds_cols = sizeof(double2) * (size_t)p.fft_m1 * p.fft_cols;
+    const int64_t m1 = int64_t(1) << a.lg1, m2 = int64_t(1) << a.lg2, cols = int64_t(1) << a.lgc;
+    const int64_t col_groups = pairs * (m2 / cols);
+    const size_t lds_cols = sizeof(double2) * (size_t)(m1 * cols);
     const int64_t rp = int64_t(1) << a.lgr;
-    const size_t lds_rows = sizeof(double2) * 2 * rp * (size_t)p.fft_m2;
-    const int64_t row_groups = p.fft_pairs * ((p.fft_m1 / 2 + 1 + rp - 1) / rp);
-    hipLaunchKernelGGL(fft_cols_fwd_kernel<kTile>, dim3((unsigned)col_groups), dim3(kTThreads),
+    const size_t lds_rows = sizeof(double2) * 2 * (size_t)(rp * m2);
+    const int64_t row_groups = pairs * ((m1 / 2 + 1 + rp - 1) / rp);
+    hipLaunchKernelGGL((fft_cols_fwd_kernel<kTile, kRagged>), grid(col_groups), dim3(kTThreads),
                        lds_cols, s, a);
-    hipLaunchKernelGGL(fft_rows_kernel<kTile>, dim3((unsigned)row_groups), dim3(kTThreads),
+    hipLaunchKernelGGL((fft_rows_kernel<kTile, kRagged>), grid(row_groups), dim3(kTThreads),
                        lds_rows, s, a);
-    hipLaunchKernelGGL(fft_cols_inv_kernel<kTile>, dim3((unsigned)col_groups), dim3(kTThreads),
+    hipLaunchKernelGGL((fft_cols_inv_kernel<kTile, kRagged>), grid(col_groups), dim3(kTThreads),
                        lds_cols, s, a);
+}
+
+// Complex fp64 entries of the twiddle tables of one transform of 2^lg points.
+int64_t twiddle_count_of(int lg) {
+    int32_t m1, m2, cols;
+    fft_geometry(lg, &m1, &m2, &cols);
+    if (m2 == 1) return (int64_t)m1 / 2;
+    return m1 / 2 + m2 / 2 + m2 + m1;
 }
 
 }  // namespace
 
-// Complex fp64 entries of the twiddle tables of a plan.
+// Complex fp64 entries of the twiddle tables of a plan (a ragged plan: those
+// of every length class, one after another).
 int64_t fft_twiddle_count(const Plan& p) {
-    if (p.fft_m2 == 1) return p.fft_len / 2;
-    return p.fft_m1 / 2 + p.fft_m2 / 2 + p.fft_m2 + p.fft_m1;
+    if (!p.fft_ragged) return twiddle_count_of(p.fft_log2);
+    int64_t total = 0;
+    for (int lg = kFftMinLog2; lg <= p.fft_log2; ++lg) total += twiddle_count_of(lg);
+    return total;
+}
+
+// int32 entries of the length-class buffers of a plan.
+int64_t fft_class_ints(const Plan& p) {
+    return p.fft_ragged ? 2 * p.fft_pairs + kFftClasses + 1 : 0;
 }
 
 namespace {
 
-void launch_twiddles(const Plan& p, const FftArgs& a, double* tw, hipStream_t s) {
-    const int64_t count = fft_twiddle_count(p);
+// Twiddle tables of the geometry in `a`, written at `tw`.
+void launch_twiddles(const FftArgs& a, double2* tw, hipStream_t s) {
+    const int64_t count = twiddle_count_of(a.lg);
     int64_t tg = (count + 255) / 256;
     if (tg > 1024) tg = 1024;
-    if (p.fft_m2 == 1) {
-        hipLaunchKernelGGL(fft_twiddle_kernel, dim3((unsigned)tg), dim3(256), 0, s,
-                           reinterpret_cast<double2*>(tw), a.lg, 1, a.lg, 0, (int64_t)0,
-                           (int64_t)0, (int64_t)0);
+    if (a.lg2 == 0) {
+        hipLaunchKernelGGL(fft_twiddle_kernel, dim3((unsigned)tg), dim3(256), 0, s, tw, a.lg, 1,
+                           a.lg, 0, (int64_t)0, (int64_t)0, (int64_t)0);
     } else {
-        hipLaunchKernelGGL(fft_twiddle_kernel, dim3((unsigned)tg), dim3(256), 0, s,
-                           reinterpret_cast<double2*>(tw), a.lg1, a.lg2, a.lg, a.lg2,
-                           (int64_t)(p.fft_m2 / 2), (int64_t)p.fft_m2, (int64_t)p.fft_m1);
+        const int64_t m1 = int64_t(1) << a.lg1, m2 = int64_t(1) << a.lg2;
+        hipLaunchKernelGGL(fft_twiddle_kernel, dim3((unsigned)tg), dim3(256), 0, s, tw, a.lg1,
+                           a.lg2, a.lg, a.lg2, m2 / 2, m2, m1);
     }
 }
 
@@ -1003,8 +1187,8 @@ void launch_spectrum(const Plan& p, const FftArgs& a, hipStream_t s) {
     const int64_t rp = int64_t(1) << a.lgr;
     const size_t lds_rows = sizeof(double2) * 2 * rp * (size_t)p.fft_m2;
     const int64_t row_groups = p.fft_pairs * ((p.fft_m1 / 2 + 1 + rp - 1) / rp);
-    hipLaunchKernelGGL(fft_cols_fwd_kernel<kTile>, dim3((unsigned)col_groups), dim3(kTThreads),
-                       lds_cols, s, a);
+    hipLaunchKernelGGL((fft_cols_fwd_kernel<kTile, false>), dim3((unsigned)col_groups),
+                       dim3(kTThreads), lds_cols, s, a);
     hipLaunchKernelGGL(spec_rows_kernel<kTile>, dim3((unsigned)row_groups), dim3(kTThreads),
                        lds_rows, s, a);
 }
@@ -1016,7 +1200,7 @@ hipError_t launch_spectral(const Plan& p, const Weights& w, const float* x, cons
                            gpoeo_pd_spectral_result* out, hipStream_t s) {
     FftArgs a = args_of(p, x, const_cast<double*>(fstat), nullptr, tw, z, nullptr);
     a.amp = amp;
-    launch_twiddles(p, a, tw, s);
+    launch_twiddles(a, reinterpret_cast<double2*>(tw), s);
     if (fft_tile_log2(a.lg) == kFftSmallTileLog2)
         launch_spectrum<kFftSmallTileLog2>(p, a, s);
     else
@@ -1044,19 +1228,53 @@ hipError_t launch_spectral(const Plan& p, const Weights& w, const float* x, cons
 }
 
 hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, double* edge,
-                             double* tw, double* z, double* part, hipStream_t s) {
+                             double* tw, double* z, double* part, int32_t* cls, hipStream_t s) {
     const FftArgs a = args_of(p, x, fstat, edge, tw, z, part);
-    launch_twiddles(p, a, tw, s);
+    double2* const tw2 = reinterpret_cast<double2*>(tw);
+    if (!p.fft_ragged) {
+        launch_twiddles(a, tw2, s);
+        hipLaunchKernelGGL(fft_edge_kernel, dim3((unsigned)(2 * a.seqs)), dim3(kThreads), 0, s, a);
+        if (fft_tile_log2(a.lg) == kFftSmallTileLog2)
+            launch_transforms<kFftSmallTileLog2, false>(a, p.fft_pairs, s);
+        else
+            launch_transforms<kFftTileLog2, false>(a, p.fft_pairs, s);
+        return hipGetLastError();
+    }
+    // ragged: classify the pairs, then every length class at its own length
+    ClassArgs ca;
+    ca.pair_lg = cls;
+    ca.list = cls + p.fft_pairs;
+    ca.bounds = cls + 2 * p.fft_pairs;
+    ca.pairs = p.fft_pairs;
+    ca.seqs = a.seqs;
+    ca.n_all = p.n;
+    ca.num_channels = p.num_channels;
+    ca.tmax = p.tmax;
+    ca.lg_max = p.fft_log2;
+    ca.tab = p.table;
+    hipLaunchKernelGGL(fft_classify_kernel, dim3(1), dim3(kClassThreads), 0, s, ca);
     hipLaunchKernelGGL(fft_edge_kernel, dim3((unsigned)(2 * a.seqs)), dim3(kThreads), 0, s, a);
-    if (fft_tile_log2(a.lg) == kFftSmallTileLog2)
-        launch_transforms<kFftSmallTileLog2>(p, a, s);
-    else
-        launch_transforms<kFftTileLog2>(p, a, s);
+    int64_t tw_off = 0;
+    for (int lg = kFftMinLog2; lg <= p.fft_log2; ++lg) {
+        FftArgs ac = a;
+        set_geometry(ac, lg);
+        ac.tw = tw2 + tw_off;
+        ac.list = ca.list;
+        ac.bounds = ca.bounds;
+        ac.cls = lg;
+        launch_twiddles(ac, tw2 + tw_off, s);
+        if (fft_tile_log2(lg) == kFftSmallTileLog2)
+            launch_transforms<kFftSmallTileLog2, true>(ac, p.fft_pairs, s);
+        else
+            launch_transforms<kFftTileLog2, true>(ac, p.fft_pairs, s);
+        tw_off += twiddle_count_of(lg);
+    }
     return hipGetLastError();
 }
 
 hipError_t launch_fft_fixup(const Plan& p, const Weights& w, const float* x, const double* fstat,
-                            double* s64, float* scores, const SelectBuffers& sb, hipStream_t s) {
+                            const int32_t* cls, double* s64, float* scores,
+                            const SelectBuffers& sb, hipStream_t s) {
     FixArgs a;
     a.x = x;
     a.fstat = fstat;
@@ -1076,6 +1294,7 @@ hipError_t launch_fft_fixup(const Plan& p, const Weights& w, const float* x, con
     a.lg = p.fft_log2;
     a.tau0 = kFftRelBound;
     a.tab = p.table;
+    a.pair_lg = p.fft_ragged ? cls : nullptr;
     hipLaunchKernelGGL(fft_fixup_kernel, dim3((unsigned)p.num_windows), dim3(kThreads), 0, s, a,
                        w);
     return hipGetLastError();

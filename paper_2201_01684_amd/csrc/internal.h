@@ -31,6 +31,8 @@ constexpr int kFftSmallTileLog2 = 11;
 constexpr int kFftTileLog2 = 12;
 constexpr int kFftThreadsLog2 = 8;
 constexpr int kFftMaxLog2 = 2 * (kFftTileLog2 - 1);
+constexpr int kFftMinLog2 = 6;
+constexpr int kFftClasses = kFftMaxLog2 + 1;   // length classes 2^lg of a ragged batch, by lg
 inline int fft_tile_log2(int lg) { return lg <= 2 * (kFftSmallTileLog2 - 1) ? kFftSmallTileLog2 : kFftTileLog2; }
 
 struct Weights {
@@ -118,7 +120,12 @@ struct Plan {
     // and imaginary parts of one complex transform.  Up to 2^12 points one
     // workgroup transforms a pair in LDS; beyond that the transform is split
     // as fft_len = fft_m1 * fft_m2 (columns of fft_m1 points, rows of fft_m2).
+    // A ragged FFT plan (windows from a table, of different lengths) gives
+    // each pair the shortest transform its two sequences need: the pairs are
+    // sorted into length classes 2^lg, lg in [kFftMinLog2, fft_log2], on the
+    // GPU, and every class runs at its own length.
     bool fft;
+    bool fft_ragged;
     int32_t fft_log2, fft_m1, fft_m2, fft_cols;
     int64_t fft_len;
     int64_t fft_pairs;
@@ -128,7 +135,7 @@ struct Plan {
     int32_t bitmap_words;    // 32-bit words per window of the exactness bitmap
     // workspace layout (byte offsets, 256-byte aligned)
     size_t off_var, off_s64, off_bits, off_state, off_queue, off_part, off_cut;
-    size_t off_fstat, off_edge, off_tw, off_z, bytes;
+    size_t off_fstat, off_edge, off_tw, off_z, off_cls, bytes;
 };
 
 // Rolling detection (Algorithm 3).
@@ -189,19 +196,26 @@ hipError_t launch_finalize(const Plan& p, const Weights& w, const double* part, 
 // centred sequence, and its absolute error bound on D(T); edge: [B*C][2][Tmax+1]
 // prefix sums of squares from the head and from the tail; tw: twiddle tables;
 // z: [pairs][fft_len] complex fp64.  Writes D_c(T) into part ([B*C][lags]).
+// cls (ragged plans): [pairs] class of each pair, [pairs] pairs sorted by class,
+// [kFftClasses + 1] start of each class; null otherwise.
 int64_t fft_twiddle_count(const Plan& p);
+int64_t fft_class_ints(const Plan& p);
 hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, double* edge,
-                             double* tw, double* z, double* part, hipStream_t s);
+                             double* tw, double* z, double* part, int32_t* cls, hipStream_t s);
 // After the finalisation: every lag whose FFT bound does not give the tier-0
 // guarantee is re-scored in fp64 (score, fp32 score and tier-1 bit).
 hipError_t launch_fft_fixup(const Plan& p, const Weights& w, const float* x, const double* fstat,
-                            double* s64, float* scores, const SelectBuffers& sb, hipStream_t s);
+                            const int32_t* cls, double* s64, float* scores,
+                            const SelectBuffers& sb, hipStream_t s);
 hipError_t launch_select_init(const Plan& p, const SelectBuffers& sb, hipStream_t s);
 // Spectral candidates (Algorithm 1's FFT front end) of every window: a plan
 // whose FFT geometry is that of L = 2^k >= N; amp: [B*C][L/2 + 1] fp64.
 hipError_t launch_spectral(const Plan& p, const Weights& w, const float* x, const double* fstat,
                            double* tw, double* z, double* amp, double c_peak, int32_t k_max,
                            gpoeo_pd_spectral_result* out, hipStream_t s);
+// Transform of 2^lg points: one workgroup (m2 = 1), or m1 columns of m2 rows
+// with `cols` columns per column workgroup.
+void fft_geometry(int32_t lg, int32_t* m1, int32_t* m2, int32_t* cols);
 // Sets the transform geometry of a plan for 2^lg points; false if too large.
 bool set_fft_geometry(Plan* p, int32_t lg);
 hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const double* var,

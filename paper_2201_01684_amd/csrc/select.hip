@@ -50,7 +50,9 @@ using exact::wave_score;
 
 constexpr int kThreads = 256;       // re-score and initialisation kernels and short windows
 // Selection passes run one workgroup per window; from this many lags on, four
-// times as many threads keep more of a window's scores in flight.
+// times as many threads keep more of a window's scores in flight.  A window
+// table (suffix windows, mostly far shorter than the plan's lag range) keeps
+// the narrow workgroups: more windows in flight at once.
 constexpr int kWideLags = 4096;
 constexpr int kRescoreGroups = 1024;   // workgroups of one re-score round
 
@@ -97,41 +99,40 @@ __device__ __forceinline__ Tri le(const Iv& a, const Iv& b) {
     return kUnk;
 }
 
+// Block reductions: a butterfly of lane shuffles inside each wavefront, the
+// per-wave results through LDS, then every thread folds them in wave order.
+// (min and integer sums: the result does not depend on the order.)
 template <int kT>
 __device__ double block_min_d(double v, double* red) {
-    red[threadIdx.x] = v;
+    for (int o = kWave / 2; o > 0; o >>= 1) v = fmin(v, __shfl_xor(v, o));
+    if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = v;
     __syncthreads();
-    for (int w = kT / 2; w > 0; w >>= 1) {
-        if ((int)threadIdx.x < w) red[threadIdx.x] = fmin(red[threadIdx.x], red[threadIdx.x + w]);
-        __syncthreads();
-    }
-    const double r = red[0];
+    double r = red[0];
+    for (int w = 1; w < kT / kWave; ++w) r = fmin(r, red[w]);
     __syncthreads();
     return r;
 }
 
 template <int kT>
 __device__ int64_t block_sum_i(int64_t v, int64_t* red) {
-    red[threadIdx.x] = v;
+    long long x = v;
+    for (int o = kWave / 2; o > 0; o >>= 1) x += __shfl_xor(x, o);
+    if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = x;
     __syncthreads();
-    for (int w = kT / 2; w > 0; w >>= 1) {
-        if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-        __syncthreads();
-    }
-    const int64_t r = red[0];
+    int64_t r = red[0];
+    for (int w = 1; w < kT / kWave; ++w) r += red[w];
     __syncthreads();
     return r;
 }
 
 template <int kT>
 __device__ int64_t block_min_i(int64_t v, int64_t* red) {
-    red[threadIdx.x] = v;
+    long long x = v;
+    for (int o = kWave / 2; o > 0; o >>= 1) x = min(x, __shfl_xor(x, o));
+    if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = x;
     __syncthreads();
-    for (int w = kT / 2; w > 0; w >>= 1) {
-        if ((int)threadIdx.x < w) red[threadIdx.x] = min(red[threadIdx.x], red[threadIdx.x + w]);
-        __syncthreads();
-    }
-    const int64_t r = red[0];
+    int64_t r = red[0];
+    for (int w = 1; w < kT / kWave; ++w) r = min(r, red[w]);
     __syncthreads();
     return r;
 }
@@ -139,10 +140,10 @@ __device__ int64_t block_min_i(int64_t v, int64_t* red) {
 
 template <int kT>
 struct Shared {
-    double red_d[kT];
-    double red_d2[kT];
-    int64_t red_i[kT];
-    int64_t red_j[kT];
+    double red_d[kT / kWave];
+    double red_d2[kT / kWave];
+    int64_t red_i[kT / kWave];
+    int64_t red_j[kT / kWave];
     int done;
     double r_approx;
     double r_err;
@@ -550,7 +551,7 @@ hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const 
     for (int pass = 0; pass < passes; ++pass) {
         a.pass = pass;
         a.last = pass == passes - 1;
-        if (p.lags >= kWideLags)
+        if (p.lags >= kWideLags && !p.table.n)
             hipLaunchKernelGGL(select_pass_kernel<1024>, grid_sel, dim3(1024), 0, s, a, w);
         else
             hipLaunchKernelGGL(select_pass_kernel<kThreads>, grid_sel, dim3(kThreads), 0, s, a, w);

@@ -11,6 +11,8 @@
 // finalize: per (window, lag), combines the fp64 chunk partials of every
 //   channel in ascending chunk order, divides by the N-T pairs and forms the
 //   weighted channel sum S(T) (the composite detection feature of Sec. 4.2).
+#include <algorithm>
+
 #include "internal.h"
 
 namespace gpoeo {
@@ -102,25 +104,29 @@ __global__ __launch_bounds__(kStatsThreads) void window_stats_kernel(
     }
 }
 
+// One workgroup per (window, block of 256 lags).  A window of a table scores
+// only its own lag range [tmin, Tmax_b]; with no fp32 scores requested, the
+// fp64 entries past it are left unwritten (nothing reads them), otherwise
+// both are zero there.
 __global__ __launch_bounds__(256) void finalize_kernel(const double* __restrict__ part,
                                                        double* __restrict__ s64,
                                                        float* __restrict__ scores, Weights w,
-                                                       int64_t num_windows, int32_t num_channels,
-                                                       int64_t n_all, int32_t tmin, int32_t lags,
-                                                       int32_t t0, int32_t lags_padded,
-                                                       int32_t chunks, WindowTable tab) {
-    const int64_t total = num_windows * (int64_t)lags;
-    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total;
-         e += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t b = e / lags;
-        const int32_t j = (int32_t)(e % lags);
-        const int64_t t = (int64_t)tmin + j;
-        const int64_t n = table_n(tab, b, n_all);
-        if (t > table_tmax(tab, b, tmin + lags - 1) || n == 0) {   // outside this window's range
+                                                       int32_t num_channels, int64_t n_all,
+                                                       int32_t tmin, int32_t lags, int32_t t0,
+                                                       int32_t lags_padded, int32_t chunks,
+                                                       WindowTable tab) {
+    const int64_t b = blockIdx.x;
+    const int64_t n = table_n(tab, b, n_all);
+    const int32_t live = n == 0 ? 0 : min(table_tmax(tab, b, tmin + lags - 1) - tmin + 1, lags);
+    const int32_t end = (tab.n && !scores) ? live : lags;
+    for (int32_t j = blockIdx.y * 256 + threadIdx.x; j < end; j += gridDim.y * 256) {
+        const int64_t e = b * (int64_t)lags + j;
+        if (j >= live) {   // outside this window's range
             s64[e] = 0.0;
             if (scores) scores[e] = 0.0f;
             continue;
         }
+        const int64_t t = (int64_t)tmin + j;
         double s = 0.0;
         for (int32_t c = 0; c < num_channels; ++c) {
             const double* p = part + ((b * num_channels + c) * chunks) * (int64_t)lags_padded +
@@ -192,12 +198,10 @@ hipError_t launch_window_stats(const Plan& p, const float* x, double* var, doubl
 
 hipError_t launch_finalize(const Plan& p, const Weights& w, const double* part, double* s64,
                            float* scores, hipStream_t s) {
-    const int64_t total = p.num_windows * (int64_t)p.lags;
-    int64_t groups = (total + 255) / 256;
-    if (groups > 65536) groups = 65536;
-    hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)groups), dim3(256), 0, s, part, s64,
-                       scores, w, p.num_windows, p.num_channels, p.n, p.tmin, p.lags, p.t0,
-                       p.lags_padded, p.chunks, p.table);
+    const int64_t lag_groups = std::min<int64_t>((p.lags + 255) / 256, 65535);
+    hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)p.num_windows, (unsigned)lag_groups),
+                       dim3(256), 0, s, part, s64, scores, w, p.num_channels, p.n, p.tmin, p.lags,
+                       p.t0, p.lags_padded, p.chunks, p.table);
     return hipGetLastError();
 }
 

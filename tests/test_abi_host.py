@@ -94,7 +94,7 @@ def test_workspace_size_valid_and_monotone(lib):
 
 
 @pytest.mark.parametrize("kw", [
-    dict(num_windows=0), dict(num_channels=0), dict(num_channels=257, channel_stride=4096),
+    dict(num_windows=0), dict(num_windows=(1 << 21) + 1, window_stride=8192), dict(num_channels=0), dict(num_channels=257, channel_stride=4096),
     dict(n=7, tmin=1, tmax=3), dict(tmin=0), dict(tmin=5, tmax=6), dict(tmax=2049),
     dict(window_stride=0), dict(channel_stride=4095), dict(window_stride=-1),
     dict(c_lag=0.0), dict(c_lag=1.0), dict(c_lag=float("nan")), dict(err_max=float("nan")),
