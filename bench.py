@@ -25,7 +25,15 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 FP32_VECTOR_PEAK_TFLOPS = 157.3   # MI355X published FP32 vector peak
+FP64_VECTOR_PEAK_TFLOPS = 78.6    # MI355X published FP64 vector peak
 HBM_PEAK_GBS = 8000.0              # MI355X published HBM3E bandwidth
+# Algorithmic fp64 FLOP of the EM per (sample, component, iteration): the
+# log-density (sub, mul, mul, sub), the exponential (counted as one), the
+# normalisation (add, mul) and the three moments (add; mul, add; mul, mul, add).
+EM_FLOP = 13
+# Mean-removed score per pair of corresponding points: the two mean sums (add,
+# add), the centred difference (sub, sub, sub) and its square accumulated (mul, add).
+CENTRED_FLOP = 7
 FLOP_PER_PAIR = 3                 # one subtraction, one multiply, one add per (x[i], x[i+T])
 METRIC = "lag·samples/sec and traces/sec for batched period detection; % FP32 peak"
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "lag_score_w3_counters.txt")
@@ -139,6 +147,58 @@ def fft_stage_bytes(wl) -> float:
     sweeps = 0 if length <= 2048 else 4
     edges = 2 * 4 * s * wl.tmax + 2 * 8 * s * (wl.tmax + 1) + 2 * 8 * s * lags
     return float(4 * s * wl.n + edges + sweeps * 16 * pairs * length + 8 * s * lags)
+
+
+def pow2_at_least(v: int, lo: int = 64) -> int:
+    length = lo
+    while length < v:
+        length *= 2
+    return length
+
+
+def transform_bytes(pairs_lengths, seq_samples: int, seqs: int, lag_counts) -> float:
+    """HBM bytes of the FFT scores of a batch: every pair of sequences (length L
+    of its transform) writes, reads, writes and reads its complex fp64 transform
+    (none of that up to 2048 points, where a pair stays in LDS); the samples
+    are read once, the head and tail sums written and read back, and D(T)
+    written per lag."""
+    sweeps = sum(16 * 4 * length for length in pairs_lengths if length > 2048)
+    edges = sum(2 * 4 * t + 2 * 8 * (t + 1) + 2 * 8 * t for t in lag_counts)
+    return float(4 * seq_samples + edges + sweeps + 8 * sum(lag_counts))
+
+
+def call_roofline(kernel, bound, work, ms, extra=None):
+    """Roofline object of a mode timed as a whole call: `work` is the algorithmic
+    FLOP (bound "alu": fp32 or fp64 given by the kernel) or bytes (bound "hbm")
+    of one call, `ms` the mean call time from HIP events on the call's stream."""
+    if bound == "hbm":
+        achieved, peak, unit = work / (ms / 1e3) / 1e9, HBM_PEAK_GBS, "GB/s"
+    else:
+        peak = FP64_VECTOR_PEAK_TFLOPS if bound == "alu_f64" else FP32_VECTOR_PEAK_TFLOPS
+        achieved, unit = work / (ms / 1e3) / 1e12, "TFLOP/s"
+    line = {"kernel": kernel, "bound": "hbm" if bound == "hbm" else "alu",
+            "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
+            "traffic": None, "timed": "whole call (HIP events on its stream)"}
+    if extra:
+        line.update(extra)
+    return line
+
+
+def timed_calls(call, steps):
+    """Runs call() `steps` times between two events on the current stream;
+    returns (wall ms per call, event ms per call, last result)."""
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record()
+    out = None
+    for _ in range(steps):
+        out = call()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / steps
+    return wall, e0.elapsed_time(e1) / steps, out
 
 
 def main():
@@ -368,14 +428,19 @@ def bench_similarity(args):
     call = pkg.score_centred if centred else pkg.similarity
     for _ in range(args.warmup):
         call(x, desc, wt, tt)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        err = call(x, desc, wt, tt)
-    torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms, ev_ms, err = timed_calls(lambda: call(x, desc, wt, tt), args.steps)
     g = err.cpu().numpy()
     samples = sum(wl.num_channels * (wl.n // t) * t for t in ts if wl.n // t >= 2)
+    # point pairs (sub-curve i against i + 1): each EM fit and each centred
+    # comparison covers one pair's T points
+    pair_points = sum(wl.num_channels * (wl.n // t - 1) * t for t in ts if wl.n // t >= 2)
+    if centred:
+        roofline = call_roofline("centred_kernel", "alu_f64", CENTRED_FLOP * pair_points, ev_ms,
+                                 {"flop_per_launch": CENTRED_FLOP * pair_points})
+    else:
+        em = EM_FLOP * 3 * 20 * pair_points
+        roofline = call_roofline("similarity_kernel<3>", "alu_f64", em, ev_ms,
+                                 {"flop_per_launch": em})
     metric = ("mean-removed score evaluations/sec (Algorithm 2 relative values, 5 finalist "
               "periods per window)" if centred else
               "grouped-similarity evaluations/sec (Algorithm 2, 5 finalist periods per window)")
@@ -389,7 +454,7 @@ def bench_similarity(args):
                    "windows": wl.num_windows, "queries": len(ts),
                    "sub_curve_samples": samples, "sha256": wl.sha256,
                    **({} if centred else {"num_groups": 3, "em_iters": 20})},
-        "roofline": None,
+        "roofline": roofline,
     }
     if not args.no_cpu_baseline:
         import oracle
@@ -431,13 +496,19 @@ def bench_spectral(args):
     det = pkg.SpectralDetector(x, desc, params, keep)
     for _ in range(args.warmup):
         det.run()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        det.run()
-    torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms, ev_ms, _ = timed_calls(det.run, args.steps)
     res = det.results_numpy()
+    # window statistics (two passes over the samples), the transforms (the
+    # samples once more; above 2048 points each pair's complex fp64 transform
+    # written and read back), the amplitudes written and read by the selection
+    seqs = wl.num_windows * wl.num_channels
+    length = pow2_at_least(wl.n)
+    half = length // 2 + 1
+    sweeps = 2 * 16 * ((seqs + 1) // 2) * length if length > 2048 else 0
+    spec_bytes = float(3 * 4 * seqs * wl.n + sweeps + 2 * 8 * seqs * half)
+    roofline = call_roofline("spectral call: window statistics, column and row transforms, "
+                             "amplitude selection", "hbm", spec_bytes, ev_ms,
+                             {"bytes_per_launch": spec_bytes})
     line = {
         "metric": "spectral candidate lists/sec (Algorithm 1's FFT front end over every window)",
         "value": wl.num_windows / (ms / 1e3), "unit": "windows/s", "n_gpus": 1,
@@ -450,7 +521,7 @@ def bench_spectral(args):
                    "c_peak": params.c_peak, "max_candidates": params.max_candidates},
         "mean_candidates": float(res["count"].mean()),
         "windows_flagged_unresolved": int(np.count_nonzero(res["flags"])),
-        "roofline": None,
+        "roofline": roofline,
     }
     if wl.truth is not None:
         d = wl.truth > 0
@@ -500,13 +571,45 @@ def bench_rolling(args):
     det = pkg.RollingDetector(x, desc, params, keep)
     for _ in range(args.warmup):
         det.run()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        det.run()
-    torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms, ev_ms, _ = timed_calls(det.run, args.steps)
     res = det.results_numpy()
+    # the work of both passes: every whole window, then every suffix window
+    # (N_j = N - start_j samples, lags up to min(Tmax, N_j / 2))
+    c = wl.num_channels
+    lag_sum = lambda n, tm: (tm - wl.tmin + 1) * n - (tm * (tm + 1) - (wl.tmin - 1) * wl.tmin) // 2
+    pairs_a = wl.num_windows * c * lag_sum(wl.n, wl.tmax)
+    suffix = [(wl.n - int(st), min(wl.tmax, (wl.n - int(st)) // 2))
+              for b in range(wl.num_windows) for st in res["starts"][b][:res["n_windows"][b]]]
+    pairs_c = sum(c * lag_sum(n, tm) for n, tm in suffix if tm >= wl.tmin)
+    if args.fft_scores:
+        la = pow2_at_least(wl.n + wl.tmax)
+        seqs_a = wl.num_windows * c
+        work = transform_bytes([la] * ((seqs_a + 1) // 2), seqs_a * wl.n, seqs_a,
+                               [wl.tmax] * seqs_a)
+        # suffix pass: slots j of window b are sequences (b * jmax + j) * C + c,
+        # paired two by two; a pair's transform holds its longer suffix
+        jmax = int(np.floor((2 + params.c_eval * params.step - params.c_measure) / params.step)) + 2
+        need = np.zeros(wl.num_windows * jmax * c, dtype=np.int64)
+        tms = []
+        for b in range(wl.num_windows):
+            for j, st in enumerate(res["starts"][b][:res["n_windows"][b]]):
+                n_j = wl.n - int(st)
+                tm = min(wl.tmax, n_j // 2)
+                for ch in range(c):
+                    need[(b * jmax + j) * c + ch] = n_j + tm
+                    tms.append(tm)
+        if need.size % 2:
+            need = np.append(need, 0)
+        lens = [pow2_at_least(int(v)) for v in need.reshape(-1, 2).max(axis=1) if v > 0]
+        work += transform_bytes(lens, sum(n * c for n, _ in suffix), len(tms), tms)
+        roofline = call_roofline("both FFT score passes (whole windows, then suffix windows "
+                                 "by length class)", "hbm", work, ev_ms,
+                                 {"bytes_per_launch": work})
+    else:
+        work = FLOP_PER_PAIR * (pairs_a + pairs_c)
+        roofline = call_roofline("lag_score_kernel, both passes (whole windows, suffix "
+                                 "windows)", "alu_f32", work, ev_ms,
+                                 {"flop_per_launch": work, "pairs": pairs_a + pairs_c})
     line = {
         "metric": "rolling detections/sec (Algorithm 3 over every window of the batch)",
         "value": wl.num_windows / (ms / 1e3), "unit": "windows/s", "n_gpus": 1,
@@ -522,7 +625,7 @@ def bench_rolling(args):
         "stable_windows": int(np.count_nonzero(res["stable"])),
         "mean_suffix_windows": float(res["n_windows"].mean()),
         "windows_flagged_unresolved": int(np.count_nonzero(res["flags"])),
-        "roofline": None,
+        "roofline": roofline,
     }
     if not args.no_cpu_baseline:
         import oracle

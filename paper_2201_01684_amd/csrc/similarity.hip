@@ -90,26 +90,42 @@ __device__ double pair_error(const float* __restrict__ a, const float* __restric
             pi[k] = 1.0 / (double)G;
         }
         for (int32_t it = 0; it < iters; ++it) {
-            double lp[G];
+            double lp[G], h[G];
 #pragma unroll
-            for (int k = 0; k < G; ++k) lp[k] = log(pi[k]) - 0.5 * log(two_pi * var[k]);
-            // responsibilities of the current parameters, normalised per sample
+            for (int k = 0; k < G; ++k) {
+                lp[k] = log(pi[k]) - 0.5 * log(two_pi * var[k]);
+                h[k] = 0.5 / var[k];
+            }
+            // responsibilities of the current parameters, normalised per
+            // sample: exp(l_k - max_k l_k), so the largest term is exactly 1
+            // and only the other G - 1 need an exponential
             auto resp = [&](double v, double (&r)[G]) {
                 double best = -INFINITY;
+                int top = 0;
 #pragma unroll
                 for (int k = 0; k < G; ++k) {
                     const double d = v - mu[k];
-                    r[k] = lp[k] - d * d / (2.0 * var[k]);
-                    best = fmax(best, r[k]);
+                    r[k] = lp[k] - d * d * h[k];
+                    if (r[k] > best) {
+                        best = r[k];
+                        top = k;
+                    }
                 }
-                double sum = 0.0;
+                double sum = 1.0;
 #pragma unroll
-                for (int k = 0; k < G; ++k) {
-                    r[k] = exp(r[k] - best);
-                    sum += r[k];
+                for (int k = 0; k + 1 < G; ++k) {   // the k-th component other than top
+                    const int idx = k < top ? k : k + 1;
+                    double val = r[0];
+#pragma unroll
+                    for (int m = 1; m < G; ++m) val = idx == m ? r[m] : val;
+                    const double e = exp(val - best);
+                    sum += e;
+#pragma unroll
+                    for (int m = 0; m < G; ++m) r[m] = idx == m ? e : r[m];
                 }
+                const double inv = 1.0 / sum;
 #pragma unroll
-                for (int k = 0; k < G; ++k) r[k] /= sum;
+                for (int k = 0; k < G; ++k) r[k] = k == top ? inv : r[k] * inv;
             };
             // One pass: responsibility-weighted count, first and second moment
             // about the sub-curve mean c; the M-step's variance about the new
@@ -148,10 +164,13 @@ __device__ double pair_error(const float* __restrict__ a, const float* __restric
     double ga[G], gb[G], gc[G];
 #pragma unroll
     for (int k = 0; k < G; ++k) ga[k] = gb[k] = gc[k] = 0.0;
-    double lp[G];
+    double lp[G], h[G];
     if (!constant) {
 #pragma unroll
-        for (int k = 0; k < G; ++k) lp[k] = log(pi[k]) - 0.5 * log(two_pi * var[k]);
+        for (int k = 0; k < G; ++k) {
+            lp[k] = log(pi[k]) - 0.5 * log(two_pi * var[k]);
+            h[k] = 0.5 / var[k];
+        }
     }
     for (int64_t j = lane; j < t; j += kWave) {
         const double va = (double)a[j], vb = (double)b[j];
@@ -161,7 +180,7 @@ __device__ double pair_error(const float* __restrict__ a, const float* __restric
 #pragma unroll
             for (int k = 0; k < G; ++k) {
                 const double d = va - mu[k];
-                const double l = lp[k] - d * d / (2.0 * var[k]);
+                const double l = lp[k] - d * d * h[k];
                 if (l > best) {
                     best = l;
                     arg = k;
