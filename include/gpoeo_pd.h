@@ -92,7 +92,12 @@ extern "C" {
 #define GPOEO_PD_SHORT 2u        /* (rolling detection) a suffix window too short for
                                     three lags starting at tmin; no period                 */
 
+/* Size limits, checked (EINVAL) before any launch, that keep every grid within
+ * HIP's 32-bit global size.  A descriptor whose work would still need a larger
+ * grid (very many sequences or lag-score waves) is rejected the same way. */
 #define GPOEO_PD_MAX_WINDOWS (1 << 21)   /* windows per call (rolling: B * suffix slots) */
+#define GPOEO_PD_MAX_QUERIES (1 << 23)   /* (window, lag) queries per similarity or
+                                            mean-removed score call                       */
 
 typedef struct {
     int64_t num_windows;     /* 1 <= B <= GPOEO_PD_MAX_WINDOWS: traces, or sliding windows  */
@@ -239,9 +244,9 @@ int gpoeo_pd_detect_rolling(const gpoeo_pd_desc* desc, const gpoeo_pd_rolling_pa
  * by SMAPE(a, b) = |a - b| / ((|a| + |b|) / 2) (0/0 = 0), weighted by group
  * size; err[k] = mean over adjacent pairs, weighted mean over channels.
  * err[k] = -1 when floor(N / T) < 2, NaN for a window or lag out of range.
- * windows, lags: device int32 [count]; err: device double [count].  The
- * window layout (and the channel weights) come from desc, whose lag range is
- * not used.  No workspace.
+ * windows, lags: device int32 [count], 0 <= count <= GPOEO_PD_MAX_QUERIES
+ * (else EINVAL); err: device double [count].  The window layout (and the
+ * channel weights) come from desc, whose lag range is not used.  No workspace.
  * ------------------------------------------------------------------------- */
 typedef struct {
     int32_t num_groups;      /* NumG, 1..8 (the paper leaves it open; 3 recommended)    */
@@ -264,9 +269,10 @@ int gpoeo_pd_similarity(const gpoeo_pd_desc* desc, const gpoeo_pd_similarity_par
  * a linear drift to a channel changes no S_c.  Short lags lose most of their
  * differences to the means, so this re-scores candidates rather than scanning
  * every T.  score[k] = -1 when floor(N / T) < 2, NaN for a window or lag out of
- * range.  windows, lags: device int32 [count]; score: device double [count];
- * layout and weights from desc (its lag range is not used).  fp64 throughout.
- * No workspace.
+ * range.  windows, lags: device int32 [count], 0 <= count <=
+ * GPOEO_PD_MAX_QUERIES (else EINVAL); score: device double [count]; layout
+ * and weights from desc (its lag range is not used).  fp64 throughout.  No
+ * workspace.
  * ------------------------------------------------------------------------- */
 int gpoeo_pd_score_centred(const gpoeo_pd_desc* desc, const float* x, const int32_t* windows,
                            const int32_t* lags, int64_t count, double* score,

@@ -15,6 +15,8 @@ from ._binding import (  # noqa: F401
     EXPORTS,
     FFT_SCORES,
     LIB_PATH,
+    MAX_QUERIES,
+    MAX_WINDOWS,
     NO_RESCUE,
     PERIODIC,
     RESULT_DTYPE,

@@ -48,6 +48,8 @@ class PlanInfo(ctypes.Structure):
 
 
 ROLLING_MAX = 16
+MAX_WINDOWS = 1 << 21       # GPOEO_PD_MAX_WINDOWS
+MAX_QUERIES = 1 << 23       # GPOEO_PD_MAX_QUERIES
 
 
 class RollingParams(ctypes.Structure):

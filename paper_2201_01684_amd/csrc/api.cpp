@@ -72,6 +72,30 @@ bool set_fft_geometry(Plan* p, int32_t lg) {
 
 namespace {
 
+// Every launch of a plan must keep its global size (workgroups times threads)
+// within HIP's 32-bit limit: one workgroup of up to 1024 threads per window
+// (selection), 256 per (window, channel) sequence (statistics) or two (FFT
+// edge sums), 64 per lag-score wave, 256 per transform tile.
+bool launches_fit(const Plan& p) {
+    const int64_t kMax = (int64_t(1) << 32) - 1;
+    auto fits = [&](int64_t blocks, int64_t threads) { return blocks <= kMax / threads; };
+    const int64_t seqs = p.num_windows * (int64_t)p.num_channels;
+    if (!fits(p.num_windows, 1024) || !fits(seqs, 256)) return false;
+    if (p.fft) {
+        if (!fits(2 * seqs, 256)) return false;
+        if (!p.fft_ragged) {   // uniform transforms: one workgroup per tile of each pair
+            const int64_t per_pair =
+                p.fft_m2 == 1 ? 1 : std::max<int64_t>(p.fft_m2 / p.fft_cols, p.fft_m1 / 2 + 1);
+            if (p.fft_pairs > kMax / 256 / per_pair) return false;
+        }
+    } else if (p.sliding) {
+        if (!fits(p.block_tasks, kWave)) return false;
+    } else if (!fits(p.tasks, kWave)) {
+        return false;
+    }
+    return true;
+}
+
 // ragged: the windows will come from a table (lengths up to d->n, Tmax up to
 // d->tmax); an FFT plan then sizes its transforms per pair (length classes).
 int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
@@ -248,6 +272,7 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
     p->off_cls = off;                             // length classes (ragged FFT plans)
     off = align_up(off + (size_t)n_cls * sizeof(int32_t));
     p->bytes = off;
+    if (!launches_fit(*p)) return GPOEO_PD_EINVAL;
     return GPOEO_PD_OK;
 }
 
@@ -586,7 +611,7 @@ extern "C" int gpoeo_pd_similarity(const gpoeo_pd_desc* desc,
     if (rc != GPOEO_PD_OK) return rc;
     if (!params || params->num_groups < 1 || params->num_groups > 8 || params->em_iters < 0)
         return GPOEO_PD_EINVAL;
-    if (count < 0 || count > INT32_MAX) return GPOEO_PD_EINVAL;
+    if (count < 0 || count > GPOEO_PD_MAX_QUERIES) return GPOEO_PD_EINVAL;
     if (count == 0) return GPOEO_PD_OK;
     if (!x || !windows || !lags || !err) return GPOEO_PD_EINVAL;
     if (gpoeo::launch_similarity(p, weights_of(desc, p.num_channels), params->num_groups,
@@ -602,7 +627,7 @@ extern "C" int gpoeo_pd_score_centred(const gpoeo_pd_desc* desc, const float* x,
     gpoeo::Plan p;
     const int rc = gpoeo::make_plan(desc, &p);
     if (rc != GPOEO_PD_OK) return rc;
-    if (count < 0 || count > INT32_MAX) return GPOEO_PD_EINVAL;
+    if (count < 0 || count > GPOEO_PD_MAX_QUERIES) return GPOEO_PD_EINVAL;
     if (count == 0) return GPOEO_PD_OK;
     if (!x || !windows || !lags || !score) return GPOEO_PD_EINVAL;
     if (gpoeo::launch_centred(p, weights_of(desc, p.num_channels), x, windows, lags, count, score,

@@ -99,6 +99,12 @@ def test_workspace_size_valid_and_monotone(lib):
     dict(window_stride=0), dict(channel_stride=4095), dict(window_stride=-1),
     dict(c_lag=0.0), dict(c_lag=1.0), dict(c_lag=float("nan")), dict(err_max=float("nan")),
     dict(flags=8), dict(flags=4, n=4 << 20, tmax=2 << 20),
+    # grids that would exceed HIP's 32-bit global size: 2^24 sequences of 256
+    # threads, 2^26 lag-score waves of 64
+    dict(num_windows=1 << 20, num_channels=16, n=64, tmax=32, window_stride=1024,
+         channel_stride=64),
+    dict(num_windows=1 << 21, num_channels=1, n=65536, tmax=32768, window_stride=65536,
+         channel_stride=65536),
 ])
 def test_invalid_descriptors_rejected(lib, kw):
     d, _ = good_desc(**kw)
@@ -113,6 +119,25 @@ def test_invalid_weights_rejected(lib, weights):
     d, _keep = good_desc(weights=np.array(weights, dtype=np.float32))
     with pytest.raises(B.GpoeoError):
         B.workspace_bytes(d)
+
+
+def test_size_limits(lib):
+    # just inside the sequence limit: accepted
+    d, _ = good_desc(num_windows=1 << 19, num_channels=16, n=64, tmax=32, window_stride=1024,
+                     channel_stride=64)
+    assert B.workspace_bytes(d) > 0
+    assert B.MAX_WINDOWS == 1 << 21 and B.MAX_QUERIES == 1 << 23
+    # too many queries: rejected before any pointer is used
+    d, _ = good_desc()
+    for name in ("gpoeo_pd_score_centred",):
+        call = getattr(lib, name)
+        assert call(ctypes.byref(d), 0x100000, 0x200000, 0x300000, B.MAX_QUERIES + 1, 0x400000,
+                    None) == B.EINVAL
+        assert call(ctypes.byref(d), 0x100000, 0x200000, 0x300000, -1, 0x400000,
+                    None) == B.EINVAL
+    sp = B.SimilarityParams(3, 20)
+    assert lib.gpoeo_pd_similarity(ctypes.byref(d), ctypes.byref(sp), 0x100000, 0x200000,
+                                   0x300000, B.MAX_QUERIES + 1, 0x400000, None) == B.EINVAL
 
 
 def test_reserved_fields_must_be_zero(lib):
