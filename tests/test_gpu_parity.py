@@ -156,6 +156,28 @@ def test_weighted_channels():
     parity(x, lay, "weighted")
 
 
+def test_maximum_channel_count():
+    # 256 channels (the most a descriptor takes), each with its own weight and
+    # scale; one window of them planted, the other noise; direct and FFT scores
+    rng = np.random.default_rng(11)
+    b, c, n = 2, 256, 1500
+    x = np.empty((b, c, n), dtype=np.float32)
+    for k in range(c):
+        x[0, k] = planted_trace(n, 97, 5, seed=100 + k, sigma=0.5) * (0.01 + k % 7)
+        x[1, k] = rng.normal(0, 1 + k % 3, n)
+    w = (0.1 + rng.random(c)).astype(np.float32)
+    lay = oracle.Layout(b, c, n, c * n, n, 2, 700, weights=w)
+    res, out = parity(x, lay, "256 channels")
+    assert res["period"][0] == 97
+    import paper_2201_01684_amd as pkg
+    g, fres = gpu_run(x, lay, flags=pkg.FFT_SCORES)
+    o, _ = oracle.detect(x, lay)
+    zero = o == 0
+    assert np.all(g[zero] == 0)
+    assert np.max(np.abs(g - o)[~zero] / np.abs(o[~zero])) <= 1e-6 + 2.0 ** -24
+    check_results(fres, out, "256 channels, FFT scores")
+
+
 def test_constant_noise_free_and_white_noise_windows():
     n = 8192
     rows = [np.full(n, 123.25, dtype=np.float32),                         # CONSTANT

@@ -76,6 +76,18 @@ def test_channels_weights_range_and_limit():
               where=f"T=[{tmin},{tmax}] c={c_peak} K={k_max}")
 
 
+def test_maximum_channel_count():
+    rng = np.random.default_rng(12)
+    b, c, n = 2, 256, 3000
+    x = np.empty((b, c, n), dtype=np.float32)
+    for k in range(c):
+        x[0, k] = planted_trace(n, 150, 4, seed=200 + k, sigma=1.0) * (1 + k % 5)
+        x[1, k] = rng.normal(0, 1, n) + np.sin(2 * np.pi * np.arange(n) / 40.0) * (k % 3)
+    w = (0.2 + rng.random(c)).astype(np.float32)
+    res = gpu_spectral(x, b, c, n, c * n, n, 2, n // 2, w)
+    check(res, x, range(b), c, n, c * n, n, 2, n // 2, w, where="256 channels")
+
+
 @pytest.mark.parametrize("name,kw", [
     ("w1", {}),
     ("w2", dict(traces=5, n=16384, tmax=2048, pmax=1500)),
