@@ -106,6 +106,42 @@ class HipEvents:
         for h in arr:
             self.hip.hipEventDestroy(h)
 
+    def attribute(self, attr: int, device: int = 0) -> int:
+        fn = self.hip.hipDeviceGetAttribute
+        fn.argtypes = [ctypes.POINTER(ctypes.c_int), ctypes.c_int, ctypes.c_int]
+        fn.restype = ctypes.c_int
+        out = ctypes.c_int()
+        if fn(ctypes.byref(out), attr, device) != 0:
+            raise RuntimeError("hipDeviceGetAttribute failed")
+        return int(out.value)
+
+
+HIP_ATTR_CLOCK_RATE_KHZ = 5      # hipDeviceAttributeClockRate (ROCm 7 hip_runtime_api.h)
+
+
+def device_info(ev: "HipEvents") -> dict:
+    """The GPU as the runtime reports it, and the FP32 peak and the lag-score
+    pair ceiling (one v_sub + one v_fmac per pair, two VALU instructions per
+    clock per CU with dual issue) recomputed from its CU count and peak clock."""
+    import torch
+    p = torch.cuda.get_device_properties(0)
+    mhz = ev.attribute(HIP_ATTR_CLOCK_RATE_KHZ) / 1e3
+    cus = p.multi_processor_count
+    return {"name": p.name, "arch": p.gcnArchName, "compute_units": cus,
+            "peak_clock_mhz": mhz, "fp32_peak_tflops_at_clock": cus * mhz * 1e6 * 256 / 1e12,
+            "pair_ceiling_per_s": cus * mhz * 1e6 * 64}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
 
 def counters_traffic(workload: str):
     """HBM bytes per lag-score launch from the committed rocprofv3 counter summary
@@ -319,6 +355,7 @@ def main():
                      "finalize": float(stage_ms[:, 2].mean()),
                      "select": float(stage_ms[:, 3].mean())},
         "roofline": roofline,
+        "device": device_info(ev),
         "windows_flagged_unresolved": int(np.count_nonzero(res["flags"] & pkg.UNRESOLVED)),
         "windows_rescored": int(np.count_nonzero(res["n_rescored"])),
     }
@@ -392,6 +429,7 @@ def main():
             done += 1
         line["cpu_baseline"] = {"value": done * per_window / t_cpu, "unit": "lag·samples/s",
                                 "cores": oracle.threads(), "kind": "oracle",
+                                "cpu_model": cpu_model(), "nproc": os.cpu_count(),
                                 "sample": f"first {done} of {wl.num_windows} windows, all "
                                           f"{wl.lags} lags each, {t_cpu:.1f} s"}
         line["parity_sample"] = {"windows": done, "period_match": match,
@@ -473,7 +511,7 @@ def bench_similarity(args):
                 worst = max(worst, float(np.max(np.abs(g[done:k][nz] - o[nz]) / o[nz])))
             done = k
         line["cpu_baseline"] = {"value": done / t_cpu, "unit": "period evaluations/s",
-                                "cores": oracle.threads(), "kind": "oracle",
+                                "cores": oracle.threads(), "kind": "oracle", "cpu_model": cpu_model(),
                                 "sample": f"first {done} of {len(ts)} queries, {t_cpu:.1f} s"}
         line["parity_sample"] = {"queries": done, "max_rel_err": worst}
     print(json.dumps(line), flush=True)
@@ -545,7 +583,7 @@ def bench_spectral(args):
             match += int(list(r["bins"][:r["count"]]) == o["bins"])
             done += 1
         line["cpu_baseline"] = {"value": done / t_cpu, "unit": "windows/s", "cores": 1,
-                                "kind": "oracle",
+                                "kind": "oracle", "cpu_model": cpu_model(),
                                 "sample": f"first {done} of {wl.num_windows} windows, "
                                           f"{t_cpu:.1f} s (numpy FFT, one thread)"}
         line["parity_sample"] = {"windows": done, "candidate_lists_equal": match}
@@ -643,6 +681,7 @@ def bench_rolling(args):
             done += 1
         line["cpu_baseline"] = {"value": done / t_cpu, "unit": "windows/s",
                                 "cores": oracle.threads(), "kind": "oracle",
+                                "cpu_model": cpu_model(),
                                 "sample": f"first {done} of {wl.num_windows} windows, {t_cpu:.1f} s"}
         line["parity_sample"] = {"windows": done, "period_stable_next_match": match}
     print(json.dumps(line), flush=True)
