@@ -166,23 +166,29 @@ def counters_traffic(workload: str):
         return None
 
 
-def fft_stage_bytes(wl) -> float:
-    """HBM bytes the FFT score stage moves per call: the samples read once by the
-    column transforms (the centring sums come with the window statistics), the
-    first and last Tmax samples of each sequence read and their head and tail
-    sums written and read back, each pair's complex fp64 transform written by
-    the column kernel, read and written by the row kernel and read by the
-    inverse column kernel (none of that up to 2048 points, where a pair stays
-    in LDS), and the per-channel D(T) written."""
+def fft_stage_bytes(wl, plan) -> float:
+    """HBM bytes the FFT score stage moves per call, for the transform lengths of
+    the plan (`describe_plan`): the samples read once by the column transforms
+    (the centring sums come with the window statistics), the first and last
+    Tmax samples of each sequence read and their head and tail sums written
+    and read back, each pair's complex fp64 transform written by the column
+    kernel, read and written by the row kernel and read by the inverse column
+    kernel (none of that up to 2048 points, where a pair stays in LDS), and the
+    per-channel D(T) written.  With the wrap correction: the first and last M
+    samples read again, the head and tail transforms written, read, the cross
+    spectrum written and read back (six sweeps of the head-tail length), and
+    the M wrap terms per sequence written and read."""
     s = wl.num_windows * wl.num_channels
     pairs = (s + 1) // 2
-    length = 64
-    while length < wl.n + wl.tmax:
-        length *= 2
+    length = plan["fft_len"]
     lags = wl.tmax - wl.tmin + 1
     sweeps = 0 if length <= 2048 else 4
     edges = 2 * 4 * s * wl.tmax + 2 * 8 * s * (wl.tmax + 1) + 2 * 8 * s * lags
-    return float(4 * s * wl.n + edges + sweeps * 16 * pairs * length + 8 * s * lags)
+    total = 4 * s * wl.n + edges + sweeps * 16 * pairs * length + 8 * s * lags
+    m = plan["fft_wrap_lags"]
+    if plan["fft_wrap_len"]:
+        total += 2 * 4 * s * m + 6 * 16 * pairs * plan["fft_wrap_len"] + 2 * 8 * s * m
+    return float(total)
 
 
 def pow2_at_least(v: int, lo: int = 64) -> int:
@@ -314,7 +320,7 @@ def main():
     res = det.results_numpy()
     scores = det.scores
     if fft:
-        fft_bytes = fft_stage_bytes(wl)
+        fft_bytes = fft_stage_bytes(wl, plan)
         roofline = {"kernel": "FFT score stage (prep, column, row and inverse-column "
                               "transform kernels)", "bound": "hbm",
                     "achieved": fft_bytes / (score_ms / 1e3) / 1e9,
@@ -620,10 +626,7 @@ def bench_rolling(args):
               for b in range(wl.num_windows) for st in res["starts"][b][:res["n_windows"][b]]]
     pairs_c = sum(c * lag_sum(n, tm) for n, tm in suffix if tm >= wl.tmin)
     if args.fft_scores:
-        la = pow2_at_least(wl.n + wl.tmax)
-        seqs_a = wl.num_windows * c
-        work = transform_bytes([la] * ((seqs_a + 1) // 2), seqs_a * wl.n, seqs_a,
-                               [wl.tmax] * seqs_a)
+        work = fft_stage_bytes(wl, pkg.describe_plan(desc))   # the whole-window pass
         # suffix pass: slots j of window b are sequences (b * jmax + j) * C + c,
         # paired two by two; a pair's transform holds its longer suffix
         jmax = int(np.floor((2 + params.c_eval * params.step - params.c_measure) / params.step)) + 2

@@ -40,12 +40,18 @@
  * zero-padded to L = 2^k >= N + Tmax points and transformed in fp64, and
  *   D_c(T) = sum_{i<N-T} y_i^2 + sum_{i>=T} y_i^2 - 2 r(T),
  * with the autocorrelation r the inverse transform of the power spectrum
- * (O(L log L) per channel instead of O(N (Tmax - Tmin))).  A rigorous
- * absolute error bound of each D_c(T), from the channel norms, decides which
- * scores are within 1e-6 relative of the exact value; every other lag
- * (exact zeros included) is recomputed as an fp64 sum before the selection,
- * which then proceeds as above.  Selections equal those of the direct scores.
- * Requires N + Tmax <= 2^22.  Sliding-window block sharing does not apply.
+ * (O(L log L) per channel instead of O(N (Tmax - Tmin))).  When a transform
+ * of only L = 2^k >= N points costs less, it is used instead: the lags T > L - N
+ * of its circular autocorrelation then carry the products of the first and
+ * the last M = Tmax - (L - N) samples, which a second transform of at least
+ * 2M points computes and which are subtracted (gpoeo_pd_describe_plan reports
+ * both lengths).  A rigorous absolute error bound of each D_c(T), from the
+ * channel norms, decides which scores are within 1e-6 relative of the exact
+ * value; every other lag (exact zeros included) is recomputed as an fp64 sum
+ * before the selection, which then proceeds as above.  Selections equal those
+ * of the direct scores.  Requires a transform of at most 2^22 points: N + Tmax
+ * <= 2^22, or N <= 2^22 with a head-tail transform of at most min(2^20, L / 2)
+ * points.  Sliding-window block sharing does not apply.
  *
  * Threading and ownership.  All buffers except `desc` and `desc->channel_weights`
  * are DEVICE memory owned by the caller.  The library never allocates or frees
@@ -84,7 +90,7 @@ extern "C" {
 #define GPOEO_PD_SCORES_ONLY 1u  /* compute scores only; `results` is not written           */
 #define GPOEO_PD_NO_RESCUE 2u    /* decide on the bounded tier-0 scores only                */
 #define GPOEO_PD_FFT_SCORES 4u   /* scores from an fp64 FFT autocorrelation instead of the
-                                    direct sums (see below); needs N + Tmax <= 2^22        */
+                                    direct sums (see below); transform limits below        */
 
 /* result->flags */
 #define GPOEO_PD_UNRESOLVED 1u   /* some comparison stayed undecided after the exact
@@ -139,6 +145,10 @@ typedef struct {
                                  the (x[i], x[i+T]) pairs the definition of S(T) sums     */
     double pairs_scored;      /* pairs with T in [tmin, tmax] the score stage evaluates   */
     size_t workspace_bytes;   /* same as gpoeo_pd_workspace_bytes                          */
+    int64_t fft_len;          /* FFT scores: points per transform (0 otherwise)           */
+    int64_t fft_wrap_len;     /* FFT scores whose transform holds only N points: points
+                                 of the head-tail transform of the wrap term; else 0      */
+    int64_t fft_wrap_lags;    /* lags T > fft_len - N that carry the wrap term; else 0   */
 } gpoeo_pd_plan_info;
 
 /* Describes the launch plan of `desc`.  Host-only; GPOEO_PD_OK or GPOEO_PD_EINVAL. */

@@ -44,7 +44,9 @@ class Result(ctypes.Structure):
 class PlanInfo(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int32), ("lags_per_lane", ctypes.c_int32),
                 ("score_waves", ctypes.c_int64), ("pairs_defined", ctypes.c_double),
-                ("pairs_scored", ctypes.c_double), ("workspace_bytes", ctypes.c_size_t)]
+                ("pairs_scored", ctypes.c_double), ("workspace_bytes", ctypes.c_size_t),
+                ("fft_len", ctypes.c_int64), ("fft_wrap_len", ctypes.c_int64),
+                ("fft_wrap_lags", ctypes.c_int64)]
 
 
 ROLLING_MAX = 16

@@ -88,6 +88,12 @@ bool launches_fit(const Plan& p) {
                 p.fft_m2 == 1 ? 1 : std::max<int64_t>(p.fft_m2 / p.fft_cols, p.fft_m1 / 2 + 1);
             if (p.fft_pairs > kMax / 256 / per_pair) return false;
         }
+        if (p.fft_wrap) {
+            int32_t m1, m2, cols;
+            fft_geometry(p.fft_wrap_log2, &m1, &m2, &cols);
+            const int64_t per_pair = std::max<int64_t>(m2 / cols, m1 / 2 + 1);
+            if (p.fft_pairs > kMax / 256 / per_pair) return false;
+        }
     } else if (p.sliding) {
         if (!fits(p.block_tasks, kWave)) return false;
     } else if (!fits(p.tasks, kWave)) {
@@ -137,8 +143,26 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
     p->fft_ragged = p->fft && ragged;
     if (p->fft) {
         // smallest power of two (at least 64) holding N + Tmax points
-        int32_t lg = 6;
+        int32_t lg = kFftMinLog2;
         while ((int64_t(1) << lg) < d->n + d->tmax) ++lg;
+        // Or one holding N, with the wrap correction, when that costs less:
+        // four sweeps of a 2^lgn transform plus six of a 2^lgw one (two
+        // forward, one inverse) against four sweeps of 2^(lgn+1); the
+        // shorter transform must itself be a split one.
+        int32_t lgn = kFftMinLog2;
+        while ((int64_t(1) << lgn) < d->n) ++lgn;
+        p->fft_wrap = false;
+        if (!ragged && lgn < lg && lgn > kFftSmallTileLog2) {
+            const int64_t m = (int64_t)d->tmax - ((int64_t(1) << lgn) - d->n);
+            int32_t lgw = kFftWrapMinLog2;
+            while ((int64_t(1) << lgw) < 2 * m) ++lgw;
+            if (lgw <= lgn - 1 && lgw <= kFftWrapMaxLog2) {
+                lg = lgn;
+                p->fft_wrap = true;
+                p->fft_wrap_m = (int32_t)m;
+                p->fft_wrap_log2 = lgw;
+            }
+        }
         if (!set_fft_geometry(p, lg)) return GPOEO_PD_EINVAL;
     }
 
@@ -238,13 +262,17 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
             return GPOEO_PD_EINVAL;
     }
     if (n_part > (INT64_MAX / 16)) return GPOEO_PD_EINVAL;
-    int64_t n_fstat = 0, n_edge = 0, n_tw = 0, n_z = 0, n_cls = 0;
+    int64_t n_fstat = 0, n_edge = 0, n_tw = 0, n_z = 0, n_cls = 0, n_zw = 0, n_wrap = 0;
     if (p->fft) {
         if (!mul_ok(bc, 4, &n_fstat) || !mul_ok(bc, 2 * ((int64_t)d->tmax + 1), &n_edge) ||
             !mul_ok(p->fft_pairs, p->fft_len, &n_z) || n_z > (INT64_MAX / 64))
             return GPOEO_PD_EINVAL;
         n_tw = fft_twiddle_count(*p);
         n_cls = fft_class_ints(*p);
+        if (p->fft_wrap &&
+            (!mul_ok(2 * p->fft_pairs, int64_t(1) << p->fft_wrap_log2, &n_zw) ||
+             n_zw > (INT64_MAX / 64) || !mul_ok(bc, p->fft_wrap_m, &n_wrap)))
+            return GPOEO_PD_EINVAL;
     }
     size_t off = 0;
     p->off_var = off;
@@ -271,6 +299,10 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
     off = align_up(off + (size_t)n_z * 2 * sizeof(double));
     p->off_cls = off;                             // length classes (ragged FFT plans)
     off = align_up(off + (size_t)n_cls * sizeof(int32_t));
+    p->off_zw = off;                              // head and tail transforms (wrap)
+    off = align_up(off + (size_t)n_zw * 2 * sizeof(double));
+    p->off_wrap = off;                            // wrap terms
+    off = align_up(off + (size_t)n_wrap * sizeof(double));
     p->bytes = off;
     if (!launches_fit(*p)) return GPOEO_PD_EINVAL;
     return GPOEO_PD_OK;
@@ -339,10 +371,12 @@ int run_plan(const gpoeo::Plan& p, const gpoeo::Weights& w, const float* x, floa
     if (p.fft) {
         char* ws = static_cast<char*>(workspace);
         int32_t* cls = p.fft_ragged ? reinterpret_cast<int32_t*>(ws + p.off_cls) : nullptr;
+        double* zw = p.fft_wrap ? reinterpret_cast<double*>(ws + p.off_zw) : nullptr;
+        double* wrap = p.fft_wrap ? reinterpret_cast<double*>(ws + p.off_wrap) : nullptr;
         if (gpoeo::launch_fft_scores(p, x, fstat, reinterpret_cast<double*>(ws + p.off_edge),
                                      reinterpret_cast<double*>(ws + p.off_tw),
-                                     reinterpret_cast<double*>(ws + p.off_z), c.part, cls,
-                                     stream) != hipSuccess)
+                                     reinterpret_cast<double*>(ws + p.off_z), c.part, cls, zw,
+                                     wrap, stream) != hipSuccess)
             return GPOEO_PD_EHIP;
         if (!mark(2)) return GPOEO_PD_EHIP;
         if (gpoeo::launch_finalize(p, w, c.part, c.s64, scores, stream) != hipSuccess ||
@@ -505,6 +539,9 @@ int gpoeo_pd_describe_plan(const gpoeo_pd_desc* desc, gpoeo_pd_plan_info* info) 
     }
     info->pairs_defined = defined;
     info->pairs_scored = p.fft ? 0.0 : (p.sliding ? scored : defined);
+    info->fft_len = p.fft ? p.fft_len : 0;
+    info->fft_wrap_len = p.fft_wrap ? int64_t(1) << p.fft_wrap_log2 : 0;
+    info->fft_wrap_lags = p.fft_wrap ? p.fft_wrap_m : 0;
     return GPOEO_PD_OK;
 }
 

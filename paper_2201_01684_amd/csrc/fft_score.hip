@@ -62,6 +62,17 @@ struct FftArgs {
     const int32_t* bounds;
     int64_t zstride;
     int32_t cls;
+    // Loads of a transform see samples [seg_start, seg_start + seg_len) of
+    // each sequence (seg_len 0: all of it): the heads and tails of the wrap
+    // correction.
+    int64_t seg_start, seg_len;
+    // Wrap correction: the inverse column kernel of the head-tail transform
+    // writes the cross-correlations cc(s), s < wm, to wout ([S][wm]); the one
+    // of the main transform subtracts wrap[s][Tmax - T] from r(T) for T > wrap_w.
+    double* wout;
+    const double* wrap;
+    int64_t wrap_w;
+    int32_t wm;
 };
 
 // Transform kernels come in two forms: uniform (kRagged false: one workgroup
@@ -220,6 +231,10 @@ __device__ __forceinline__ Seq seq_of(const FftArgs& a, int64_t s) {
     q.n = table_n(a.tab, b, a.n_all);
     q.p = a.x + table_off(a.tab, b, a.window_stride) + c * a.channel_stride;
     q.mu = a.fstat[4 * s];
+    if (a.seg_len > 0) {
+        q.p += a.seg_start;
+        q.n = min(q.n - a.seg_start, a.seg_len);
+    }
     return q;
 }
 
@@ -234,7 +249,8 @@ __device__ __forceinline__ void write_d(const FftArgs& a, int64_t s, int64_t t, 
     const int64_t n = table_n(a.tab, b, a.n_all);
     double d = 0.0;
     if (n > 0 && t <= table_tmax(a.tab, b, a.tmax)) {
-        const double r = ldexp(w, -(a.lg + 2));
+        double r = ldexp(w, -(a.lg + 2));
+        if (a.wrap && t > a.wrap_w) r -= a.wrap[s * a.wm + (a.tmax - t)];   // circular term
         const double e = a.fstat[4 * s + 1];
         const double* ed = a.edge + s * 2 * (int64_t)(a.tmax + 1);
         d = ((e - ed[a.tmax + 1 + t]) + (e - ed[t])) - 2.0 * r;
@@ -550,6 +566,114 @@ __global__ __launch_bounds__(kTThreads) void fft_rows_kernel(FftArgs a) {
     }
 }
 
+// 4 Q(k) of the wrap correction from the head transform Z1 = FFT(h_a + i h_b)
+// and the tail transform Z2 = FFT(u_a + i u_b) at k and L - k:
+// with H_a = (Z1(k) + conj Z1(L-k)) / 2, H_b = (Z1(k) - conj Z1(L-k)) / 2i and
+// U_a, U_b likewise from Z2, Q = U_a conj(H_a) + i U_b conj(H_b), whose
+// inverse transform is cc_a + i cc_b, cc(s) = sum_j h_j u_{j+s}.
+__device__ __forceinline__ double2 cross_pair(double2 z1k, double2 z1m, double2 z2k, double2 z2m) {
+    const double2 ha = make_double2(z1k.x + z1m.x, z1k.y - z1m.y);   // 2 H_a
+    const double2 hb = make_double2(z1k.y + z1m.y, z1m.x - z1k.x);   // 2 H_b
+    const double2 ua = make_double2(z2k.x + z2m.x, z2k.y - z2m.y);   // 2 U_a
+    const double2 ub = make_double2(z2k.y + z2m.y, z2m.x - z2k.x);   // 2 U_b
+    const double2 pa = cmul_conj(ua, ha), pb = cmul_conj(ub, hb);
+    return make_double2(pa.x - pb.y, pa.y + pb.x);
+}
+
+// Wrap correction, step 2: rows k1 and L1 - k1 of both the head transform
+// (at z) and the tail transform (at z + zoff2) of 2^lgr consecutive row pairs:
+// forward row transforms, the cross spectrum Q of the pair, inverse row
+// transforms of Q and the inverse twiddles; Q's rows go over the head
+// transform's rows.  LDS: point i of slot q at i * 4 * 2^lgr + q, slot q =
+// (row pair, side, transform) from the high bits down; Q then takes the
+// layout of two slots per row pair.
+template <int kTile>
+__global__ __launch_bounds__(kTThreads) void fft_wrap_rows_kernel(FftArgs a, int64_t zoff2) {
+    constexpr int kRegPoints = (1 << kTile) / kTThreads;
+    extern __shared__ double2 lds[];
+    const int64_t per = (int64_t(1) << (a.lg1 - 1)) + 1;
+    const int64_t wgs = (per + (1 << a.lgr) - 1) >> a.lgr;
+    const int64_t id = xcd_remap(blockIdx.x, gridDim.x);
+    const int64_t pair = id / wgs;
+    const int64_t g0 = (id % wgs) << a.lgr;
+    const uint32_t l1 = 1u << a.lg1;
+    const int lgs = a.lgr + 2;
+    const int slots = 1 << lgs;
+    const int l2 = 1 << a.lg2;
+    const int npts = l2 << lgs;
+    double2* __restrict__ z1 = a.z + pair * a.zstride;
+    const double2* __restrict__ z2 = z1 + zoff2;
+    auto k1_of = [&](int64_t g, int side, bool& valid, bool& self) -> uint32_t {
+        valid = g < per;
+        const uint32_t ka = (uint32_t)g, kb = (l1 - (uint32_t)g) & (l1 - 1);
+        self = ka == kb;
+        return side ? kb : ka;
+    };
+    {
+        double2 v[kRegPoints];
+#pragma unroll
+        for (int r = 0; r < kRegPoints; ++r) {
+            const int f = threadIdx.x + r * kTThreads;
+            const int q = f & (slots - 1);
+            bool valid, self;
+            const uint32_t k1 = k1_of(g0 + (q >> 2), (q >> 1) & 1, valid, self);
+            const double2* src = (q & 1) ? z2 : z1;
+            v[r] = (valid && f < npts) ? src[(int64_t)bitrev(k1, a.lg1) * l2 + (f >> lgs)]
+                                       : make_double2(0.0, 0.0);
+        }
+#pragma unroll
+        for (int r = 0; r < kRegPoints; ++r) {
+            const int f = threadIdx.x + r * kTThreads;
+            if (f < npts) lds[f] = v[r];
+        }
+    }
+    __syncthreads();
+    lds_fft_fwd<kTile>(lds, a.lg2, lgs, a.tw + a.tw_b);
+    double2 wv[kRegPoints];
+#pragma unroll
+    for (int r = 0; r < kRegPoints; ++r) {   // at the head transform's slots
+        const int f = threadIdx.x + r * kTThreads;
+        const int q = f & (slots - 1);
+        if (f < npts && (q & 1) == 0) {
+            bool valid, self;
+            const uint32_t k1 = k1_of(g0 + (q >> 2), (q >> 1) & 1, valid, self);
+            const uint32_t k2 = bitrev(f >> lgs, a.lg2);
+            const uint32_t k2m = k1 == 0 ? ((l2 - k2) & (l2 - 1)) : (l2 - 1 - k2);
+            const int qm = self ? q : (q ^ 2);
+            const int fm = (int)(bitrev(k2m, a.lg2) << lgs) + qm;
+            wv[r] = cross_pair(lds[f], lds[fm], lds[f + 1], lds[fm + 1]);
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kRegPoints; ++r) {   // Q: point i of slot q >> 1 at i * slots / 2 + (q >> 1)
+        const int f = threadIdx.x + r * kTThreads;
+        const int q = f & (slots - 1);
+        if (f < npts && (q & 1) == 0) lds[(f >> lgs) * (slots >> 1) + (q >> 1)] = wv[r];
+    }
+    __syncthreads();
+    lds_fft_inv<kTile>(lds, a.lg2, lgs - 1, a.tw + a.tw_b);
+    const int half = npts >> 1;
+#pragma unroll
+    for (int r = 0; r < kRegPoints; ++r) {   // twiddle loads first
+        const int f = threadIdx.x + r * kTThreads;
+        const int q2 = f & ((slots >> 1) - 1);
+        bool valid, self;
+        const uint32_t k1 = k1_of(g0 + (q2 >> 1), q2 & 1, valid, self);
+        wv[r] = (f < half && valid) ? twiddle(a, (int64_t)k1 * (f >> (lgs - 1)))
+                                    : make_double2(1.0, 0.0);
+    }
+#pragma unroll
+    for (int r = 0; r < kRegPoints; ++r) {
+        const int f = threadIdx.x + r * kTThreads;
+        const int q2 = f & ((slots >> 1) - 1);
+        bool valid, self;
+        const uint32_t k1 = k1_of(g0 + (q2 >> 1), q2 & 1, valid, self);
+        if (f >= half || !valid || ((q2 & 1) && self)) continue;
+        z1[(int64_t)bitrev(k1, a.lg1) * l2 + (f >> (lgs - 1))] = cmul_conj(lds[f], wv[r]);
+    }
+}
+
 // Split transform, step 3: inverse column transforms (row p holds k1 =
 // bitrev(p): the bit-reversed input order of the decimation in time), and
 // D(T) for the lags T = n1 L2 + n2 in [tmin, tmax].
@@ -584,11 +708,21 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_inv_kernel(FftArgs a) {
     }
     __syncthreads();
     lds_fft_inv<kTile>(lds, a.lg1, a.lgc, a.tw + a.tw_a);
-    const int rows = (int)min((int64_t)(a.tmax / l2) + 1, int64_t(1) << a.lg1);
-    for (int f = threadIdx.x; f < rows * cols; f += kTThreads) {
-        const int64_t t = (int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1));
-        write_d(a, 2 * pair, t, lds[f].x);
-        write_d(a, 2 * pair + 1, t, lds[f].y);
+    if (a.wout) {   // head-tail transform: cc_a(s) + i cc_b(s) for shifts s < wm
+        const int rows = (int)min((int64_t)((a.wm - 1) / l2) + 1, int64_t(1) << a.lg1);
+        for (int f = threadIdx.x; f < rows * cols; f += kTThreads) {
+            const int64_t sh = (int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1));
+            if (sh >= a.wm) continue;
+            a.wout[2 * pair * a.wm + sh] = ldexp(lds[f].x, -(a.lg + 2));
+            if (2 * pair + 1 < a.seqs) a.wout[(2 * pair + 1) * a.wm + sh] = ldexp(lds[f].y, -(a.lg + 2));
+        }
+    } else {
+        const int rows = (int)min((int64_t)(a.tmax / l2) + 1, int64_t(1) << a.lg1);
+        for (int f = threadIdx.x; f < rows * cols; f += kTThreads) {
+            const int64_t t = (int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1));
+            write_d(a, 2 * pair, t, lds[f].x);
+            write_d(a, 2 * pair + 1, t, lds[f].y);
+        }
     }
     if (!kRagged) break;
     __syncthreads();   // the next item reuses the LDS
@@ -739,6 +873,38 @@ __device__ double fft_bound(const double* fstat, int64_t s, int64_t seqs, int64_
     return 2.0 * (2.02 * (fwd + inv) + (2.0 * ge + 17.0 * u) * ea);
 }
 
+// Absolute error bound of the wrap term's share of D(T) (any T > W): the
+// head-tail transform of 2^lg points takes z1 = h_a + i h_b and z2 = u_a + i u_b
+// (the first and last M samples of a and of its partner b), whose norms the
+// whole sequences' norms bound.  Each separated spectrum errs by e1 sqrt(L) zeta
+// as in fft_bound; the products U conj H, summed over all frequencies and
+// divided by L, err by 2 e1 zeta |y_a| + (e1 zeta)^2, their rounding and the
+// assembly of Q (a product of two perturbed spectra and one addition each,
+// within gamma_4) by g4 ((|y_a| + e1 zeta)^2 + (|y_b| + e1 zeta)^2), and the
+// inverse transform by phi (1 + g3) ((|y_a|_1 + e1 sqrt(L) zeta)(|y_a| + e1 zeta)
+// + the same for b).  The sum bounds |cc_computed(s) - cc(s)|; D takes it
+// twice (D = ... - 2 (r_circ - cc)), with 1% margin, and the result is doubled.
+__device__ double fft_bound_wrap(const double* fstat, int64_t s, int64_t seqs, int lg) {
+    const double u = 1.1102230246251565e-16;
+    const double ea = fstat[4 * s + 1], la = fstat[4 * s + 2];
+    const int64_t o = s ^ 1;
+    const double eb = o < seqs ? fstat[4 * o + 1] : 0.0;
+    const double lb = o < seqs ? fstat[4 * o + 2] : 0.0;
+    const double ya = sqrt(ea), yb = sqrt(eb), zeta = sqrt(ea + eb);
+    const double mu = 16.0 * u;
+    const double g3 = 3.0 * u / (1.0 - 3.0 * u);
+    const double g4 = 4.0 * u / (1.0 - 4.0 * u);
+    const double eta = mu + g4 * (1.4142135623730951 + mu);
+    const double keta = (double)(lg + 1) * eta;
+    const double phi = keta / (1.0 - keta);
+    const double e1 = phi + 4.0 * u;
+    const double sl = sqrt(ldexp(1.0, lg));
+    const double pa = ya + e1 * zeta, pb = yb + e1 * zeta;
+    const double fwd = 2.0 * e1 * zeta * ya + e1 * e1 * zeta * zeta + g4 * (pa * pa + pb * pb);
+    const double inv = phi * (1.0 + g3) * ((la + e1 * sl * zeta) * pa + (lb + e1 * sl * zeta) * pb);
+    return 2.0 * (2.02 * (fwd + inv));
+}
+
 struct FixArgs {
     const float* x;
     const double* fstat;
@@ -752,6 +918,7 @@ struct FixArgs {
     double tau0;
     WindowTable tab;
     const int32_t* pair_lg;    // per pair: log2 of its transform length, or null (all lg)
+    int32_t wrap_lg;           // log2 of the head-tail transform (wrap correction), or -1
 };
 
 // One workgroup per window: lags whose score the FFT bound cannot place within
@@ -769,7 +936,9 @@ __global__ __launch_bounds__(kThreads) void fft_fixup_kernel(FixArgs a, Weights 
         for (int32_t c = 0; c < a.num_channels; ++c) {
             const int64_t sq = b * a.num_channels + c;
             const int lg = a.pair_lg ? a.pair_lg[sq >> 1] : a.lg;
-            acc += (double)w.w[c] * fft_bound(a.fstat, sq, a.seqs, n, lg);
+            double e = fft_bound(a.fstat, sq, a.seqs, n, lg);
+            if (a.wrap_lg >= 0) e += fft_bound_wrap(a.fstat, sq, a.seqs, a.wrap_lg);
+            acc += (double)w.w[c] * e;
         }
         abound = acc * (1.0 + 1e-12);
     }
@@ -1097,6 +1266,12 @@ FftArgs args_of(const Plan& p, const float* x, double* fstat, double* edge, doub
     a.bounds = nullptr;
     a.zstride = p.fft_len;
     a.cls = 0;
+    a.seg_start = 0;
+    a.seg_len = 0;
+    a.wout = nullptr;
+    a.wrap = nullptr;
+    a.wrap_w = 0;
+    a.wm = 0;
     set_geometry(a, p.fft_log2);
     return a;
 }
@@ -1146,7 +1321,8 @@ int64_t twiddle_count_of(int lg) {
 // Complex fp64 entries of the twiddle tables of a plan (a ragged plan: those
 // of every length class, one after another).
 int64_t fft_twiddle_count(const Plan& p) {
-    if (!p.fft_ragged) return twiddle_count_of(p.fft_log2);
+    if (!p.fft_ragged)
+        return twiddle_count_of(p.fft_log2) + (p.fft_wrap ? twiddle_count_of(p.fft_wrap_log2) : 0);
     int64_t total = 0;
     for (int lg = kFftMinLog2; lg <= p.fft_log2; ++lg) total += twiddle_count_of(lg);
     return total;
@@ -1227,13 +1403,77 @@ hipError_t launch_spectral(const Plan& p, const Weights& w, const float* x, cons
     return hipGetLastError();
 }
 
+namespace {
+
+// The wrap term of every sequence into `wrap` ([S][M]): head and tail
+// transforms (column kernels on the segments), the cross spectrum and its
+// inverse rows, then the inverse columns.  Twiddles of the 2^lgw geometry at
+// `tw`.
+template <int kTile>
+void launch_wrap(const Plan& p, FftArgs aw, double2* tw, double2* zw, double* wrap,
+                 hipStream_t s) {
+    const int64_t lw = int64_t(1) << p.fft_wrap_log2;
+    aw.tw = tw;
+    aw.zstride = lw;
+    aw.len = lw;
+    launch_twiddles(aw, tw, s);
+    const int64_t m1 = int64_t(1) << aw.lg1, m2 = int64_t(1) << aw.lg2, cols = int64_t(1) << aw.lgc;
+    const int64_t col_groups = p.fft_pairs * (m2 / cols);
+    const size_t lds_cols = sizeof(double2) * (size_t)(m1 * cols);
+    aw.seg_len = p.fft_wrap_m;
+    aw.seg_start = 0;                                  // heads
+    aw.z = zw;
+    hipLaunchKernelGGL((fft_cols_fwd_kernel<kTile, false>), dim3((unsigned)col_groups),
+                       dim3(kTThreads), lds_cols, s, aw);
+    aw.seg_start = p.n - p.fft_wrap_m;                 // tails
+    aw.z = zw + p.fft_pairs * lw;
+    hipLaunchKernelGGL((fft_cols_fwd_kernel<kTile, false>), dim3((unsigned)col_groups),
+                       dim3(kTThreads), lds_cols, s, aw);
+    aw.seg_len = 0;
+    aw.z = zw;
+    // four rows (two row pairs' sides, two transforms) of m2 points per row pair
+    const int rows_tile = 4 * m2 <= (int64_t(1) << kFftSmallTileLog2) ? kFftSmallTileLog2
+                                                                       : kFftTileLog2;
+    aw.lgr = rows_tile - 2 - aw.lg2;
+    if (aw.lgr > aw.lg1 - 1) aw.lgr = aw.lg1 - 1;
+    const int64_t rp = int64_t(1) << aw.lgr;
+    const int64_t row_groups = p.fft_pairs * ((m1 / 2 + 1 + rp - 1) / rp);
+    const size_t lds_rows = sizeof(double2) * 4 * (size_t)(rp * m2);
+    if (rows_tile == kFftSmallTileLog2)
+        hipLaunchKernelGGL((fft_wrap_rows_kernel<kFftSmallTileLog2>), dim3((unsigned)row_groups),
+                           dim3(kTThreads), lds_rows, s, aw, p.fft_pairs * lw);
+    else
+        hipLaunchKernelGGL((fft_wrap_rows_kernel<kFftTileLog2>), dim3((unsigned)row_groups),
+                           dim3(kTThreads), lds_rows, s, aw, p.fft_pairs * lw);
+    aw.wout = wrap;
+    aw.wm = p.fft_wrap_m;
+    hipLaunchKernelGGL((fft_cols_inv_kernel<kTile, false>), dim3((unsigned)col_groups),
+                       dim3(kTThreads), lds_cols, s, aw);
+}
+
+}  // namespace
+
 hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, double* edge,
-                             double* tw, double* z, double* part, int32_t* cls, hipStream_t s) {
-    const FftArgs a = args_of(p, x, fstat, edge, tw, z, part);
+                             double* tw, double* z, double* part, int32_t* cls, double* zw,
+                             double* wrap, hipStream_t s) {
+    FftArgs a = args_of(p, x, fstat, edge, tw, z, part);
     double2* const tw2 = reinterpret_cast<double2*>(tw);
     if (!p.fft_ragged) {
         launch_twiddles(a, tw2, s);
         hipLaunchKernelGGL(fft_edge_kernel, dim3((unsigned)(2 * a.seqs)), dim3(kThreads), 0, s, a);
+        if (p.fft_wrap) {
+            FftArgs aw = a;
+            set_geometry(aw, p.fft_wrap_log2);
+            double2* const tww = tw2 + twiddle_count_of(p.fft_log2);
+            double2* const zw2 = reinterpret_cast<double2*>(zw);
+            if (fft_tile_log2(p.fft_wrap_log2) == kFftSmallTileLog2)
+                launch_wrap<kFftSmallTileLog2>(p, aw, tww, zw2, wrap, s);
+            else
+                launch_wrap<kFftTileLog2>(p, aw, tww, zw2, wrap, s);
+            a.wrap = wrap;
+            a.wrap_w = p.fft_len - p.n;
+            a.wm = p.fft_wrap_m;
+        }
         if (fft_tile_log2(a.lg) == kFftSmallTileLog2)
             launch_transforms<kFftSmallTileLog2, false>(a, p.fft_pairs, s);
         else
@@ -1295,6 +1535,7 @@ hipError_t launch_fft_fixup(const Plan& p, const Weights& w, const float* x, con
     a.tau0 = kFftRelBound;
     a.tab = p.table;
     a.pair_lg = p.fft_ragged ? cls : nullptr;
+    a.wrap_lg = p.fft_wrap ? p.fft_wrap_log2 : -1;
     hipLaunchKernelGGL(fft_fixup_kernel, dim3((unsigned)p.num_windows), dim3(kThreads), 0, s, a,
                        w);
     return hipGetLastError();

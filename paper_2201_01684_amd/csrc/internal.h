@@ -32,6 +32,11 @@ constexpr int kFftTileLog2 = 12;
 constexpr int kFftThreadsLog2 = 8;
 constexpr int kFftMaxLog2 = 2 * (kFftTileLog2 - 1);
 constexpr int kFftMinLog2 = 6;
+// Wrap-corrected transforms (see Plan): the head-tail transform is always a
+// split one (at least 2^12 points) and at most 2^20 points (its row kernel
+// holds four rows of up to 2^10 points in one 2^12-point tile).
+constexpr int kFftWrapMinLog2 = 12;
+constexpr int kFftWrapMaxLog2 = 20;
 constexpr int kFftClasses = kFftMaxLog2 + 1;   // length classes 2^lg of a ragged batch, by lg
 inline int fft_tile_log2(int lg) { return lg <= 2 * (kFftSmallTileLog2 - 1) ? kFftSmallTileLog2 : kFftTileLog2; }
 
@@ -129,13 +134,20 @@ struct Plan {
     int32_t fft_log2, fft_m1, fft_m2, fft_cols;
     int64_t fft_len;
     int64_t fft_pairs;
+    // Wrap correction (uniform FFT plans): fft_len >= N only, so lags T > W =
+    // fft_len - N also collect the circular term sum_{j < T-W} y_j y_{j+L-T},
+    // the cross-correlation at shift Tmax - T of the first and the last M =
+    // Tmax - W samples of the sequence.  A second transform of
+    // 2^fft_wrap_log2 >= 2M points per pair computes it, and it is subtracted.
+    bool fft_wrap;
+    int32_t fft_wrap_m, fft_wrap_log2;
     double c_lag, err_max;
     uint32_t flags;
     WindowTable table;       // per-window offsets / lengths / Tmax, or all null
     int32_t bitmap_words;    // 32-bit words per window of the exactness bitmap
     // workspace layout (byte offsets, 256-byte aligned)
     size_t off_var, off_s64, off_bits, off_state, off_queue, off_part, off_cut;
-    size_t off_fstat, off_edge, off_tw, off_z, off_cls, bytes;
+    size_t off_fstat, off_edge, off_tw, off_z, off_cls, off_zw, off_wrap, bytes;
 };
 
 // Rolling detection (Algorithm 3).
@@ -200,8 +212,11 @@ hipError_t launch_finalize(const Plan& p, const Weights& w, const double* part, 
 // [kFftClasses + 1] start of each class; null otherwise.
 int64_t fft_twiddle_count(const Plan& p);
 int64_t fft_class_ints(const Plan& p);
+// zw, wrap (wrap-corrected plans): [2][pairs][2^fft_wrap_log2] complex fp64
+// head and tail transforms; [B*C][M] fp64 wrap terms.  Null otherwise.
 hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, double* edge,
-                             double* tw, double* z, double* part, int32_t* cls, hipStream_t s);
+                             double* tw, double* z, double* part, int32_t* cls, double* zw,
+                             double* wrap, hipStream_t s);
 // After the finalisation: every lag whose FFT bound does not give the tier-0
 // guarantee is re-scored in fp64 (score, fp32 score and tier-1 bit).
 hipError_t launch_fft_fixup(const Plan& p, const Weights& w, const float* x, const double* fstat,

@@ -230,14 +230,32 @@ def test_fft_plan(lib):
     # 8 complex fp64 transforms of 8192 points (4096 + 1024 <= 2^13) at least
     assert info["workspace_bytes"] >= 4 * 8192 * 16
     assert info["workspace_bytes"] != direct
-    # the largest transform: N + Tmax <= 2^22
+    assert info["fft_len"] == 8192 and info["fft_wrap_len"] == 0 and info["fft_wrap_lags"] == 0
+    # the largest transform, 2^22 points: N + Tmax <= 2^22 without the wrap term ...
     d, _ = good_desc(flags=B.FFT_SCORES, num_windows=1, n=(1 << 22) - 1000, tmax=1000,
                      channel_stride=1 << 22)
-    assert B.describe_plan(d)["mode"] == 2
+    info = B.describe_plan(d)
+    assert info["mode"] == 2 and info["fft_len"] == 1 << 22 and info["fft_wrap_len"] == 0
+    # ... or with it: 1 wrapped lag, a head-tail transform of 2^12 points
     d, _ = good_desc(flags=B.FFT_SCORES, num_windows=1, n=(1 << 22) - 1000, tmax=1001,
                      channel_stride=1 << 22)
+    info = B.describe_plan(d)
+    assert (info["fft_len"], info["fft_wrap_len"], info["fft_wrap_lags"]) == (1 << 22, 4096, 1)
+    # a wrap term longer than 2^19 lags (a head-tail transform beyond 2^20): rejected
+    d, _ = good_desc(flags=B.FFT_SCORES, num_windows=1, n=(1 << 22) - 1000,
+                     tmax=(1 << 19) + 1000 + 1, channel_stride=1 << 22)
     with pytest.raises(B.GpoeoError):
         B.workspace_bytes(d)
+    # the rule on the five workloads' shapes: N a power of two with Tmax up to
+    # N / 4 takes the wrap term; 4096 + 1024 keeps the padded transform
+    for n, tmax, want in [(4096, 1024, (8192, 0, 0)), (65536, 8192, (65536, 16384, 8192)),
+                          (262144, 32768, (262144, 65536, 32768)),
+                          (16384, 4096, (16384, 8192, 4096)),
+                          (131072, 16384, (131072, 32768, 16384))]:
+        d, _ = good_desc(flags=B.FFT_SCORES, num_windows=2, n=n, tmax=tmax, window_stride=n,
+                         channel_stride=n, num_channels=1)
+        info = B.describe_plan(d)
+        assert (info["fft_len"], info["fft_wrap_len"], info["fft_wrap_lags"]) == want, (n, tmax)
     # rolling accepts the FFT flag
     d, _ = good_desc(flags=B.FFT_SCORES)
     assert B.rolling_workspace_bytes(d, B.rolling_params()) > 0

@@ -185,13 +185,55 @@ def test_full_size(name):
         check_results(rf[b:b + 1], o_out, f"fft {name} window {b}")
 
 
-def test_transform_beyond_2_20_points_uses_the_large_tile():
-    # N + Tmax = 1,100,000 > 2^20: a 2^21-point transform, row pairs of 2^11
-    # points in 4096-point tiles
+def plan_of(lay):
     import paper_2201_01684_amd as pkg
-    n, tmax = 1_000_000, 100_000
+    desc, _ = pkg.make_desc(lay.num_windows, lay.num_channels, lay.n, lay.window_stride,
+                            lay.channel_stride, lay.tmin, lay.tmax, weights=lay.weights,
+                            flags=pkg.FFT_SCORES)
+    info = pkg.describe_plan(desc)
+    return info["fft_len"], info["fft_wrap_len"], info["fft_wrap_lags"]
+
+
+@pytest.mark.parametrize("n,tmin,tmax,plan", [
+    (16284, 2, 1000, (16384, 4096, 900)),      # lags 2..100 plain, 101..1000 wrapped
+    (16384, 2001, 3000, (16384, 8192, 3000)),  # every lag wrapped
+    (30000, 2, 2769, (32768, 4096, 1)),        # only Tmax wrapped
+    (65536, 2, 16384, (65536, 32768, 16384)),  # wrap term of L / 4 lags: still taken
+    (65536, 2, 16385, (131072, 0, 0)),         # one more lag: the padded transform
+])
+def test_wrap_correction_shapes(n, tmin, tmax, plan):
+    x = planted_trace(n, 1013, 7, seed=n + tmax, sigma=1.5)
+    lay = oracle.Layout(1, 1, n, n, n, tmin, tmax)
+    assert plan_of(lay) == plan
+    fft_parity(x, lay, f"wrap n={n} T=[{tmin},{tmax}]")
+
+
+def test_wrap_correction_odd_channel_count():
+    # three weighted channels: the last sequence has no partner in its transforms
+    n = 8192
+    x = np.stack([planted_trace(n, 700, 6, seed=31, sigma=1.0),
+                  planted_trace(n, 700, 4, seed=32, sigma=0.1) * 40,
+                  planted_trace(n, 350, 5, seed=33, sigma=2.0)])
+    lay = oracle.Layout(1, 3, n, 3 * n, n, 2, 2048,
+                        weights=np.array([1.0, 0.05, 3.0], dtype=np.float32))
+    assert plan_of(lay) == (8192, 4096, 2048)
+    fft_parity(x, lay, "wrap, 3 channels")
+
+
+@pytest.mark.parametrize("n,tmax,plan", [
+    # N + Tmax = 1,100,000 > 2^20 with N <= 2^20: a 2^20-point transform and a
+    # wrap term of 51,424 lags from a 2^17-point head-tail transform
+    (1_000_000, 100_000, (1 << 20, 1 << 17, 51_424)),
+    # N > 2^20: a 2^21-point transform, row pairs of 2^11 points in 4096-point tiles
+    (1_100_000, 100_000, (1 << 21, 0, 0)),
+    # a 2^19-point head-tail transform: four rows of 2^10 points in a 4096-point tile
+    (1 << 21, 200_000, (1 << 21, 1 << 19, 200_000)),
+])
+def test_large_transforms(n, tmax, plan):
+    import paper_2201_01684_amd as pkg
     x = planted_trace(n, 3001, 9, seed=21, sigma=2.0)
     lay = oracle.Layout(1, 1, n, n, n, 2, tmax)
+    assert plan_of(lay) == plan
     g, res = gpu_run(x, lay, flags=fft_flag())
     gd, rd = gpu_run(x, lay)
     for f in ("period", "verdict", "t_cand", "t_low", "t_up", "n_candidates"):
@@ -199,5 +241,9 @@ def test_transform_beyond_2_20_points_uses_the_large_tile():
     assert res["period"][0] == 3001
     rng = np.random.default_rng(2)
     ts = np.concatenate([rng.integers(2, tmax + 1, size=48), [2, 3001, 6002, tmax]])
+    w = plan[0] - n
+    if plan[1]:   # the last plain lag and the first wrapped one (those in range)
+        ts = np.concatenate([ts, np.array([t for t in (w, w + 1) if 2 <= t <= tmax],
+                                          dtype=ts.dtype)])
     o = oracle.score_list(x, lay, np.zeros(ts.size, dtype=np.int64), ts)
-    check_fft_scores(g[0, ts - 2], o, "2^21-point transform")
+    check_fft_scores(g[0, ts - 2], o, f"n={n} Tmax={tmax}")
