@@ -376,10 +376,11 @@ int run_plan(const gpoeo::Plan& p, const gpoeo::Weights& w, const float* x, floa
         if (gpoeo::launch_fft_scores(p, x, fstat, reinterpret_cast<double*>(ws + p.off_edge),
                                      reinterpret_cast<double*>(ws + p.off_tw),
                                      reinterpret_cast<double*>(ws + p.off_z), c.part, cls, zw,
-                                     wrap, stream) != hipSuccess)
+                                     wrap, c.s64, scores, w.w[0], stream) != hipSuccess)
             return GPOEO_PD_EHIP;
         if (!mark(2)) return GPOEO_PD_EHIP;
-        if (gpoeo::launch_finalize(p, w, c.part, c.s64, scores, stream) != hipSuccess ||
+        if ((!gpoeo::fft_fused_finalize(p) &&
+             gpoeo::launch_finalize(p, w, c.part, c.s64, scores, stream) != hipSuccess) ||
             gpoeo::launch_select_init(p, c.sb, stream) != hipSuccess ||
             gpoeo::launch_fft_fixup(p, w, x, fstat, cls, c.s64, scores, c.sb, stream) !=
                 hipSuccess)

@@ -73,6 +73,10 @@ struct FftArgs {
     const double* wrap;
     int64_t wrap_w;
     int32_t wm;
+    // Fused finalisation (one channel, uniform batch): S(T) to s64 and scores.
+    double* s64;
+    float* scores;
+    float w0;
 };
 
 // Transform kernels come in two forms: uniform (kRagged false: one workgroup
@@ -255,7 +259,14 @@ __device__ __forceinline__ void write_d(const FftArgs& a, int64_t s, int64_t t, 
         const double* ed = a.edge + s * 2 * (int64_t)(a.tmax + 1);
         d = ((e - ed[a.tmax + 1 + t]) + (e - ed[t])) - 2.0 * r;
     }
-    a.part[s * a.lags + (t - a.tmin)] = d;
+    const int64_t k = s * a.lags + (t - a.tmin);
+    if (a.s64) {   // the finalisation of a single channel, in its own arithmetic
+        const double v = 0.0 + (double)a.w0 * (d / (double)(n - t));
+        a.s64[k] = v;
+        if (a.scores) a.scores[k] = (float)v;
+    } else {
+        a.part[k] = d;
+    }
 }
 
 // Sums of y^2 over the first T samples (head) and the last T samples (tail)
@@ -1272,6 +1283,9 @@ FftArgs args_of(const Plan& p, const float* x, double* fstat, double* edge, doub
     a.wrap = nullptr;
     a.wrap_w = 0;
     a.wm = 0;
+    a.s64 = nullptr;
+    a.scores = nullptr;
+    a.w0 = 1.0f;
     set_geometry(a, p.fft_log2);
     return a;
 }
@@ -1455,9 +1469,15 @@ void launch_wrap(const Plan& p, FftArgs aw, double2* tw, double2* zw, double* wr
 
 hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, double* edge,
                              double* tw, double* z, double* part, int32_t* cls, double* zw,
-                             double* wrap, hipStream_t s) {
+                             double* wrap, double* s64, float* scores, float w0,
+                             hipStream_t s) {
     FftArgs a = args_of(p, x, fstat, edge, tw, z, part);
     double2* const tw2 = reinterpret_cast<double2*>(tw);
+    if (fft_fused_finalize(p)) {
+        a.s64 = s64;
+        a.scores = scores;
+        a.w0 = w0;
+    }
     if (!p.fft_ragged) {
         launch_twiddles(a, tw2, s);
         hipLaunchKernelGGL(fft_edge_kernel, dim3((unsigned)(2 * a.seqs)), dim3(kThreads), 0, s, a);

@@ -214,9 +214,16 @@ int64_t fft_twiddle_count(const Plan& p);
 int64_t fft_class_ints(const Plan& p);
 // zw, wrap (wrap-corrected plans): [2][pairs][2^fft_wrap_log2] complex fp64
 // head and tail transforms; [B*C][M] fp64 wrap terms.  Null otherwise.
+// With one channel and no window table the transforms also do the
+// finalisation: s64 and scores (nullable) receive S(T) = w_0 D(T) / (N - T)
+// directly and `part` is not written.
+inline bool fft_fused_finalize(const Plan& p) {
+    return p.fft && !p.fft_ragged && p.num_channels == 1;
+}
 hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, double* edge,
                              double* tw, double* z, double* part, int32_t* cls, double* zw,
-                             double* wrap, hipStream_t s);
+                             double* wrap, double* s64, float* scores, float w0,
+                             hipStream_t s);
 // After the finalisation: every lag whose FFT bound does not give the tier-0
 // guarantee is re-scored in fp64 (score, fp32 score and tier-1 bit).
 hipError_t launch_fft_fixup(const Plan& p, const Weights& w, const float* x, const double* fstat,
