@@ -138,12 +138,18 @@ __device__ int64_t block_min_i(int64_t v, int64_t* red) {
 }
 
 
+// Windows of up to this many lags keep the outcome of the first peak scan
+// (bit t - tmin set: a decided peak) in LDS, so that the later scans test a
+// bit instead of evaluating three score intervals again.
+constexpr int kPeakWords = 2048;
+
 template <int kT>
 struct Shared {
     double red_d[kT / kWave];
     double red_d2[kT / kWave];
     int64_t red_i[kT / kWave];
     int64_t red_j[kT / kWave];
+    uint32_t peaks[kPeakWords];
     int done;
     double r_approx;
     double r_err;
@@ -200,6 +206,10 @@ __global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, 
     const bool r_exact = a.pass > 0 && st->r_is_exact;
     const double r_x = r_exact ? st->r_exact : 0.0;
     const double c_lag = a.c_lag;
+    // the window's lags as bits of the peak cache (bit t - tmin)
+    const int64_t lag_span = (int64_t)tmax - tmin + 1;
+    const bool cache = lag_span <= 32 * (int64_t)kPeakWords;
+    const int words_of_window = cache ? (int)((lag_span + 31) >> 5) : 0;
 
     // Queue (window b, lag t) for the next tier; lag -1 queues R.
     auto enqueue = [&](int tier, int32_t t) {
@@ -271,6 +281,11 @@ __global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, 
         // are left open.
         int64_t npk = 0, unk = 0;
         double pk_lo = INFINITY, pk_hi = INFINITY, unk_lo = INFINITY;
+        if (cache) {   // (after the scans of an earlier evaluation of the rule)
+            __syncthreads();
+            for (int i = tid; i < words_of_window; i += kSelThreads) sh.peaks[i] = 0u;
+            __syncthreads();
+        }
         for (int64_t t = tmin + 1 + tid; t < tmax; t += kSelThreads) {
             Iv z;
             const Tri q = peak(t, z, false);
@@ -278,6 +293,10 @@ __global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, 
                 ++npk;
                 pk_lo = fmin(pk_lo, z.lo);
                 pk_hi = fmin(pk_hi, z.hi);
+                if (cache) {
+                    const int64_t j = t - tmin;
+                    atomicOr(&sh.peaks[j >> 5], 1u << (j & 31));
+                }
             } else if (q == kUnk) {
                 ++unk;
                 unk_lo = fmin(unk_lo, z.lo);
@@ -317,7 +336,13 @@ __global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, 
         unk = 0;
         for (int64_t t = tmin + 1 + tid; t < tmax; t += kSelThreads) {
             Iv z;
-            if (peak(t, z, false) != kYes) continue;
+            if (cache) {
+                const int64_t j = t - tmin;
+                if (!((sh.peaks[j >> 5] >> (j & 31)) & 1u)) continue;
+                z = iv(t);
+            } else if (peak(t, z, false) != kYes) {
+                continue;
+            }
             const Tri q = lt(z, thr);
             if (q == kYes) {
                 ++ncand;
@@ -337,7 +362,14 @@ __global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, 
             if (pk_lo != pk_hi) {
                 for (int64_t t = tmin + 1 + tid; t < tmax; t += kSelThreads) {
                     Iv z;
-                    if (peak(t, z, false) == kYes && z.lo <= pk_hi) push(t, z);
+                    if (cache) {
+                        const int64_t j = t - tmin;
+                        if (!((sh.peaks[j >> 5] >> (j & 31)) & 1u)) continue;
+                        z = iv(t);
+                        if (z.lo <= pk_hi) push(t, z);
+                    } else if (peak(t, z, false) == kYes && z.lo <= pk_hi) {
+                        push(t, z);
+                    }
                 }
             }
             return false;
