@@ -1445,7 +1445,7 @@ void launch_wrap(const Plan& p, FftArgs aw, double2* tw, double2* zw, double* wr
                        dim3(kTThreads), lds_cols, s, aw);
     aw.seg_len = 0;
     aw.z = zw;
-    // four rows (two row pairs' sides, two transforms) of m2 points per row pair
+    // a row pair holds four rows of m2 points: its two rows in each transform
     const int rows_tile = 4 * m2 <= (int64_t(1) << kFftSmallTileLog2) ? kFftSmallTileLog2
                                                                        : kFftTileLog2;
     aw.lgr = rows_tile - 2 - aw.lg2;
