@@ -379,7 +379,7 @@ int run_plan(const gpoeo::Plan& p, const gpoeo::Weights& w, const float* x, floa
                                      wrap, c.s64, scores, w.w[0], stream) != hipSuccess)
             return GPOEO_PD_EHIP;
         if (!mark(2)) return GPOEO_PD_EHIP;
-        if ((!gpoeo::fft_fused_finalize(p) &&
+        if ((!gpoeo::fft_fused_finalize(p, scores != nullptr) &&
              gpoeo::launch_finalize(p, w, c.part, c.s64, scores, stream) != hipSuccess) ||
             gpoeo::launch_select_init(p, c.sb, stream) != hipSuccess ||
             gpoeo::launch_fft_fixup(p, w, x, fstat, cls, c.s64, scores, c.sb, stream) !=

@@ -251,8 +251,9 @@ __device__ __forceinline__ void write_d(const FftArgs& a, int64_t s, int64_t t, 
     if (s >= a.seqs || t < a.tmin || t > a.tmax) return;
     const int64_t b = s / a.num_channels;
     const int64_t n = table_n(a.tab, b, a.n_all);
+    const bool live = n > 0 && t <= table_tmax(a.tab, b, a.tmax);
     double d = 0.0;
-    if (n > 0 && t <= table_tmax(a.tab, b, a.tmax)) {
+    if (live) {
         double r = ldexp(w, -(a.lg + 2));
         if (a.wrap && t > a.wrap_w) r -= a.wrap[s * a.wm + (a.tmax - t)];   // circular term
         const double e = a.fstat[4 * s + 1];
@@ -261,6 +262,7 @@ __device__ __forceinline__ void write_d(const FftArgs& a, int64_t s, int64_t t, 
     }
     const int64_t k = s * a.lags + (t - a.tmin);
     if (a.s64) {   // the finalisation of a single channel, in its own arithmetic
+        if (!live && !a.scores) return;   // past a table window's lags: left unwritten
         const double v = 0.0 + (double)a.w0 * (d / (double)(n - t));
         a.s64[k] = v;
         if (a.scores) a.scores[k] = (float)v;
@@ -1473,7 +1475,7 @@ hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, doubl
                              hipStream_t s) {
     FftArgs a = args_of(p, x, fstat, edge, tw, z, part);
     double2* const tw2 = reinterpret_cast<double2*>(tw);
-    if (fft_fused_finalize(p)) {
+    if (fft_fused_finalize(p, scores != nullptr)) {
         a.s64 = s64;
         a.scores = scores;
         a.w0 = w0;

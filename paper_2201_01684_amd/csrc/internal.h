@@ -214,11 +214,12 @@ int64_t fft_twiddle_count(const Plan& p);
 int64_t fft_class_ints(const Plan& p);
 // zw, wrap (wrap-corrected plans): [2][pairs][2^fft_wrap_log2] complex fp64
 // head and tail transforms; [B*C][M] fp64 wrap terms.  Null otherwise.
-// With one channel and no window table the transforms also do the
-// finalisation: s64 and scores (nullable) receive S(T) = w_0 D(T) / (N - T)
-// directly and `part` is not written.
-inline bool fft_fused_finalize(const Plan& p) {
-    return p.fft && !p.fft_ragged && p.num_channels == 1;
+// With one channel the transforms also do the finalisation: s64 and scores
+// (nullable) receive S(T) = w_0 D(T) / (N - T) directly and `part` is not
+// written.  Not for a window table (ragged plans) with fp32 scores requested:
+// lags past a short window's transform are then zeroed by the finalisation.
+inline bool fft_fused_finalize(const Plan& p, bool with_scores) {
+    return p.fft && p.num_channels == 1 && (!p.fft_ragged || !with_scores);
 }
 hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, double* edge,
                              double* tw, double* z, double* part, int32_t* cls, double* zw,
