@@ -53,6 +53,21 @@
  * <= 2^22, or N <= 2^22 with a head-tail transform of at most min(2^20, L / 2)
  * points.  Sliding-window block sharing does not apply.
  *
+ * Matrix-core scores (GPOEO_PD_MFMA_SCORES).  The same decomposition of D_c(T)
+ * with r(T) evaluated directly, as an integer cross-correlation on the int8
+ * matrix instructions: each (window, channel) sequence is centred by its mean
+ * rounded to fp32, scaled by a power of two 2^s into integers
+ * X_i = rint((x_i - c) 2^s) with |X_i| <= 2^30, and split into four signed
+ * base-256 digits; the 16 digit-pair correlations accumulate exactly in int32
+ * and are combined in fp64.  When every x_i - c is a multiple of 2^-s (the
+ * samples of the sequence span at most about 2^7 in magnitude, as sampled
+ * power does) the X_i are the samples exactly and the only error is the fp64
+ * combination; otherwise the rounding of X_i adds a bounded error.  Each lag
+ * whose bound exceeds 1.25e-5 of its score (exact zeros included) is
+ * recomputed as an fp64 sum before the selection, which then uses the same
+ * tier-0 width as the direct scores.  Selections equal those of the direct
+ * scores.  Not with GPOEO_PD_FFT_SCORES, and not for rolling detection.
+ *
  * Threading and ownership.  All buffers except `desc` and `desc->channel_weights`
  * are DEVICE memory owned by the caller.  The library never allocates or frees
  * memory and keeps no mutable global state: calls on different streams with
@@ -91,6 +106,8 @@ extern "C" {
 #define GPOEO_PD_NO_RESCUE 2u    /* decide on the bounded tier-0 scores only                */
 #define GPOEO_PD_FFT_SCORES 4u   /* scores from an fp64 FFT autocorrelation instead of the
                                     direct sums (see below); transform limits below        */
+#define GPOEO_PD_MFMA_SCORES 8u  /* scores from an integer cross-correlation on the matrix
+                                    cores instead of the direct sums (see below)           */
 
 /* result->flags */
 #define GPOEO_PD_UNRESOLVED 1u   /* some comparison stayed undecided after the exact
@@ -119,7 +136,7 @@ typedef struct {
     double err_max;          /* APERIODIC if S(period)/R >= err_max (1.0: never for a
                                 selected period)                                            */
     const float* channel_weights; /* HOST array of C weights > 0, or NULL for all 1          */
-    uint32_t flags;          /* GPOEO_PD_SCORES_ONLY | GPOEO_PD_NO_RESCUE | _FFT_SCORES     */
+    uint32_t flags;          /* GPOEO_PD_SCORES_ONLY | _NO_RESCUE | _FFT_SCORES | _MFMA_SCORES */
     uint32_t reserved1;      /* must be 0                                                   */
 } gpoeo_pd_desc;
 
@@ -138,7 +155,8 @@ typedef struct {
 typedef struct {
     int32_t mode;             /* 0: every window scored on its own; 1: overlapping windows
                                  at a stride dividing N share per-block partials; 2: FFT
-                                 scores (score_waves and pairs_scored are then 0)         */
+                                 scores (score_waves and pairs_scored are then 0); 3:
+                                 matrix-core scores (score_waves: lag tiles of 1024)      */
     int32_t lags_per_lane;    /* consecutive lags per lane of the score kernel (8 or 16)  */
     int64_t score_waves;      /* wavefronts the score stage launches                      */
     double pairs_defined;     /* sum over windows, channels and T in [tmin, tmax] of N - T:

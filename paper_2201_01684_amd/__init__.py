@@ -14,6 +14,7 @@ from ._binding import (  # noqa: F401
     DEFAULT_ERR_MAX,
     EXPORTS,
     FFT_SCORES,
+    MFMA_SCORES,
     LIB_PATH,
     MAX_QUERIES,
     MAX_WINDOWS,

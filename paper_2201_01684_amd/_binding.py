@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(HERE, "libgpoeo_pd.so")
 
 OK, EINVAL, ENOMEM, EHIP = 0, -1, -2, -3
 PERIODIC, APERIODIC, CONSTANT = 0, 1, 2
-SCORES_ONLY, NO_RESCUE, FFT_SCORES = 1, 2, 4
+SCORES_ONLY, NO_RESCUE, FFT_SCORES, MFMA_SCORES = 1, 2, 4, 8
 UNRESOLVED = 1
 DEFAULT_C_LAG = 0.9
 DEFAULT_ERR_MAX = 1.0

@@ -24,13 +24,13 @@ LIB_NAME = "libgpoeo_pd.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
 
 SOURCES = ["api.cpp", "lag_score.hip", "window_stats.hip", "select.hip", "rolling.hip",
-           "similarity.hip", "fft_score.hip", "centred.hip"]
+           "similarity.hip", "fft_score.hip", "centred.hip", "mfma_score.hip"]
 # The selection re-evaluates scores and thresholds as plain fp64 expressions
 # (one rounding per operation, as written); no multiply-add contraction there,
 # nor in the FFT, whose error bound assumes separately rounded products.
 EXTRA_FLAGS = {"select.hip": ["-ffp-contract=off"], "rolling.hip": ["-ffp-contract=off"],
                "similarity.hip": ["-ffp-contract=off"], "fft_score.hip": ["-ffp-contract=off"],
-               "centred.hip": ["-ffp-contract=off"]}
+               "centred.hip": ["-ffp-contract=off"], "mfma_score.hip": ["-ffp-contract=off"]}
 ARCH = os.environ.get("GPOEO_PD_ARCH", "gfx950")
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

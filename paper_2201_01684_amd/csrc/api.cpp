@@ -94,6 +94,8 @@ bool launches_fit(const Plan& p) {
             const int64_t per_pair = std::max<int64_t>(m2 / cols, m1 / 2 + 1);
             if (p.fft_pairs > kMax / 256 / per_pair) return false;
         }
+    } else if (p.mfma) {   // statistics and edge sums per sequence, four lag tiles a workgroup
+        if (!fits(2 * seqs, 256) || !fits(seqs * ((p.mfma_tiles + 3) / 4), 256)) return false;
     } else if (p.sliding) {
         if (!fits(p.block_tasks, kWave)) return false;
     } else if (!fits(p.tasks, kWave)) {
@@ -107,8 +109,12 @@ bool launches_fit(const Plan& p) {
 int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
     if (!d) return GPOEO_PD_EINVAL;
     if (d->reserved0 != 0 || d->reserved1 != 0) return GPOEO_PD_EINVAL;
-    if (d->flags & ~(GPOEO_PD_SCORES_ONLY | GPOEO_PD_NO_RESCUE | GPOEO_PD_FFT_SCORES))
+    if (d->flags & ~(GPOEO_PD_SCORES_ONLY | GPOEO_PD_NO_RESCUE | GPOEO_PD_FFT_SCORES |
+                     GPOEO_PD_MFMA_SCORES))
         return GPOEO_PD_EINVAL;
+    const bool mfma = (d->flags & GPOEO_PD_MFMA_SCORES) != 0;
+    // one score source per call; matrix-core scores take whole windows only
+    if (mfma && ((d->flags & GPOEO_PD_FFT_SCORES) || ragged)) return GPOEO_PD_EINVAL;
     if (d->num_windows < 1 || d->num_windows > GPOEO_PD_MAX_WINDOWS) return GPOEO_PD_EINVAL;
     if (d->num_channels < 1 || d->num_channels > kMaxChannels) return GPOEO_PD_EINVAL;
     if (d->n < 8 || d->n > (int64_t(1) << 40)) return GPOEO_PD_EINVAL;
@@ -177,7 +183,7 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
     // Overlapping windows whose stride divides N (and is a whole number of lag
     // blocks) share block partials when that saves at least a third of the work.
     const int64_t ws_ = d->window_stride;
-    if (!p->fft && d->num_windows >= 2 && ws_ > 0 && ws_ < d->n && d->n % ws_ == 0 &&
+    if (!p->fft && !mfma && d->num_windows >= 2 && ws_ > 0 && ws_ < d->n && d->n % ws_ == 0 &&
         ws_ % lags_per_block == 0) {
         const int64_t m = d->n / ws_;
         const double direct =
@@ -246,6 +252,15 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
         p->chunks = 1;
         p->fft_pairs = (bc + 1) / 2;
     }
+    p->mfma = mfma;
+    if (p->mfma) {   // as FFT plans: one D(T) per (window, channel, lag)
+        p->t0 = d->tmin;
+        p->lags_padded = p->lags;
+        p->chunks = 1;
+        p->mfma_t0 = d->tmin & ~15;               // B operand rows 16-byte aligned
+        p->mfma_tiles = (d->tmax - p->mfma_t0) / kMfmaTileLags + 1;
+        p->mfma_plane = (kMfmaPadL + d->n + kMfmaPadR + 255) / 256 * 256;
+    }
     p->bitmap_words = (p->lags + 31) / 32;
 
     int64_t n_var, n_s, n_bits, n_part;
@@ -263,6 +278,11 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
     }
     if (n_part > (INT64_MAX / 16)) return GPOEO_PD_EINVAL;
     int64_t n_fstat = 0, n_edge = 0, n_tw = 0, n_z = 0, n_cls = 0, n_zw = 0, n_wrap = 0;
+    int64_t n_dig = 0, n_qstat = 0;
+    if (p->mfma &&
+        (!mul_ok(bc, 4, &n_qstat) || !mul_ok(bc, 2 * ((int64_t)d->tmax + 1), &n_edge) ||
+         !mul_ok(bc, 4 * p->mfma_plane, &n_dig) || n_dig > (INT64_MAX / 4)))
+        return GPOEO_PD_EINVAL;
     if (p->fft) {
         if (!mul_ok(bc, 4, &n_fstat) || !mul_ok(bc, 2 * ((int64_t)d->tmax + 1), &n_edge) ||
             !mul_ok(p->fft_pairs, p->fft_len, &n_z) || n_z > (INT64_MAX / 64))
@@ -303,6 +323,10 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
     off = align_up(off + (size_t)n_zw * 2 * sizeof(double));
     p->off_wrap = off;                            // wrap terms
     off = align_up(off + (size_t)n_wrap * sizeof(double));
+    p->off_dig = off;                             // matrix-core scores: int8 digit planes
+    off = align_up(off + (size_t)n_dig);
+    p->off_qstat = off;                           // centre, scale, exactness, sum X^2
+    off = align_up(off + (size_t)n_qstat * sizeof(double));
     p->bytes = off;
     if (!launches_fit(*p)) return GPOEO_PD_EINVAL;
     return GPOEO_PD_OK;
@@ -385,6 +409,19 @@ int run_plan(const gpoeo::Plan& p, const gpoeo::Weights& w, const float* x, floa
             gpoeo::launch_fft_fixup(p, w, x, fstat, cls, c.s64, scores, c.sb, stream) !=
                 hipSuccess)
             return GPOEO_PD_EHIP;
+    } else if (p.mfma) {
+        char* ws = static_cast<char*>(workspace);
+        double* qstat = reinterpret_cast<double*>(ws + p.off_qstat);
+        if (gpoeo::launch_mfma_scores(p, x, qstat, reinterpret_cast<int8_t*>(ws + p.off_dig),
+                                      reinterpret_cast<double*>(ws + p.off_edge), c.part, c.s64,
+                                      scores, w.w[0], stream) != hipSuccess)
+            return GPOEO_PD_EHIP;
+        if (!mark(2)) return GPOEO_PD_EHIP;
+        if ((!gpoeo::mfma_fused_finalize(p) &&
+             gpoeo::launch_finalize(p, w, c.part, c.s64, scores, stream) != hipSuccess) ||
+            gpoeo::launch_select_init(p, c.sb, stream) != hipSuccess ||
+            gpoeo::launch_mfma_fixup(p, w, x, qstat, c.s64, scores, c.sb, stream) != hipSuccess)
+            return GPOEO_PD_EHIP;
     } else if (p.sliding) {
         if (gpoeo::launch_lag_score_blocks(p, x, c.part, c.cut, stream) != hipSuccess)
             return GPOEO_PD_EHIP;
@@ -399,7 +436,7 @@ int run_plan(const gpoeo::Plan& p, const gpoeo::Weights& w, const float* x, floa
     }
     if (!mark(3)) return GPOEO_PD_EHIP;
     if (!scores_only) {
-        if (!p.fft && gpoeo::launch_select_init(p, c.sb, stream) != hipSuccess)
+        if (!p.fft && !p.mfma && gpoeo::launch_select_init(p, c.sb, stream) != hipSuccess)
             return GPOEO_PD_EHIP;
         if (gpoeo::launch_select(p, w, x, c.var, c.s64, c.sb, results, stream) != hipSuccess)
             return GPOEO_PD_EHIP;
@@ -514,9 +551,11 @@ int gpoeo_pd_describe_plan(const gpoeo_pd_desc* desc, gpoeo_pd_plan_info* info) 
     gpoeo::Plan p;
     const int rc = gpoeo::make_plan(desc, &p);
     if (rc != GPOEO_PD_OK) return rc;
-    info->mode = p.fft ? 2 : (p.sliding ? 1 : 0);
+    info->mode = p.fft ? 2 : (p.mfma ? 3 : (p.sliding ? 1 : 0));
     info->lags_per_lane = p.lags_per_lane;
-    info->score_waves = p.fft ? 0 : (p.sliding ? 2 * p.block_tasks : p.tasks);
+    info->score_waves = p.fft ? 0
+                        : p.mfma ? (int64_t)p.num_windows * p.num_channels * p.mfma_tiles
+                        : (p.sliding ? 2 * p.block_tasks : p.tasks);
     info->workspace_bytes = p.bytes;
     const double wc = (double)p.num_windows * p.num_channels;
     double defined = 0.0, scored = 0.0;

@@ -38,6 +38,15 @@ constexpr int kFftMinLog2 = 6;
 constexpr int kFftWrapMinLog2 = 12;
 constexpr int kFftWrapMaxLog2 = 20;
 constexpr int kFftClasses = kFftMaxLog2 + 1;   // length classes 2^lg of a ragged batch, by lg
+// Matrix-core scores (GPOEO_PD_MFMA_SCORES): lags per wavefront tile, zero
+// padding before and after each digit plane (bytes; every read of the tile
+// loop stays within it), and the steps between two flushes of the int32
+// shift groups (each stays below 2^31: 4 digit pairs x 32 products of at most
+// 2^14 per step).
+constexpr int kMfmaTileLags = 1024;
+constexpr int kMfmaPadL = 64;
+constexpr int kMfmaPadR = 1152;
+constexpr int kMfmaFlush = 512;
 inline int fft_tile_log2(int lg) { return lg <= 2 * (kFftSmallTileLog2 - 1) ? kFftSmallTileLog2 : kFftTileLog2; }
 
 struct Weights {
@@ -141,13 +150,19 @@ struct Plan {
     // 2^fft_wrap_log2 >= 2M points per pair computes it, and it is subtracted.
     bool fft_wrap;
     int32_t fft_wrap_m, fft_wrap_log2;
+    // Matrix-core scores: every sequence as four int8 digit planes of
+    // mfma_plane bytes (padded); lag tiles of kMfmaTileLags from mfma_t0
+    // (Tmin rounded down to a multiple of 16).
+    bool mfma;
+    int32_t mfma_t0, mfma_tiles;
+    int64_t mfma_plane;
     double c_lag, err_max;
     uint32_t flags;
     WindowTable table;       // per-window offsets / lengths / Tmax, or all null
     int32_t bitmap_words;    // 32-bit words per window of the exactness bitmap
     // workspace layout (byte offsets, 256-byte aligned)
     size_t off_var, off_s64, off_bits, off_state, off_queue, off_part, off_cut;
-    size_t off_fstat, off_edge, off_tw, off_z, off_cls, off_zw, off_wrap, bytes;
+    size_t off_fstat, off_edge, off_tw, off_z, off_cls, off_zw, off_wrap, off_dig, off_qstat, bytes;
 };
 
 // Rolling detection (Algorithm 3).
@@ -230,6 +245,18 @@ hipError_t launch_fft_scores(const Plan& p, const float* x, double* fstat, doubl
 hipError_t launch_fft_fixup(const Plan& p, const Weights& w, const float* x, const double* fstat,
                             const int32_t* cls, double* s64, float* scores,
                             const SelectBuffers& sb, hipStream_t s);
+
+// Matrix-core scores: per sequence the centre, scale and exactness (qstat
+// [S][4]), the digit planes, the edge sums and D(T) into `part`, or with one
+// channel S(T) straight into s64 and scores (nullable).  Then the fix-up of
+// the lags whose bound exceeds half the tier-0 width, before the selection.
+inline bool mfma_fused_finalize(const Plan& p) { return p.mfma && p.num_channels == 1; }
+hipError_t launch_mfma_scores(const Plan& p, const float* x, double* qstat, int8_t* dig,
+                              double* edge, double* part, double* s64, float* scores, float w0,
+                              hipStream_t s);
+hipError_t launch_mfma_fixup(const Plan& p, const Weights& w, const float* x,
+                             const double* qstat, double* s64, float* scores,
+                             const SelectBuffers& sb, hipStream_t s);
 hipError_t launch_select_init(const Plan& p, const SelectBuffers& sb, hipStream_t s);
 // Spectral candidates (Algorithm 1's FFT front end) of every window: a plan
 // whose FFT geometry is that of L = 2^k >= N; amp: [B*C][L/2 + 1] fp64.

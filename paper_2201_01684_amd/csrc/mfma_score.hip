@@ -1,0 +1,455 @@
+// Lag scores from an integer cross-correlation on the matrix cores
+// (GPOEO_PD_MFMA_SCORES).
+//
+// The score of Algorithm 2's point-wise reading, D(T) = sum_{i < N-T}
+// (y_i - y_{i+T})^2, equals E1(T) + E2(T) - 2 r(T) with r(T) = sum_i y_i y_{i+T}
+// and the energies E1, E2 of the first N-T and the last N-T samples.  Each
+// (window, channel) sequence is centred by c = its mean rounded to fp32 and
+// scaled by 2^s into integers X_i = rint((x_i - c) 2^s), |X_i| < 2^30.  When
+// every x_i - c is a multiple of 2^-s (all of a sequence's samples within a
+// few binades, as sampled power is) the X_i represent the samples exactly;
+// otherwise the rounding is bounded below.  X splits into four balanced base-256
+// digits d_p in [-128, 127], X = sum_p 256^p d_p, and the cross term is the sum
+// over digit pairs of 256^(p+q) sum_i d_p(i) d_q(i+T), exact int8 products
+// accumulated exactly in int32 by v_mfma_i32_32x32x32_i8.
+//
+// Tile of one wavefront: 1024 lags T0 + 32 b + a (a, b < 32) over 32-sample
+// steps i0: A[a][k] = d_p(i0 - a + k), B[k][b] = d_q(i0 + T0 + 32 b + k), so
+// (A B)[a][b] sums the products of samples i = i0 - a + k and i + T.  Zero
+// padding around each digit plane makes every read in range and every pair
+// outside [0, N) contribute nothing, so the steps i0 = 0, 32, ... cover each
+// lag's pairs exactly once.  The 16 digit-pair products go to 7 shift groups
+// p + q; every 512 steps the groups are added, scaled by 256^(p+q), into fp64.
+//
+// The fix-up re-scores in fp64 every lag whose error bound (rounding of the
+// fp64 sums, and the quantisation of inexact sequences) is not within half the
+// selection's tier-0 width of its score.
+#include <cmath>
+
+#include "exact.h"
+#include "internal.h"
+
+namespace gpoeo {
+namespace {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+constexpr int kThreads = 256;
+constexpr int kEdgeTile = 4096;
+constexpr int kEdgePer = kEdgeTile / kThreads;
+constexpr int kEdgeWaves = kThreads / kWave;
+
+struct MfmaArgs {
+    const float* x;
+    double* qstat;       // [S][4]: centre c, scale exponent s, exact (1 or 0), E = sum X^2
+    int8_t* dig;         // [S][4][plane]: digit p of sample i at p * plane + kMfmaPadL + i
+    double* edge;        // [S][2][tmax + 1]: head and tail sums of X^2
+    double* part;        // [S][lags]: D(T) (unless fused)
+    double* s64;         // fused finalisation (one channel): S(T)
+    float* scores;
+    float w0;
+    int64_t seqs, n, window_stride, channel_stride, plane;
+    int32_t num_channels, tmin, tmax, lags, t0, tiles;
+};
+
+__device__ __forceinline__ const float* seq_ptr(const MfmaArgs& a, int64_t s) {
+    return a.x + (s / a.num_channels) * a.window_stride + (s % a.num_channels) * a.channel_stride;
+}
+
+// The integer sample of x under centre c and scale 2^s (the same expression in
+// every kernel, so all of them see the same X).
+__device__ __forceinline__ double quantised(float x, double c, double scale) {
+    return rint(((double)x - c) * scale);
+}
+
+__device__ double block_sum(double v, double* red) {
+    for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_down(v, o);
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    __syncthreads();
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    double r = 0.0;
+    for (int w = 0; w < kThreads / kWave; ++w) r += red[w];
+    return r;
+}
+
+__device__ float block_min(float v, float* red) {
+    for (int o = kWave / 2; o > 0; o >>= 1) v = fminf(v, __shfl_down(v, o));
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    __syncthreads();
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    float r = red[0];
+    for (int w = 1; w < kThreads / kWave; ++w) r = fminf(r, red[w]);
+    return r;
+}
+
+// One workgroup per sequence.  Pass 1: mean, smallest and largest sample.
+// Pass 2: X_i, its digits, E = sum X_i^2, and whether every X_i 2^-s equals
+// x_i - c exactly.  Also zeroes the padding of the four digit planes.
+__global__ __launch_bounds__(kThreads) void mfma_prep_kernel(MfmaArgs a) {
+    __shared__ double red[kThreads / kWave];
+    __shared__ float redf[kThreads / kWave];
+    const int64_t s = blockIdx.x;
+    const float* __restrict__ xs = seq_ptr(a, s);
+    const int64_t n = a.n;
+    double sum = 0.0;
+    float mn = INFINITY, mx = -INFINITY;
+    for (int64_t i = threadIdx.x; i < n; i += kThreads) {
+        const float v = xs[i];
+        sum += (double)v;
+        mn = fminf(mn, v);
+        mx = fmaxf(mx, v);
+    }
+    const double mean = block_sum(sum, red) / (double)n;
+    mn = block_min(mn, redf);
+    mx = -block_min(-mx, redf);
+    const double c = (double)(float)mean;
+    const double dev = fmax((double)mx - c, c - (double)mn);   // differences of fp32 values: exact
+    int e = 0;
+    if (dev > 0.0) frexp(dev, &e);                             // dev < 2^e
+    const int sc = 30 - e;                                     // |X| <= dev 2^sc < 2^30
+    const double scale = ldexp(1.0, sc);
+    int8_t* __restrict__ d0 = a.dig + s * 4 * a.plane + kMfmaPadL;
+    double ex = 0.0;
+    int exact = 1;
+    for (int64_t i = threadIdx.x; i < n; i += kThreads) {
+        const double xv = (double)xs[i];
+        const double y = xv - c;
+        const double bb = y - xv;                              // two-sum error of xv + (-c)
+        const double err = (xv - (y - bb)) + (-c - bb);
+        const double t = y * scale;
+        const double q = rint(t);
+        exact &= (err == 0.0 && q == t) ? 1 : 0;
+        ex += q * q;
+        const int32_t v = (int32_t)q;
+        const int32_t g0 = (int32_t)(int8_t)(v & 0xff);
+        const int32_t r1 = (v - g0) >> 8;
+        const int32_t g1 = (int32_t)(int8_t)(r1 & 0xff);
+        const int32_t r2 = (r1 - g1) >> 8;
+        const int32_t g2 = (int32_t)(int8_t)(r2 & 0xff);
+        const int32_t g3 = (r2 - g2) >> 8;
+        d0[i] = (int8_t)g0;
+        d0[a.plane + i] = (int8_t)g1;
+        d0[2 * a.plane + i] = (int8_t)g2;
+        d0[3 * a.plane + i] = (int8_t)g3;
+    }
+    const int64_t pad_r = a.plane - kMfmaPadL - n;
+    for (int64_t k = threadIdx.x; k < 4 * (kMfmaPadL + pad_r); k += kThreads) {
+        const int64_t p = k / (kMfmaPadL + pad_r), j = k % (kMfmaPadL + pad_r);
+        const int64_t i = j < kMfmaPadL ? j - kMfmaPadL : n + (j - kMfmaPadL);
+        d0[p * a.plane + i] = 0;
+    }
+    const double etot = block_sum(ex, red);
+    const double ex_all = block_sum(exact ? 0.0 : 1.0, red);
+    if (threadIdx.x == 0) {
+        a.qstat[4 * s] = c;
+        a.qstat[4 * s + 1] = (double)sc;
+        a.qstat[4 * s + 2] = ex_all == 0.0 ? 1.0 : 0.0;
+        a.qstat[4 * s + 3] = etot;
+    }
+}
+
+// Head and tail sums of X^2 for T = 0 .. Tmax, one workgroup per (sequence,
+// side): tiles of 4096 terms staged in LDS, per-thread runs of 16, a scan of
+// the thread totals, coalesced stores.
+__device__ __forceinline__ int edge_slot(int k) { return k + (k >> 4); }
+
+__global__ __launch_bounds__(kThreads) void mfma_edge_kernel(MfmaArgs a) {
+    __shared__ double tile[kEdgeTile + kEdgeTile / 16];
+    __shared__ double wsum[kEdgeWaves];
+    const int64_t s = blockIdx.x >> 1;
+    const int side = blockIdx.x & 1;
+    const float* __restrict__ p = seq_ptr(a, s);
+    const int64_t n = a.n;
+    const double c = a.qstat[4 * s];
+    const double scale = ldexp(1.0, (int)a.qstat[4 * s + 1]);
+    double* __restrict__ out = a.edge + (s * 2 + side) * ((int64_t)a.tmax + 1);
+    const int64_t span = (int64_t)a.tmax + 1;
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    if (threadIdx.x == 0) out[0] = 0.0;
+    double carry = 0.0;
+    for (int64_t k0 = 0; k0 < span - 1; k0 += kEdgeTile) {
+        {
+            float v[kEdgePer];
+#pragma unroll
+            for (int r = 0; r < kEdgePer; ++r) {
+                const int64_t kk = k0 + (int)threadIdx.x + r * kThreads;
+                v[r] = kk < span - 1 ? p[side == 0 ? kk : n - 1 - kk] : 0.0f;
+            }
+#pragma unroll
+            for (int r = 0; r < kEdgePer; ++r) {
+                const int k = (int)threadIdx.x + r * kThreads;
+                const double q = k0 + k < span - 1 ? quantised(v[r], c, scale) : 0.0;
+                tile[edge_slot(k)] = q * q;
+            }
+        }
+        __syncthreads();
+        double part = 0.0;
+        for (int r = 0; r < kEdgePer; ++r) part += tile[edge_slot((int)threadIdx.x * kEdgePer + r)];
+        double inc = part;
+        for (int o = 1; o < kWave; o <<= 1) {
+            const double u = __shfl_up(inc, o);
+            if (lane >= o) inc += u;
+        }
+        if (lane == kWave - 1) wsum[wave] = inc;
+        __syncthreads();
+        double run = carry, total = carry;
+        for (int w = 0; w < kEdgeWaves; ++w) {
+            if (w < wave) run += wsum[w];
+            total += wsum[w];
+        }
+        run += inc - part;
+        for (int r = 0; r < kEdgePer; ++r) {
+            const int k = (int)threadIdx.x * kEdgePer + r;
+            run += tile[edge_slot(k)];
+            tile[edge_slot(k)] = run;
+        }
+        __syncthreads();
+        for (int r = 0; r < kEdgePer; ++r) {
+            const int k = (int)threadIdx.x + r * kThreads;
+            const int64_t t = k0 + k + 1;
+            if (t < span) out[t] = tile[edge_slot(k)];
+        }
+        carry = total;
+        __syncthreads();
+    }
+}
+
+// One wavefront per (sequence, tile of 1024 lags); four tiles of a sequence per
+// workgroup, so that their waves share the digit loads in L1.
+__global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const int groups = (a.tiles + 3) / 4;
+    const int64_t s = blockIdx.x / groups;
+    const int tile = (int)(blockIdx.x % groups) * 4 + wave;
+    if (tile >= a.tiles) return;
+    const int32_t t0 = a.t0 + tile * kMfmaTileLags;
+    const int8_t* __restrict__ base = a.dig + s * 4 * a.plane + kMfmaPadL;
+    const int m = lane & 31, h = lane >> 5;
+    const int off = (4 - (m & 3)) & 3;   // byte offset of this lane's A row within its first dword
+    v16i acc[7];
+#pragma unroll
+    for (int g = 0; g < 7; ++g) acc[g] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+    double r[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) r[j] = 0.0;
+    // steps while some pair (i, i + T) of the tile has i + T < N
+    const int64_t iend = a.n - t0 + 31;
+    int since = 0;
+    for (int64_t i0 = 0; i0 < iend; i0 += 32) {
+        v4i A[4], B[4];
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {   // A row a = m: bytes i0 - m + 16 h .. + 15, dword-aligned loads
+            const uint32_t* w =
+                reinterpret_cast<const uint32_t*>(base + p * a.plane + i0 - m + 16 * h - off);
+            const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], w3 = w[3], w4 = w[4];
+            A[p][0] = (int)__builtin_amdgcn_alignbyte(w1, w0, off);
+            A[p][1] = (int)__builtin_amdgcn_alignbyte(w2, w1, off);
+            A[p][2] = (int)__builtin_amdgcn_alignbyte(w3, w2, off);
+            A[p][3] = (int)__builtin_amdgcn_alignbyte(w4, w3, off);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q)   // B column b = m: bytes i0 + T0 + 32 m + 16 h .. + 15 (aligned)
+            B[q] = *reinterpret_cast<const v4i*>(base + q * a.plane + i0 + t0 + 32 * m + 16 * h);
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                acc[p + q] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[p], B[q], acc[p + q], 0, 0, 0);
+        if (++since == kMfmaFlush) {   // each group sum stays below 2^31 over kMfmaFlush steps
+            since = 0;
+#pragma unroll
+            for (int g = 6; g >= 0; --g)
+#pragma unroll
+                for (int j = 0; j < 16; ++j) r[j] += ldexp((double)acc[g][j], 8 * g);
+#pragma unroll
+            for (int g = 0; g < 7; ++g)
+                acc[g] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+        }
+    }
+#pragma unroll
+    for (int g = 6; g >= 0; --g)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) r[j] += ldexp((double)acc[g][j], 8 * g);
+    // D(T) = (E - tail(T)) + (E - head(T)) - 2 r(T), scaled back by 2^-2s
+    const double e = a.qstat[4 * s + 3];
+    const int sc = (int)a.qstat[4 * s + 1];
+    const double* __restrict__ ed = a.edge + s * 2 * ((int64_t)a.tmax + 1);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {   // register j of lane (m, h): row 8 (j / 4) + 4 h + j % 4, column m
+        const int row = 8 * (j >> 2) + 4 * h + (j & 3);
+        const int64_t t = (int64_t)t0 + 32 * m + row;
+        if (t < a.tmin || t > a.tmax) continue;
+        const double d = ((e - ed[a.tmax + 1 + t]) + (e - ed[t])) - 2.0 * r[j];
+        const double dy = ldexp(d, -2 * sc);
+        const int64_t k = s * a.lags + (t - a.tmin);
+        if (a.s64) {   // the finalisation of a single channel, in its own arithmetic
+            const double v = 0.0 + (double)a.w0 * (dy / (double)(a.n - t));
+            a.s64[k] = v;
+            if (a.scores) a.scores[k] = (float)v;
+        } else {
+            a.part[k] = dy;
+        }
+    }
+}
+
+struct MfixArgs {
+    const float* x;
+    const double* qstat;
+    double* s64;
+    float* scores;
+    uint32_t* tier1;
+    WinState* state;
+    int64_t n, window_stride, channel_stride;
+    int32_t num_channels, tmin, tmax, lags, words, t0;
+    double tau0;
+};
+
+// One workgroup per window.  Per channel (X units): the rounding of E and of
+// the edge sums (each within gamma_{N+1} E), of the three operations forming
+// D, and of the fp64 sum of the shift groups into r (7 additions per flush,
+// over terms whose magnitudes sum to at most (N - T) 2^62 1.008, because a
+// balanced four-digit X has sum_p 256^p |d_p| < 2^31 1.004) give R, lag-
+// independent with N - T <= N.  An inexact sequence adds the quantisation:
+// with |X_i - 2^s (x_i - c)| <= 1/2 + 2^-23, D_X - 2^2s D is at most
+// 4 sqrt(m D_X) + 6 m over m = N - T pairs.  D_X is bounded through the
+// computed score: w_c D_c <= m S + sum_c' w_c' R_c'.  Lags whose total bound,
+// divided by m, exceeds tau0 / 2 of the score (the other half covers the
+// finalisation and the fp32 output) are re-scored by a wavefront in fp64 and
+// marked tier 1; so is every score of exactly zero.
+__global__ __launch_bounds__(kThreads) void mfma_fixup_kernel(MfixArgs a, Weights w) {
+    __shared__ double rr[kMaxChannels], qa[kMaxChannels], qb[kMaxChannels];
+    __shared__ double total_r;
+    const int64_t b = blockIdx.x;
+    const int64_t n = a.n;
+    const double u = 1.1102230246251565e-16;
+    const double steps = (double)((n + 62) / 32);
+    const double flushes = floor(steps / (double)kMfmaFlush) + 2.0;
+    for (int32_t c = threadIdx.x; c < a.num_channels; c += kThreads) {
+        const int64_t sq = b * a.num_channels + c;
+        const double sc = a.qstat[4 * sq + 1];
+        const double e = a.qstat[4 * sq + 3];
+        const double round_x = u * (4.04 * ((double)n + 1.0) + 12.0) * e +
+                               2.0 * 7.0 * flushes * u * 1.01 * (double)n * ldexp(1.008, 62);
+        rr[c] = 1.01 * ldexp(round_x, -2 * (int)sc);
+        const bool inexact = a.qstat[4 * sq + 2] == 0.0;
+        qa[c] = inexact ? 1.01 * 4.0 * ldexp(1.0, -(int)sc) : 0.0;
+        qb[c] = inexact ? 1.01 * 6.0 * ldexp(1.0, -2 * (int)sc) : 0.0;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double acc = 0.0;
+        for (int32_t c = 0; c < a.num_channels; ++c) acc += (double)w.w[c] * rr[c];
+        total_r = acc * (1.0 + 1e-12);
+    }
+    __syncthreads();
+    const double ar = total_r;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x >> 6;
+    const float* __restrict__ xw = a.x + b * a.window_stride;
+    for (int32_t j0 = wave * kWave; j0 < a.lags; j0 += kThreads) {
+        const int32_t j = j0 + lane;
+        bool fix = false;
+        if (j < a.lags) {
+            const int64_t t = (int64_t)a.tmin + j;
+            const double m = (double)(n - t);
+            const double v = a.s64[b * a.lags + j];
+            double bound = ar;
+            for (int32_t c = 0; c < a.num_channels; ++c) {
+                if (qa[c] == 0.0) continue;
+                const double wc = (double)w.w[c];
+                const double dup = (m * fmax(v, 0.0) * (1.0 + 1e-12) + ar) / wc + rr[c];
+                bound += wc * (qa[c] * sqrt(m * dup) + qb[c] * m);
+            }
+            fix = !(bound * (1.0 + 1e-12) / m <= 0.5 * a.tau0 * v);
+        }
+        uint64_t mask = __ballot(fix);
+        while (mask) {
+            const int k = __builtin_ctzll(mask);
+            mask &= mask - 1;
+            const int32_t jj = j0 + k;
+            const int64_t t = (int64_t)a.tmin + jj;
+            const double v =
+                exact::wave_score(xw, a.num_channels, a.channel_stride, n, t, w, lane);
+            if (lane == 0) {
+                a.s64[b * a.lags + jj] = v;
+                if (a.scores) a.scores[b * a.lags + jj] = (float)v;
+                atomicOr(&a.tier1[b * a.words + (jj >> 5)], 1u << (jj & 31));
+                atomicAdd(&a.state[b].rescored, 1);
+            }
+        }
+    }
+}
+
+MfmaArgs args_of(const Plan& p, const float* x, double* qstat, int8_t* dig, double* edge,
+                 double* part) {
+    MfmaArgs a;
+    a.x = x;
+    a.qstat = qstat;
+    a.dig = dig;
+    a.edge = edge;
+    a.part = part;
+    a.s64 = nullptr;
+    a.scores = nullptr;
+    a.w0 = 1.0f;
+    a.seqs = p.num_windows * (int64_t)p.num_channels;
+    a.n = p.n;
+    a.window_stride = p.window_stride;
+    a.channel_stride = p.channel_stride;
+    a.plane = p.mfma_plane;
+    a.num_channels = p.num_channels;
+    a.tmin = p.tmin;
+    a.tmax = p.tmax;
+    a.lags = p.lags;
+    a.t0 = p.mfma_t0;
+    a.tiles = p.mfma_tiles;
+    return a;
+}
+
+}  // namespace
+
+hipError_t launch_mfma_scores(const Plan& p, const float* x, double* qstat, int8_t* dig,
+                              double* edge, double* part, double* s64, float* scores, float w0,
+                              hipStream_t s) {
+    MfmaArgs a = args_of(p, x, qstat, dig, edge, part);
+    if (mfma_fused_finalize(p)) {
+        a.s64 = s64;
+        a.scores = scores;
+        a.w0 = w0;
+    }
+    hipLaunchKernelGGL(mfma_prep_kernel, dim3((unsigned)a.seqs), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(mfma_edge_kernel, dim3((unsigned)(2 * a.seqs)), dim3(kThreads), 0, s, a);
+    const int64_t groups = (p.mfma_tiles + 3) / 4;
+    hipLaunchKernelGGL(mfma_xcorr_kernel, dim3((unsigned)(a.seqs * groups)), dim3(kThreads), 0,
+                       s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_mfma_fixup(const Plan& p, const Weights& w, const float* x,
+                             const double* qstat, double* s64, float* scores,
+                             const SelectBuffers& sb, hipStream_t s) {
+    MfixArgs a;
+    a.x = x;
+    a.qstat = qstat;
+    a.s64 = s64;
+    a.scores = scores;
+    a.tier1 = sb.tier1;
+    a.state = sb.state;
+    a.n = p.n;
+    a.window_stride = p.window_stride;
+    a.channel_stride = p.channel_stride;
+    a.num_channels = p.num_channels;
+    a.tmin = p.tmin;
+    a.tmax = p.tmax;
+    a.lags = p.lags;
+    a.words = p.bitmap_words;
+    a.t0 = p.mfma_t0;
+    a.tau0 = kScoreRelBound;
+    hipLaunchKernelGGL(mfma_fixup_kernel, dim3((unsigned)p.num_windows), dim3(kThreads), 0, s, a,
+                       w);
+    return hipGetLastError();
+}
+
+}  // namespace gpoeo

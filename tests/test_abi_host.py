@@ -98,7 +98,7 @@ def test_workspace_size_valid_and_monotone(lib):
     dict(n=7, tmin=1, tmax=3), dict(tmin=0), dict(tmin=5, tmax=6), dict(tmax=2049),
     dict(window_stride=0), dict(channel_stride=4095), dict(window_stride=-1),
     dict(c_lag=0.0), dict(c_lag=1.0), dict(c_lag=float("nan")), dict(err_max=float("nan")),
-    dict(flags=8), dict(flags=4, n=4 << 20, tmax=2 << 20),
+    dict(flags=16), dict(flags=4, n=4 << 20, tmax=2 << 20),
     # grids that would exceed HIP's 32-bit global size: 2^24 sequences of 256
     # threads, 2^26 lag-score waves of 64
     dict(num_windows=1 << 20, num_channels=16, n=64, tmax=32, window_stride=1024,
@@ -259,6 +259,31 @@ def test_fft_plan(lib):
     # rolling accepts the FFT flag
     d, _ = good_desc(flags=B.FFT_SCORES)
     assert B.rolling_workspace_bytes(d, B.rolling_params()) > 0
+
+
+def test_mfma_plan(lib):
+    d, _ = good_desc(flags=B.MFMA_SCORES)
+    info = B.describe_plan(d)
+    # lags 2..1024 from tile start 0: two tiles of 1024 lags per sequence
+    assert info["mode"] == 3 and info["score_waves"] == 4 * 2 * 2
+    assert info["pairs_defined"] == 4 * 2 * sum(4096 - t for t in range(2, 1025))
+    # four int8 digit planes per sequence (padded), edge sums, per-sequence statistics
+    assert info["workspace_bytes"] >= 4 * 2 * 4 * 4096 + 4 * 2 * 2 * 1025 * 8
+    assert info["fft_len"] == 0
+    # tiles start at Tmin rounded down to a multiple of 16
+    d, _ = good_desc(flags=B.MFMA_SCORES, tmin=1021, tmax=2045)
+    assert B.describe_plan(d)["score_waves"] == 4 * 2 * 2          # 1008 .. 3055
+    d, _ = good_desc(flags=B.MFMA_SCORES, tmin=1024, tmax=2047)
+    assert B.describe_plan(d)["score_waves"] == 4 * 2 * 1
+    # one score source per call, and whole windows only (no rolling)
+    d, _ = good_desc(flags=B.MFMA_SCORES | B.FFT_SCORES)
+    with pytest.raises(B.GpoeoError) as e:
+        B.workspace_bytes(d)
+    assert e.value.status == B.EINVAL
+    d, _ = good_desc(flags=B.MFMA_SCORES)
+    with pytest.raises(B.GpoeoError) as e:
+        B.rolling_workspace_bytes(d, B.rolling_params())
+    assert e.value.status == B.EINVAL
 
 
 @pytest.mark.parametrize("kw", [dict(c_peak=0.0), dict(c_peak=1.0), dict(max_candidates=0),

@@ -33,10 +33,10 @@ def _check(det, ref, where):
         assert torch.equal(s, ref[0]), f"{where}: scores differ"
 
 
-@pytest.mark.parametrize("fft", [False, True])
+@pytest.mark.parametrize("mode", ["direct", "fft", "mfma"])
 @pytest.mark.parametrize("name,kw", [("w1", {}), ("w3", dict(traces=4, n=32768, tmax=4096,
                                                               pmax=3000))])
-def test_detect_captured_and_replayed(name, kw, fft):
+def test_detect_captured_and_replayed(name, kw, mode):
     import paper_2201_01684_amd as pkg
     dev = _device()
     wl = make_workload(name, **kw)
@@ -45,7 +45,8 @@ def test_detect_captured_and_replayed(name, kw, fft):
     x = xa.clone()
     desc, keep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
                                wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights,
-                               flags=pkg.FFT_SCORES if fft else 0)
+                               flags={"direct": 0, "fft": pkg.FFT_SCORES,
+                                      "mfma": pkg.MFMA_SCORES}[mode])
     det = pkg.Detector(x, desc, keep)
     det.run()
     ref_a = _snapshot(det)
@@ -75,7 +76,7 @@ def test_detect_captured_and_replayed(name, kw, fft):
         if det.scores is not None:
             det.scores.zero_()
         g.replay()
-        _check(det, ref, f"{name} fft={fft} replay {k}")
+        _check(det, ref, f"{name} {mode} replay {k}")
 
 
 def test_rolling_captured_and_replayed():

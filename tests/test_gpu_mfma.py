@@ -1,0 +1,182 @@
+"""GPU parity of the matrix-core scores (GPOEO_PD_MFMA_SCORES) against the fp64 oracle.
+
+The path promises every score within 1.25e-5 relative of the exact value
+(half the direct path's tier-0 width; lags its bound cannot certify are
+re-scored in fp64 first), exact zeros where the oracle has them, and
+selections identical to the oracle's.  On sequences whose samples the
+integer scaling represents exactly (every workload here but the normalised
+counters of w5) the only error left is the fp64 combination, so their scores
+are held to the fp32 output rounding.  Covered: the smallest windows, ragged
+N, lag ranges that start inside a tile and end on, before and after a tile
+boundary, weighted channels at different scales, samples spanning many
+binades (inexact, bounded), exactly periodic and constant windows, scores
+only, determinism, and the five workloads at full size (sampled windows
+against the oracle, every window against the direct path).
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+import oracle  # noqa: E402
+from gen import make_workload, planted_trace  # noqa: E402
+
+from test_gpu_parity import check_results, gpu_run  # noqa: E402
+
+MFMA_RTOL = 1.25e-5 + 2.0 ** -24     # the fix-up's bound plus the fp32 output rounding
+EXACT_RTOL = 1e-7                    # exactly represented samples: fp64 combination + fp32 output
+
+
+def mfma_flag():
+    import paper_2201_01684_amd as pkg
+    return pkg.MFMA_SCORES
+
+
+def check_mfma_scores(g, o, where="", rtol=MFMA_RTOL):
+    assert g.shape == o.shape
+    zero = o == 0
+    assert np.all(g[zero] == 0), f"{where}: zero scores not reproduced"
+    rel = np.abs(g - o)[~zero] / np.abs(o[~zero])
+    assert rel.size == 0 or rel.max() <= rtol, f"{where}: rel {rel.max():.3e}"
+    return float(rel.max()) if rel.size else 0.0
+
+
+def mfma_parity(x, lay, where="", flags=0, rtol=MFMA_RTOL):
+    g, res = gpu_run(x, lay, flags=mfma_flag() | flags)
+    o, out = oracle.detect(x, lay)
+    check_mfma_scores(g, o, where, rtol)
+    if res is not None:
+        check_results(res, out, where)
+    return g, res, out
+
+
+@pytest.mark.parametrize("n,tmin,tmax", [
+    (8, 1, 4),            # the smallest window: one tile, two steps
+    (100, 2, 50),
+    (1500, 2, 500),
+    (4099, 3, 2049),      # ragged N, three tiles
+    (3000, 1021, 1500),   # first tile starts at 1008, below Tmin
+    (5000, 2, 1023),      # Tmax on the last lag of the first tile
+    (5000, 2, 1024),      # Tmax the first lag of a second tile
+    (5000, 17, 2047),
+    (20000, 6, 3333),
+])
+def test_edge_shapes(n, tmin, tmax):
+    x = planted_trace(n, max(3, min(97, n // 3)), 3, seed=n + tmin, sigma=1.0)
+    mfma_parity(x, oracle.Layout(1, 1, n, n, n, tmin, tmax), f"n={n} T=[{tmin},{tmax}]",
+                rtol=EXACT_RTOL)
+
+
+@pytest.mark.parametrize("name,kw,rtol", [
+    ("w1", {}, EXACT_RTOL),
+    ("w2", dict(traces=5, n=16384, tmax=2048, pmax=1500), EXACT_RTOL),
+    ("w3", dict(traces=4, n=32768, tmax=4096, pmax=3000), EXACT_RTOL),
+    ("w4", dict(total=131072, n=16384, stride=2048, tmax=4096), EXACT_RTOL),
+    ("w5", dict(traces=3, n=16384, tmax=2048, pmax=1500), MFMA_RTOL),   # normalised counters
+])
+def test_reduced_workloads(name, kw, rtol):
+    wl = make_workload(name, **kw)
+    mfma_parity(wl.x, oracle.Layout.of(wl), f"mfma {name}{kw}", rtol=rtol)
+
+
+def test_weighted_channels_at_different_scales():
+    rng = np.random.default_rng(3)
+    b, c, n = 3, 3, 6000
+    base = np.stack([planted_trace(n, 300 + 17 * k, 6, seed=k, sigma=0.5) for k in range(b)])
+    x = np.stack([base * s + rng.normal(0, 0.3, size=(b, n)) for s in (1.0, 0.01, 30.0)], axis=1)
+    lay = oracle.Layout(b, c, n, c * n, n, 2, 3000,
+                        weights=np.array([1.0, 250.0, 0.003], dtype=np.float32))
+    mfma_parity(x.astype(np.float32), lay, "mfma weighted")
+
+
+def test_samples_over_many_binades():
+    # magnitudes from 1e-6 to 1e3 in one sequence: no power-of-two scaling
+    # represents them in 31 bits, so the quantisation bound decides which lags
+    # are re-scored
+    n = 8192
+    rng = np.random.default_rng(11)
+    p = planted_trace(n, 211, 5, seed=12, sigma=0.5).astype(np.float64)
+    tiny = rng.normal(0, 1e-6, n)
+    x = np.stack([(p + tiny).astype(np.float32),
+                  (p * 10.0 ** rng.uniform(-6, 0, n)).astype(np.float32),
+                  (1e3 + rng.normal(0, 1e-3, n)).astype(np.float32)])
+    g, res, out = mfma_parity(x, oracle.Layout(3, 1, n, n, n, 2, 4096), "mfma binades")
+    assert res["period"][0] == 211
+
+
+def test_exact_periods_and_constant_windows():
+    n = 8192
+    rows = [np.full(n, 123.25, dtype=np.float32),                         # CONSTANT
+            planted_trace(n, 64, 4, seed=1, integer=True),                  # zeros at 64 k
+            planted_trace(n, 301, 9, seed=2, sigma=0.0),                    # real-valued repeats
+            np.random.default_rng(4).normal(0, 1, n).astype(np.float32),
+            np.zeros(n, dtype=np.float32)]
+    x = np.stack(rows)
+    lay = oracle.Layout(len(rows), 1, n, n, n, 2, 4096)
+    g, res, out = mfma_parity(x, lay, "mfma special windows")
+    assert res["period"][1] == 64 and res["period"][2] == 301
+    assert res["verdict"][0] == 2 and res["verdict"][4] == 2
+    assert np.all(g[1, np.arange(64, 4097, 64) - 2] == 0)
+    assert np.all(g[0] == 0) and np.all(g[4] == 0)
+
+
+def test_scores_only_and_no_rescue():
+    import paper_2201_01684_amd as pkg
+    wl = make_workload("w2", traces=4, n=16384, tmax=2048, pmax=1500)
+    lay = oracle.Layout.of(wl)
+    g, _ = gpu_run(wl.x, lay, flags=mfma_flag() | pkg.SCORES_ONLY)
+    o, out = oracle.detect(wl.x, lay)
+    check_mfma_scores(g, o, "mfma scores only", EXACT_RTOL)
+    _, res = gpu_run(wl.x, lay, flags=mfma_flag() | pkg.NO_RESCUE)
+    assert np.all(np.abs(res["period"] - out["period"]) <= 2)
+
+
+def test_deterministic_bitwise():
+    wl = make_workload("w5", traces=2, n=16384, tmax=2048, pmax=1500)
+    lay = oracle.Layout.of(wl)
+    a, ra = gpu_run(wl.x, lay, flags=mfma_flag())
+    b, rb = gpu_run(wl.x, lay, flags=mfma_flag())
+    assert np.array_equal(a, b) and np.array_equal(ra, rb)
+
+
+@pytest.mark.parametrize("name", ["w1", "w2", "w3", "w4", "w5"])
+def test_full_size(name):
+    import paper_2201_01684_amd as pkg
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    wl = make_workload(name)
+    print(f"\n[mfma {name}] {wl.num_windows} windows x {wl.num_channels} ch x {wl.n}", flush=True)
+    x = torch.from_numpy(wl.x).to("cuda:0")
+    out = {}
+    for mode, flags in (("mfma", mfma_flag()), ("direct", 0)):
+        desc, keep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
+                                   wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights,
+                                   flags=flags)
+        det = pkg.Detector(x, desc, keep)
+        det.run()
+        torch.cuda.synchronize()
+        out[mode] = (det.scores.cpu().numpy(), det.results_numpy())
+        del det
+        torch.cuda.empty_cache()
+    del x
+    torch.cuda.empty_cache()
+    gm, rm = out["mfma"]
+    gd, rd = out["direct"]
+    assert np.all(rm["flags"] == 0)
+    for f in ("period", "verdict", "t_cand", "t_low", "t_up", "n_candidates"):
+        assert np.array_equal(rm[f], rd[f]), f"{name}: {f} differs from the direct path"
+    # both within their bounds of the exact scores: 2.5e-5 + 1.25e-5 (+ fp32 rounding)
+    nz = gd != 0
+    assert np.all(gm[~nz] == 0)
+    assert np.all(np.abs(gm[nz].astype(np.float64) - gd[nz]) <= 3.8e-5 * np.abs(gd[nz]))
+    rng = np.random.default_rng(99)
+    lay1 = oracle.Layout.of(wl, num_windows=1)
+    span = (wl.num_channels - 1) * wl.channel_stride + wl.n
+    rtol = MFMA_RTOL if name == "w5" else EXACT_RTOL
+    for b in sorted({0, wl.num_windows - 1, int(rng.integers(0, wl.num_windows))}):
+        sub = wl.x[b * wl.window_stride: b * wl.window_stride + span]
+        o_scores, o_out = oracle.detect(sub, lay1)
+        check_mfma_scores(gm[b:b + 1].astype(np.float64), o_scores, f"mfma {name} window {b}",
+                          rtol)
+        check_results(rm[b:b + 1], o_out, f"mfma {name} window {b}")
