@@ -235,44 +235,63 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
     double r[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) r[j] = 0.0;
-    // steps while some pair (i, i + T) of the tile has i + T < N
+    // Steps while some pair (i, i + T) of the tile has i + T < N, rounded up to
+    // an even count: a step past that reads only the zero padding of B.  The
+    // operands of one step are loaded while the products of the previous one
+    // run (two register sets; the scheduling barriers keep that order).
     const int64_t iend = a.n - t0 + 31;
-    int since = 0;
-    for (int64_t i0 = 0; i0 < iend; i0 += 32) {
-        v4i A[4], B[4];
+    const int64_t steps = ((iend + 31) / 32 + 1) & ~int64_t(1);
+    uint32_t w0[4][5], w1[4][5];
+    v4i b0[4], b1[4];
+    auto load = [&](uint32_t (&w)[4][5], v4i (&bq)[4], int64_t i0) {
 #pragma unroll
         for (int p = 0; p < 4; ++p) {   // A row a = m: bytes i0 - m + 16 h .. + 15, dword-aligned loads
-            const uint32_t* w =
+            const uint32_t* src =
                 reinterpret_cast<const uint32_t*>(base + p * a.plane + i0 - m + 16 * h - off);
-            const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], w3 = w[3], w4 = w[4];
-            A[p][0] = (int)__builtin_amdgcn_alignbyte(w1, w0, off);
-            A[p][1] = (int)__builtin_amdgcn_alignbyte(w2, w1, off);
-            A[p][2] = (int)__builtin_amdgcn_alignbyte(w3, w2, off);
-            A[p][3] = (int)__builtin_amdgcn_alignbyte(w4, w3, off);
+#pragma unroll
+            for (int e = 0; e < 5; ++e) w[p][e] = src[e];
         }
 #pragma unroll
         for (int q = 0; q < 4; ++q)   // B column b = m: bytes i0 + T0 + 32 m + 16 h .. + 15 (aligned)
-            B[q] = *reinterpret_cast<const v4i*>(base + q * a.plane + i0 + t0 + 32 * m + 16 * h);
+            bq[q] = *reinterpret_cast<const v4i*>(base + q * a.plane + i0 + t0 + 32 * m + 16 * h);
+    };
+    auto step = [&](const uint32_t (&w)[4][5], const v4i (&bq)[4]) {
+        v4i A[4];
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            A[p][0] = (int)__builtin_amdgcn_alignbyte(w[p][1], w[p][0], off);
+            A[p][1] = (int)__builtin_amdgcn_alignbyte(w[p][2], w[p][1], off);
+            A[p][2] = (int)__builtin_amdgcn_alignbyte(w[p][3], w[p][2], off);
+            A[p][3] = (int)__builtin_amdgcn_alignbyte(w[p][4], w[p][3], off);
+        }
 #pragma unroll
         for (int p = 0; p < 4; ++p)
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-                acc[p + q] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[p], B[q], acc[p + q], 0, 0, 0);
-        if (++since == kMfmaFlush) {   // each group sum stays below 2^31 over kMfmaFlush steps
-            since = 0;
-#pragma unroll
-            for (int g = 6; g >= 0; --g)
-#pragma unroll
-                for (int j = 0; j < 16; ++j) r[j] += ldexp((double)acc[g][j], 8 * g);
-#pragma unroll
-            for (int g = 0; g < 7; ++g)
-                acc[g] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+                acc[p + q] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[p], bq[q], acc[p + q], 0, 0, 0);
+    };
+    for (int64_t k0 = 0; k0 < steps; k0 += kMfmaFlush) {
+        // each group sum stays below 2^31 over kMfmaFlush steps (an even count)
+        const int64_t k1 = min(steps, k0 + (int64_t)kMfmaFlush);
+        load(w0, b0, 32 * k0);
+        for (int64_t k = k0; k < k1; k += 2) {
+            load(w1, b1, 32 * (k + 1));
+            __builtin_amdgcn_sched_barrier(0);
+            step(w0, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            load(w0, b0, 32 * (k + 2));
+            __builtin_amdgcn_sched_barrier(0);
+            step(w1, b1);
+            __builtin_amdgcn_sched_barrier(0);
         }
+#pragma unroll
+        for (int g = 6; g >= 0; --g)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) r[j] += ldexp((double)acc[g][j], 8 * g);
+#pragma unroll
+        for (int g = 0; g < 7; ++g)
+            acc[g] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
     }
-#pragma unroll
-    for (int g = 6; g >= 0; --g)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) r[j] += ldexp((double)acc[g][j], 8 * g);
     // D(T) = (E - tail(T)) + (E - head(T)) - 2 r(T), scaled back by 2^-2s
     const double e = a.qstat[4 * s + 3];
     const int sc = (int)a.qstat[4 * s + 1];
