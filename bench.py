@@ -27,6 +27,10 @@ sys.path.insert(0, ROOT)
 FP32_VECTOR_PEAK_TFLOPS = 157.3   # MI355X published FP32 vector peak
 FP64_VECTOR_PEAK_TFLOPS = 78.6    # MI355X published FP64 vector peak
 HBM_PEAK_GBS = 8000.0              # MI355X published HBM3E bandwidth
+INT8_MFMA_PEAK_TOPS = 5000.0       # MI355X published dense int8 matrix peak
+# Matrix-core scores: 16 digit-pair products (four int8 digits per sample on
+# each side) per (x[i], x[i+T]) pair, one multiply and one add each.
+MFMA_OPS_PER_PAIR = 32
 # Algorithmic fp64 FLOP of the EM per (sample, component, iteration): the
 # log-density (sub, mul, mul, sub), the exponential (counted as one), the
 # normalisation (add, mul) and the three moments (add; mul, add; mul, mul, add).
@@ -49,11 +53,13 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=("detect", "fft", "rolling", "similarity", "centred",
-                                       "spectral"),
+    ap.add_argument("--mode", choices=("detect", "fft", "mfma", "rolling", "similarity",
+                                       "centred", "spectral"),
                     default="detect",
                     help="detect: gpoeo_pd_detect (the default measurement); fft: the same "
                          "call with GPOEO_PD_FFT_SCORES (fp64 FFT autocorrelation scores); "
+                         "mfma: the same call with GPOEO_PD_MFMA_SCORES (integer "
+                         "cross-correlation on the int8 matrix cores); "
                          "rolling: "
                          "Algorithm 3's rolling detection, gpoeo_pd_detect_rolling; "
                          "similarity: Algorithm 2's grouped similarity of 5 finalist periods "
@@ -61,9 +67,11 @@ def parse():
                          "centred: the mean-removed score of the same 5 finalists; "
                          "spectral: Algorithm 1's FFT front end (candidate periods)")
     ap.add_argument("--graph", action="store_true",
-                    help="detect/fft mode: also time replays of one call captured in a HIP graph")
+                    help="detect/fft/mfma mode: also time replays of one call captured in a HIP "
+                         "graph")
     ap.add_argument("--no-fft-compare", action="store_true",
-                    help="detect mode: skip the untimed FFT-scores run of the same batch")
+                    help="detect mode: skip the untimed FFT- and matrix-core-scores runs of the "
+                         "same batch")
     ap.add_argument("--fft-scores", action="store_true",
                     help="rolling mode: score with GPOEO_PD_FFT_SCORES")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -285,9 +293,10 @@ def main():
     pairs = wl.pairs()
     x = torch.from_numpy(wl.x).to(dev)
     fft = args.mode == "fft"
+    mfma = args.mode == "mfma"
     desc, keep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
                                wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights,
-                               flags=pkg.FFT_SCORES if fft else 0)
+                               flags=pkg.FFT_SCORES if fft else (pkg.MFMA_SCORES if mfma else 0))
     det = pkg.Detector(x, desc, keep, want_scores=True)
     plan = pkg.describe_plan(desc)
     scored = plan["pairs_scored"]
@@ -327,6 +336,14 @@ def main():
                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": fft_bytes / (score_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
                     "traffic": None, "bytes_per_launch": fft_bytes}
+    elif mfma:
+        ops = MFMA_OPS_PER_PAIR * scored
+        roofline = {"kernel": "mfma_xcorr_kernel (score stage: digit preparation, edge sums, "
+                              "matrix-core lag tiles)", "bound": "mfma",
+                    "achieved": ops / (score_ms / 1e3) / 1e12, "peak": INT8_MFMA_PEAK_TOPS,
+                    "unit": "TOP/s", "frac": ops / (score_ms / 1e3) / 1e12 / INT8_MFMA_PEAK_TOPS,
+                    "traffic": None, "ops_per_launch": ops,
+                    "fp32_equivalent_tflops": FLOP_PER_PAIR * scored / (score_ms / 1e3) / 1e12}
     else:
         roofline = {"kernel": "lag_score_kernel", "bound": "alu", "achieved": achieved,
                     "peak": FP32_VECTOR_PEAK_TFLOPS, "unit": "TFLOP/s",
@@ -338,7 +355,7 @@ def main():
         "value": value,
         "unit": "lag·samples/s",
         "traces_per_sec": wl.num_windows / (ms_per_step / 1e3),
-        "pct_fp32_peak": None if fft else 100.0 * FLOP_PER_PAIR * scored
+        "pct_fp32_peak": None if (fft or mfma) else 100.0 * FLOP_PER_PAIR * scored
                          / (ms_per_step / 1e3) / 1e12 / FP32_VECTOR_PEAK_TFLOPS,
         "n_gpus": 1,
         "steps": args.steps,
@@ -347,13 +364,15 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f64" if fft else "f32",
+        "dtype": "f64" if fft else ("i8" if mfma else "f32"),
         "data": "synthetic",
         "config": {"workload": wl.name, "description": wl.meta["description"],
                    "windows": wl.num_windows, "channels": wl.num_channels, "n": wl.n,
                    "tmin": wl.tmin, "tmax": wl.tmax, "pairs": pairs, "sha256": sha,
                    "scoring": {0: "per window", 1: "shared block partials",
-                               2: "fp64 FFT autocorrelation"}[plan["mode"]],
+                               2: "fp64 FFT autocorrelation",
+                               3: "int8-digit cross-correlation on the matrix cores"}[
+                                   plan["mode"]],
                    "pairs_scored": scored, "lags_per_lane": plan["lags_per_lane"]},
         "call_ms": {"median": float(np.median(call_ms)), "min": float(call_ms.min())},
         "stage_ms": {"window_stats": float(stage_ms[:, 0].mean()),
@@ -379,30 +398,31 @@ def main():
         line["graph_replay"] = {"ms_per_step": g_ms, "value": pairs / (g_ms / 1e3),
                                 "traces_per_sec": wl.num_windows / (g_ms / 1e3)}
         del g
-    if not fft and not args.no_fft_compare:
-        # the same batch with FFT scores (GPOEO_PD_FFT_SCORES), after and outside
-        # the timed region: its time per call and whether every selection matches
-        fdesc, fkeep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
-                                     wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights,
-                                     flags=pkg.FFT_SCORES)
+    if not fft and not mfma and not args.no_fft_compare:
+        # the same batch with FFT scores and with matrix-core scores, after and
+        # outside the timed region: time per call and whether every selection matches
         del det
         torch.cuda.empty_cache()
-        fdet = pkg.Detector(x, fdesc, fkeep, want_scores=False)
-        fdet.run()
-        torch.cuda.synchronize()
-        t = time.perf_counter()
-        for _ in range(args.steps):
-            fdet.run()
-        torch.cuda.synchronize()
-        f_ms = (time.perf_counter() - t) * 1e3 / args.steps
-        fres = fdet.results_numpy()
-        same = all(np.array_equal(fres[k], res[k]) for k in
-                   ("period", "verdict", "t_cand", "t_low", "t_up", "n_candidates"))
-        line["fft_scores"] = {"ms_per_step": f_ms, "value": pairs / (f_ms / 1e3),
-                              "traces_per_sec": wl.num_windows / (f_ms / 1e3),
-                              "selections_equal_direct": bool(same)}
-        del fdet
-        torch.cuda.empty_cache()
+        for key, flag in (("fft_scores", pkg.FFT_SCORES), ("mfma_scores", pkg.MFMA_SCORES)):
+            adesc, akeep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n,
+                                         wl.window_stride, wl.channel_stride, wl.tmin, wl.tmax,
+                                         weights=wl.weights, flags=flag)
+            adet = pkg.Detector(x, adesc, akeep, want_scores=False)
+            adet.run()
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            for _ in range(args.steps):
+                adet.run()
+            torch.cuda.synchronize()
+            a_ms = (time.perf_counter() - t) * 1e3 / args.steps
+            ares = adet.results_numpy()
+            same = all(np.array_equal(ares[k], res[k]) for k in
+                       ("period", "verdict", "t_cand", "t_low", "t_up", "n_candidates"))
+            line[key] = {"ms_per_step": a_ms, "value": pairs / (a_ms / 1e3),
+                         "traces_per_sec": wl.num_windows / (a_ms / 1e3),
+                         "selections_equal_direct": bool(same)}
+            del adet
+            torch.cuda.empty_cache()
     if wl.truth is not None:
         d = wl.truth > 0
         if wl.jitter:

@@ -87,7 +87,8 @@ __device__ float block_min(float v, float* red) {
 
 // One workgroup per sequence.  Pass 1: mean, smallest and largest sample.
 // Pass 2: X_i, its digits, E = sum X_i^2, and whether every X_i 2^-s equals
-// x_i - c exactly.  Also zeroes the padding of the four digit planes.
+// x_i - c exactly.  Also zeroes the padding of the four digit planes (the
+// plane length and kMfmaPadL are multiples of 4 bytes, so are its stores).
 __global__ __launch_bounds__(kThreads) void mfma_prep_kernel(MfmaArgs a) {
     __shared__ double red[kThreads / kWave];
     __shared__ float redf[kThreads / kWave];
@@ -114,32 +115,43 @@ __global__ __launch_bounds__(kThreads) void mfma_prep_kernel(MfmaArgs a) {
     int8_t* __restrict__ d0 = a.dig + s * 4 * a.plane + kMfmaPadL;
     double ex = 0.0;
     int exact = 1;
-    for (int64_t i = threadIdx.x; i < n; i += kThreads) {
-        const double xv = (double)xs[i];
-        const double y = xv - c;
-        const double bb = y - xv;                              // two-sum error of xv + (-c)
-        const double err = (xv - (y - bb)) + (-c - bb);
-        const double t = y * scale;
-        const double q = rint(t);
-        exact &= (err == 0.0 && q == t) ? 1 : 0;
-        ex += q * q;
-        const int32_t v = (int32_t)q;
-        const int32_t g0 = (int32_t)(int8_t)(v & 0xff);
-        const int32_t r1 = (v - g0) >> 8;
-        const int32_t g1 = (int32_t)(int8_t)(r1 & 0xff);
-        const int32_t r2 = (r1 - g1) >> 8;
-        const int32_t g2 = (int32_t)(int8_t)(r2 & 0xff);
-        const int32_t g3 = (r2 - g2) >> 8;
-        d0[i] = (int8_t)g0;
-        d0[a.plane + i] = (int8_t)g1;
-        d0[2 * a.plane + i] = (int8_t)g2;
-        d0[3 * a.plane + i] = (int8_t)g3;
+    // four consecutive samples per thread and step: one 32-bit store per digit
+    // plane (samples past N, in the padding, get zero digits)
+    const int64_t n4 = (n + 3) & ~int64_t(3);
+    for (int64_t i = 4 * (int64_t)threadIdx.x; i < n4; i += 4 * kThreads) {
+        uint32_t word[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (i + k >= n) break;
+            const double xv = (double)xs[i + k];
+            const double y = xv - c;
+            const double bb = y - xv;                          // two-sum error of xv + (-c)
+            const double err = (xv - (y - bb)) + (-c - bb);
+            const double t = y * scale;
+            const double q = rint(t);
+            exact &= (err == 0.0 && q == t) ? 1 : 0;
+            ex += q * q;
+            const int32_t v = (int32_t)q;                      // balanced base-256 digits
+            const int32_t g0 = (int32_t)(int8_t)(v & 0xff);
+            const int32_t r1 = (v - g0) >> 8;
+            const int32_t g1 = (int32_t)(int8_t)(r1 & 0xff);
+            const int32_t r2 = (r1 - g1) >> 8;
+            const int32_t g2 = (int32_t)(int8_t)(r2 & 0xff);
+            const int32_t g3 = (r2 - g2) >> 8;
+            word[0] |= (uint32_t)(g0 & 0xff) << (8 * k);
+            word[1] |= (uint32_t)(g1 & 0xff) << (8 * k);
+            word[2] |= (uint32_t)(g2 & 0xff) << (8 * k);
+            word[3] |= (uint32_t)(g3 & 0xff) << (8 * k);
+        }
+#pragma unroll
+        for (int p = 0; p < 4; ++p) *reinterpret_cast<uint32_t*>(d0 + p * a.plane + i) = word[p];
     }
-    const int64_t pad_r = a.plane - kMfmaPadL - n;
-    for (int64_t k = threadIdx.x; k < 4 * (kMfmaPadL + pad_r); k += kThreads) {
-        const int64_t p = k / (kMfmaPadL + pad_r), j = k % (kMfmaPadL + pad_r);
-        const int64_t i = j < kMfmaPadL ? j - kMfmaPadL : n + (j - kMfmaPadL);
-        d0[p * a.plane + i] = 0;
+    // the rest of the padding: [-kMfmaPadL, 0) and [n4, plane - kMfmaPadL), 4 bytes a store
+    const int64_t pl = kMfmaPadL / 4, pr = (a.plane - kMfmaPadL - n4) / 4;
+    for (int64_t k = threadIdx.x; k < 4 * (pl + pr); k += kThreads) {
+        const int64_t p = k / (pl + pr), j = k % (pl + pr);
+        const int64_t i = j < pl ? 4 * (j - pl) : n4 + 4 * (j - pl);
+        *reinterpret_cast<uint32_t*>(d0 + p * a.plane + i) = 0u;
     }
     const double etot = block_sum(ex, red);
     const double ex_all = block_sum(exact ? 0.0 : 1.0, red);
