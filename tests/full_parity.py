@@ -5,7 +5,8 @@ about 8 minutes of oracle time on 16 host threads).
     python tests/full_parity.py --rolling [w1 w2 w3 w4 w5]
 
 For each workload: one gpoeo_pd_detect call over the whole batch with the
-direct scores and one with GPOEO_PD_FFT_SCORES, then the fp64 oracle on every
+direct scores, one with GPOEO_PD_FFT_SCORES and one with GPOEO_PD_MFMA_SCORES,
+then the fp64 oracle on every
 window (in chunks, printing progress).  Reports, per path, the windows whose
 selection differs from the oracle (period, verdict, T_c, local-search window,
 candidate count), the largest relative score error over every (window, lag),
@@ -47,7 +48,7 @@ def main(names):
               f"sha256 {wl.sha256[:16]}", flush=True)
         x = torch.from_numpy(wl.x).to(dev)
         gpu = {}
-        for mode, flags in (("direct", 0), ("fft", pkg.FFT_SCORES)):
+        for mode, flags in (("direct", 0), ("fft", pkg.FFT_SCORES), ("mfma", pkg.MFMA_SCORES)):
             desc, keep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
                                        wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights,
                                        flags=flags)
@@ -94,7 +95,7 @@ def main(names):
         print(json.dumps(line), flush=True)
         summary[name] = line
     ok = all(s[m]["selection_mismatch"] == 0 and s[m]["zeros_ok"] and s[m]["unresolved"] == 0
-             and s[m]["max_rel"] <= 1e-4 for s in summary.values() for m in ("direct", "fft"))
+             and s[m]["max_rel"] <= 1e-4 for s in summary.values() for m in ("direct", "fft", "mfma"))
     print(json.dumps({"all_windows_match": ok,
                       "oracle_threads": oracle.threads()}), flush=True)
     return 0 if ok else 1
