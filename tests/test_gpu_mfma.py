@@ -10,8 +10,10 @@ are held to the fp32 output rounding.  Covered: the smallest windows, ragged
 N, lag ranges that start inside a tile and end on, before and after a tile
 boundary, weighted channels at different scales, samples spanning many
 binades (inexact, bounded), exactly periodic and constant windows, scores
-only, determinism, and the five workloads at full size (sampled windows
-against the oracle, every window against the direct path).
+only, determinism, 256 channels, windows and channels at odd sample offsets,
+one window of 2^22 samples (sampled lags), and the five workloads at full
+size (sampled windows against the oracle, every window against the direct
+path).
 """
 import numpy as np
 import pytest
@@ -180,3 +182,50 @@ def test_full_size(name):
         check_mfma_scores(gm[b:b + 1].astype(np.float64), o_scores, f"mfma {name} window {b}",
                           rtol)
         check_results(rm[b:b + 1], o_out, f"mfma {name} window {b}")
+
+
+def test_maximum_channel_count():
+    # 256 channels, each with its own weight and scale (several of them inexact)
+    rng = np.random.default_rng(11)
+    b, c, n = 2, 256, 1500
+    x = np.empty((b, c, n), dtype=np.float32)
+    for k in range(c):
+        x[0, k] = planted_trace(n, 97, 5, seed=100 + k, sigma=0.5) * (0.01 + k % 7)
+        x[1, k] = rng.normal(0, 1 + k % 3, n)
+    w = (0.1 + rng.random(c)).astype(np.float32)
+    lay = oracle.Layout(b, c, n, c * n, n, 2, 700, weights=w)
+    g, res, out = mfma_parity(x, lay, "mfma 256 channels")
+    assert res["period"][0] == 97
+
+
+def test_unaligned_strides():
+    # windows and channels at odd sample offsets: the samples are read one by
+    # one, the digit planes stay aligned in the workspace
+    rng = np.random.default_rng(21)
+    n, c, b = 5001, 2, 3
+    cs, ws = n + 3, 2 * (n + 3) + 7
+    x = rng.normal(0, 0.2, size=(b - 1) * ws + (c - 1) * cs + n + 5).astype(np.float32)
+    for k in range(b):
+        for ch in range(c):
+            o = k * ws + ch * cs
+            x[o:o + n] += planted_trace(n, 123 + 40 * k, 6, seed=7 * k + ch, sigma=0.0)
+    lay = oracle.Layout(b, c, n, ws, cs, 3, 2400)
+    g, res, out = mfma_parity(x, lay, "mfma odd strides")
+    assert list(res["period"]) == [123, 163, 203]
+
+
+def test_long_window_sampled_lags():
+    # one window of 2^22 samples, lags to 2^16: sampled lags against the oracle,
+    # the selection against the direct scores
+    n, tmax = 1 << 22, 1 << 16
+    x = planted_trace(n, 3001, 9, seed=21, sigma=2.0)
+    lay = oracle.Layout(1, 1, n, n, n, 2, tmax)
+    g, res = gpu_run(x, lay, flags=mfma_flag())
+    gd, rd = gpu_run(x, lay)
+    for f in ("period", "verdict", "t_cand", "t_low", "t_up", "n_candidates"):
+        assert np.array_equal(res[f], rd[f]), f
+    assert res["period"][0] == 3001
+    rng = np.random.default_rng(2)
+    ts = np.concatenate([rng.integers(2, tmax + 1, size=40), [2, 1023, 1024, 3001, 6002, tmax]])
+    o = oracle.score_list(x, lay, np.zeros(ts.size, dtype=np.int64), ts)
+    check_mfma_scores(g[0, ts - 2].astype(np.float64), o, "mfma 2^22 samples", EXACT_RTOL)
