@@ -40,8 +40,15 @@ EM_FLOP = 13
 CENTRED_FLOP = 7
 FLOP_PER_PAIR = 3                 # one subtraction, one multiply, one add per (x[i], x[i+T])
 METRIC = "lag·samples/sec and traces/sec for batched period detection; % FP32 peak"
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "lag_score_w3_counters.txt")
-SCORE_SOURCE = os.path.join(ROOT, "paper_2201_01684_amd", "csrc", "lag_score.hip")
+CSRC = os.path.join(ROOT, "paper_2201_01684_amd", "csrc")
+# committed rocprofv3 HBM counter summaries per score mode (w3), and the source
+# whose hash they were taken with
+COUNTERS = {"detect": (os.path.join(ROOT, "profiles", "lag_score_w3_counters.txt"),
+                       os.path.join(CSRC, "lag_score.hip")),
+            "fft": (os.path.join(ROOT, "profiles", "fft_stage_w3_counters.txt"),
+                    os.path.join(CSRC, "fft_score.hip")),
+            "mfma": (os.path.join(ROOT, "profiles", "mfma_xcorr_w3_counters.txt"),
+                     os.path.join(CSRC, "mfma_score.hip"))}
 
 
 def parse():
@@ -151,22 +158,23 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def counters_traffic(workload: str):
-    """HBM bytes per lag-score launch from the committed rocprofv3 counter summary
-    (FETCH_SIZE and WRITE_SIZE scaled by a copy kernel of known size), or None
-    if the summary is missing, covers another workload, or the kernel source
-    changed since the counters were taken."""
-    if workload != "w3":
+def counters_traffic(workload: str, mode: str = "detect"):
+    """HBM bytes per launch of the mode's score stage from the committed
+    rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE scaled by a copy kernel
+    of known size), or None if the summary is missing, covers another workload,
+    or the kernel source changed since the counters were taken."""
+    if workload != "w3" or mode not in COUNTERS:
         return None
+    counters_file, source = COUNTERS[mode]
     try:
         fields = {}
-        with open(COUNTERS_FILE) as f:
+        with open(counters_file) as f:
             for line in f:
                 if line.startswith("#") or ":" not in line:
                     continue
                 k, v = line.split(":", 1)
                 fields[k.strip()] = v.strip()
-        src = hashlib.sha256(open(SCORE_SOURCE, "rb").read()).hexdigest()
+        src = hashlib.sha256(open(source, "rb").read()).hexdigest()
         if fields.get("source_sha256") != src:
             return None
         return float(fields["hbm_bytes_per_launch"])
@@ -335,14 +343,14 @@ def main():
                     "achieved": fft_bytes / (score_ms / 1e3) / 1e9,
                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": fft_bytes / (score_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
-                    "traffic": None, "bytes_per_launch": fft_bytes}
+                    "traffic": counters_traffic(wl.name, "fft"), "bytes_per_launch": fft_bytes}
     elif mfma:
         ops = MFMA_OPS_PER_PAIR * scored
         roofline = {"kernel": "mfma_xcorr_kernel (score stage: digit preparation, edge sums, "
                               "matrix-core lag tiles)", "bound": "mfma",
                     "achieved": ops / (score_ms / 1e3) / 1e12, "peak": INT8_MFMA_PEAK_TOPS,
                     "unit": "TOP/s", "frac": ops / (score_ms / 1e3) / 1e12 / INT8_MFMA_PEAK_TOPS,
-                    "traffic": None, "ops_per_launch": ops,
+                    "traffic": counters_traffic(wl.name, "mfma"), "ops_per_launch": ops,
                     "fp32_equivalent_tflops": FLOP_PER_PAIR * scored / (score_ms / 1e3) / 1e12}
     else:
         roofline = {"kernel": "lag_score_kernel", "bound": "alu", "achieved": achieved,
