@@ -81,6 +81,8 @@ def parse():
                          "same batch")
     ap.add_argument("--fft-scores", action="store_true",
                     help="rolling mode: score with GPOEO_PD_FFT_SCORES")
+    ap.add_argument("--mfma-scores", action="store_true",
+                    help="rolling mode: score with GPOEO_PD_MFMA_SCORES")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a device-to-device copy of this many MiB (the reference "
                          "kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -227,14 +229,16 @@ def transform_bytes(pairs_lengths, seq_samples: int, seqs: int, lag_counts) -> f
 
 def call_roofline(kernel, bound, work, ms, extra=None):
     """Roofline object of a mode timed as a whole call: `work` is the algorithmic
-    FLOP (bound "alu": fp32 or fp64 given by the kernel) or bytes (bound "hbm")
-    of one call, `ms` the mean call time from HIP events on the call's stream."""
+    FLOP (bound "alu": fp32 or fp64 given by the kernel), int8 matrix operations
+    (bound "mfma") or bytes (bound "hbm") of one call, `ms` the mean call time from HIP events on the call's stream."""
     if bound == "hbm":
         achieved, peak, unit = work / (ms / 1e3) / 1e9, HBM_PEAK_GBS, "GB/s"
+    elif bound == "mfma":   # int8 matrix operations
+        achieved, peak, unit = work / (ms / 1e3) / 1e12, INT8_MFMA_PEAK_TOPS, "TOP/s"
     else:
         peak = FP64_VECTOR_PEAK_TFLOPS if bound == "alu_f64" else FP32_VECTOR_PEAK_TFLOPS
         achieved, unit = work / (ms / 1e3) / 1e12, "TFLOP/s"
-    line = {"kernel": kernel, "bound": "hbm" if bound == "hbm" else "alu",
+    line = {"kernel": kernel, "bound": bound if bound in ("hbm", "mfma") else "alu",
             "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
             "traffic": None, "timed": "whole call (HIP events on its stream)"}
     if extra:
@@ -638,7 +642,8 @@ def bench_rolling(args):
     x = torch.from_numpy(wl.x).to("cuda:0")
     desc, keep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
                                wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights,
-                               flags=pkg.FFT_SCORES if args.fft_scores else 0)
+                               flags=pkg.FFT_SCORES if args.fft_scores
+                               else (pkg.MFMA_SCORES if args.mfma_scores else 0))
     params = pkg.rolling_params()
     det = pkg.RollingDetector(x, desc, params, keep)
     for _ in range(args.warmup):
@@ -674,6 +679,11 @@ def bench_rolling(args):
         roofline = call_roofline("both FFT score passes (whole windows, then suffix windows "
                                  "by length class)", "hbm", work, ev_ms,
                                  {"bytes_per_launch": work})
+    elif args.mfma_scores:
+        work = MFMA_OPS_PER_PAIR * (pairs_a + pairs_c)
+        roofline = call_roofline("mfma_xcorr_kernel, both passes (whole windows, suffix "
+                                 "windows)", "mfma", work, ev_ms,
+                                 {"ops_per_launch": work, "pairs": pairs_a + pairs_c})
     else:
         work = FLOP_PER_PAIR * (pairs_a + pairs_c)
         roofline = call_roofline("lag_score_kernel, both passes (whole windows, suffix "
@@ -683,14 +693,17 @@ def bench_rolling(args):
         "metric": "rolling detections/sec (Algorithm 3 over every window of the batch)",
         "value": wl.num_windows / (ms / 1e3), "unit": "windows/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64" if args.fft_scores else ("i8" if args.mfma_scores else "f32"),
         "data": "synthetic",
         "config": {"workload": wl.name, "description": wl.meta["description"],
                    "windows": wl.num_windows, "channels": wl.num_channels, "n": wl.n,
                    "tmin": wl.tmin, "tmax": wl.tmax, "sha256": wl.sha256,
                    "c_measure": params.c_measure, "step": params.step, "c_eval": params.c_eval,
                    "diff_threshold": params.diff_threshold,
-                   "scoring": "fp64 FFT autocorrelation" if args.fft_scores else "direct"},
+                   "scoring": "fp64 FFT autocorrelation" if args.fft_scores
+                   else ("int8-digit cross-correlation on the matrix cores" if args.mfma_scores
+                         else "direct")},
         "stable_windows": int(np.count_nonzero(res["stable"])),
         "mean_suffix_windows": float(res["n_windows"].mean()),
         "windows_flagged_unresolved": int(np.count_nonzero(res["flags"])),

@@ -66,7 +66,8 @@
  * whose bound exceeds 1.25e-5 of its score (exact zeros included) is
  * recomputed as an fp64 sum before the selection, which then uses the same
  * tier-0 width as the direct scores.  Selections equal those of the direct
- * scores.  Not with GPOEO_PD_FFT_SCORES, and not for rolling detection.
+ * scores.  Not with GPOEO_PD_FFT_SCORES.  Rolling detection takes it too (its
+ * suffix windows come from a window table that every kernel reads).
  *
  * Threading and ownership.  All buffers except `desc` and `desc->channel_weights`
  * are DEVICE memory owned by the caller.  The library never allocates or frees
@@ -249,8 +250,9 @@ typedef struct {
     int64_t starts[GPOEO_PD_ROLLING_MAX];    /* first sample of each suffix window            */
 } gpoeo_pd_rolling_result;
 
-/* Validates desc (flags may hold GPOEO_PD_NO_RESCUE and GPOEO_PD_FFT_SCORES) and params and writes
- * the device workspace size of gpoeo_pd_detect_rolling.  EINVAL if the schedule
+/* Validates desc (flags may hold GPOEO_PD_NO_RESCUE and one of GPOEO_PD_FFT_SCORES and
+ * GPOEO_PD_MFMA_SCORES) and params and writes the device workspace size of
+ * gpoeo_pd_detect_rolling.  EINVAL if the schedule
  * could exceed GPOEO_PD_ROLLING_MAX suffix windows, or if B times the suffix
  * slots per window (floor((2 + c_eval step - c_measure) / step) + 2) exceeds
  * GPOEO_PD_MAX_WINDOWS. */

@@ -113,8 +113,8 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
                      GPOEO_PD_MFMA_SCORES))
         return GPOEO_PD_EINVAL;
     const bool mfma = (d->flags & GPOEO_PD_MFMA_SCORES) != 0;
-    // one score source per call; matrix-core scores take whole windows only
-    if (mfma && ((d->flags & GPOEO_PD_FFT_SCORES) || ragged)) return GPOEO_PD_EINVAL;
+    // one score source per call
+    if (mfma && (d->flags & GPOEO_PD_FFT_SCORES)) return GPOEO_PD_EINVAL;
     if (d->num_windows < 1 || d->num_windows > GPOEO_PD_MAX_WINDOWS) return GPOEO_PD_EINVAL;
     if (d->num_channels < 1 || d->num_channels > kMaxChannels) return GPOEO_PD_EINVAL;
     if (d->n < 8 || d->n > (int64_t(1) << 40)) return GPOEO_PD_EINVAL;
@@ -253,6 +253,7 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
         p->fft_pairs = (bc + 1) / 2;
     }
     p->mfma = mfma;
+    p->mfma_table = mfma && ragged;
     if (p->mfma) {   // as FFT plans: one D(T) per (window, channel, lag)
         p->t0 = d->tmin;
         p->lags_padded = p->lags;
@@ -417,7 +418,7 @@ int run_plan(const gpoeo::Plan& p, const gpoeo::Weights& w, const float* x, floa
                                       scores, w.w[0], stream) != hipSuccess)
             return GPOEO_PD_EHIP;
         if (!mark(2)) return GPOEO_PD_EHIP;
-        if ((!gpoeo::mfma_fused_finalize(p) &&
+        if ((!gpoeo::mfma_fused_finalize(p, scores != nullptr) &&
              gpoeo::launch_finalize(p, w, c.part, c.s64, scores, stream) != hipSuccess) ||
             gpoeo::launch_select_init(p, c.sb, stream) != hipSuccess ||
             gpoeo::launch_mfma_fixup(p, w, x, qstat, c.s64, scores, c.sb, stream) != hipSuccess)

@@ -155,6 +155,7 @@ struct Plan {
     // mfma_plane bytes (padded); lag tiles of kMfmaTileLags from mfma_t0
     // (Tmin rounded down to a multiple of 16).
     bool mfma;
+    bool mfma_table;         // windows from a table (rolling suffixes)
     int32_t mfma_t0, mfma_tiles;
     int64_t mfma_plane;
     double c_lag, err_max;
@@ -249,9 +250,13 @@ hipError_t launch_fft_fixup(const Plan& p, const Weights& w, const float* x, con
 
 // Matrix-core scores: per sequence the centre, scale and exactness (qstat
 // [S][4]), the digit planes, the edge sums and D(T) into `part`, or with one
-// channel S(T) straight into s64 and scores (nullable).  Then the fix-up of
-// the lags whose bound exceeds half the tier-0 width, before the selection.
-inline bool mfma_fused_finalize(const Plan& p) { return p.mfma && p.num_channels == 1; }
+// channel S(T) straight into s64 and scores (nullable; not for a window table
+// with fp32 scores requested, whose lags past a window's own Tmax the
+// finalisation zeroes).  Then the fix-up of the lags whose bound exceeds half
+// the tier-0 width, before the selection.
+inline bool mfma_fused_finalize(const Plan& p, bool with_scores) {
+    return p.mfma && p.num_channels == 1 && (!p.mfma_table || !with_scores);
+}
 hipError_t launch_mfma_scores(const Plan& p, const float* x, double* qstat, int8_t* dig,
                               double* edge, double* part, double* s64, float* scores, float w0,
                               hipStream_t s);

@@ -51,10 +51,19 @@ struct MfmaArgs {
     float w0;
     int64_t seqs, n, window_stride, channel_stride, plane;
     int32_t num_channels, tmin, tmax, lags, t0, tiles;
+    WindowTable tab;     // per-window offsets, lengths and Tmax (rolling suffixes), or null
 };
 
 __device__ __forceinline__ const float* seq_ptr(const MfmaArgs& a, int64_t s) {
-    return a.x + (s / a.num_channels) * a.window_stride + (s % a.num_channels) * a.channel_stride;
+    return a.x + table_off(a.tab, s / a.num_channels, a.window_stride) +
+           (s % a.num_channels) * a.channel_stride;
+}
+// samples of sequence s (0: an empty slot of a window table) and its largest lag
+__device__ __forceinline__ int64_t seq_n(const MfmaArgs& a, int64_t s) {
+    return table_n(a.tab, s / a.num_channels, a.n);
+}
+__device__ __forceinline__ int64_t seq_tmax(const MfmaArgs& a, int64_t s) {
+    return min((int64_t)table_tmax(a.tab, s / a.num_channels, a.tmax), (int64_t)a.tmax);
 }
 
 // The integer sample of x under centre c and scale 2^s (the same expression in
@@ -94,7 +103,14 @@ __global__ __launch_bounds__(kThreads) void mfma_prep_kernel(MfmaArgs a) {
     __shared__ float redf[kThreads / kWave];
     const int64_t s = blockIdx.x;
     const float* __restrict__ xs = seq_ptr(a, s);
-    const int64_t n = a.n;
+    const int64_t n = seq_n(a, s);
+    if (n == 0) {   // an empty slot: nothing reads its planes
+        if (threadIdx.x == 0) {
+            a.qstat[4 * s] = a.qstat[4 * s + 1] = a.qstat[4 * s + 3] = 0.0;
+            a.qstat[4 * s + 2] = 1.0;
+        }
+        return;
+    }
     double sum = 0.0;
     float mn = INFINITY, mx = -INFINITY;
     for (int64_t i = threadIdx.x; i < n; i += kThreads) {
@@ -174,11 +190,12 @@ __global__ __launch_bounds__(kThreads) void mfma_edge_kernel(MfmaArgs a) {
     const int64_t s = blockIdx.x >> 1;
     const int side = blockIdx.x & 1;
     const float* __restrict__ p = seq_ptr(a, s);
-    const int64_t n = a.n;
+    const int64_t n = seq_n(a, s);
     const double c = a.qstat[4 * s];
     const double scale = ldexp(1.0, (int)a.qstat[4 * s + 1]);
     double* __restrict__ out = a.edge + (s * 2 + side) * ((int64_t)a.tmax + 1);
-    const int64_t span = (int64_t)a.tmax + 1;
+    // T = 0 .. this window's largest lag (nothing for an empty slot)
+    const int64_t span = n > 0 ? seq_tmax(a, s) + 1 : 1;
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     if (threadIdx.x == 0) out[0] = 0.0;
     double carry = 0.0;
@@ -236,8 +253,10 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
     const int groups = (a.tiles + 3) / 4;
     const int64_t s = blockIdx.x / groups;
     const int tile = (int)(blockIdx.x % groups) * 4 + wave;
-    if (tile >= a.tiles) return;
     const int32_t t0 = a.t0 + tile * kMfmaTileLags;
+    const int64_t n = seq_n(a, s);
+    const int64_t tm = seq_tmax(a, s);
+    if (tile >= a.tiles || n == 0 || t0 > tm) return;   // no lag of this window in the tile
     const int8_t* __restrict__ base = a.dig + s * 4 * a.plane + kMfmaPadL;
     const int m = lane & 31, h = lane >> 5;
     const int off = (4 - (m & 3)) & 3;   // byte offset of this lane's A row within its first dword
@@ -251,7 +270,7 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
     // an even count: a step past that reads only the zero padding of B.  The
     // operands of one step are loaded while the products of the previous one
     // run (two register sets; the scheduling barriers keep that order).
-    const int64_t iend = a.n - t0 + 31;
+    const int64_t iend = n - t0 + 31;
     const int64_t steps = ((iend + 31) / 32 + 1) & ~int64_t(1);
     uint32_t w0[4][5], w1[4][5];
     v4i b0[4], b1[4];
@@ -312,12 +331,12 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
     for (int j = 0; j < 16; ++j) {   // register j of lane (m, h): row 8 (j / 4) + 4 h + j % 4, column m
         const int row = 8 * (j >> 2) + 4 * h + (j & 3);
         const int64_t t = (int64_t)t0 + 32 * m + row;
-        if (t < a.tmin || t > a.tmax) continue;
+        if (t < a.tmin || t > tm) continue;   // lags past a table window's own: left unwritten
         const double d = ((e - ed[a.tmax + 1 + t]) + (e - ed[t])) - 2.0 * r[j];
         const double dy = ldexp(d, -2 * sc);
         const int64_t k = s * a.lags + (t - a.tmin);
         if (a.s64) {   // the finalisation of a single channel, in its own arithmetic
-            const double v = 0.0 + (double)a.w0 * (dy / (double)(a.n - t));
+            const double v = 0.0 + (double)a.w0 * (dy / (double)(n - t));
             a.s64[k] = v;
             if (a.scores) a.scores[k] = (float)v;
         } else {
@@ -336,6 +355,7 @@ struct MfixArgs {
     int64_t n, window_stride, channel_stride;
     int32_t num_channels, tmin, tmax, lags, words, t0;
     double tau0;
+    WindowTable tab;
 };
 
 // One workgroup per window.  Per channel (X units): the rounding of E and of
@@ -354,7 +374,9 @@ __global__ __launch_bounds__(kThreads) void mfma_fixup_kernel(MfixArgs a, Weight
     __shared__ double rr[kMaxChannels], qa[kMaxChannels], qb[kMaxChannels];
     __shared__ double total_r;
     const int64_t b = blockIdx.x;
-    const int64_t n = a.n;
+    const int64_t n = table_n(a.tab, b, a.n);
+    if (n == 0) return;   // an empty slot of a window table
+    const int32_t tm = min(table_tmax(a.tab, b, a.tmax), a.tmax);
     const double u = 1.1102230246251565e-16;
     const double steps = (double)((n + 62) / 32);
     const double flushes = floor(steps / (double)kMfmaFlush) + 2.0;
@@ -379,11 +401,12 @@ __global__ __launch_bounds__(kThreads) void mfma_fixup_kernel(MfixArgs a, Weight
     const double ar = total_r;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x >> 6;
-    const float* __restrict__ xw = a.x + b * a.window_stride;
-    for (int32_t j0 = wave * kWave; j0 < a.lags; j0 += kThreads) {
+    const float* __restrict__ xw = a.x + table_off(a.tab, b, a.window_stride);
+    const int32_t nlags = tm - a.tmin + 1;
+    for (int32_t j0 = wave * kWave; j0 < nlags; j0 += kThreads) {
         const int32_t j = j0 + lane;
         bool fix = false;
-        if (j < a.lags) {
+        if (j < nlags) {
             const int64_t t = (int64_t)a.tmin + j;
             const double m = (double)(n - t);
             const double v = a.s64[b * a.lags + j];
@@ -436,6 +459,7 @@ MfmaArgs args_of(const Plan& p, const float* x, double* qstat, int8_t* dig, doub
     a.lags = p.lags;
     a.t0 = p.mfma_t0;
     a.tiles = p.mfma_tiles;
+    a.tab = p.table;
     return a;
 }
 
@@ -445,7 +469,7 @@ hipError_t launch_mfma_scores(const Plan& p, const float* x, double* qstat, int8
                               double* edge, double* part, double* s64, float* scores, float w0,
                               hipStream_t s) {
     MfmaArgs a = args_of(p, x, qstat, dig, edge, part);
-    if (mfma_fused_finalize(p)) {
+    if (mfma_fused_finalize(p, scores != nullptr)) {
         a.s64 = s64;
         a.scores = scores;
         a.w0 = w0;
@@ -478,6 +502,7 @@ hipError_t launch_mfma_fixup(const Plan& p, const Weights& w, const float* x,
     a.words = p.bitmap_words;
     a.t0 = p.mfma_t0;
     a.tau0 = kScoreRelBound;
+    a.tab = p.table;
     hipLaunchKernelGGL(mfma_fixup_kernel, dim3((unsigned)p.num_windows), dim3(kThreads), 0, s, a,
                        w);
     return hipGetLastError();

@@ -14,7 +14,8 @@ whether every oracle zero is reproduced, and the windows flagged UNRESOLVED.
 Prints one JSON line per workload and a final summary line.
 
 With --rolling: one gpoeo_pd_detect_rolling call over the whole batch with
-each scoring, then the oracle's rolling detection on every window; reports the
+each scoring (direct, FFT, matrix cores), then the oracle's rolling detection
+on every window; reports the
 windows whose verdict, T_init, suffix schedule (count, starts, periods),
 selected window and period, stability or next sampling duration differ, the
 largest relative difference of diff and of err, and the flagged windows.
@@ -120,7 +121,7 @@ def main_rolling(names):
               f"sha256 {wl.sha256[:16]}", flush=True)
         x = torch.from_numpy(wl.x).to(dev)
         gpu = {}
-        for mode, flags in (("direct", 0), ("fft", pkg.FFT_SCORES)):
+        for mode, flags in (("direct", 0), ("fft", pkg.FFT_SCORES), ("mfma", pkg.MFMA_SCORES)):
             desc, keep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
                                        wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights,
                                        flags=flags)
@@ -170,7 +171,7 @@ def main_rolling(names):
         print(json.dumps(line), flush=True)
         summary[name] = line
     ok = all(s[m]["mismatch"] == 0 and s[m]["flagged"] == 0 and s[m]["err_rel"] <= 1e-4
-             and s[m]["diff_rel"] <= 1e-6 for s in summary.values() for m in ("direct", "fft"))
+             and s[m]["diff_rel"] <= 1e-6 for s in summary.values() for m in ("direct", "fft", "mfma"))
     print(json.dumps({"all_rolling_windows_match": ok, "oracle_threads": oracle.threads()}),
           flush=True)
     return 0 if ok else 1

@@ -275,15 +275,13 @@ def test_mfma_plan(lib):
     assert B.describe_plan(d)["score_waves"] == 4 * 2 * 2          # 1008 .. 3055
     d, _ = good_desc(flags=B.MFMA_SCORES, tmin=1024, tmax=2047)
     assert B.describe_plan(d)["score_waves"] == 4 * 2 * 1
-    # one score source per call, and whole windows only (no rolling)
+    # one score source per call; rolling detection takes the flag too
     d, _ = good_desc(flags=B.MFMA_SCORES | B.FFT_SCORES)
     with pytest.raises(B.GpoeoError) as e:
         B.workspace_bytes(d)
     assert e.value.status == B.EINVAL
     d, _ = good_desc(flags=B.MFMA_SCORES)
-    with pytest.raises(B.GpoeoError) as e:
-        B.rolling_workspace_bytes(d, B.rolling_params())
-    assert e.value.status == B.EINVAL
+    assert B.rolling_workspace_bytes(d, B.rolling_params()) > B.workspace_bytes(d)
 
 
 @pytest.mark.parametrize("kw", [dict(c_peak=0.0), dict(c_peak=1.0), dict(max_candidates=0),

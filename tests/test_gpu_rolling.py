@@ -3,7 +3,8 @@
 Identical: verdict, T_init, the number of suffix windows and their starts and
 periods, the selected window and period, stability and the next sampling
 duration.  diff to float rounding, err within 1e-4 relative.  Each case runs
-with the direct scores and with the FFT scores; the FFT scores of the suffix
+with the direct scores, the FFT scores and the matrix-core scores (whose
+suffix pass reads the window table in every kernel); the FFT scores of the suffix
 pass give every pair of sequences the transform length its own suffixes need
 (length classes from 2^6 up), so the mixed batches below span several classes,
 both transform shapes (one workgroup, split) and, with an odd channel count,
@@ -19,14 +20,18 @@ import oracle  # noqa: E402
 from gen import make_workload, planted_trace  # noqa: E402
 
 
-def gpu_rolling(x_np, lay, fft=False, **params):
+MODES = ("direct", "fft", "mfma")
+
+
+def gpu_rolling(x_np, lay, mode="direct", **params):
     import paper_2201_01684_amd as pkg
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     x = torch.from_numpy(np.ascontiguousarray(x_np).reshape(-1)).to("cuda:0")
     desc, keep = pkg.make_desc(lay.num_windows, lay.num_channels, lay.n, lay.window_stride,
                                lay.channel_stride, lay.tmin, lay.tmax, lay.c_lag, lay.err_max,
-                               lay.weights, flags=pkg.FFT_SCORES if fft else 0)
+                               lay.weights, flags={"direct": 0, "fft": pkg.FFT_SCORES,
+                                                   "mfma": pkg.MFMA_SCORES}[mode])
     det = pkg.RollingDetector(x, desc, pkg.rolling_params(**params), keep)
     det.run()
     torch.cuda.synchronize()
@@ -50,8 +55,8 @@ def check(g, o, where):
     assert np.all(np.abs(g["err"][nz] - o["err"][nz]) <= 1e-4 * o["err"][nz]), where
 
 
-@pytest.mark.parametrize("fft", [False, True])
-def test_rolling_matches_oracle_on_mixed_batch(fft):
+@pytest.mark.parametrize("mode", MODES)
+def test_rolling_matches_oracle_on_mixed_batch(mode):
     n = 12000
     rows = [planted_trace(n, 250, 7, seed=3, sigma=4.0),              # noisy, stable
             planted_trace(n, 137, 5, seed=4, integer=True),            # exact period
@@ -61,9 +66,9 @@ def test_rolling_matches_oracle_on_mixed_batch(fft):
             planted_trace(n, 1900, 9, seed=7, sigma=2.0)]              # few periods
     x = np.stack(rows).astype(np.float32)
     lay = oracle.Layout(len(rows), 1, n, n, n, 2, n // 2)
-    g = gpu_rolling(x, lay, fft)
+    g = gpu_rolling(x, lay, mode)
     o = oracle.rolling(x, lay)
-    check(g, o, f"mixed fft={fft}")
+    check(g, o, f"mixed {mode}")
     assert g["stable"][1] == 1 and g["period"][1] == 137
     assert o["stable"][2] == 0 and o["smpdur_next"][2] > 0     # the switch is seen
 
@@ -73,13 +78,13 @@ def test_rolling_matches_oracle_on_mixed_batch(fft):
     ("w3", dict(traces=4, n=32768, tmax=8192, pmax=3000)),
     ("w5", dict(traces=3, n=16384, tmax=4096, pmax=1500)),
 ])
-@pytest.mark.parametrize("fft", [False, True])
-def test_rolling_reduced_workloads(name, kw, fft):
+@pytest.mark.parametrize("mode", MODES)
+def test_rolling_reduced_workloads(name, kw, mode):
     wl = make_workload(name, **kw)
     lay = oracle.Layout.of(wl)
-    g = gpu_rolling(wl.x, lay, fft)
+    g = gpu_rolling(wl.x, lay, mode)
     o = oracle.rolling(wl.x, lay)
-    check(g, o, f"{name} fft={fft}")
+    check(g, o, f"{name} {mode}")
 
 
 def test_rolling_fft_periods_across_length_classes():
@@ -92,8 +97,8 @@ def test_rolling_fft_periods_across_length_classes():
     w = np.array([1.0, 0.5, 2.0], dtype=np.float32)
     lay = oracle.Layout(len(periods), 3, n, 3 * n, n, 2, n // 2, weights=w)
     o = oracle.rolling(x, lay)
-    for fft in (False, True):
-        check(gpu_rolling(x, lay, fft), o, f"classes fft={fft}")
+    for mode in MODES:
+        check(gpu_rolling(x, lay, mode), o, f"classes {mode}")
     assert list(o["t_init"]) == periods
 
 
