@@ -162,8 +162,11 @@ __global__ __launch_bounds__(kThreads) void mfma_prep_kernel(MfmaArgs a) {
 #pragma unroll
         for (int p = 0; p < 4; ++p) *reinterpret_cast<uint32_t*>(d0 + p * a.plane + i) = word[p];
     }
-    // the rest of the padding: [-kMfmaPadL, 0) and [n4, plane - kMfmaPadL), 4 bytes a store
-    const int64_t pl = kMfmaPadL / 4, pr = (a.plane - kMfmaPadL - n4) / 4;
+    // the rest of the padding, 4 bytes a store: [-kMfmaPadL, 0) and the kMfmaPadR
+    // bytes after the samples, all that the tile loop reads of a window of n
+    // samples (a window of a table may be shorter than the plane)
+    const int64_t pl = kMfmaPadL / 4;
+    const int64_t pr = min(a.plane - kMfmaPadL - n4, (int64_t)kMfmaPadR) / 4;
     for (int64_t k = threadIdx.x; k < 4 * (pl + pr); k += kThreads) {
         const int64_t p = k / (pl + pr), j = k % (pl + pr);
         const int64_t i = j < pl ? 4 * (j - pl) : n4 + 4 * (j - pl);
