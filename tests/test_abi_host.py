@@ -275,6 +275,13 @@ def test_mfma_plan(lib):
     assert B.describe_plan(d)["score_waves"] == 4 * 2 * 2          # 1008 .. 3055
     d, _ = good_desc(flags=B.MFMA_SCORES, tmin=1024, tmax=2047)
     assert B.describe_plan(d)["score_waves"] == 4 * 2 * 1
+    # a tile grid beyond HIP's 32-bit global size: 2^21 windows x 9 groups of 4
+    # lag tiles x 256 threads
+    d, _ = good_desc(flags=B.MFMA_SCORES, num_windows=1 << 21, num_channels=1, n=65536,
+                     tmax=32768, window_stride=65536, channel_stride=65536)
+    with pytest.raises(B.GpoeoError) as e:
+        B.workspace_bytes(d)
+    assert e.value.status == B.EINVAL
     # one score source per call; rolling detection takes the flag too
     d, _ = good_desc(flags=B.MFMA_SCORES | B.FFT_SCORES)
     with pytest.raises(B.GpoeoError) as e:
