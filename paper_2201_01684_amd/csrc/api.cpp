@@ -95,7 +95,10 @@ bool launches_fit(const Plan& p) {
             if (p.fft_pairs > kMax / 256 / per_pair) return false;
         }
     } else if (p.mfma) {   // statistics and edge sums per sequence, four lag tiles a workgroup
-        if (!fits(2 * seqs, 256) || !fits(seqs * ((p.mfma_tiles + 3) / 4), 256)) return false;
+        if (!fits(2 * seqs, 256) ||
+            !fits(seqs * ((p.mfma_tiles + 3) / 4) * p.mfma_chunks, 256) ||
+            !fits(seqs * ((p.lags + 255) / 256), 256))
+            return false;
     } else if (p.sliding) {
         if (!fits(p.block_tasks, kWave)) return false;
     } else if (!fits(p.tasks, kWave)) {
@@ -261,6 +264,15 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
         p->mfma_t0 = d->tmin & ~15;               // B operand rows 16-byte aligned
         p->mfma_tiles = (d->tmax - p->mfma_t0) / kMfmaTileLags + 1;
         p->mfma_plane = (kMfmaPadL + d->n + kMfmaPadR + 255) / 256 * 256;
+        // steps of the first tile (the most), even; chunks when the waves are few
+        const int64_t steps = ((d->n - p->mfma_t0 + 62) / 32 + 1) & ~int64_t(1);
+        const int64_t waves = bc * (int64_t)p->mfma_tiles;
+        int64_t k = (kMfmaTargetWaves + waves - 1) / waves;
+        k = std::min<int64_t>(k, std::max<int64_t>(1, steps / kMfmaMinChunkSteps));
+        int64_t cs = (steps + k - 1) / k;
+        cs = (cs + 1) & ~int64_t(1);
+        p->mfma_chunk_steps = cs;
+        p->mfma_chunks = (int32_t)((steps + cs - 1) / cs);
     }
     p->bitmap_words = (p->lags + 31) / 32;
 
@@ -279,10 +291,14 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
     }
     if (n_part > (INT64_MAX / 16)) return GPOEO_PD_EINVAL;
     int64_t n_fstat = 0, n_edge = 0, n_tw = 0, n_z = 0, n_cls = 0, n_zw = 0, n_wrap = 0;
-    int64_t n_dig = 0, n_qstat = 0;
+    int64_t n_dig = 0, n_qstat = 0, n_rpart = 0;
     if (p->mfma &&
         (!mul_ok(bc, 4, &n_qstat) || !mul_ok(bc, 2 * ((int64_t)d->tmax + 1), &n_edge) ||
          !mul_ok(bc, 4 * p->mfma_plane, &n_dig) || n_dig > (INT64_MAX / 4)))
+        return GPOEO_PD_EINVAL;
+    if (p->mfma && p->mfma_chunks > 1 &&   // per-chunk cross terms of every tile lag
+        (!mul_ok(bc * p->mfma_chunks, (int64_t)p->mfma_tiles * kMfmaTileLags, &n_rpart) ||
+         n_rpart > (INT64_MAX / 16)))
         return GPOEO_PD_EINVAL;
     if (p->fft) {
         if (!mul_ok(bc, 4, &n_fstat) || !mul_ok(bc, 2 * ((int64_t)d->tmax + 1), &n_edge) ||
@@ -328,6 +344,8 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
     off = align_up(off + (size_t)n_dig);
     p->off_qstat = off;                           // centre, scale, exactness, sum X^2
     off = align_up(off + (size_t)n_qstat * sizeof(double));
+    p->off_rpart = off;                           // per-chunk cross terms (chunked tiles)
+    off = align_up(off + (size_t)n_rpart * sizeof(double));
     p->bytes = off;
     if (!launches_fit(*p)) return GPOEO_PD_EINVAL;
     return GPOEO_PD_OK;
@@ -414,7 +432,8 @@ int run_plan(const gpoeo::Plan& p, const gpoeo::Weights& w, const float* x, floa
         char* ws = static_cast<char*>(workspace);
         double* qstat = reinterpret_cast<double*>(ws + p.off_qstat);
         if (gpoeo::launch_mfma_scores(p, x, qstat, reinterpret_cast<int8_t*>(ws + p.off_dig),
-                                      reinterpret_cast<double*>(ws + p.off_edge), c.part, c.s64,
+                                      reinterpret_cast<double*>(ws + p.off_edge),
+                                      reinterpret_cast<double*>(ws + p.off_rpart), c.part, c.s64,
                                       scores, w.w[0], stream) != hipSuccess)
             return GPOEO_PD_EHIP;
         if (!mark(2)) return GPOEO_PD_EHIP;
@@ -555,7 +574,8 @@ int gpoeo_pd_describe_plan(const gpoeo_pd_desc* desc, gpoeo_pd_plan_info* info) 
     info->mode = p.fft ? 2 : (p.mfma ? 3 : (p.sliding ? 1 : 0));
     info->lags_per_lane = p.lags_per_lane;
     info->score_waves = p.fft ? 0
-                        : p.mfma ? (int64_t)p.num_windows * p.num_channels * p.mfma_tiles
+                        : p.mfma ? (int64_t)p.num_windows * p.num_channels * p.mfma_tiles *
+                                       p.mfma_chunks
                         : (p.sliding ? 2 * p.block_tasks : p.tasks);
     info->workspace_bytes = p.bytes;
     const double wc = (double)p.num_windows * p.num_channels;

@@ -48,6 +48,11 @@ constexpr int kMfmaTileLags = 1024;
 constexpr int kMfmaPadL = 64;
 constexpr int kMfmaPadR = 1344;
 constexpr int kMfmaFlush = 512;
+// A batch with fewer than kMfmaTargetWaves (sequence, lag tile) waves splits
+// each tile's sample steps into chunks of at least kMfmaMinChunkSteps, whose
+// partial cross terms a combination kernel adds in chunk order.
+constexpr int kMfmaTargetWaves = 4096;
+constexpr int kMfmaMinChunkSteps = 64;
 inline int fft_tile_log2(int lg) { return lg <= 2 * (kFftSmallTileLog2 - 1) ? kFftSmallTileLog2 : kFftTileLog2; }
 
 struct Weights {
@@ -157,6 +162,8 @@ struct Plan {
     bool mfma;
     bool mfma_table;         // windows from a table (rolling suffixes)
     int32_t mfma_t0, mfma_tiles;
+    int32_t mfma_chunks;     // sample chunks per tile (1: one wave per tile)
+    int64_t mfma_chunk_steps;   // 32-sample steps per chunk (even)
     int64_t mfma_plane;
     double c_lag, err_max;
     uint32_t flags;
@@ -164,7 +171,8 @@ struct Plan {
     int32_t bitmap_words;    // 32-bit words per window of the exactness bitmap
     // workspace layout (byte offsets, 256-byte aligned)
     size_t off_var, off_s64, off_bits, off_state, off_queue, off_part, off_cut;
-    size_t off_fstat, off_edge, off_tw, off_z, off_cls, off_zw, off_wrap, off_dig, off_qstat, bytes;
+    size_t off_fstat, off_edge, off_tw, off_z, off_cls, off_zw, off_wrap, off_dig, off_qstat,
+        off_rpart, bytes;
 };
 
 // Rolling detection (Algorithm 3).
@@ -258,8 +266,8 @@ inline bool mfma_fused_finalize(const Plan& p, bool with_scores) {
     return p.mfma && p.num_channels == 1 && (!p.mfma_table || !with_scores);
 }
 hipError_t launch_mfma_scores(const Plan& p, const float* x, double* qstat, int8_t* dig,
-                              double* edge, double* part, double* s64, float* scores, float w0,
-                              hipStream_t s);
+                              double* edge, double* rpart, double* part, double* s64,
+                              float* scores, float w0, hipStream_t s);
 hipError_t launch_mfma_fixup(const Plan& p, const Weights& w, const float* x,
                              const double* qstat, double* s64, float* scores,
                              const SelectBuffers& sb, hipStream_t s);

@@ -46,11 +46,13 @@ struct MfmaArgs {
     int8_t* dig;         // [S][4][plane]: digit p of sample i at p * plane + kMfmaPadL + i
     double* edge;        // [S][2][tmax + 1]: head and tail sums of X^2
     double* part;        // [S][lags]: D(T) (unless fused)
+    double* rpart;       // chunked tiles: [S][chunks][tiles * 1024] cross terms from lag t0 on
     double* s64;         // fused finalisation (one channel): S(T)
     float* scores;
     float w0;
     int64_t seqs, n, window_stride, channel_stride, plane;
-    int32_t num_channels, tmin, tmax, lags, t0, tiles;
+    int32_t num_channels, tmin, tmax, lags, t0, tiles, chunks;
+    int64_t chunk_steps;
     WindowTable tab;     // per-window offsets, lengths and Tmax (rolling suffixes), or null
 };
 
@@ -70,6 +72,26 @@ __device__ __forceinline__ int64_t seq_tmax(const MfmaArgs& a, int64_t s) {
 // every kernel, so all of them see the same X).
 __device__ __forceinline__ double quantised(float x, double c, double scale) {
     return rint(((double)x - c) * scale);
+}
+
+// D(T) = (E - tail(T)) + (E - head(T)) - 2 r(T), scaled back by 2^-2s, into
+// part, or with one channel S(T) = w0 D / (N - T) into s64 (and scores), with
+// the finalisation's own operations in its order.
+__device__ __forceinline__ void write_d(const MfmaArgs& a, int64_t s, int64_t n, int64_t t,
+                                        double r) {
+    const double e = a.qstat[4 * s + 3];
+    const int sc = (int)a.qstat[4 * s + 1];
+    const double* __restrict__ ed = a.edge + s * 2 * ((int64_t)a.tmax + 1);
+    const double d = ((e - ed[a.tmax + 1 + t]) + (e - ed[t])) - 2.0 * r;
+    const double dy = ldexp(d, -2 * sc);
+    const int64_t k = s * a.lags + (t - a.tmin);
+    if (a.s64) {
+        const double v = 0.0 + (double)a.w0 * (dy / (double)(n - t));
+        a.s64[k] = v;
+        if (a.scores) a.scores[k] = (float)v;
+    } else {
+        a.part[k] = dy;
+    }
 }
 
 __device__ double block_sum(double v, double* red) {
@@ -249,18 +271,25 @@ __global__ __launch_bounds__(kThreads) void mfma_edge_kernel(MfmaArgs a) {
     }
 }
 
-// One wavefront per (sequence, tile of 1024 lags); four tiles of a sequence per
-// workgroup, so that their waves share the digit loads in L1.
+// One wavefront per (sequence, tile of 1024 lags, chunk of sample steps); four
+// tiles of a sequence per workgroup, so that their waves share the digit loads
+// in L1.  With one chunk the wave forms D(T) itself; with several it writes its
+// partial cross terms for the combination.
+template <bool kChunked>
 __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
-    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    // the wave index is uniform over the wave: said so, the tile, its step
+    // count and the loop control stay scalar
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int groups = (a.tiles + 3) / 4;
-    const int64_t s = blockIdx.x / groups;
-    const int tile = (int)(blockIdx.x % groups) * 4 + wave;
+    const int chunk = kChunked ? (int)(blockIdx.x % a.chunks) : 0;
+    const int64_t gi = kChunked ? blockIdx.x / a.chunks : blockIdx.x;
+    const int64_t s = gi / groups;
+    const int tile = (int)(gi % groups) * 4 + wave;
     const int32_t t0 = a.t0 + tile * kMfmaTileLags;
     const int64_t n = seq_n(a, s);
     const int64_t tm = seq_tmax(a, s);
     if (tile >= a.tiles || n == 0 || t0 > tm) return;   // no lag of this window in the tile
-    const int8_t* __restrict__ base = a.dig + s * 4 * a.plane + kMfmaPadL;
     const int m = lane & 31, h = lane >> 5;
     const int off = (4 - (m & 3)) & 3;   // byte offset of this lane's A row within its first dword
     v16i acc[7];
@@ -274,7 +303,15 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
     // operands of one step are loaded while the products of the previous one
     // run (two register sets; the scheduling barriers keep that order).
     const int64_t iend = n - t0 + 31;
-    const int64_t steps = ((iend + 31) / 32 + 1) & ~int64_t(1);
+    int64_t steps = ((iend + 31) / 32 + 1) & ~int64_t(1);
+    // a chunk: the steps [kbeg, kbeg + steps) of the tile's (even counts, none
+    // past the tile's own), read from a base moved 32 kbeg samples on
+    int64_t kbeg = 0;
+    if (kChunked) {
+        kbeg = min(steps, (int64_t)chunk * a.chunk_steps);
+        steps = min(steps - kbeg, a.chunk_steps);
+    }
+    const int8_t* __restrict__ base = a.dig + s * 4 * a.plane + kMfmaPadL + 32 * kbeg;
     uint32_t w0[4][5], w1[4][5];
     v4i b0[4], b1[4];
     auto load = [&](uint32_t (&w)[4][5], v4i (&bq)[4], int64_t i0) {
@@ -326,26 +363,31 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
         for (int g = 0; g < 7; ++g)
             acc[g] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
     }
-    // D(T) = (E - tail(T)) + (E - head(T)) - 2 r(T), scaled back by 2^-2s
-    const double e = a.qstat[4 * s + 3];
-    const int sc = (int)a.qstat[4 * s + 1];
-    const double* __restrict__ ed = a.edge + s * 2 * ((int64_t)a.tmax + 1);
 #pragma unroll
     for (int j = 0; j < 16; ++j) {   // register j of lane (m, h): row 8 (j / 4) + 4 h + j % 4, column m
         const int row = 8 * (j >> 2) + 4 * h + (j & 3);
         const int64_t t = (int64_t)t0 + 32 * m + row;
         if (t < a.tmin || t > tm) continue;   // lags past a table window's own: left unwritten
-        const double d = ((e - ed[a.tmax + 1 + t]) + (e - ed[t])) - 2.0 * r[j];
-        const double dy = ldexp(d, -2 * sc);
-        const int64_t k = s * a.lags + (t - a.tmin);
-        if (a.s64) {   // the finalisation of a single channel, in its own arithmetic
-            const double v = 0.0 + (double)a.w0 * (dy / (double)(n - t));
-            a.s64[k] = v;
-            if (a.scores) a.scores[k] = (float)v;
-        } else {
-            a.part[k] = dy;
-        }
+        if (!kChunked)
+            write_d(a, s, n, t, r[j]);
+        else
+            a.rpart[(s * a.chunks + chunk) * ((int64_t)a.tiles * kMfmaTileLags) + (t - a.t0)] = r[j];
     }
+}
+
+// Chunked tiles: r(T) as the sum of the chunks' partial cross terms in chunk
+// order, then D(T) as above; one thread per (sequence, lag).
+__global__ __launch_bounds__(kThreads) void mfma_combine_kernel(MfmaArgs a) {
+    const int64_t s = blockIdx.x;
+    const int64_t n = seq_n(a, s);
+    const int64_t tm = seq_tmax(a, s);
+    const int64_t t = (int64_t)a.tmin + (int64_t)blockIdx.y * kThreads + threadIdx.x;
+    if (n == 0 || t > tm) return;
+    const int64_t tl = (int64_t)a.tiles * kMfmaTileLags;
+    const double* __restrict__ rp = a.rpart + s * a.chunks * tl + (t - a.t0);
+    double r = 0.0;
+    for (int c = 0; c < a.chunks; ++c) r += rp[c * tl];
+    write_d(a, s, n, t, r);
 }
 
 struct MfixArgs {
@@ -356,7 +398,7 @@ struct MfixArgs {
     uint32_t* tier1;
     WinState* state;
     int64_t n, window_stride, channel_stride;
-    int32_t num_channels, tmin, tmax, lags, words, t0;
+    int32_t num_channels, tmin, tmax, lags, words, t0, chunks;
     double tau0;
     WindowTable tab;
 };
@@ -382,13 +424,15 @@ __global__ __launch_bounds__(kThreads) void mfma_fixup_kernel(MfixArgs a, Weight
     const int32_t tm = min(table_tmax(a.tab, b, a.tmax), a.tmax);
     const double u = 1.1102230246251565e-16;
     const double steps = (double)((n + 62) / 32);
-    const double flushes = floor(steps / (double)kMfmaFlush) + 2.0;
+    // flushes over all chunks, and the additions of the chunks' partial sums
+    const double flushes = floor(steps / (double)kMfmaFlush) + 2.0 + (double)a.chunks;
     for (int32_t c = threadIdx.x; c < a.num_channels; c += kThreads) {
         const int64_t sq = b * a.num_channels + c;
         const double sc = a.qstat[4 * sq + 1];
         const double e = a.qstat[4 * sq + 3];
         const double round_x = u * (4.04 * ((double)n + 1.0) + 12.0) * e +
-                               2.0 * 7.0 * flushes * u * 1.01 * (double)n * ldexp(1.008, 62);
+                               2.0 * (7.0 * flushes + (double)a.chunks) * u * 1.01 * (double)n *
+                                   ldexp(1.008, 62);
         rr[c] = 1.01 * ldexp(round_x, -2 * (int)sc);
         const bool inexact = a.qstat[4 * sq + 2] == 0.0;
         qa[c] = inexact ? 1.01 * 4.0 * ldexp(1.0, -(int)sc) : 0.0;
@@ -441,13 +485,14 @@ __global__ __launch_bounds__(kThreads) void mfma_fixup_kernel(MfixArgs a, Weight
 }
 
 MfmaArgs args_of(const Plan& p, const float* x, double* qstat, int8_t* dig, double* edge,
-                 double* part) {
+                 double* rpart, double* part) {
     MfmaArgs a;
     a.x = x;
     a.qstat = qstat;
     a.dig = dig;
     a.edge = edge;
     a.part = part;
+    a.rpart = rpart;
     a.s64 = nullptr;
     a.scores = nullptr;
     a.w0 = 1.0f;
@@ -462,6 +507,8 @@ MfmaArgs args_of(const Plan& p, const float* x, double* qstat, int8_t* dig, doub
     a.lags = p.lags;
     a.t0 = p.mfma_t0;
     a.tiles = p.mfma_tiles;
+    a.chunks = p.mfma_chunks;
+    a.chunk_steps = p.mfma_chunk_steps;
     a.tab = p.table;
     return a;
 }
@@ -469,9 +516,9 @@ MfmaArgs args_of(const Plan& p, const float* x, double* qstat, int8_t* dig, doub
 }  // namespace
 
 hipError_t launch_mfma_scores(const Plan& p, const float* x, double* qstat, int8_t* dig,
-                              double* edge, double* part, double* s64, float* scores, float w0,
-                              hipStream_t s) {
-    MfmaArgs a = args_of(p, x, qstat, dig, edge, part);
+                              double* edge, double* rpart, double* part, double* s64,
+                              float* scores, float w0, hipStream_t s) {
+    MfmaArgs a = args_of(p, x, qstat, dig, edge, rpart, part);
     if (mfma_fused_finalize(p, scores != nullptr)) {
         a.s64 = s64;
         a.scores = scores;
@@ -480,8 +527,17 @@ hipError_t launch_mfma_scores(const Plan& p, const float* x, double* qstat, int8
     hipLaunchKernelGGL(mfma_prep_kernel, dim3((unsigned)a.seqs), dim3(kThreads), 0, s, a);
     hipLaunchKernelGGL(mfma_edge_kernel, dim3((unsigned)(2 * a.seqs)), dim3(kThreads), 0, s, a);
     const int64_t groups = (p.mfma_tiles + 3) / 4;
-    hipLaunchKernelGGL(mfma_xcorr_kernel, dim3((unsigned)(a.seqs * groups)), dim3(kThreads), 0,
-                       s, a);
+    if (p.mfma_chunks == 1) {
+        hipLaunchKernelGGL(mfma_xcorr_kernel<false>, dim3((unsigned)(a.seqs * groups)),
+                           dim3(kThreads), 0, s, a);
+    } else {
+        hipLaunchKernelGGL(mfma_xcorr_kernel<true>,
+                           dim3((unsigned)(a.seqs * groups * p.mfma_chunks)), dim3(kThreads), 0,
+                           s, a);
+        hipLaunchKernelGGL(mfma_combine_kernel,
+                           dim3((unsigned)a.seqs, (unsigned)((p.lags + kThreads - 1) / kThreads)),
+                           dim3(kThreads), 0, s, a);
+    }
     return hipGetLastError();
 }
 
@@ -505,6 +561,7 @@ hipError_t launch_mfma_fixup(const Plan& p, const Weights& w, const float* x,
     a.words = p.bitmap_words;
     a.t0 = p.mfma_t0;
     a.tau0 = kScoreRelBound;
+    a.chunks = p.mfma_chunks;
     a.tab = p.table;
     hipLaunchKernelGGL(mfma_fixup_kernel, dim3((unsigned)p.num_windows), dim3(kThreads), 0, s, a,
                        w);

@@ -11,9 +11,10 @@ N, lag ranges that start inside a tile and end on, before and after a tile
 boundary, weighted channels at different scales, samples spanning many
 binades (inexact, bounded), exactly periodic and constant windows, scores
 only, determinism, 256 channels, windows and channels at odd sample offsets,
-one window of 2^22 samples (sampled lags), and the five workloads at full
-size (sampled windows against the oracle, every window against the direct
-path).
+one window of 2^22 samples (sampled lags), small batches whose tiles split
+their samples into chunks (a ragged last chunk, chunks left empty for the
+later tiles), and the five workloads at full size (sampled windows against
+the oracle, every window against the direct path).
 """
 import numpy as np
 import pytest
@@ -229,3 +230,25 @@ def test_long_window_sampled_lags():
     ts = np.concatenate([rng.integers(2, tmax + 1, size=40), [2, 1023, 1024, 3001, 6002, tmax]])
     o = oracle.score_list(x, lay, np.zeros(ts.size, dtype=np.int64), ts)
     check_mfma_scores(g[0, ts - 2].astype(np.float64), o, "mfma 2^22 samples", EXACT_RTOL)
+
+
+@pytest.mark.parametrize("b,c,n,tmin,tmax,chunks", [
+    (3, 1, 65536, 2, 2047, 32),     # 2050 steps in chunks of 66: the last holds 4; tile 1 leaves chunk 31 empty
+    (1, 2, 30001, 5, 3100, 14),     # ragged N, four tiles, weighted channels
+    (2, 1, 8192, 1500, 4000, 3),    # tiles from 1488, fewer steps than the window
+])
+def test_chunked_tiles(b, c, n, tmin, tmax, chunks):
+    # Few waves: each tile's sample steps are split into chunks whose partial
+    # cross terms are summed in a fixed order before D(T) is formed.
+    import paper_2201_01684_amd as pkg
+    x = np.stack([np.stack([planted_trace(n, 211 + 90 * k + 7 * ch, 6, seed=10 * k + ch,
+                                          sigma=0.5) for ch in range(c)]) for k in range(b)])
+    lay = oracle.Layout(b, c, n, c * n, n, tmin, tmax,
+                        weights=np.linspace(1.0, 2.0, c).astype(np.float32))
+    desc, _ = pkg.make_desc(b, c, n, c * n, n, tmin, tmax, weights=lay.weights,
+                            flags=mfma_flag())
+    tiles = (tmax - tmin // 16 * 16) // 1024 + 1
+    assert pkg.describe_plan(desc)["score_waves"] == b * c * tiles * chunks
+    g, res, out = mfma_parity(x, lay, f"mfma chunked {b}x{c}x{n}")
+    g2, res2 = gpu_run(x, lay, flags=mfma_flag())
+    assert np.array_equal(g, g2) and np.array_equal(res, res2)
