@@ -66,7 +66,9 @@
  * whose bound exceeds 1.25e-5 of its score (exact zeros included) is
  * recomputed as an fp64 sum before the selection, which then uses the same
  * tier-0 width as the direct scores.  Selections equal those of the direct
- * scores.  Not with GPOEO_PD_FFT_SCORES.  Rolling detection takes it too (its
+ * scores.  A batch with too few lag tiles to fill the chip splits each tile's
+ * samples into chunks whose partial sums are added in a fixed order, so the
+ * results never depend on scheduling.  Not with GPOEO_PD_FFT_SCORES.  Rolling detection takes it too (its
  * suffix windows come from a window table that every kernel reads).
  *
  * Threading and ownership.  All buffers except `desc` and `desc->channel_weights`
@@ -157,7 +159,8 @@ typedef struct {
     int32_t mode;             /* 0: every window scored on its own; 1: overlapping windows
                                  at a stride dividing N share per-block partials; 2: FFT
                                  scores (score_waves and pairs_scored are then 0); 3:
-                                 matrix-core scores (score_waves: lag tiles of 1024)      */
+                                 matrix-core scores (score_waves: lag tiles of 1024 times
+                                 the sample chunks of each tile)                          */
     int32_t lags_per_lane;    /* consecutive lags per lane of the score kernel (8 or 16)  */
     int64_t score_waves;      /* wavefronts the score stage launches                      */
     double pairs_defined;     /* sum over windows, channels and T in [tmin, tmax] of N - T:
