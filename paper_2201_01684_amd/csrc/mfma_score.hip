@@ -271,12 +271,37 @@ __global__ __launch_bounds__(kThreads) void mfma_edge_kernel(MfmaArgs a) {
     }
 }
 
+// The workgroup's four tiles read the same A rows and B ranges that overlap
+// from one step to the next, so a workgroup stages its digits in LDS a stage
+// of kStageSteps steps at a time: per plane, an A block of the samples
+// [i0s - 64, i0s + 32 kStageSteps + 96) and a B block of the samples
+// [i0s + T0, i0s + T0 + 32 (kStageSteps + 1) + 3072 + 1024), where i0s is the
+// stage's first sample and T0 the first lag of the workgroup's first tile.
+// Samples at or past N are staged as zeros.  The B block is stored as two
+// halves, the first and the second 16 bytes of every 32-byte row, so that the
+// lanes of a B read (one 16-byte half of 32 consecutive rows) cover 512
+// contiguous bytes, free of bank conflicts.  Two stage buffers: the next
+// stage's digits are loaded from HBM into registers while this one's products
+// run, then written to the other buffer before the stage's one barrier.
+constexpr int kStageSteps = 32;
+constexpr int kStageA = 32 * kStageSteps + 160;                  // 1184 bytes
+constexpr int kStageB = 32 * (kStageSteps + 1) + 4 * kMfmaTileLags;   // 5152 bytes
+constexpr int kStageHalf = kStageB / 2;                          // 2576 bytes
+constexpr int kStagePlane = kStageA + kStageB;
+constexpr int kStageBytes = 4 * kStagePlane;                     // 25344 bytes
+constexpr int kStageChunks = kStageBytes / 16;
+constexpr int kStageRounds = (kStageChunks + kThreads - 1) / kThreads;
+static_assert(kStageA % 16 == 0 && kStageB % 32 == 0 && kStageHalf % 16 == 0,
+              "16-byte staging chunks, 32-byte B rows");
+static_assert(kMfmaFlush % kStageSteps == 0 && kStageSteps % 2 == 0, "stage and flush cadence");
+
 // One wavefront per (sequence, tile of 1024 lags, chunk of sample steps); four
-// tiles of a sequence per workgroup, so that their waves share the digit loads
-// in L1.  With one chunk the wave forms D(T) itself; with several it writes its
-// partial cross terms for the combination.
+// tiles of a sequence per workgroup, sharing the staged digits.  With one chunk
+// the wave forms D(T) itself; with several it writes its partial cross terms
+// for the combination.
 template <bool kChunked>
 __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
+    __shared__ __attribute__((aligned(16))) int8_t stage_buf[2 * kStageBytes];
     // the wave index is uniform over the wave: said so, the tile, its step
     // count and the loop control stay scalar
     const int lane = threadIdx.x & (kWave - 1);
@@ -285,11 +310,63 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
     const int chunk = kChunked ? (int)(blockIdx.x % a.chunks) : 0;
     const int64_t gi = kChunked ? blockIdx.x / a.chunks : blockIdx.x;
     const int64_t s = gi / groups;
-    const int tile = (int)(gi % groups) * 4 + wave;
+    const int tile0 = (int)(gi % groups) * 4;
+    const int tile = tile0 + wave;
+    const int64_t tg0 = (int64_t)a.t0 + (int64_t)tile0 * kMfmaTileLags;   // the workgroup's first lag
     const int32_t t0 = a.t0 + tile * kMfmaTileLags;
     const int64_t n = seq_n(a, s);
     const int64_t tm = seq_tmax(a, s);
-    if (tile >= a.tiles || n == 0 || t0 > tm) return;   // no lag of this window in the tile
+    if (n == 0 || tg0 > tm) return;   // the whole workgroup: no lag of this window in its tiles
+    const bool active = tile < a.tiles && t0 <= tm;
+    // Steps while some pair (i, i + T) of a tile has i + T < N, rounded up to
+    // an even count (a step past that reads only zeros); the chunk's share of
+    // them, from its first step kbeg.
+    auto steps_of = [&](int64_t first_lag) {
+        const int64_t all = ((n - first_lag + 62) / 32 + 1) & ~int64_t(1);
+        const int64_t kbeg = kChunked ? min(all, (int64_t)chunk * a.chunk_steps) : 0;
+        return kChunked ? min(all - kbeg, a.chunk_steps) : all;
+    };
+    const int64_t kbeg = kChunked ? (int64_t)chunk * a.chunk_steps : 0;
+    const int64_t wg_steps = max((int64_t)0, steps_of(tg0));   // the first tile has the most
+    const int64_t my_steps = active ? max((int64_t)0, steps_of(t0)) : 0;
+    const int64_t stages = (wg_steps + kStageSteps - 1) / kStageSteps;
+    const int8_t* __restrict__ seq = a.dig + s * 4 * a.plane + kMfmaPadL;
+
+    // staging: 16-byte chunk c of a stage, plane p and chunk j of the plane's
+    // blocks, lands at byte 16 c of its buffer (A), or in the B half j' % 2 at
+    // row j' / 2 (B, with j' = j - kStageA / 16)
+    auto stage_pos = [&](int c) {
+        const int p = c / (kStagePlane / 16), j = c % (kStagePlane / 16);
+        if (j < kStageA / 16) return 16 * c;
+        const int jb = j - kStageA / 16;
+        return p * kStagePlane + kStageA + (jb & 1) * kStageHalf + 16 * (jb >> 1);
+    };
+    v4i held[kStageRounds];
+    auto fetch = [&](int64_t st) {
+        const int64_t i0s = 32 * (kbeg + st * kStageSteps);
+#pragma unroll
+        for (int rr = 0; rr < kStageRounds; ++rr) {
+            const int c = rr * kThreads + threadIdx.x;
+            held[rr] = v4i{0, 0, 0, 0};
+            if (c < kStageChunks) {
+                const int p = c / (kStagePlane / 16), j = c % (kStagePlane / 16);
+                const int64_t i = j < kStageA / 16 ? i0s - 64 + 16 * j
+                                                   : i0s + tg0 + 16 * (j - kStageA / 16);
+                // a chunk starting before N: its samples, and zeros from the
+                // plane's padding past N
+                if (i < n) held[rr] = *reinterpret_cast<const v4i*>(seq + p * a.plane + i);
+            }
+        }
+    };
+    auto deposit = [&](int buf) {
+#pragma unroll
+        for (int rr = 0; rr < kStageRounds; ++rr) {
+            const int c = rr * kThreads + threadIdx.x;
+            if (c < kStageChunks)
+                *reinterpret_cast<v4i*>(stage_buf + buf * kStageBytes + stage_pos(c)) = held[rr];
+        }
+    };
+
     const int m = lane & 31, h = lane >> 5;
     const int off = (4 - (m & 3)) & 3;   // byte offset of this lane's A row within its first dword
     v16i acc[7];
@@ -298,36 +375,33 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
     double r[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) r[j] = 0.0;
-    // Steps while some pair (i, i + T) of the tile has i + T < N, rounded up to
-    // an even count: a step past that reads only the zero padding of B.  The
-    // operands of one step are loaded while the products of the previous one
-    // run (two register sets; the scheduling barriers keep that order).
-    const int64_t iend = n - t0 + 31;
-    int64_t steps = ((iend + 31) / 32 + 1) & ~int64_t(1);
-    // a chunk: the steps [kbeg, kbeg + steps) of the tile's (even counts, none
-    // past the tile's own), read from a base moved 32 kbeg samples on
-    int64_t kbeg = 0;
-    if (kChunked) {
-        kbeg = min(steps, (int64_t)chunk * a.chunk_steps);
-        steps = min(steps - kbeg, a.chunk_steps);
-    }
-    const int8_t* __restrict__ base = a.dig + s * 4 * a.plane + kMfmaPadL + 32 * kbeg;
+    // Per step, from the stage buffer: A row a = m, bytes i0 - m + 16 h .. + 15
+    // (dword-aligned reads shifted into place); B column b = m, bytes
+    // i0 + T0 + 32 m + 16 h .. + 15.  The operands of the next step are read
+    // while this step's products run (two register sets), from its fifth
+    // product on: the LDS counter holds 15 reads and a step takes 16, so reads
+    // issued before all of its products would make the first product wait for
+    // reads of the next step.  Two reads follow each of the next eight
+    // products, so that no run of reads leaves the matrix unit idle (one wave
+    // per SIMD issues everything in order).  The scheduling barriers keep that
+    // order.
     uint32_t w0[4][5], w1[4][5];
     v4i b0[4], b1[4];
-    auto load = [&](uint32_t (&w)[4][5], v4i (&bq)[4], int64_t i0) {
+    auto load = [&](const int8_t* sb, uint32_t (&w)[4][5], v4i (&bq)[4], int k) {
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {   // A row a = m: bytes i0 - m + 16 h .. + 15, dword-aligned loads
-            const uint32_t* src =
-                reinterpret_cast<const uint32_t*>(base + p * a.plane + i0 - m + 16 * h - off);
+        for (int p = 0; p < 4; ++p) {
+            const uint32_t* src = reinterpret_cast<const uint32_t*>(
+                sb + p * kStagePlane + 32 * k + 64 - m + 16 * h - off);
 #pragma unroll
             for (int e = 0; e < 5; ++e) w[p][e] = src[e];
         }
 #pragma unroll
-        for (int q = 0; q < 4; ++q)   // B column b = m: bytes i0 + T0 + 32 m + 16 h .. + 15 (aligned)
-            bq[q] = *reinterpret_cast<const v4i*>(base + q * a.plane + i0 + t0 + 32 * m + 16 * h);
+        for (int q = 0; q < 4; ++q)
+            bq[q] = *reinterpret_cast<const v4i*>(sb + q * kStagePlane + kStageA + h * kStageHalf +
+                                                  16 * (k + wave * (kMfmaTileLags / 32) + m));
     };
-    auto step = [&](const uint32_t (&w)[4][5], const v4i (&bq)[4]) {
-        v4i A[4];
+    v4i A[4];
+    auto step_first = [&](const uint32_t (&w)[4][5], const v4i (&bq)[4]) {
 #pragma unroll
         for (int p = 0; p < 4; ++p) {
             A[p][0] = (int)__builtin_amdgcn_alignbyte(w[p][1], w[p][0], off);
@@ -336,25 +410,26 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
             A[p][3] = (int)__builtin_amdgcn_alignbyte(w[p][4], w[p][3], off);
         }
 #pragma unroll
-        for (int p = 0; p < 4; ++p)
+        for (int q = 0; q < 4; ++q)
+            acc[q] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[0], bq[q], acc[q], 0, 0, 0);
+    };
+    auto step_rest = [&](const v4i (&bq)[4]) {
+#pragma unroll
+        for (int p = 1; p < 4; ++p)
 #pragma unroll
             for (int q = 0; q < 4; ++q)
                 acc[p + q] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[p], bq[q], acc[p + q], 0, 0, 0);
     };
-    for (int64_t k0 = 0; k0 < steps; k0 += kMfmaFlush) {
-        // each group sum stays below 2^31 over kMfmaFlush steps (an even count)
-        const int64_t k1 = min(steps, k0 + (int64_t)kMfmaFlush);
-        load(w0, b0, 32 * k0);
-        for (int64_t k = k0; k < k1; k += 2) {
-            load(w1, b1, 32 * (k + 1));
-            __builtin_amdgcn_sched_barrier(0);
-            step(w0, b0);
-            __builtin_amdgcn_sched_barrier(0);
-            load(w0, b0, 32 * (k + 2));
-            __builtin_amdgcn_sched_barrier(0);
-            step(w1, b1);
-            __builtin_amdgcn_sched_barrier(0);
+    // the order of a region holding the next step's reads and step_rest
+    auto interleave = [&]() {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one product
+            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // two LDS reads
         }
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    };
+    auto flush = [&]() {   // each group sum stays below 2^31 over kMfmaFlush steps
 #pragma unroll
         for (int g = 6; g >= 0; --g)
 #pragma unroll
@@ -362,7 +437,40 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
 #pragma unroll
         for (int g = 0; g < 7; ++g)
             acc[g] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+    };
+
+    if (stages > 0) {
+        fetch(0);
+        deposit(0);
     }
+    __syncthreads();
+    for (int64_t st = 0; st < stages; ++st) {
+        if (st + 1 < stages) fetch(st + 1);   // in flight while this stage's products run
+        const int8_t* sb = stage_buf + (st & 1) * kStageBytes;
+        // this wave's steps in the stage (even; none once its tile's run out)
+        const int nk = (int)min((int64_t)kStageSteps, max((int64_t)0, my_steps - st * kStageSteps));
+        if (nk > 0) {
+            load(sb, w0, b0, 0);
+            for (int k = 0; k < nk; k += 2) {
+                step_first(w0, b0);
+                __builtin_amdgcn_sched_barrier(0);
+                load(sb, w1, b1, k + 1);
+                step_rest(b0);
+                interleave();
+                __builtin_amdgcn_sched_barrier(0);
+                step_first(w1, b1);
+                __builtin_amdgcn_sched_barrier(0);
+                load(sb, w0, b0, k + 2);
+                step_rest(b1);
+                interleave();
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        if ((st + 1) % (kMfmaFlush / kStageSteps) == 0 || st + 1 == stages) flush();
+        if (st + 1 < stages) deposit((int)((st + 1) & 1));
+        __syncthreads();
+    }
+    if (!active) return;
 #pragma unroll
     for (int j = 0; j < 16; ++j) {   // register j of lane (m, h): row 8 (j / 4) + 4 h + j % 4, column m
         const int row = 8 * (j >> 2) + 4 * h + (j & 3);
@@ -378,10 +486,11 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
 // Chunked tiles: r(T) as the sum of the chunks' partial cross terms in chunk
 // order, then D(T) as above; one thread per (sequence, lag).
 __global__ __launch_bounds__(kThreads) void mfma_combine_kernel(MfmaArgs a) {
-    const int64_t s = blockIdx.x;
+    const int64_t lag_groups = ((int64_t)a.lags + kThreads - 1) / kThreads;
+    const int64_t s = blockIdx.x / lag_groups;
     const int64_t n = seq_n(a, s);
     const int64_t tm = seq_tmax(a, s);
-    const int64_t t = (int64_t)a.tmin + (int64_t)blockIdx.y * kThreads + threadIdx.x;
+    const int64_t t = (int64_t)a.tmin + (int64_t)(blockIdx.x % lag_groups) * kThreads + threadIdx.x;
     if (n == 0 || t > tm) return;
     const int64_t tl = (int64_t)a.tiles * kMfmaTileLags;
     const double* __restrict__ rp = a.rpart + s * a.chunks * tl + (t - a.t0);
@@ -535,7 +644,7 @@ hipError_t launch_mfma_scores(const Plan& p, const float* x, double* qstat, int8
                            dim3((unsigned)(a.seqs * groups * p.mfma_chunks)), dim3(kThreads), 0,
                            s, a);
         hipLaunchKernelGGL(mfma_combine_kernel,
-                           dim3((unsigned)a.seqs, (unsigned)((p.lags + kThreads - 1) / kThreads)),
+                           dim3((unsigned)(a.seqs * ((p.lags + kThreads - 1) / kThreads))),
                            dim3(kThreads), 0, s, a);
     }
     return hipGetLastError();
