@@ -283,12 +283,14 @@ __global__ __launch_bounds__(kThreads) void mfma_edge_kernel(MfmaArgs a) {
 // contiguous bytes, free of bank conflicts.  Two stage buffers: the next
 // stage's digits are loaded from HBM into registers while this one's products
 // run, then written to the other buffer before the stage's one barrier.
-constexpr int kStageSteps = 32;
-constexpr int kStageA = 32 * kStageSteps + 160;                  // 1184 bytes
-constexpr int kStageB = 32 * (kStageSteps + 1) + 4 * kMfmaTileLags;   // 5152 bytes
-constexpr int kStageHalf = kStageB / 2;                          // 2576 bytes
+// Two workgroups share a CU (67 KB of LDS and at most 256 registers a lane
+// each), so one wave's operand reads overlap the other's products.
+constexpr int kStageSteps = 64;
+constexpr int kStageA = 32 * kStageSteps + 160;                  // 2208 bytes
+constexpr int kStageB = 32 * (kStageSteps + 1) + 4 * kMfmaTileLags;   // 6176 bytes
+constexpr int kStageHalf = kStageB / 2;                          // 3088 bytes
 constexpr int kStagePlane = kStageA + kStageB;
-constexpr int kStageBytes = 4 * kStagePlane;                     // 25344 bytes
+constexpr int kStageBytes = 4 * kStagePlane;                     // 33536 bytes
 constexpr int kStageChunks = kStageBytes / 16;
 constexpr int kStageRounds = (kStageChunks + kThreads - 1) / kThreads;
 static_assert(kStageA % 16 == 0 && kStageB % 32 == 0 && kStageHalf % 16 == 0,
@@ -300,7 +302,7 @@ static_assert(kMfmaFlush % kStageSteps == 0 && kStageSteps % 2 == 0, "stage and 
 // the wave forms D(T) itself; with several it writes its partial cross terms
 // for the combination.
 template <bool kChunked>
-__global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
+__global__ __launch_bounds__(kThreads, 2) void mfma_xcorr_kernel(MfmaArgs a) {
     __shared__ __attribute__((aligned(16))) int8_t stage_buf[2 * kStageBytes];
     // the wave index is uniform over the wave: said so, the tile, its step
     // count and the loop control stay scalar
@@ -372,21 +374,11 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
     v16i acc[7];
 #pragma unroll
     for (int g = 0; g < 7; ++g) acc[g] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
-    double r[16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j) r[j] = 0.0;
     // Per step, from the stage buffer: A row a = m, bytes i0 - m + 16 h .. + 15
     // (dword-aligned reads shifted into place); B column b = m, bytes
-    // i0 + T0 + 32 m + 16 h .. + 15.  The operands of the next step are read
-    // while this step's products run (two register sets), from its fifth
-    // product on: the LDS counter holds 15 reads and a step takes 16, so reads
-    // issued before all of its products would make the first product wait for
-    // reads of the next step.  Two reads follow each of the next eight
-    // products, so that no run of reads leaves the matrix unit idle (one wave
-    // per SIMD issues everything in order).  The scheduling barriers keep that
-    // order.
-    uint32_t w0[4][5], w1[4][5];
-    v4i b0[4], b1[4];
+    // i0 + T0 + 32 m + 16 h .. + 15.
+    uint32_t w0[4][5];
+    v4i b0[4];
     auto load = [&](const int8_t* sb, uint32_t (&w)[4][5], v4i (&bq)[4], int k) {
 #pragma unroll
         for (int p = 0; p < 4; ++p) {
@@ -400,8 +392,8 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
             bq[q] = *reinterpret_cast<const v4i*>(sb + q * kStagePlane + kStageA + h * kStageHalf +
                                                   16 * (k + wave * (kMfmaTileLags / 32) + m));
     };
-    v4i A[4];
-    auto step_first = [&](const uint32_t (&w)[4][5], const v4i (&bq)[4]) {
+    auto step = [&](const uint32_t (&w)[4][5], const v4i (&bq)[4]) {
+        v4i A[4];
 #pragma unroll
         for (int p = 0; p < 4; ++p) {
             A[p][0] = (int)__builtin_amdgcn_alignbyte(w[p][1], w[p][0], off);
@@ -410,30 +402,33 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
             A[p][3] = (int)__builtin_amdgcn_alignbyte(w[p][4], w[p][3], off);
         }
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            acc[q] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[0], bq[q], acc[q], 0, 0, 0);
-    };
-    auto step_rest = [&](const v4i (&bq)[4]) {
-#pragma unroll
-        for (int p = 1; p < 4; ++p)
+        for (int p = 0; p < 4; ++p)
 #pragma unroll
             for (int q = 0; q < 4; ++q)
                 acc[p + q] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[p], bq[q], acc[p + q], 0, 0, 0);
     };
-    // the order of a region holding the next step's reads and step_rest
-    auto interleave = [&]() {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one product
-            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // two LDS reads
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    // Every kMfmaFlush steps (each group sum stays below 2^31 over that many)
+    // the shift groups are added, scaled by 256^(p+q), into r(T) in fp64.
+    // Between flushes r(T) waits in the lane's own output slot (its D(T) or
+    // S(T), or the chunk's partial), so that two waves fit each SIMD.
+    // Register j of lane (m, h) holds row 8 (j / 4) + 4 h + j % 4, column m.
+    auto slot_of = [&](int64_t t) {
+        return kChunked
+            ? a.rpart + (s * a.chunks + chunk) * ((int64_t)a.tiles * kMfmaTileLags) + (t - a.t0)
+            : (a.s64 ? a.s64 : a.part) + s * a.lags + (t - a.tmin);
     };
-    auto flush = [&]() {   // each group sum stays below 2^31 over kMfmaFlush steps
+    auto flush = [&](bool first) {
 #pragma unroll
-        for (int g = 6; g >= 0; --g)
+        for (int j = 0; j < 16; ++j) {
+            const int row = 8 * (j >> 2) + 4 * h + (j & 3);
+            const int64_t t = (int64_t)t0 + 32 * m + row;
+            if (t < a.tmin || t > tm) continue;   // lags past a table window's own: left unwritten
+            double* slot = slot_of(t);
+            double r = first ? 0.0 : *slot;
 #pragma unroll
-            for (int j = 0; j < 16; ++j) r[j] += ldexp((double)acc[g][j], 8 * g);
+            for (int g = 6; g >= 0; --g) r += ldexp((double)acc[g][j], 8 * g);
+            *slot = r;
+        }
 #pragma unroll
         for (int g = 0; g < 7; ++g)
             acc[g] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
@@ -447,39 +442,26 @@ __global__ __launch_bounds__(kThreads) void mfma_xcorr_kernel(MfmaArgs a) {
     for (int64_t st = 0; st < stages; ++st) {
         if (st + 1 < stages) fetch(st + 1);   // in flight while this stage's products run
         const int8_t* sb = stage_buf + (st & 1) * kStageBytes;
-        // this wave's steps in the stage (even; none once its tile's run out)
+        // this wave's steps in the stage (none once its tile's run out)
         const int nk = (int)min((int64_t)kStageSteps, max((int64_t)0, my_steps - st * kStageSteps));
-        if (nk > 0) {
-            load(sb, w0, b0, 0);
-            for (int k = 0; k < nk; k += 2) {
-                step_first(w0, b0);
-                __builtin_amdgcn_sched_barrier(0);
-                load(sb, w1, b1, k + 1);
-                step_rest(b0);
-                interleave();
-                __builtin_amdgcn_sched_barrier(0);
-                step_first(w1, b1);
-                __builtin_amdgcn_sched_barrier(0);
-                load(sb, w0, b0, k + 2);
-                step_rest(b1);
-                interleave();
-                __builtin_amdgcn_sched_barrier(0);
-            }
+        for (int k = 0; k < nk; ++k) {
+            load(sb, w0, b0, k);
+            step(w0, b0);
         }
-        if ((st + 1) % (kMfmaFlush / kStageSteps) == 0 || st + 1 == stages) flush();
+        if (active && ((st + 1) % (kMfmaFlush / kStageSteps) == 0 || st + 1 == stages))
+            flush(st < kMfmaFlush / kStageSteps);
         if (st + 1 < stages) deposit((int)((st + 1) & 1));
         __syncthreads();
     }
     if (!active) return;
+    if (stages == 0) flush(true);   // a chunk past this tile's steps: r = 0
+    if (kChunked) return;           // the partials stay for the combination
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {   // register j of lane (m, h): row 8 (j / 4) + 4 h + j % 4, column m
+    for (int j = 0; j < 16; ++j) {
         const int row = 8 * (j >> 2) + 4 * h + (j & 3);
         const int64_t t = (int64_t)t0 + 32 * m + row;
-        if (t < a.tmin || t > tm) continue;   // lags past a table window's own: left unwritten
-        if (!kChunked)
-            write_d(a, s, n, t, r[j]);
-        else
-            a.rpart[(s * a.chunks + chunk) * ((int64_t)a.tiles * kMfmaTileLags) + (t - a.t0)] = r[j];
+        if (t < a.tmin || t > tm) continue;
+        write_d(a, s, n, t, *slot_of(t));
     }
 }
 
