@@ -96,7 +96,7 @@ bool launches_fit(const Plan& p) {
         }
     } else if (p.mfma) {   // statistics and edge sums per sequence, four lag tiles a workgroup
         if (!fits(2 * seqs, 256) ||
-            !fits(seqs * ((p.mfma_tiles + 3) / 4) * p.mfma_chunks, 256) ||
+            !fits((seqs + 7) / 8 * 8 * ((p.mfma_tiles + 3) / 4) * p.mfma_chunks, 256) ||
             !fits(seqs * ((p.lags + 255) / 256), 256))
             return false;
     } else if (p.sliding) {
@@ -261,7 +261,7 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
         p->t0 = d->tmin;
         p->lags_padded = p->lags;
         p->chunks = 1;
-        p->mfma_t0 = d->tmin & ~15;               // B operand rows 16-byte aligned
+        p->mfma_t0 = d->tmin;                     // lag tiles from Tmin: the lags past Tmax cost least
         p->mfma_tiles = (d->tmax - p->mfma_t0) / kMfmaTileLags + 1;
         p->mfma_plane = (kMfmaPadL + d->n + kMfmaPadR + 255) / 256 * 256;
         // steps of the first tile (the most), even; chunks when the waves are few

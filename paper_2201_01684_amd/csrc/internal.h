@@ -158,7 +158,7 @@ struct Plan {
     int32_t fft_wrap_m, fft_wrap_log2;
     // Matrix-core scores: every sequence as four int8 digit planes of
     // mfma_plane bytes (padded); lag tiles of kMfmaTileLags from mfma_t0
-    // (Tmin rounded down to a multiple of 16).
+    // (Tmin).
     bool mfma;
     bool mfma_table;         // windows from a table (rolling suffixes)
     int32_t mfma_t0, mfma_tiles;

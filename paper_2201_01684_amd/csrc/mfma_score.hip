@@ -36,6 +36,7 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
 constexpr int kThreads = 256;
+constexpr int kXcds = 8;   // MI355X: workgroups are dealt to its 8 XCDs in turn
 constexpr int kEdgeTile = 4096;
 constexpr int kEdgePer = kEdgeTile / kThreads;
 constexpr int kEdgeWaves = kThreads / kWave;
@@ -308,10 +309,18 @@ __global__ __launch_bounds__(kThreads, 2) void mfma_xcorr_kernel(MfmaArgs a) {
     // count and the loop control stay scalar
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    // Workgroups go to the 8 XCDs in turn, workgroup b to XCD b % 8.  Every
+    // workgroup of sequence s = 8 u + v takes an index with b % 8 == (u + v) % 8:
+    // the sequence's digits stay in one XCD's L2, and sequences of any stride
+    // (the suffix slots of rolling detection, whose lengths differ) rotate
+    // over all XCDs.  The grid is padded to a multiple of 8 sequences.
     const int groups = (a.tiles + 3) / 4;
-    const int chunk = kChunked ? (int)(blockIdx.x % a.chunks) : 0;
-    const int64_t gi = kChunked ? blockIdx.x / a.chunks : blockIdx.x;
-    const int64_t s = gi / groups;
+    const int64_t rest = blockIdx.x / kXcds;
+    const int chunk = kChunked ? (int)(rest % a.chunks) : 0;
+    const int64_t gi = kChunked ? rest / a.chunks : rest;
+    const int64_t su = gi / groups;
+    const int64_t s = su * kXcds + (int64_t)((blockIdx.x - su) & (kXcds - 1));
+    if (s >= a.seqs) return;   // padding of the grid
     const int tile0 = (int)(gi % groups) * 4;
     const int tile = tile0 + wave;
     const int64_t tg0 = (int64_t)a.t0 + (int64_t)tile0 * kMfmaTileLags;   // the workgroup's first lag
@@ -343,6 +352,32 @@ __global__ __launch_bounds__(kThreads, 2) void mfma_xcorr_kernel(MfmaArgs a) {
         const int jb = j - kStageA / 16;
         return p * kStagePlane + kStageA + (jb & 1) * kStageHalf + 16 * (jb >> 1);
     };
+    // The B block starts at lag tg0 = Tmin + 4096 g, which need not be a
+    // multiple of 16: its chunks are taken from 32 aligned bytes at an offset
+    // shift, the same for every chunk of the launch.
+    const int shift = (int)(tg0 & 15);
+    auto bytes_from = [&](const v4i& lo, const v4i& hi) {
+        const uint32_t w[8] = {(uint32_t)lo[0], (uint32_t)lo[1], (uint32_t)lo[2], (uint32_t)lo[3],
+                               (uint32_t)hi[0], (uint32_t)hi[1], (uint32_t)hi[2], (uint32_t)hi[3]};
+        const int rb = shift & 3;
+        v4i out;
+        switch (shift >> 2) {   // uniform: constant register indices in each case
+#define GPOEO_BYTES_AT(q)                                                     \
+    case q:                                                                   \
+        out[0] = (int)__builtin_amdgcn_alignbyte(w[q + 1], w[q + 0], rb);     \
+        out[1] = (int)__builtin_amdgcn_alignbyte(w[q + 2], w[q + 1], rb);     \
+        out[2] = (int)__builtin_amdgcn_alignbyte(w[q + 3], w[q + 2], rb);     \
+        out[3] = (int)__builtin_amdgcn_alignbyte(w[q + 4], w[q + 3], rb);     \
+        break;
+            GPOEO_BYTES_AT(0)
+            GPOEO_BYTES_AT(1)
+            GPOEO_BYTES_AT(2)
+            default:
+            GPOEO_BYTES_AT(3)
+#undef GPOEO_BYTES_AT
+        }
+        return out;
+    };
     v4i held[kStageRounds];
     auto fetch = [&](int64_t st) {
         const int64_t i0s = 32 * (kbeg + st * kStageSteps);
@@ -352,11 +387,19 @@ __global__ __launch_bounds__(kThreads, 2) void mfma_xcorr_kernel(MfmaArgs a) {
             held[rr] = v4i{0, 0, 0, 0};
             if (c < kStageChunks) {
                 const int p = c / (kStagePlane / 16), j = c % (kStagePlane / 16);
-                const int64_t i = j < kStageA / 16 ? i0s - 64 + 16 * j
-                                                   : i0s + tg0 + 16 * (j - kStageA / 16);
-                // a chunk starting before N: its samples, and zeros from the
-                // plane's padding past N
-                if (i < n) held[rr] = *reinterpret_cast<const v4i*>(seq + p * a.plane + i);
+                const int8_t* plane = seq + p * a.plane;
+                if (j < kStageA / 16) {   // A: 16-byte aligned (i0s is a multiple of 32)
+                    const int64_t i = i0s - 64 + 16 * j;
+                    // a chunk starting before N: its samples, and zeros from
+                    // the plane's padding past N
+                    if (i < n) held[rr] = *reinterpret_cast<const v4i*>(plane + i);
+                } else {   // B: from the two aligned chunks around it
+                    const int64_t i = i0s + tg0 + 16 * (j - kStageA / 16) - shift;
+                    v4i lo = v4i{0, 0, 0, 0}, hi = v4i{0, 0, 0, 0};
+                    if (i < n) lo = *reinterpret_cast<const v4i*>(plane + i);
+                    if (shift != 0 && i + 16 < n) hi = *reinterpret_cast<const v4i*>(plane + i + 16);
+                    held[rr] = bytes_from(lo, hi);
+                }
             }
         }
     };
@@ -618,12 +661,13 @@ hipError_t launch_mfma_scores(const Plan& p, const float* x, double* qstat, int8
     hipLaunchKernelGGL(mfma_prep_kernel, dim3((unsigned)a.seqs), dim3(kThreads), 0, s, a);
     hipLaunchKernelGGL(mfma_edge_kernel, dim3((unsigned)(2 * a.seqs)), dim3(kThreads), 0, s, a);
     const int64_t groups = (p.mfma_tiles + 3) / 4;
+    const int64_t seqs8 = (a.seqs + kXcds - 1) / kXcds * kXcds;
     if (p.mfma_chunks == 1) {
-        hipLaunchKernelGGL(mfma_xcorr_kernel<false>, dim3((unsigned)(a.seqs * groups)),
+        hipLaunchKernelGGL(mfma_xcorr_kernel<false>, dim3((unsigned)(seqs8 * groups)),
                            dim3(kThreads), 0, s, a);
     } else {
         hipLaunchKernelGGL(mfma_xcorr_kernel<true>,
-                           dim3((unsigned)(a.seqs * groups * p.mfma_chunks)), dim3(kThreads), 0,
+                           dim3((unsigned)(seqs8 * groups * p.mfma_chunks)), dim3(kThreads), 0,
                            s, a);
         hipLaunchKernelGGL(mfma_combine_kernel,
                            dim3((unsigned)(a.seqs * ((p.lags + kThreads - 1) / kThreads))),

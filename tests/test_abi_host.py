@@ -264,30 +264,29 @@ def test_fft_plan(lib):
 def test_mfma_plan(lib):
     d, _ = good_desc(flags=B.MFMA_SCORES)
     info = B.describe_plan(d)
-    # lags 2..1024 from tile start 0: two tiles of 1024 lags per sequence; 16
-    # waves are too few, so each tile's 130 sample steps split into two chunks
-    # (no chunk shorter than 64 steps)
-    assert info["mode"] == 3 and info["score_waves"] == 4 * 2 * 2 * 2
+    # lags 2..1024 in one tile of 1024 lags from Tmin per sequence; 8 waves are
+    # too few, so each tile's 130 sample steps split into two chunks (no chunk
+    # shorter than 64 steps)
+    assert info["mode"] == 3 and info["score_waves"] == 4 * 2 * 1 * 2
     assert info["pairs_defined"] == 4 * 2 * sum(4096 - t for t in range(2, 1025))
     # four int8 digit planes per sequence (padded), edge sums, per-sequence statistics
     assert info["workspace_bytes"] >= 4 * 2 * 4 * 4096 + 4 * 2 * 2 * 1025 * 8
     assert info["fft_len"] == 0
-    # tiles start at Tmin rounded down to a multiple of 16
-    # (98 steps from there: one chunk)
+    # tiles start at Tmin itself (98 steps from there: one chunk)
     d, _ = good_desc(flags=B.MFMA_SCORES, tmin=1021, tmax=2045)
-    assert B.describe_plan(d)["score_waves"] == 4 * 2 * 2          # 1008 .. 3055
+    assert B.describe_plan(d)["score_waves"] == 4 * 2 * 2          # 1021 .. 3068
     d, _ = good_desc(flags=B.MFMA_SCORES, tmin=1024, tmax=2047)
     assert B.describe_plan(d)["score_waves"] == 4 * 2 * 1
-    # a small batch of long windows: 64 sequences x 2 tiles, 8194 steps each,
-    # split into 32 chunks of 258 steps (about 4096 waves)
+    # a small batch of long windows: 64 sequences x 1 tile, 8194 steps each,
+    # split into 64 chunks of 130 steps (4096 waves)
     d, _ = good_desc(flags=B.MFMA_SCORES, num_windows=64, num_channels=1, n=262144,
                      tmax=1024, window_stride=262144, channel_stride=262144)
-    assert B.describe_plan(d)["score_waves"] == 64 * 2 * 32
+    assert B.describe_plan(d)["score_waves"] == 64 * 1 * 64
     # a large batch keeps one chunk per tile: 1024 sequences x 32 tiles
     d, _ = good_desc(flags=B.MFMA_SCORES, num_windows=1024, num_channels=1, n=262144,
                      tmax=32767, window_stride=262144, channel_stride=262144)
     assert B.describe_plan(d)["score_waves"] == 1024 * 32
-    # a tile grid beyond HIP's 32-bit global size: 2^21 windows x 9 groups of 4
+    # a tile grid beyond HIP's 32-bit global size: 2^21 windows x 8 groups of 4
     # lag tiles x 256 threads
     d, _ = good_desc(flags=B.MFMA_SCORES, num_windows=1 << 21, num_channels=1, n=65536,
                      tmax=32768, window_stride=65536, channel_stride=65536)

@@ -59,11 +59,14 @@ def mfma_parity(x, lay, where="", flags=0, rtol=MFMA_RTOL):
     (100, 2, 50),
     (1500, 2, 500),
     (4099, 3, 2049),      # ragged N, three tiles
-    (3000, 1021, 1500),   # first tile starts at 1008, below Tmin
-    (5000, 2, 1023),      # Tmax on the last lag of the first tile
-    (5000, 2, 1024),      # Tmax the first lag of a second tile
+    (3000, 1021, 1500),   # tiles from Tmin: B staged 13 bytes past a 16-byte boundary
+    (5000, 2, 1024),      # Tmax below the last lag of the first tile
+    (5000, 2, 1025),      # Tmax on the last lag of the first tile
+    (5000, 2, 1026),      # Tmax the first lag of a second tile
+    (5000, 9, 2047),      # B offset 9: the third dword of the aligned pair
     (5000, 17, 2047),
     (20000, 6, 3333),
+    (20000, 4106, 9000),  # offset 10, workgroups of four tiles from lag 4106
 ])
 def test_edge_shapes(n, tmin, tmax):
     x = planted_trace(n, max(3, min(97, n // 3)), 3, seed=n + tmin, sigma=1.0)
@@ -247,7 +250,7 @@ def test_chunked_tiles(b, c, n, tmin, tmax, chunks):
                         weights=np.linspace(1.0, 2.0, c).astype(np.float32))
     desc, _ = pkg.make_desc(b, c, n, c * n, n, tmin, tmax, weights=lay.weights,
                             flags=mfma_flag())
-    tiles = (tmax - tmin // 16 * 16) // 1024 + 1
+    tiles = (tmax - tmin) // 1024 + 1
     assert pkg.describe_plan(desc)["score_waves"] == b * c * tiles * chunks
     g, res, out = mfma_parity(x, lay, f"mfma chunked {b}x{c}x{n}")
     g2, res2 = gpu_run(x, lay, flags=mfma_flag())
