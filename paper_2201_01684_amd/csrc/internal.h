@@ -39,14 +39,14 @@ constexpr int kFftWrapMinLog2 = 12;
 constexpr int kFftWrapMaxLog2 = 20;
 constexpr int kFftClasses = kFftMaxLog2 + 1;   // length classes 2^lg of a ragged batch, by lg
 // Matrix-core scores (GPOEO_PD_MFMA_SCORES): lags per wavefront tile, zero
-// padding before and after each digit plane (bytes; every read of the tile
-// loop, including the loads one and two steps ahead, stays within it: the
-// last reads reach 1023 + 95 + 35 bytes past N), and the steps between two
-// flushes of the int32 shift groups (each stays below 2^31: 4 digit pairs x
-// 32 products of at most 2^14 per step).
+// padding before and after each digit plane (bytes; the LDS staging reads
+// 16-byte chunks that start before N, so at most 15 bytes past N, and A rows
+// from 64 bytes before sample 0), and the steps between two flushes of the
+// int32 shift groups (each stays below 2^31: 4 digit pairs x 32 products of at
+// most 2^14 per step).
 constexpr int kMfmaTileLags = 1024;
 constexpr int kMfmaPadL = 64;
-constexpr int kMfmaPadR = 1344;
+constexpr int kMfmaPadR = 64;
 constexpr int kMfmaFlush = 512;
 // A batch with fewer than kMfmaTargetWaves (sequence, lag tile) waves splits
 // each tile's sample steps into chunks of at least kMfmaMinChunkSteps, whose
