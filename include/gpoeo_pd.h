@@ -124,10 +124,16 @@ extern "C" {
 #define GPOEO_PD_MAX_WINDOWS (1 << 21)   /* windows per call (rolling: B * suffix slots) */
 #define GPOEO_PD_MAX_QUERIES (1 << 23)   /* (window, lag) queries per similarity or
                                             mean-removed score call                       */
+/* Channels per window.  The composite detection feature of Sec. 4.2 combines a
+ * handful of sampled metrics (power, SM and memory utilisation); the weights
+ * of up to this many channels travel with every launch as a kernel argument,
+ * so a descriptor with more channels is EINVAL. */
+#define GPOEO_PD_MAX_CHANNELS 256
 
 typedef struct {
     int64_t num_windows;     /* 1 <= B <= GPOEO_PD_MAX_WINDOWS: traces, or sliding windows  */
-    int32_t num_channels;    /* C >= 1: per-lag channel scores are summed with weights      */
+    int32_t num_channels;    /* 1 <= C <= GPOEO_PD_MAX_CHANNELS: per-lag channel scores are
+                                summed with weights (the composite feature of Sec. 4.2)     */
     int32_t reserved0;       /* must be 0                                                   */
     int64_t n;               /* N >= 8 samples per window                                   */
     int64_t window_stride;   /* samples between window starts (N*C when packed)            */

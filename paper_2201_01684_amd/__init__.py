@@ -16,6 +16,7 @@ from ._binding import (  # noqa: F401
     FFT_SCORES,
     MFMA_SCORES,
     LIB_PATH,
+    MAX_CHANNELS,
     MAX_QUERIES,
     MAX_WINDOWS,
     NO_RESCUE,
@@ -25,6 +26,7 @@ from ._binding import (  # noqa: F401
     UNRESOLVED,
     ROLLING_DTYPE,
     Desc,
+    DetectParams,
     Detector,
     RollingDetector,
     GpoeoError,

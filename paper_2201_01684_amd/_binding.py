@@ -52,6 +52,7 @@ class PlanInfo(ctypes.Structure):
 ROLLING_MAX = 16
 MAX_WINDOWS = 1 << 21       # GPOEO_PD_MAX_WINDOWS
 MAX_QUERIES = 1 << 23       # GPOEO_PD_MAX_QUERIES
+MAX_CHANNELS = 256          # GPOEO_PD_MAX_CHANNELS
 
 
 class RollingParams(ctypes.Structure):
@@ -278,20 +279,40 @@ def results_to_numpy(results: torch.Tensor) -> np.ndarray:
     return host.view(RESULT_DTYPE).reshape(-1)
 
 
-def detect_period(traces: torch.Tensor, tmin: int, tmax: int, *, n: int | None = None,
+class DetectParams:
+    """Selection parameters and flags of one detect_period call (defaults: c_lag 0.9,
+    err_max 1.0, no flags)."""
+
+    def __init__(self, c_lag: float = DEFAULT_C_LAG, err_max: float = DEFAULT_ERR_MAX,
+                 flags: int = 0, weights=None):
+        self.c_lag, self.err_max, self.flags, self.weights = c_lag, err_max, flags, weights
+
+
+def detect_period(traces: torch.Tensor, n: int | None, tmin: int, tmax: int, params=None, *,
                   window_stride: int | None = None, num_windows: int | None = None,
-                  weights=None, c_lag: float = DEFAULT_C_LAG,
-                  err_max: float = DEFAULT_ERR_MAX, flags: int = 0, want_scores: bool = True,
-                  stream=None):
+                  want_scores: bool = True, stream=None):
     """Score every lag in [tmin, tmax] of every window and select each window's period.
 
-    ``traces`` is a float32 GPU tensor shaped [B, N] (one channel), [B, C, N]
-    (channel scores summed with ``weights``), or a 1-D long trace cut into
+    The call of Algorithm 1's problem statement: a batch of sample sequences
+    (T_s = 1 sample) in, per-window scores S(T) and the iteration period out.
+
+    ``traces`` is a float32 GPU tensor shaped [B, M] (one channel), [B, C, M]
+    (channel scores summed with ``params.weights``), or a 1-D long trace cut into
     ``num_windows`` windows of ``n`` samples starting every ``window_stride``
-    samples.  Returns ``(scores, results)``: scores is a float32 [B, L] tensor
-    (L = tmax - tmin + 1, scores[b, T - tmin] = S(T)) or None, and results a
-    numpy structured array with one record per window (period, verdict, err, ...).
+    samples.  ``n`` is the window length N; with a 2-D or 3-D tensor each window
+    is the first N of its row's M samples, and None means N = M.  ``params`` is
+    a DetectParams, a dict of its fields, or None for the defaults.
+
+    Returns ``(scores, period, results)``: scores is a float32 [B, L] GPU tensor
+    (L = tmax - tmin + 1, scores[b, T - tmin] = S(T)) or None, period an int32
+    [B] GPU tensor (0 where no period was selected), and results a numpy
+    structured array with one record per window (period, verdict, err, ...), or
+    None with GPOEO_PD_SCORES_ONLY (period is then all zeros).
     """
+    if params is None:
+        params = DetectParams()
+    elif isinstance(params, dict):
+        params = DetectParams(**params)
     if traces.dim() == 1:
         if n is None or window_stride is None:
             raise ValueError("a 1-D trace needs n and window_stride")
@@ -299,19 +320,26 @@ def detect_period(traces: torch.Tensor, tmin: int, tmax: int, *, n: int | None =
             num_windows = (traces.numel() - n) // window_stride + 1
         b, c, cs = num_windows, 1, n
     elif traces.dim() == 2:
-        b, n_ = traces.shape
-        c, n, window_stride, cs = 1, n_, n_, n_
+        b, m = traces.shape
+        c, window_stride, cs = 1, m, m
     elif traces.dim() == 3:
-        b, c, n_ = traces.shape
-        n, window_stride, cs = n_, c * n_, n_
+        b, c, m = traces.shape
+        window_stride, cs = c * m, m
     else:
         raise ValueError("traces must be 1-D, 2-D or 3-D")
-    desc, w = make_desc(b, c, n, window_stride, cs, tmin, tmax, c_lag, err_max, weights, flags)
+    if traces.dim() > 1:
+        if n is None:
+            n = m
+        if not 0 < n <= m:
+            raise ValueError(f"window length {n} does not fit rows of {m} samples")
+    desc, w = make_desc(b, c, n, window_stride, cs, tmin, tmax, params.c_lag, params.err_max,
+                        params.weights, params.flags)
     det = Detector(traces.contiguous(), desc, w, want_scores=want_scores)
     det.run(stream)
-    torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
-    res = None if (flags & SCORES_ONLY) else det.results_numpy()
-    return det.scores, res
+    period = det.results[:, 0].clone()
+    (torch.cuda.current_stream() if stream is None else stream).synchronize()
+    res = None if (params.flags & SCORES_ONLY) else det.results_numpy()
+    return det.scores, period, res
 
 
 def rolling_params(c_measure: float = C_MEASURE, step: float = STEP, c_eval: float = C_EVAL,

@@ -11,7 +11,7 @@ namespace gpoeo {
 constexpr int kWave = 64;            // CDNA wavefront width
 constexpr int kBlockSamples = 16;    // samples per register block of the score kernel
 constexpr int kRunSamples = 256;     // samples per fp32 run before the fp64 flush
-constexpr int kMaxChannels = 256;    // channel weights travel as a kernel argument
+constexpr int kMaxChannels = GPOEO_PD_MAX_CHANNELS;   // weights travel as a kernel argument
 
 // Relative error bound of a score accumulated in fp32 runs of kRunSamples
 // non-negative terms (each run: kRunSamples roundings plus the rounding of the

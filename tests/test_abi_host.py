@@ -140,6 +140,24 @@ def test_size_limits(lib):
                                    0x300000, B.MAX_QUERIES + 1, 0x400000, None) == B.EINVAL
 
 
+def test_channel_limit_is_the_header_limit(lib):
+    """The header states 1 <= C <= GPOEO_PD_MAX_CHANNELS; the library enforces
+    exactly that bound, and the binding carries the same constant."""
+    text = open(HEADER).read()
+    m = re.search(r"#define GPOEO_PD_MAX_CHANNELS (\d+)", text)
+    assert m, "the header must define GPOEO_PD_MAX_CHANNELS"
+    limit = int(m.group(1))
+    assert limit == B.MAX_CHANNELS == 256
+    assert re.search(r"num_channels;\s*/\*\s*1 <= C <= GPOEO_PD_MAX_CHANNELS", text)
+    ok, _ = good_desc(num_channels=limit, channel_stride=4096, window_stride=4096 * limit)
+    assert B.workspace_bytes(ok) > 0
+    bad, _ = good_desc(num_channels=limit + 1, channel_stride=4096,
+                       window_stride=4096 * (limit + 1))
+    with pytest.raises(B.GpoeoError) as e:
+        B.workspace_bytes(bad)
+    assert e.value.status == B.EINVAL
+
+
 def test_reserved_fields_must_be_zero(lib):
     d, _ = good_desc()
     d.reserved0 = 1

@@ -218,3 +218,48 @@ def test_very_long_windows(n, tmin, tmax):
     # block, combined in fp64 in chunk order; every lag against the oracle
     x = planted_trace(n, 61 if tmax < 100 else 1234, 6, seed=n % 97, sigma=1.0)
     parity(x, oracle.Layout(1, 1, n, n, n, tmin, tmax), f"n={n}")
+
+
+def test_detect_period_convenience_returns_scores_period_results():
+    """detect_period(traces, N, Tmin, Tmax, params) -> (scores [B, L] fp32,
+    period [B] int32 on the GPU, results): 2-D, 3-D with N shorter than the rows,
+    and a 1-D long trace cut at a stride, each against the oracle."""
+    import paper_2201_01684_amd as pkg
+    dev = _device()
+    wl = make_workload("w2", traces=3, n=8192, tmax=1024, pmax=800)
+    x2 = torch.from_numpy(wl.x.reshape(3, -1)).to(dev)
+    scores, period, res = pkg.detect_period(x2, wl.n, wl.tmin, wl.tmax)
+    assert scores.dtype == torch.float32 and tuple(scores.shape) == (3, wl.tmax - wl.tmin + 1)
+    assert period.dtype == torch.int32 and period.is_cuda and tuple(period.shape) == (3,)
+    o, out = oracle.detect(wl.x, oracle.Layout.of(wl))
+    check_scores(scores.double().cpu().numpy(), o, "2-D")
+    check_results(res, out, "2-D")
+    assert np.array_equal(period.cpu().numpy(), out["period"])
+
+    # [B, C, M] with N < M: each window is the first N samples of its rows
+    m, n = 6000, 5000
+    xb = planted_trace(3 * 2 * m, 211, 5, seed=7, sigma=1.0).reshape(3, 2, m)
+    w = np.array([1.0, 0.5], dtype=np.float32)
+    scores, period, res = pkg.detect_period(torch.from_numpy(xb).to(dev), n, 2, 2000,
+                                            pkg.DetectParams(weights=w))
+    lay = oracle.Layout(3, 2, n, 2 * m, m, 2, 2000, weights=w)
+    o, out = oracle.detect(xb.reshape(-1), lay)
+    check_scores(scores.double().cpu().numpy(), o, "3-D")
+    check_results(res, out, "3-D")
+    assert np.array_equal(period.cpu().numpy(), out["period"])
+
+    # one long trace, windows of N at a stride, parameters as a dict
+    xl = planted_trace(40000, 333, 6, seed=9, sigma=1.5)
+    scores, period, res = pkg.detect_period(torch.from_numpy(xl).to(dev), 16384, 2, 4096,
+                                            {"c_lag": 0.9}, window_stride=4000)
+    lay = oracle.Layout(6, 1, 16384, 4000, 16384, 2, 4096)
+    o, out = oracle.detect(xl, lay)
+    check_scores(scores.double().cpu().numpy(), o, "1-D")
+    check_results(res, out, "1-D")
+    assert np.array_equal(period.cpu().numpy(), out["period"])
+    assert np.all(out["period"] == 333)
+
+    # scores only: no results, period all zeros
+    scores, period, res = pkg.detect_period(x2, wl.n, wl.tmin, wl.tmax,
+                                            pkg.DetectParams(flags=pkg.SCORES_ONLY))
+    assert res is None and int(period.abs().sum()) == 0
