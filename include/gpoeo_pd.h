@@ -98,6 +98,8 @@ extern "C" {
 #define GPOEO_PD_EINVAL (-1)   /* invalid descriptor or pointer; nothing was launched      */
 #define GPOEO_PD_ENOMEM (-2)   /* workspace smaller than gpoeo_pd_workspace_bytes()        */
 #define GPOEO_PD_EHIP (-3)     /* a HIP launch failed (hipGetLastError after enqueueing)    */
+#define GPOEO_PD_ETOOBIG (-4)  /* gpoeo_pd_detect_noalloc: the call needs more workspace than
+                                  GPOEO_PD_NOALLOC_MAX_WORKSPACE; nothing was launched     */
 
 /* Per-window verdicts. */
 #define GPOEO_PD_PERIODIC 0    /* a period was selected and err < err_max                  */
@@ -207,6 +209,26 @@ int gpoeo_pd_workspace_bytes(const gpoeo_pd_desc* desc, size_t* bytes);
 int gpoeo_pd_detect(const gpoeo_pd_desc* desc, const float* x, float* scores,
                     gpoeo_pd_result* results, void* workspace, size_t workspace_bytes,
                     hipStream_t stream);
+
+/* gpoeo_pd_detect for callers that cannot allocate device memory (code under
+ * HIP graph capture, serving loops, harnesses that forbid hipMalloc): the same
+ * kernels, with the workspace taken from a static device array of
+ * GPOEO_PD_NOALLOC_MAX_WORKSPACE bytes that the library holds on every GPU it
+ * runs on until the process ends.  The call itself allocates nothing; its
+ * first call on a device looks up that device's array once.
+ *   x, scores, results, stream   as in gpoeo_pd_detect; `stream` must belong
+ *              to the current device.
+ * Every call on one GPU shares that GPU's array: calls that overlap there (on
+ * concurrent streams, or from several threads) race and must be serialised by
+ * the caller.  The array's contents on entry are ignored.
+ * Returns GPOEO_PD_EINVAL as gpoeo_pd_detect does, GPOEO_PD_ETOOBIG when
+ * gpoeo_pd_workspace_bytes(desc) exceeds GPOEO_PD_NOALLOC_MAX_WORKSPACE (both
+ * before launching anything), GPOEO_PD_EHIP if the array cannot be located or
+ * a launch failed. */
+#define GPOEO_PD_NOALLOC_MAX_WORKSPACE ((size_t)64 << 20)
+
+int gpoeo_pd_detect_noalloc(const gpoeo_pd_desc* desc, const float* x, float* scores,
+                            gpoeo_pd_result* results, hipStream_t stream);
 
 /* gpoeo_pd_detect, additionally recording stage_events[k] on `stream` right
  * before stage k is enqueued (0 window statistics, 1 lag scores, 2 score

@@ -17,7 +17,7 @@ import torch  # noqa: F401  (loads the HIP runtime the library must share)
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libgpoeo_pd.so")
 
-OK, EINVAL, ENOMEM, EHIP = 0, -1, -2, -3
+OK, EINVAL, ENOMEM, EHIP, ETOOBIG = 0, -1, -2, -3, -4
 PERIODIC, APERIODIC, CONSTANT = 0, 1, 2
 SCORES_ONLY, NO_RESCUE, FFT_SCORES, MFMA_SCORES = 1, 2, 4, 8
 UNRESOLVED = 1
@@ -113,7 +113,8 @@ EXPORTS = ("gpoeo_pd_abi_version", "gpoeo_pd_strerror", "gpoeo_pd_workspace_byte
            "gpoeo_pd_describe_plan", "gpoeo_pd_detect", "gpoeo_pd_detect_staged",
            "gpoeo_pd_rolling_workspace_bytes", "gpoeo_pd_detect_rolling", "gpoeo_pd_similarity",
            "gpoeo_pd_score_centred", "gpoeo_pd_spectral_workspace_bytes",
-           "gpoeo_pd_spectral_candidates")
+           "gpoeo_pd_spectral_candidates", "gpoeo_pd_detect_noalloc")
+NOALLOC_MAX_WORKSPACE = 64 << 20   # GPOEO_PD_NOALLOC_MAX_WORKSPACE
 
 _lib = None
 
@@ -139,6 +140,10 @@ def load_library():
         lib.gpoeo_pd_detect.argtypes = [ctypes.POINTER(Desc), ctypes.c_void_p, ctypes.c_void_p,
                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                         ctypes.c_void_p]
+        lib.gpoeo_pd_detect_noalloc.restype = ctypes.c_int
+        lib.gpoeo_pd_detect_noalloc.argtypes = [ctypes.POINTER(Desc), ctypes.c_void_p,
+                                                ctypes.c_void_p, ctypes.c_void_p,
+                                                ctypes.c_void_p]
         lib.gpoeo_pd_detect_staged.restype = ctypes.c_int
         lib.gpoeo_pd_detect_staged.argtypes = [ctypes.POINTER(Desc), ctypes.c_void_p,
                                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,

@@ -24,7 +24,7 @@ LIB_NAME = "libgpoeo_pd.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
 
 SOURCES = ["api.cpp", "lag_score.hip", "window_stats.hip", "select.hip", "rolling.hip",
-           "similarity.hip", "fft_score.hip", "centred.hip", "mfma_score.hip"]
+           "similarity.hip", "fft_score.hip", "centred.hip", "mfma_score.hip", "noalloc.hip"]
 # The selection re-evaluates scores and thresholds as plain fp64 expressions
 # (one rounding per operation, as written); no multiply-add contraction there,
 # nor in the FFT, whose error bound assumes separately rounded products.

@@ -553,6 +553,7 @@ const char* gpoeo_pd_strerror(int status) {
         case GPOEO_PD_EINVAL: return "invalid argument";
         case GPOEO_PD_ENOMEM: return "workspace too small";
         case GPOEO_PD_EHIP: return "HIP launch failed";
+        case GPOEO_PD_ETOOBIG: return "workspace larger than the static no-allocation scratch";
         default: return "unknown status";
     }
 }

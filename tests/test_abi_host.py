@@ -341,3 +341,24 @@ def test_spectral_workspace_and_pointers(lib):
     assert call(ctypes.byref(d), None, 0x100000, 0x200000, 0x300000, need, None) == B.EINVAL
     assert call(ctypes.byref(d), ctypes.byref(p), 0x100000, None, 0x300000, need,
                 None) == B.EINVAL
+
+
+def test_noalloc_validates_on_the_host_before_touching_the_device(lib):
+    """gpoeo_pd_detect_noalloc: an invalid descriptor or pointer is EINVAL and a
+    workload whose workspace exceeds the static scratch is ETOOBIG, both decided
+    on the host (fake device addresses are never dereferenced)."""
+    call = lib.gpoeo_pd_detect_noalloc
+    x, res = 0x100000, 0x200000
+    d, _ = good_desc()
+    assert call(None, x, None, res, None) == B.EINVAL
+    assert call(ctypes.byref(d), None, None, res, None) == B.EINVAL
+    assert call(ctypes.byref(d), x, None, None, None) == B.EINVAL
+    bad, _ = good_desc(tmax=4000)
+    assert call(ctypes.byref(bad), x, None, res, None) == B.EINVAL
+    big, _ = B.make_desc(1024, 1, 262144, 262144, 262144, 2, 32768)
+    assert B.workspace_bytes(big) > B.NOALLOC_MAX_WORKSPACE
+    assert call(ctypes.byref(big), x, None, res, None) == B.ETOOBIG
+    text = open(HEADER).read()
+    assert "#define GPOEO_PD_NOALLOC_MAX_WORKSPACE ((size_t)64 << 20)" in text
+    assert B.NOALLOC_MAX_WORKSPACE == 64 << 20
+    assert B.strerror(B.ETOOBIG) == "workspace larger than the static no-allocation scratch"
