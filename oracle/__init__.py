@@ -20,23 +20,33 @@ from dataclasses import dataclass
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "liboracle_pd.so")
+# GPOEO_ORACLE_LIBRARY names another build of oracle.c to load instead (the
+# sanitized build of the CPU sanitizer check); by default the in-tree one.
+LIB_PATH = os.environ.get("GPOEO_ORACLE_LIBRARY") or os.path.join(HERE, "liboracle_pd.so")
+SAN_LIB_PATH = os.path.join(os.path.dirname(HERE), "_build", "oraclesan", "liboracle_pd.so")
 
 PERIODIC, APERIODIC, CONSTANT = 0, 1, 2
 DEFAULT_C_LAG = 0.9
 DEFAULT_ERR_MAX = 1.0
 
 
-def build(verbose: bool = False) -> str:
-    """Compile oracle.c into liboracle_pd.so (always recompiles)."""
-    cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+def build(verbose: bool = False, sanitize: bool = False) -> str:
+    """Compile oracle.c into liboracle_pd.so (always recompiles).  sanitize=True
+    builds it with AddressSanitizer and UndefinedBehaviorSanitizer (any finding
+    aborts) into SAN_LIB_PATH instead; a process loading that build preloads
+    gcc's libasan and libubsan."""
+    out = SAN_LIB_PATH if sanitize else os.path.join(HERE, "liboracle_pd.so")
+    opt = ["-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+           "-fno-omit-frame-pointer"] if sanitize else ["-O2"]
+    cmd = ["gcc", *opt, "-std=c11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
            "-fPIC", "-shared", "-Wall", "-Wextra", "-Werror",
-           os.path.join(HERE, "oracle.c"), "-o", LIB_PATH + ".tmp", "-lm"]
+           os.path.join(HERE, "oracle.c"), "-o", out + ".tmp", "-lm"]
     if verbose:
         print(" ".join(cmd))
+    os.makedirs(os.path.dirname(out), exist_ok=True)
     subprocess.run(cmd, check=True)
-    os.replace(LIB_PATH + ".tmp", LIB_PATH)
-    return LIB_PATH
+    os.replace(out + ".tmp", out)
+    return out
 
 
 class _Params(ctypes.Structure):

@@ -15,7 +15,9 @@ import numpy as np
 import torch  # noqa: F401  (loads the HIP runtime the library must share)
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libgpoeo_pd.so")
+# GPOEO_PD_LIBRARY names another build of the same library to load instead (the
+# host-sanitized build of the CPU sanitizer check); by default the in-tree one.
+LIB_PATH = os.environ.get("GPOEO_PD_LIBRARY") or os.path.join(HERE, "libgpoeo_pd.so")
 
 OK, EINVAL, ENOMEM, EHIP, ETOOBIG = 0, -1, -2, -3, -4
 PERIODIC, APERIODIC, CONSTANT = 0, 1, 2

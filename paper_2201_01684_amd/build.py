@@ -58,9 +58,32 @@ def _torch_lib_dir() -> str | None:
     return None
 
 
-def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(OBJ_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [_hipcc(), *HIP_FLAGS, *EXTRA_FLAGS.get(src, []), "-x", "hip", "-c",
+# Host-code sanitizer build (a CPU check of the argument validation, plan and
+# workspace arithmetic): AddressSanitizer and UndefinedBehaviorSanitizer on the
+# host side of every source only (each flag after -Xarch_host; the gfx950 code
+# is built as usual), into _build/, never next to the package.  Its runtime is
+# not linked in: the process that loads it preloads ROCm clang's ASan runtime.
+SAN_DIR = os.path.join(ROOT, "_build", "hostsan")
+SAN_LIB_PATH = os.path.join(SAN_DIR, LIB_NAME)
+SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-Xarch_host", "-fno-sanitize-recover=all", "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def sanitizer_runtime() -> str:
+    """ROCm clang's shared ASan runtime (it carries the UBSan handlers too)."""
+    import glob
+    hits = sorted(glob.glob("/opt/rocm/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so"))
+    if not hits:
+        raise RuntimeError("clang ASan runtime not found under /opt/rocm/llvm")
+    return hits[-1]
+
+
+def _compile(src: str, verbose: bool, sanitize: bool = False) -> str:
+    obj_dir = os.path.join(SAN_DIR, "obj") if sanitize else OBJ_DIR
+    obj = os.path.join(obj_dir, os.path.splitext(src)[0] + ".o")
+    flags = [f for f in HIP_FLAGS if f != "-O3"] + ["-O1", "-g", *SAN_FLAGS] if sanitize \
+        else HIP_FLAGS
+    cmd = [_hipcc(), *flags, *EXTRA_FLAGS.get(src, []), "-x", "hip", "-c",
            os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -70,12 +93,14 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and link the shared library (always rebuilds)."""
-    os.makedirs(OBJ_DIR, exist_ok=True)
+def build(verbose: bool = False, sanitize: bool = False) -> str:
+    """Compile every source and link the shared library (always rebuilds).
+    sanitize=True builds the host-sanitized library at SAN_LIB_PATH instead."""
+    lib_path = SAN_LIB_PATH if sanitize else LIB_PATH
+    os.makedirs(os.path.join(SAN_DIR, "obj") if sanitize else OBJ_DIR, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=min(4, len(SOURCES))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    link = [_hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", LIB_PATH + ".tmp"]
+        objs = list(ex.map(lambda s: _compile(s, verbose, sanitize), SOURCES))
+    link = [_hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", lib_path + ".tmp"]
     tl = _torch_lib_dir()
     if tl:
         link += [f"-L{tl}", f"-Wl,-rpath,{tl}"]
@@ -84,10 +109,9 @@ def build(verbose: bool = False) -> str:
     r = subprocess.run(link, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(LIB_PATH + ".tmp", LIB_PATH)
-    return LIB_PATH
+    os.replace(lib_path + ".tmp", lib_path)
+    return lib_path
 
 
 if __name__ == "__main__":
-    build(verbose="-v" in sys.argv)
-    print(LIB_PATH)
+    print(build(verbose="-v" in sys.argv, sanitize="--sanitize-host" in sys.argv))
