@@ -79,6 +79,9 @@ def parse():
     ap.add_argument("--no-fft-compare", action="store_true",
                     help="detect mode: skip the untimed FFT- and matrix-core-scores runs of the "
                          "same batch")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="detect mode: skip the per-configuration timings (c1-c5) after the "
+                         "timed region")
     ap.add_argument("--fft-scores", action="store_true",
                     help="rolling mode: score with GPOEO_PD_FFT_SCORES")
     ap.add_argument("--mfma-scores", action="store_true",
@@ -244,6 +247,109 @@ def call_roofline(kernel, bound, work, ms, extra=None):
     if extra:
         line.update(extra)
     return line
+
+
+# The five trace configurations, timed after the headline's timed region:
+# repeats of the per-call timing (median and minimum), and the windows the
+# oracle checks.  c3 is the headline workload itself.
+CONFIGS = (("c1", "w1", 1000, (0,)), ("c2", "w2", 100, (0, 63)), ("c3", "w3", 5, (0,)),
+           ("c4", "w4", 20, (0, 2040, 2044, 2048, 4088)), ("c5", "w5", 5, (0,)))
+
+
+def bench_config(pkg, ev, wl, repeats, check_windows, x=None, warmup=2):
+    """One configuration: `repeats` back-to-back gpoeo_pd_detect calls timed by
+    wall clock around the loop (throughput), then up to 100 calls with per-stage
+    HIP events (median and minimum per call, the lag-score stage for the
+    roofline), planted-period hits and the oracle on a few windows."""
+    import numpy as np
+    import torch
+    import oracle
+    dev = torch.device("cuda:0")
+    if x is None:
+        x = torch.from_numpy(wl.x).to(dev)
+    desc, keep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
+                               wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights)
+    det = pkg.Detector(x, desc, keep, want_scores=True)
+    plan = pkg.describe_plan(desc)
+    pairs, scored = float(wl.pairs()), plan["pairs_scored"]
+    for _ in range(warmup):
+        det.run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(repeats):
+        det.run()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / repeats
+    n_ev = min(repeats, 100)
+    sets = [ev.create(5) for _ in range(n_ev)]
+    torch.cuda.synchronize()
+    for k in range(n_ev):
+        det.run_staged(sets[k])
+    torch.cuda.synchronize()
+    call = np.array([ev.elapsed_ms(s_[0], s_[4]) for s_ in sets])
+    score = np.array([ev.elapsed_ms(s_[1], s_[2]) for s_ in sets])
+    select = np.array([ev.elapsed_ms(s_[3], s_[4]) for s_ in sets])
+    for s_ in sets:
+        ev.destroy(s_)
+    res = det.results_numpy()
+    med = float(np.median(call))
+    out = {"workload": wl.name, "description": wl.meta["description"], "sha256": wl.sha256,
+           "windows": wl.num_windows, "channels": wl.num_channels, "n": wl.n,
+           "tmin": wl.tmin, "tmax": wl.tmax, "pairs": pairs, "pairs_scored": scored,
+           "repeats": repeats, "ms_per_call_back_to_back": wall,
+           "call_ms": {"median": med, "min": float(call.min()), "calls": n_ev},
+           "lag_samples_per_sec": pairs / (med / 1e3),
+           "traces_per_sec": wl.num_windows / (med / 1e3),
+           "lag_score_ms": float(np.median(score)),
+           "select_ms": float(np.median(select)),
+           "frac_fp32_lag_score": FLOP_PER_PAIR * scored / (float(np.median(score)) / 1e3)
+                                  / 1e12 / FP32_VECTOR_PEAK_TFLOPS,
+           "frac_fp32_call": FLOP_PER_PAIR * scored / (med / 1e3) / 1e12
+                             / FP32_VECTOR_PEAK_TFLOPS,
+           "windows_rescored": int(np.count_nonzero(res["n_rescored"])),
+           "windows_flagged_unresolved": int(np.count_nonzero(res["flags"] & pkg.UNRESOLVED))}
+    if wl.truth is not None:
+        d = wl.truth > 0
+        ok = (np.abs(res["period"][d] - wl.truth[d]) <= np.ceil(0.02 * wl.truth[d])
+              if wl.jitter else res["period"][d] == wl.truth[d])
+        out["planted_period_hits"] = f"{int(ok.sum())}/{int(d.sum())}"
+    s_host = det.scores.double().cpu().numpy()
+    match, worst = 0, 0.0
+    for b in check_windows:
+        base = b * wl.window_stride
+        sub = wl.x[base: base + (wl.num_channels - 1) * wl.channel_stride + wl.n]
+        o_s, o_out = oracle.detect(sub, oracle.Layout.of(wl, num_windows=1))
+        nz = o_s[0] != 0
+        worst = max(worst, float(np.max(np.abs(s_host[b][nz] - o_s[0][nz]) / o_s[0][nz])))
+        match += int(all(o_out[f][0] == res[f][b] for f in
+                         ("period", "verdict", "t_cand", "t_low", "t_up", "n_candidates")))
+    out["oracle_check"] = {"windows": list(check_windows), "selections_equal": match,
+                           "max_score_rel_err": worst}
+    del det
+    # the same batch with FFT scores and with matrix-core scores: wall time per
+    # call over back-to-back calls, and whether every selection field equals
+    # the direct path's
+    for key, flag in (("fft_scores", pkg.FFT_SCORES), ("mfma_scores", pkg.MFMA_SCORES)):
+        adesc, akeep = pkg.make_desc(wl.num_windows, wl.num_channels, wl.n, wl.window_stride,
+                                     wl.channel_stride, wl.tmin, wl.tmax, weights=wl.weights,
+                                     flags=flag)
+        adet = pkg.Detector(x, adesc, akeep, want_scores=False)
+        adet.run()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(repeats):
+            adet.run()
+        torch.cuda.synchronize()
+        a_ms = (time.perf_counter() - t0) * 1e3 / repeats
+        ares = adet.results_numpy()
+        same = all(np.array_equal(ares[f], res[f]) for f in
+                   ("period", "verdict", "t_cand", "t_low", "t_up", "n_candidates"))
+        out[key] = {"ms_per_call_back_to_back": a_ms, "lag_samples_per_sec": pairs / (a_ms / 1e3),
+                    "traces_per_sec": wl.num_windows / (a_ms / 1e3),
+                    "selections_equal_direct": bool(same)}
+        del adet
+        torch.cuda.empty_cache()
+    return out
 
 
 def timed_calls(call, steps):
@@ -442,6 +548,23 @@ def main():
         else:
             ok = res["period"][d] == wl.truth[d]
         line["planted_period_hits"] = f"{int(ok.sum())}/{int(d.sum())}"
+    if args.mode == "detect" and not args.no_configs:
+        # every trace configuration, after and outside the timed region
+        if "det" in locals():
+            del det
+        torch.cuda.empty_cache()
+        configs = {}
+        for key, name, repeats, check in CONFIGS:
+            if name == wl.name:
+                cwl, cx = wl, x
+            else:
+                cwl, cx = make_workload(name), None
+            configs[key] = bench_config(pkg, ev, cwl, repeats, check, x=cx)
+            del cwl, cx
+            torch.cuda.empty_cache()
+            print(f"# {key} ({name}): {configs[key]['call_ms']['median']:.4f} ms per call",
+                  file=sys.stderr, flush=True)
+        line["configs"] = configs
 
     if not args.no_cpu_baseline:
         import oracle
@@ -472,6 +595,12 @@ def main():
                                           f"{wl.lags} lags each, {t_cpu:.1f} s"}
         line["parity_sample"] = {"windows": done, "period_match": match,
                                  "max_score_rel_err": worst}
+    # Device memory is released and the stream drained before the line is
+    # printed; bench.py starts no child process (the oracle's OpenMP workers
+    # are threads of this one), so nothing outlives the JSON line.
+    del x, scores
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
     print(json.dumps(line), flush=True)
 
 

@@ -85,9 +85,9 @@ def _template(levels: np.ndarray, lengths: np.ndarray) -> np.ndarray:
 
 
 def _tile(template: np.ndarray, n: int, start: int = 0) -> np.ndarray:
+    """template[(i + start) mod P] for i < n, as a cyclic copy."""
     p = template.shape[0]
-    idx = (np.arange(n, dtype=np.int64) + start) % p
-    return template[idx]
+    return np.resize(np.roll(template, -(start % p)), n)
 
 
 def planted_trace(n: int, period: int, k: int, *, seed: int = 0, lo: float = 100.0,

@@ -318,6 +318,21 @@ int gpoeo_pd_similarity(const gpoeo_pd_desc* desc, const gpoeo_pd_similarity_par
                         const float* x, const int32_t* windows, const int32_t* lags,
                         int64_t count, double* err, hipStream_t stream);
 
+/* gpoeo_pd_similarity, also reporting queries whose result rounding could
+ * change (Algorithm 2's grouping step).  Err depends on the fitted mixture
+ * only through the hard labels, and a plain fp64 fit in another evaluation
+ * order moves the fitted parameters by at most a few 1e-13 relative.  For
+ * every sample, the margin between its two largest log-densities is compared
+ * with the change that relative errors of 1e-11 in each parameter (mu, var,
+ * pi), plus the rounding of the densities, can cause in either; if it is not
+ * larger, the label could differ from an exact evaluation's and flags[k] is
+ * GPOEO_PD_UNRESOLVED (else 0).  err[k] is still written.
+ * flags: device uint32 [count], required when count > 0 (else EINVAL). */
+int gpoeo_pd_similarity_flagged(const gpoeo_pd_desc* desc,
+                                const gpoeo_pd_similarity_params* params, const float* x,
+                                const int32_t* windows, const int32_t* lags, int64_t count,
+                                double* err, uint32_t* flags, hipStream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Mean-removed score of finalist periods (Algorithm 2's relative values, Sec.
  * 4.1.2, with one group per sample).  For query k, window windows[k] and

@@ -115,7 +115,8 @@ EXPORTS = ("gpoeo_pd_abi_version", "gpoeo_pd_strerror", "gpoeo_pd_workspace_byte
            "gpoeo_pd_describe_plan", "gpoeo_pd_detect", "gpoeo_pd_detect_staged",
            "gpoeo_pd_rolling_workspace_bytes", "gpoeo_pd_detect_rolling", "gpoeo_pd_similarity",
            "gpoeo_pd_score_centred", "gpoeo_pd_spectral_workspace_bytes",
-           "gpoeo_pd_spectral_candidates", "gpoeo_pd_detect_noalloc")
+           "gpoeo_pd_spectral_candidates", "gpoeo_pd_detect_noalloc",
+           "gpoeo_pd_similarity_flagged")
 NOALLOC_MAX_WORKSPACE = 64 << 20   # GPOEO_PD_NOALLOC_MAX_WORKSPACE
 
 _lib = None
@@ -167,6 +168,13 @@ def load_library():
         lib.gpoeo_pd_similarity.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(SimilarityParams),
                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                             ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+        lib.gpoeo_pd_similarity_flagged.restype = ctypes.c_int
+        lib.gpoeo_pd_similarity_flagged.argtypes = [ctypes.POINTER(Desc),
+                                                    ctypes.POINTER(SimilarityParams),
+                                                    ctypes.c_void_p, ctypes.c_void_p,
+                                                    ctypes.c_void_p, ctypes.c_int64,
+                                                    ctypes.c_void_p, ctypes.c_void_p,
+                                                    ctypes.c_void_p]
         lib.gpoeo_pd_spectral_workspace_bytes.restype = ctypes.c_int
         lib.gpoeo_pd_spectral_workspace_bytes.argtypes = [ctypes.POINTER(Desc),
                                                           ctypes.POINTER(SpectralParams),
@@ -419,9 +427,11 @@ def detect_rolling(traces: torch.Tensor, tmin: int, tmax: int, *, weights=None,
 
 def similarity(x: torch.Tensor, desc: Desc, windows: torch.Tensor, lags: torch.Tensor,
                num_groups: int = DEFAULT_GROUPS, em_iters: int = DEFAULT_EM_ITERS,
-               stream=None) -> torch.Tensor:
+               stream=None, with_flags: bool = False):
     """Algorithm 2's Err_T for (windows[k], lags[k]) (int32 GPU tensors); returns a
-    float64 GPU tensor (-1: fewer than two sub-curves, NaN: out of range)."""
+    float64 GPU tensor (-1: fewer than two sub-curves, NaN: out of range), and
+    with ``with_flags`` also an int32 GPU tensor of per-query flags
+    (UNRESOLVED: a hard label could change under rounding)."""
     if windows.dtype != torch.int32 or lags.dtype != torch.int32:
         raise TypeError("windows and lags must be int32 tensors")
     if windows.shape != lags.shape or windows.dim() != 1:
@@ -429,10 +439,19 @@ def similarity(x: torch.Tensor, desc: Desc, windows: torch.Tensor, lags: torch.T
     windows, lags = windows.contiguous(), lags.contiguous()
     err = torch.empty(windows.shape, dtype=torch.float64, device=x.device)
     p = SimilarityParams(int(num_groups), int(em_iters))
-    rc = load_library().gpoeo_pd_similarity(ctypes.byref(desc), ctypes.byref(p), x.data_ptr(),
-                                            windows.data_ptr(), lags.data_ptr(),
-                                            int(windows.numel()), err.data_ptr(),
-                                            _stream_handle(stream))
+    lib = load_library()
+    if with_flags:
+        flags = torch.empty(windows.shape, dtype=torch.int32, device=x.device)
+        rc = lib.gpoeo_pd_similarity_flagged(ctypes.byref(desc), ctypes.byref(p), x.data_ptr(),
+                                             windows.data_ptr(), lags.data_ptr(),
+                                             int(windows.numel()), err.data_ptr(),
+                                             flags.data_ptr(), _stream_handle(stream))
+        if rc != OK:
+            raise GpoeoError(rc, "gpoeo_pd_similarity_flagged")
+        return err, flags
+    rc = lib.gpoeo_pd_similarity(ctypes.byref(desc), ctypes.byref(p), x.data_ptr(),
+                                 windows.data_ptr(), lags.data_ptr(), int(windows.numel()),
+                                 err.data_ptr(), _stream_handle(stream))
     if rc != OK:
         raise GpoeoError(rc, "gpoeo_pd_similarity")
     return err

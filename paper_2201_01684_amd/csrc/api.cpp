@@ -701,10 +701,11 @@ int gpoeo_pd_detect_rolling(const gpoeo_pd_desc* desc, const gpoeo_pd_rolling_pa
 
 }  // extern "C"
 
-extern "C" int gpoeo_pd_similarity(const gpoeo_pd_desc* desc,
-                                   const gpoeo_pd_similarity_params* params, const float* x,
-                                   const int32_t* windows, const int32_t* lags, int64_t count,
-                                   double* err, hipStream_t stream) {
+namespace {
+
+int similarity_impl(const gpoeo_pd_desc* desc, const gpoeo_pd_similarity_params* params,
+                    const float* x, const int32_t* windows, const int32_t* lags, int64_t count,
+                    double* err, uint32_t* flags, hipStream_t stream) {
     gpoeo::Plan p;
     const int rc = gpoeo::make_plan(desc, &p);
     if (rc != GPOEO_PD_OK) return rc;
@@ -714,10 +715,28 @@ extern "C" int gpoeo_pd_similarity(const gpoeo_pd_desc* desc,
     if (count == 0) return GPOEO_PD_OK;
     if (!x || !windows || !lags || !err) return GPOEO_PD_EINVAL;
     if (gpoeo::launch_similarity(p, weights_of(desc, p.num_channels), params->num_groups,
-                                 params->em_iters, x, windows, lags, count, err,
+                                 params->em_iters, x, windows, lags, count, err, flags,
                                  stream) != hipSuccess)
         return GPOEO_PD_EHIP;
     return GPOEO_PD_OK;
+}
+
+}  // namespace
+
+extern "C" int gpoeo_pd_similarity(const gpoeo_pd_desc* desc,
+                                   const gpoeo_pd_similarity_params* params, const float* x,
+                                   const int32_t* windows, const int32_t* lags, int64_t count,
+                                   double* err, hipStream_t stream) {
+    return similarity_impl(desc, params, x, windows, lags, count, err, nullptr, stream);
+}
+
+extern "C" int gpoeo_pd_similarity_flagged(const gpoeo_pd_desc* desc,
+                                           const gpoeo_pd_similarity_params* params,
+                                           const float* x, const int32_t* windows,
+                                           const int32_t* lags, int64_t count, double* err,
+                                           uint32_t* flags, hipStream_t stream) {
+    if (count > 0 && !flags) return GPOEO_PD_EINVAL;
+    return similarity_impl(desc, params, x, windows, lags, count, err, flags, stream);
 }
 
 extern "C" int gpoeo_pd_score_centred(const gpoeo_pd_desc* desc, const float* x,

@@ -291,8 +291,9 @@ hipError_t launch_rolling_combine(const RollingCombineArgs& a, const Weights& w,
                                   int64_t num_windows, hipStream_t s);
 hipError_t launch_centred(const Plan& p, const Weights& w, const float* x, const int32_t* windows,
                           const int32_t* lags, int64_t count, double* out, hipStream_t s);
+// flags (nullable): [count] GPOEO_PD_UNRESOLVED where a hard label is fragile.
 hipError_t launch_similarity(const Plan& p, const Weights& w, int32_t groups, int32_t iters,
                              const float* x, const int32_t* windows, const int32_t* lags,
-                             int64_t count, double* err, hipStream_t s);
+                             int64_t count, double* err, uint32_t* flags, hipStream_t s);
 
 }  // namespace gpoeo

@@ -13,32 +13,73 @@
 // group-size weighted average is err_i, and Err_T is the mean of err_i over
 // the pairs, then the weighted mean over channels.  Err_T = -1 when Num_T < 2.
 //
-// One workgroup of kWaves wavefronts per (window, lag) query: wavefront v takes
-// the pairs i = v, v + kWaves, ...; its lanes stride over the samples of a
-// sub-curve, and every sum is a per-lane partial sum combined by a fixed
-// shuffle tree, so all lanes hold the same mixture parameters.  The pair
-// errors of the wavefronts are added in wavefront order.
+// Work mapping.  One workgroup of kThreads lanes per (window, lag) query.  The
+// lanes form segments of S lanes (S a power of two, 1..64, chosen per query
+// from T and the number of pairs so that the segments stay busy): segment g
+// takes the pairs g, g + kThreads/S, ...; its lanes stride over the samples of
+// a sub-curve and combine their partial sums with a butterfly of lane
+// shuffles inside the segment, so every lane of a segment holds the same
+// mixture parameters.  Short periods (many pairs) run one pair per lane with
+// no shuffles at all; long ones spread a pair over up to a wavefront.  Each
+// segment adds its pair errors in pair order, and the segments' sums are added
+// in segment order, so the result does not depend on scheduling.  Queries are
+// dealt to the XCDs in contiguous ranges, so the queries of one window (which
+// callers list together) share that XCD's L2.
+//
+// Arithmetic.  The E-step works with base-2 log-densities
+//   l_k(v) = log2 pi_k - log2(2 pi var_k) / 2 - (v - mu_k)^2 log2(e) / (2 var_k),
+// responsibilities 2^(l_k - max_j l_j) / sum (gmm_exp2_nonpos, a reciprocal
+// refined by two Newton steps), and accumulates the responsibility-weighted
+// count and first and second moments about the sub-curve mean in one pass;
+// the M-step's variance about the new mean follows from them.  These differ
+// from the definition's natural-log, divide-and-two-pass evaluation only by
+// roundings, which move the fitted parameters by a few 1e-13 relative at most
+// (measured between fp64 evaluation orders on the 1024-trace workload).
+//
+// Fragile labels.  Err depends on the parameters only through the hard
+// labels.  For every sample the final pass compares the margin between the
+// two largest log-densities with the change that a relative error of
+// kParamRel in each fitted parameter (mu, var, pi) can cause in each of them,
+// plus their own rounding; a sample whose label such errors could flip marks
+// its query GPOEO_PD_UNRESOLVED in the optional flags output.
 #include <cmath>
 
+#include "gmm_math.h"
 #include "internal.h"
 
 namespace gpoeo {
 namespace {
 
 constexpr int kMaxGroups = 8;
-constexpr int kWaves = 4;
+constexpr int kThreads = 256;
+// Relative parameter error assumed by the label margin test: 25 times the
+// largest difference measured between fp64 evaluation orders of the EM.
+constexpr double kParamRel = 1e-11;
+constexpr double kLog2e = 1.4426950408889634;
+constexpr double kTwoPi = 6.283185307179586;
 
-__device__ __forceinline__ double wave_sum(double v) {
-    for (int off = 32; off > 0; off >>= 1) v = v + __shfl_down(v, off);
-    return __shfl(v, 0);
+// Butterfly sums over the S lanes of a segment (S a power of two <= 64,
+// segments aligned within the wavefront); every lane ends with the same value.
+__device__ __forceinline__ double seg_sum(double v, int s) {
+    for (int o = s >> 1; o > 0; o >>= 1) v = v + __shfl_xor(v, o);
+    return v;
 }
-__device__ __forceinline__ double wave_min(double v) {
-    for (int off = 32; off > 0; off >>= 1) v = fmin(v, __shfl_down(v, off));
-    return __shfl(v, 0);
+__device__ __forceinline__ double seg_min(double v, int s) {
+    for (int o = s >> 1; o > 0; o >>= 1) v = fmin(v, __shfl_xor(v, o));
+    return v;
 }
-__device__ __forceinline__ double wave_max(double v) {
-    for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_down(v, off));
-    return __shfl(v, 0);
+__device__ __forceinline__ double seg_max(double v, int s) {
+    for (int o = s >> 1; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o));
+    return v;
+}
+
+// 1/x for x in [1, G] (a sum of responsibilities, the largest one 1): the
+// hardware estimate refined by two Newton steps.
+__device__ __forceinline__ double recip(double x) {
+    double r = __builtin_amdgcn_rcp(x);
+    r = fma(fma(-x, r, 1.0), r, r);
+    r = fma(fma(-x, r, 1.0), r, r);
+    return r;
 }
 
 __device__ __forceinline__ double smape(double a, double b) {
@@ -51,6 +92,7 @@ struct SimArgs {
     const int32_t* windows;
     const int32_t* lags;
     double* err;
+    uint32_t* flags;         // nullable
     int64_t count;
     int64_t num_windows;
     int64_t n;
@@ -61,22 +103,56 @@ struct SimArgs {
     int32_t iters;
 };
 
+// Segment width for a query: the S that minimises the pair rounds times the
+// sample steps of a round (plus a per-round allowance for the parameter
+// updates and the shuffles).  Every lane computes the same value.
+__device__ __forceinline__ int choose_segment(int64_t pairs, int64_t t) {
+    int best_s = 1;
+    double best = INFINITY;
+    for (int s = 1, lg = 0; s <= kWave; s <<= 1, ++lg) {
+        const int64_t per_round = kThreads / s;
+        const int64_t rounds = (pairs + per_round - 1) / per_round;
+        const double cost = (double)rounds * ((double)((t + s - 1) / s) + 3.0 + 0.3 * lg);
+        if (cost < best) {
+            best = cost;
+            best_s = s;
+        }
+    }
+    return best_s;
+}
+
+// Base-2 log-density coefficients of the current parameters.
+template <int G>
+__device__ __forceinline__ void log_coeffs(const double (&mu)[G], const double (&var)[G],
+                                           const double (&pi)[G], double (&lp)[G],
+                                           double (&h)[G]) {
+    (void)mu;
+#pragma unroll
+    for (int k = 0; k < G; ++k) {
+        lp[k] = log2(pi[k]) - 0.5 * log2(kTwoPi * var[k]);
+        h[k] = (0.5 * kLog2e) / var[k];
+    }
+}
+
+// Err_i of the pair (a, b) of sub-curves of t samples, computed by the s lanes
+// of a segment (this lane is number ls); also whether a hard label is fragile.
 template <int G>
 __device__ double pair_error(const float* __restrict__ a, const float* __restrict__ b, int64_t t,
-                             int32_t iters, int lane) {
-    const double two_pi = 6.283185307179586;
+                             int32_t iters, int s, int ls, bool& fragile) {
     double s_a = 0.0, s_b = 0.0, lo = INFINITY, hi = -INFINITY;
-    for (int64_t j = lane; j < t; j += kWave) {
+    for (int64_t j = ls; j < t; j += s) {
         const double va = (double)a[j], vb = (double)b[j];
         s_a += va;
         s_b += vb;
         lo = fmin(lo, va);
         hi = fmax(hi, va);
     }
-    const double mean_prev = wave_sum(s_a) / (double)t;
-    const double mean_back = wave_sum(s_b) / (double)t;
-    lo = wave_min(lo);
-    hi = wave_max(hi);
+    s_a = seg_sum(s_a, s);
+    s_b = seg_sum(s_b, s);
+    lo = seg_min(lo, s);
+    hi = seg_max(hi, s);
+    const double mean_prev = s_a / (double)t;
+    const double mean_back = s_b / (double)t;
 
     double mu[G], var[G], pi[G];
     const bool constant = hi == lo;
@@ -91,66 +167,41 @@ __device__ double pair_error(const float* __restrict__ a, const float* __restric
         }
         for (int32_t it = 0; it < iters; ++it) {
             double lp[G], h[G];
-#pragma unroll
-            for (int k = 0; k < G; ++k) {
-                lp[k] = log(pi[k]) - 0.5 * log(two_pi * var[k]);
-                h[k] = 0.5 / var[k];
-            }
-            // responsibilities of the current parameters, normalised per
-            // sample: exp(l_k - max_k l_k), so the largest term is exactly 1
-            // and only the other G - 1 need an exponential
-            auto resp = [&](double v, double (&r)[G]) {
-                double best = -INFINITY;
-                int top = 0;
-#pragma unroll
-                for (int k = 0; k < G; ++k) {
-                    const double d = v - mu[k];
-                    r[k] = lp[k] - d * d * h[k];
-                    if (r[k] > best) {
-                        best = r[k];
-                        top = k;
-                    }
-                }
-                double sum = 1.0;
-#pragma unroll
-                for (int k = 0; k + 1 < G; ++k) {   // the k-th component other than top
-                    const int idx = k < top ? k : k + 1;
-                    double val = r[0];
-#pragma unroll
-                    for (int m = 1; m < G; ++m) val = idx == m ? r[m] : val;
-                    const double e = exp(val - best);
-                    sum += e;
-#pragma unroll
-                    for (int m = 0; m < G; ++m) r[m] = idx == m ? e : r[m];
-                }
-                const double inv = 1.0 / sum;
-#pragma unroll
-                for (int k = 0; k < G; ++k) r[k] = k == top ? inv : r[k] * inv;
-            };
-            // One pass: responsibility-weighted count, first and second moment
-            // about the sub-curve mean c; the M-step's variance about the new
-            // mean m_k is then sum r (x-c)^2 / n_k - (m_k - c)^2 (the same value
-            // as a second pass about m_k, up to rounding).
+            log_coeffs<G>(mu, var, pi, lp, h);
             double nk[G], s1[G], s2[G];
 #pragma unroll
             for (int k = 0; k < G; ++k) nk[k] = s1[k] = s2[k] = 0.0;
-            for (int64_t j = lane; j < t; j += kWave) {
+            for (int64_t j = ls; j < t; j += s) {
                 const double v = (double)a[j];
-                const double d = v - mean_prev;
-                double r[G];
-                resp(v, r);
+                double l[G], best = -INFINITY;
 #pragma unroll
                 for (int k = 0; k < G; ++k) {
-                    nk[k] += r[k];
-                    s1[k] += r[k] * d;
-                    s2[k] += r[k] * d * d;
+                    const double d = v - mu[k];
+                    l[k] = fma(-(d * d), h[k], lp[k]);
+                    best = fmax(best, l[k]);
+                }
+                double e[G], sum = 0.0;
+#pragma unroll
+                for (int k = 0; k < G; ++k) {
+                    e[k] = gmm_exp2_nonpos(l[k] - best);
+                    sum += e[k];
+                }
+                const double inv = recip(sum);
+                const double dd = v - mean_prev;
+#pragma unroll
+                for (int k = 0; k < G; ++k) {
+                    const double r = e[k] * inv;
+                    const double rd = r * dd;
+                    nk[k] += r;
+                    s1[k] += rd;
+                    s2[k] = fma(rd, dd, s2[k]);
                 }
             }
 #pragma unroll
             for (int k = 0; k < G; ++k) {
-                nk[k] = wave_sum(nk[k]);
-                s1[k] = wave_sum(s1[k]);
-                s2[k] = wave_sum(s2[k]);
+                nk[k] = seg_sum(nk[k], s);
+                s1[k] = seg_sum(s1[k], s);
+                s2[k] = seg_sum(s2[k], s);
                 if (!(nk[k] > 0.0)) continue;
                 const double dm = s1[k] / nk[k];
                 mu[k] = mean_prev + dm;
@@ -160,32 +211,43 @@ __device__ double pair_error(const float* __restrict__ a, const float* __restric
             }
         }
     }
-    // hard groups and their sums on both sub-curves
+    // hard groups, their sums on both sub-curves (in the order of the sums of
+    // the means above, so a single group reproduces them exactly), and the
+    // label margins
     double ga[G], gb[G], gc[G];
 #pragma unroll
     for (int k = 0; k < G; ++k) ga[k] = gb[k] = gc[k] = 0.0;
     double lp[G], h[G];
-    if (!constant) {
-#pragma unroll
-        for (int k = 0; k < G; ++k) {
-            lp[k] = log(pi[k]) - 0.5 * log(two_pi * var[k]);
-            h[k] = 0.5 / var[k];
-        }
-    }
-    for (int64_t j = lane; j < t; j += kWave) {
+    if (!constant) log_coeffs<G>(mu, var, pi, lp, h);
+    double frag = 0.0;
+    for (int64_t j = ls; j < t; j += s) {
         const double va = (double)a[j], vb = (double)b[j];
         int arg = 0;
-        if (!constant) {
-            double best = -INFINITY;
+        if (!constant && G > 1) {
+            double l[G], e[G];
 #pragma unroll
             for (int k = 0; k < G; ++k) {
                 const double d = va - mu[k];
-                const double l = lp[k] - d * d * h[k];
-                if (l > best) {
-                    best = l;
+                const double q = d * d * h[k];
+                l[k] = lp[k] - q;
+                // change of l_k under relative errors kParamRel of mu_k, var_k
+                // and pi_k, plus four roundings of its terms
+                e[k] = kParamRel * (2.0 * fabs(d) * fabs(mu[k]) * h[k] + q + 1.5 * kLog2e) +
+                       1e-15 * (fabs(lp[k]) + q);
+            }
+            double best = l[0], eb = e[0];
+#pragma unroll
+            for (int k = 1; k < G; ++k)
+                if (l[k] > best) {
+                    best = l[k];
+                    eb = e[k];
                     arg = k;
                 }
-            }
+            double gap = INFINITY;
+#pragma unroll
+            for (int k = 0; k < G; ++k)
+                if (k != arg && best - l[k] <= eb + e[k]) gap = 0.0;
+            if (gap == 0.0) frag = 1.0;
         }
 #pragma unroll
         for (int k = 0; k < G; ++k) {
@@ -196,10 +258,11 @@ __device__ double pair_error(const float* __restrict__ a, const float* __restric
             }
         }
     }
+    if (seg_max(frag, s) > 0.0) fragile = true;
     double err = 0.0;
 #pragma unroll
     for (int k = 0; k < G; ++k) {
-        const double ca = wave_sum(ga[k]), cb = wave_sum(gb[k]), cnt = wave_sum(gc[k]);
+        const double ca = seg_sum(ga[k], s), cb = seg_sum(gb[k], s), cnt = seg_sum(gc[k], s);
         if (cnt == 0.0) continue;
         err += cnt * smape(ca / cnt - mean_prev, cb / cnt - mean_back);
     }
@@ -207,56 +270,76 @@ __device__ double pair_error(const float* __restrict__ a, const float* __restric
 }
 
 template <int G>
-__global__ __launch_bounds__(kWave * kWaves) void similarity_kernel(SimArgs a, Weights w) {
-    __shared__ double part[kWaves];
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t q = blockIdx.x;
+__global__ __launch_bounds__(kThreads) void similarity_kernel(SimArgs a, Weights w) {
+    __shared__ double part[kThreads];
+    __shared__ int any_fragile;
+    const int tid = threadIdx.x;
+    // contiguous query ranges per XCD (workgroups are dealt to the 8 XCDs in turn)
+    const int64_t groups = gridDim.x;
+    int64_t q = blockIdx.x;
+    const int64_t full = groups - groups % 8;
+    if (q < full) q = (q % 8) * (full / 8) + q / 8;
     const int64_t win = a.windows[q];
     const int64_t t = a.lags[q];
     if (win < 0 || win >= a.num_windows || t < 1 || t > a.n) {
-        if (threadIdx.x == 0) a.err[q] = NAN;
+        if (tid == 0) {
+            a.err[q] = NAN;
+            if (a.flags) a.flags[q] = 0u;
+        }
         return;
     }
     const int64_t num_t = a.n / t;
     if (num_t < 2) {
-        if (threadIdx.x == 0) a.err[q] = -1.0;
+        if (tid == 0) {
+            a.err[q] = -1.0;
+            if (a.flags) a.flags[q] = 0u;
+        }
         return;
     }
+    const int64_t pairs = num_t - 1;
+    const int s = choose_segment(pairs, t);
+    const int seg = tid / s, ls = tid % s, nseg = kThreads / s;
+    if (tid == 0) any_fragile = 0;
+    bool fragile = false;
     double acc = 0.0, wsum = 0.0;
     for (int32_t c = 0; c < a.num_channels; ++c) {
         const float* xc = a.x + win * a.window_stride + (int64_t)c * a.channel_stride;
         double mine = 0.0;
-        for (int64_t i = wave; i + 1 < num_t; i += kWaves)
-            mine += pair_error<G>(xc + i * t, xc + (i + 1) * t, t, a.iters, lane);
-        if (lane == 0) part[wave] = mine;
+        for (int64_t i = seg; i < pairs; i += nseg)
+            mine += pair_error<G>(xc + i * t, xc + (i + 1) * t, t, a.iters, s, ls, fragile);
+        __syncthreads();
+        if (ls == 0) part[seg] = mine;
         __syncthreads();
         double total = 0.0;
-        for (int v = 0; v < kWaves; ++v) total += part[v];
-        __syncthreads();
+        for (int g = 0; g < nseg; ++g) total += part[g];
         const double wc = (double)w.w[c];
-        acc += wc * (total / (double)(num_t - 1));
+        acc += wc * (total / (double)pairs);
         wsum += wc;
     }
-    if (threadIdx.x == 0) a.err[q] = acc / wsum;
+    if (fragile) any_fragile = 1;
+    __syncthreads();
+    if (tid == 0) {
+        a.err[q] = acc / wsum;
+        if (a.flags) a.flags[q] = any_fragile ? GPOEO_PD_UNRESOLVED : 0u;
+    }
 }
 
 template <int G>
 void launch_g(const SimArgs& a, const Weights& w, hipStream_t s) {
-    hipLaunchKernelGGL(similarity_kernel<G>, dim3((unsigned)a.count), dim3(kWave * kWaves), 0, s,
-                       a, w);
+    hipLaunchKernelGGL(similarity_kernel<G>, dim3((unsigned)a.count), dim3(kThreads), 0, s, a, w);
 }
 
 }  // namespace
 
 hipError_t launch_similarity(const Plan& p, const Weights& w, int32_t groups, int32_t iters,
                              const float* x, const int32_t* windows, const int32_t* lags,
-                             int64_t count, double* err, hipStream_t s) {
+                             int64_t count, double* err, uint32_t* flags, hipStream_t s) {
     SimArgs a;
     a.x = x;
     a.windows = windows;
     a.lags = lags;
     a.err = err;
+    a.flags = flags;
     a.count = count;
     a.num_windows = p.num_windows;
     a.n = p.n;

@@ -96,3 +96,60 @@ def test_weighted_channels():
                         weights=np.array([0.25, 3.0], dtype=np.float32))
     ts = [100, 101, 150, 300, 7]
     check(gpu_similarity(x, lay, [0] * 5, ts), oracle.similarity(x, lay, [0] * 5, ts), "weights")
+
+
+def gpu_similarity_flagged(x_np, lay, windows, lags, **kw):
+    import paper_2201_01684_amd as pkg
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    x = torch.from_numpy(np.ascontiguousarray(x_np).reshape(-1)).to("cuda:0")
+    desc, _keep = pkg.make_desc(lay.num_windows, lay.num_channels, lay.n, lay.window_stride,
+                                lay.channel_stride, lay.tmin, lay.tmax, weights=lay.weights)
+    w = torch.tensor(np.asarray(windows, dtype=np.int32), device="cuda:0")
+    t = torch.tensor(np.asarray(lags, dtype=np.int32), device="cuda:0")
+    err, flags = pkg.similarity(x, desc, w, t, with_flags=True, **kw)
+    plain = pkg.similarity(x, desc, w, t, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(err, plain)          # the flags change nothing else
+    return err.cpu().numpy(), flags.cpu().numpy()
+
+
+def test_sample_on_a_group_boundary_is_flagged():
+    """A sub-curve symmetric about 5 (eight samples at 0, eight at 10, one at 5)
+    keeps a two-component fit symmetric, so the sample at 5 sits exactly on the
+    boundary: its label is a tie that rounding decides, and the query is
+    flagged.  Moving that sample off the middle clears the flag."""
+    import paper_2201_01684_amd as pkg
+    sub = [0.0] * 8 + [5.0] + [10.0] * 8
+    for mid, want in ((5.0, pkg.UNRESOLVED), (3.0, 0)):
+        a = np.array(sub, dtype=np.float32)
+        a[8] = mid
+        x = np.concatenate([a, a + 1.0]).astype(np.float32)
+        lay = oracle.Layout(1, 1, x.size, x.size, x.size, 1, x.size // 2)
+        err, flags = gpu_similarity_flagged(x, lay, [0], [a.size], num_groups=2, em_iters=20)
+        assert flags[0] == want, (mid, flags)
+        check(err, oracle.similarity(x, lay, [0], [a.size], num_groups=2, em_iters=20),
+              f"boundary {mid}")
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("w1", {}),
+    ("w2", dict(traces=8, n=65536, tmax=8192)),
+    ("w3", dict(traces=6, n=262144, tmax=32768)),
+    ("w5", dict(traces=3, n=131072, tmax=16384)),
+])
+def test_workload_finalists_unflagged_and_equal(name, kw):
+    """The five finalists of each window (the planted period, its neighbours,
+    its double and half) at full window length: no query flagged, every Err
+    equal to the oracle's within 1e-6."""
+    wl = make_workload(name, **kw)
+    lay = oracle.Layout.of(wl)
+    ws, ts = [], []
+    for b in range(wl.num_windows):
+        p = int(wl.truth[b])
+        for t in (p, p - 1, p + 1, 2 * p, max(1, p // 2)):
+            ws.append(b)
+            ts.append(t)
+    err, flags = gpu_similarity_flagged(wl.x, lay, ws, ts)
+    assert not flags.any(), f"{name}: flagged queries {np.nonzero(flags)[0][:10]}"
+    check(err, oracle.similarity(wl.x, lay, ws, ts), name)
