@@ -113,12 +113,23 @@ extern "C" {
                                     direct sums (see below); transform limits below        */
 #define GPOEO_PD_MFMA_SCORES 8u  /* scores from an integer cross-correlation on the matrix
                                     cores instead of the direct sums (see below)           */
+#define GPOEO_PD_UNFUSED 16u     /* windows of at most GPOEO_PD_FUSED_MAX_N samples and
+                                    GPOEO_PD_FUSED_MAX_LAGS lags with direct scores, each
+                                    scored on its own, normally run everything after the
+                                    lag scores (statistics, finalisation, selection and
+                                    its re-scores) as one kernel; this flag runs those
+                                    stages as separate kernels, with identical results   */
+#define GPOEO_PD_FUSED_MAX_N 16384
+#define GPOEO_PD_FUSED_MAX_LAGS 6144
 
 /* result->flags */
 #define GPOEO_PD_UNRESOLVED 1u   /* some comparison stayed undecided after the exact
                                     re-scoring limit; the result uses bounded scores       */
 #define GPOEO_PD_SHORT 2u        /* (rolling detection) a suffix window too short for
                                     three lags starting at tmin; no period                 */
+#define GPOEO_PD_TIER2 4u        /* some decision of this window used scores (or R)
+                                    recomputed as plain sequential fp64 sums: they were
+                                    too close for the bounded fp64 re-scores           */
 
 /* Size limits, checked (EINVAL) before any launch, that keep every grid within
  * HIP's 32-bit global size.  A descriptor whose work would still need a larger
@@ -147,7 +158,8 @@ typedef struct {
     double err_max;          /* APERIODIC if S(period)/R >= err_max (1.0: never for a
                                 selected period)                                            */
     const float* channel_weights; /* HOST array of C weights > 0, or NULL for all 1          */
-    uint32_t flags;          /* GPOEO_PD_SCORES_ONLY | _NO_RESCUE | _FFT_SCORES | _MFMA_SCORES */
+    uint32_t flags;          /* GPOEO_PD_SCORES_ONLY | _NO_RESCUE | _FFT_SCORES | _MFMA_SCORES
+                                | _UNFUSED                                                  */
     uint32_t reserved1;      /* must be 0                                                   */
 } gpoeo_pd_desc;
 

@@ -23,6 +23,8 @@ from ._binding import (  # noqa: F401
     PERIODIC,
     RESULT_DTYPE,
     SCORES_ONLY,
+    TIER2,
+    UNFUSED,
     UNRESOLVED,
     ROLLING_DTYPE,
     Desc,

@@ -21,8 +21,9 @@ LIB_PATH = os.environ.get("GPOEO_PD_LIBRARY") or os.path.join(HERE, "libgpoeo_pd
 
 OK, EINVAL, ENOMEM, EHIP, ETOOBIG = 0, -1, -2, -3, -4
 PERIODIC, APERIODIC, CONSTANT = 0, 1, 2
-SCORES_ONLY, NO_RESCUE, FFT_SCORES, MFMA_SCORES = 1, 2, 4, 8
-UNRESOLVED = 1
+SCORES_ONLY, NO_RESCUE, FFT_SCORES, MFMA_SCORES, UNFUSED = 1, 2, 4, 8, 16
+FUSED_MAX_N = 16384          # GPOEO_PD_FUSED_MAX_N
+UNRESOLVED, SHORT, TIER2 = 1, 2, 4
 DEFAULT_C_LAG = 0.9
 DEFAULT_ERR_MAX = 1.0
 

@@ -27,8 +27,11 @@ SOURCES = ["api.cpp", "lag_score.hip", "window_stats.hip", "select.hip", "rollin
            "similarity.hip", "fft_score.hip", "centred.hip", "mfma_score.hip", "noalloc.hip"]
 # The selection re-evaluates scores and thresholds as plain fp64 expressions
 # (one rounding per operation, as written); no multiply-add contraction there,
-# nor in the FFT, whose error bound assumes separately rounded products.
+# nor in the FFT, whose error bound assumes separately rounded products, nor in
+# the statistics and finalisation, which the fused small-window kernel repeats
+# bit for bit.
 EXTRA_FLAGS = {"select.hip": ["-ffp-contract=off"], "rolling.hip": ["-ffp-contract=off"],
+               "window_stats.hip": ["-ffp-contract=off"],
                "similarity.hip": ["-ffp-contract=off"], "fft_score.hip": ["-ffp-contract=off"],
                "centred.hip": ["-ffp-contract=off"], "mfma_score.hip": ["-ffp-contract=off"]}
 ARCH = os.environ.get("GPOEO_PD_ARCH", "gfx950")

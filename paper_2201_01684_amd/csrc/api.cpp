@@ -113,7 +113,7 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
     if (!d) return GPOEO_PD_EINVAL;
     if (d->reserved0 != 0 || d->reserved1 != 0) return GPOEO_PD_EINVAL;
     if (d->flags & ~(GPOEO_PD_SCORES_ONLY | GPOEO_PD_NO_RESCUE | GPOEO_PD_FFT_SCORES |
-                     GPOEO_PD_MFMA_SCORES))
+                     GPOEO_PD_MFMA_SCORES | GPOEO_PD_UNFUSED))
         return GPOEO_PD_EINVAL;
     const bool mfma = (d->flags & GPOEO_PD_MFMA_SCORES) != 0;
     // one score source per call
@@ -275,6 +275,24 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
         p->mfma_chunks = (int32_t)((steps + cs - 1) / cs);
     }
     p->bitmap_words = (p->lags + 31) / 32;
+    {
+        // Tiny plans: few pairs in short windows, each scored on its own.
+        const double lags = (double)p->lags;
+        const double pairs = (double)bc * lags * ((double)d->n - 0.5 * ((double)d->tmin + d->tmax));
+        p->tiny = !p->fft && !mfma && !p->sliding && !ragged && d->n <= kFusedMaxN &&
+                  pairs <= kTinyMaxPairs;
+        if (p->tiny) {
+            p->t0 = d->tmin;
+            p->lag_blocks = (p->lags + kTinyLags - 1) / kTinyLags;
+            p->lags_padded = p->lag_blocks * kTinyLags;
+            p->chunk = kTinyChunk;
+            p->chunks = (int32_t)((d->n - d->tmin + kTinyChunk - 1) / kTinyChunk);
+            if (!mul_ok(bc * p->lag_blocks, (int64_t)p->chunks * (kTinyLags / kWave), &p->tasks))
+                return GPOEO_PD_EINVAL;
+        }
+    }
+    p->fused = !p->fft && !p->mfma && !p->sliding && !ragged && d->n <= kFusedMaxN &&
+               p->lags <= kFusedMaxLags && !(d->flags & GPOEO_PD_UNFUSED);
 
     int64_t n_var, n_s, n_bits, n_part;
     if (!mul_ok(bc, 2, &n_var)) return GPOEO_PD_EINVAL;      // variance, mean |x|
@@ -407,7 +425,7 @@ int run_plan(const gpoeo::Plan& p, const gpoeo::Weights& w, const float* x, floa
     if (!mark(0)) return GPOEO_PD_EHIP;
     double* fstat = p.fft ? reinterpret_cast<double*>(static_cast<char*>(workspace) + p.off_fstat)
                           : nullptr;
-    if ((!scores_only || p.fft) &&
+    if ((!scores_only || p.fft) && !p.fused &&
         gpoeo::launch_window_stats(p, x, c.var, fstat, stream) != hipSuccess)
         return GPOEO_PD_EHIP;
     if (!mark(1)) return GPOEO_PD_EHIP;
@@ -448,6 +466,16 @@ int run_plan(const gpoeo::Plan& p, const gpoeo::Weights& w, const float* x, floa
         if (!mark(2)) return GPOEO_PD_EHIP;
         if (gpoeo::launch_finalize_blocks(p, w, c.part, c.cut, c.s64, scores, stream) != hipSuccess)
             return GPOEO_PD_EHIP;
+    } else if (p.fused) {
+        // statistics, finalisation and selection all run in the finish kernel
+        // (timed as the finalisation stage; the other two stages are empty)
+        if (gpoeo::launch_lag_score(p, x, c.part, stream) != hipSuccess) return GPOEO_PD_EHIP;
+        if (!mark(2)) return GPOEO_PD_EHIP;
+        if (gpoeo::launch_finish(p, w, x, c.var, c.part, c.s64, scores, c.sb, results, stream) !=
+            hipSuccess)
+            return GPOEO_PD_EHIP;
+        if (!mark(3) || !mark(4)) return GPOEO_PD_EHIP;
+        return GPOEO_PD_OK;
     } else {
         if (gpoeo::launch_lag_score(p, x, c.part, stream) != hipSuccess) return GPOEO_PD_EHIP;
         if (!mark(2)) return GPOEO_PD_EHIP;

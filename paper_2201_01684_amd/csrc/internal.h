@@ -12,6 +12,12 @@ constexpr int kWave = 64;            // CDNA wavefront width
 constexpr int kBlockSamples = 16;    // samples per register block of the score kernel
 constexpr int kRunSamples = 256;     // samples per fp32 run before the fp64 flush
 constexpr int kMaxChannels = GPOEO_PD_MAX_CHANNELS;   // weights travel as a kernel argument
+// Tiny plans (at most kTinyMaxPairs pairs, windows of at most kFusedMaxN
+// samples): one LDS-staged workgroup per (sequence, kTinyLags lags,
+// kTinyChunk samples) instead of the register-blocked wavefronts.
+constexpr int kTinyLags = 256;
+constexpr int kTinyChunk = 256;
+constexpr double kTinyMaxPairs = 1e8;
 
 // Relative error bound of a score accumulated in fp32 runs of kRunSamples
 // non-negative terms (each run: kRunSamples roundings plus the rounding of the
@@ -79,6 +85,14 @@ __device__ __forceinline__ int32_t table_tmax(const WindowTable& t, int64_t b, i
     return t.tmax ? t.tmax[b] : tmax;
 }
 
+// Longest window of a fused plan: a tier-1 re-score of one lag is then at most
+// 256 fp64 steps per lane of one wavefront.
+constexpr int64_t kFusedMaxN = GPOEO_PD_FUSED_MAX_N;
+// Most lags of a fused plan: the kernel keeps the window's fp64 scores and
+// four bitmaps in LDS (at most about 49 KiB, so the workgroup stays within
+// 64 KiB of LDS).
+constexpr int32_t kFusedMaxLags = GPOEO_PD_FUSED_MAX_LAGS;
+
 // Selection passes (with one re-score round between consecutive passes) and the
 // capacity of each re-score queue (per tier, per round, all windows together).
 constexpr int kPasses = 4;
@@ -91,6 +105,7 @@ struct WinState {
     int32_t r_queued;        // R queued for the sequential evaluation
     int32_t r_is_exact;
     int32_t rescored;        // lags re-scored in fp64 so far
+    int32_t tier2;           // a score or R was recomputed as a plain sequential sum
 };
 
 // Workspace buffers of the selection.
@@ -165,6 +180,13 @@ struct Plan {
     int32_t mfma_chunks;     // sample chunks per tile (1: one wave per tile)
     int64_t mfma_chunk_steps;   // 32-sample steps per chunk (even)
     int64_t mfma_plane;
+    // Fused plans: after the lag scores, one kernel (one workgroup per window)
+    // computes the statistics, finalises the scores and runs the whole
+    // selection, re-scoring in place: direct scores of windows of at most
+    // kFusedMaxN samples, each scored on its own (no table, no shared blocks).
+    bool fused;
+    bool tiny;               // lag_score_tiny_kernel (t0 = tmin, kTinyLags-lag blocks,
+                             // kTinyChunk-sample chunks)
     double c_lag, err_max;
     uint32_t flags;
     WindowTable table;       // per-window offsets / lengths / Tmax, or all null
@@ -284,6 +306,12 @@ void fft_geometry(int32_t lg, int32_t* m1, int32_t* m2, int32_t* cols);
 bool set_fft_geometry(Plan* p, int32_t lg);
 hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const double* var,
                          double* s64, const SelectBuffers& sb, void* results, hipStream_t s);
+// Fused plans (p.fused): window statistics, finalisation of the lag-score
+// partials and the whole selection with its re-scores, one workgroup per
+// window, in one launch after the lag scores.
+hipError_t launch_finish(const Plan& p, const Weights& w, const float* x, double* var,
+                         const double* part, double* s64, float* scores,
+                         const SelectBuffers& sb, void* results, hipStream_t s);
 hipError_t launch_rolling_schedule(const Plan& p, const RollingConfig& rc,
                                    const gpoeo_pd_result* res_a, int64_t* tab_off, int64_t* tab_n,
                                    int32_t* tab_tmax, RollState* state, hipStream_t s);

@@ -166,16 +166,33 @@ __global__ __launch_bounds__(kWave * kWavesPerGroup) void lag_score_kernel(Score
     const int64_t runs_per = kRunSamples / kBlockSamples;
 
     // Unmasked blocks, flushed to fp64 every kRunSamples samples.
+    auto load_block = [&](int64_t q, float(&xs)[16], float(&y)[kW]) {
+        const int64_t i = i_begin + q * kBlockSamples;
+#pragma unroll
+        for (int s = 0; s < 16; ++s) xs[s] = xw[i + s];
+        load_window<kBT, kShift>(xw + i + t_lane, y);
+    };
     for (int64_t q0 = 0; q0 < nb_full; q0 += runs_per) {
         const int64_t q1 = min(nb_full, q0 + runs_per);
-        for (int64_t q = q0; q < q1; ++q) {
-            const int64_t i = i_begin + q * kBlockSamples;
-            float xs[16];
-#pragma unroll
-            for (int s = 0; s < 16; ++s) xs[s] = xw[i + s];
-            float y[kW];
-            load_window<kBT, kShift>(xw + i + t_lane, y);
-            block_full<kBT>(xs, y, acc);
+        if constexpr (kBT == 8) {
+            // Two register sets: the loads of the next block are in flight
+            // while this block's products run (a wave's own latency stays
+            // hidden even when few waves share a SIMD, as for short windows).
+            float xa[16], ya[kW], xb[16], yb[kW];
+            load_block(q0, xa, ya);
+            for (int64_t q = q0; q < q1; q += 2) {
+                if (q + 1 < q1) load_block(q + 1, xb, yb);
+                block_full<kBT>(xa, ya, acc);
+                if (q + 1 >= q1) break;
+                if (q + 2 < q1) load_block(q + 2, xa, ya);
+                block_full<kBT>(xb, yb, acc);
+            }
+        } else {
+            for (int64_t q = q0; q < q1; ++q) {
+                float xs[16], y[kW];
+                load_block(q, xs, y);
+                block_full<kBT>(xs, y, acc);
+            }
         }
 #pragma unroll
         for (int j = 0; j < kBT; ++j) {
@@ -208,6 +225,47 @@ __global__ __launch_bounds__(kWave * kWavesPerGroup) void lag_score_kernel(Score
     double* out = a.part + (bc * a.chunks + k) * (int64_t)a.lags_padded + (t_lane - a.t0);
 #pragma unroll
     for (int j = 0; j < kBT; ++j) out[j] = acc64[j];
+}
+
+// Tiny problems (one short trace, a few lags: the online case of Algorithm
+// 3): one workgroup of kTinyLags lanes per (sequence, block of kTinyLags lags,
+// chunk of kTinyChunk samples).  The chunk x[i0 .. i0 + kTinyChunk) and its
+// partners x[i0 + T0 .. i0 + T0 + kTinyChunk + kTinyLags) are staged in LDS
+// once (zeros past the window); lane l sums the pairs of lag T0 + l whose
+// partner lies in the window, as one fp32 run of at most kTinyChunk terms
+// (the same bound as the main kernel), and writes it as that chunk's partial.
+// Every load is issued at the start, so the kernel takes about one memory
+// round trip plus kTinyChunk steps.
+__global__ __launch_bounds__(kTinyLags) void lag_score_tiny_kernel(ScoreArgs a) {
+    __shared__ float xa[kTinyChunk];
+    __shared__ float xb[kTinyChunk + kTinyLags];
+    const int tid = threadIdx.x;
+    const int64_t task = blockIdx.x;
+    const int32_t k = (int32_t)(task % a.chunks);
+    const int64_t rest = task / a.chunks;
+    const int32_t blk = (int32_t)(rest % a.lag_blocks);
+    const int64_t bc = rest / a.lag_blocks;
+    const int64_t b = bc / a.num_channels;
+    const int32_t c = (int32_t)(bc % a.num_channels);
+    const float* __restrict__ xw = a.x + b * a.window_stride + (int64_t)c * a.channel_stride;
+    const int64_t n = a.n;
+    const int64_t i0 = (int64_t)k * kTinyChunk;
+    const int64_t t_blk = (int64_t)a.t0 + (int64_t)blk * kTinyLags;
+    for (int j = tid; j < kTinyChunk; j += kTinyLags) xa[j] = i0 + j < n ? xw[i0 + j] : 0.0f;
+    for (int j = tid; j < kTinyChunk + kTinyLags; j += kTinyLags) {
+        const int64_t idx = i0 + t_blk + j;
+        xb[j] = idx < n ? xw[idx] : 0.0f;
+    }
+    __syncthreads();
+    const int64_t t = t_blk + tid;
+    int64_t m = n - t - i0;                 // pairs (i0 + i, i0 + i + t) with i0 + i + t < n
+    m = m < 0 ? 0 : (m > kTinyChunk ? kTinyChunk : m);
+    float acc = 0.0f;
+    for (int i = 0; i < (int)m; ++i) {
+        const float d = xa[i] - xb[i + tid];
+        acc = __builtin_fmaf(d, d, acc);
+    }
+    a.part[(bc * a.chunks + k) * (int64_t)a.lags_padded + (t - a.t0)] = (double)acc;
 }
 
 template <int kBT, int kWPG>
@@ -259,7 +317,13 @@ ScoreArgs common(const Plan& p, const float* x) {
 hipError_t launch_lag_score(const Plan& p, const float* x, double* part, hipStream_t s) {
     ScoreArgs a = common(p, x);
     a.part = part;
-    launch(p, a, s);
+    if (p.tiny) {
+        const int64_t groups = p.num_windows * p.num_channels * p.lag_blocks * (int64_t)p.chunks;
+        hipLaunchKernelGGL(lag_score_tiny_kernel, dim3((unsigned)groups), dim3(kTinyLags), 0, s,
+                           a);
+    } else {
+        launch(p, a, s);
+    }
     return hipGetLastError();
 }
 

@@ -39,6 +39,7 @@
 #include "internal.h"
 #include "exact.h"
 #include "gpoeo_pd.h"
+#include "stats.h"
 
 namespace gpoeo {
 namespace {
@@ -155,25 +156,40 @@ struct Shared {
     double r_err;
 };
 
-template <int kSelThreads>
-__global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, Weights w) {
-    __shared__ Shared<kSelThreads> sh;
+// Where the rule reads window b's fp64 scores and tier bitmaps and marks its
+// re-score requests: the workspace (global), or copies in LDS (fused kernel).
+struct WindowView {
+    const double* s;
+    const uint32_t* t1;
+    const uint32_t* t2;
+    uint32_t* qd1;
+    uint32_t* qd2;
+};
+
+// One evaluation of the rule for window b (every thread of the workgroup
+// calls it).  Returns true once the window's result is written (now or in an
+// earlier pass).  Requests for higher tiers are marked in the window's queued
+// bitmaps; kLocal = false also appends them to the global re-score queues
+// (one re-score kernel serves every window), kLocal = true leaves them to the
+// caller, which re-scores the marked lags of its own window.
+template <int kSelThreads, bool kLocal>
+__device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, int pass,
+                              bool last, Shared<kSelThreads>& sh, const WindowView& view) {
     const int tid = threadIdx.x;
-    const int64_t b = blockIdx.x;
     const int32_t tmin = a.tmin;
     const int32_t tmax = table_tmax(a.tab, b, a.tmax);   // this window's lag range and length
     const int64_t n = table_n(a.tab, b, a.n);
-    double* __restrict__ s = a.s64 + b * (int64_t)a.lags;
-    uint32_t* __restrict__ t1 = a.tier1 + b * (int64_t)a.words;
-    uint32_t* __restrict__ t2 = a.tier2 + b * (int64_t)a.words;
-    uint32_t* __restrict__ qd1 = a.queued1 + b * (int64_t)a.words;
-    uint32_t* __restrict__ qd2 = a.queued2 + b * (int64_t)a.words;
+    const double* __restrict__ s = view.s;
+    const uint32_t* __restrict__ t1 = view.t1;
+    const uint32_t* __restrict__ t2 = view.t2;
+    uint32_t* __restrict__ qd1 = view.qd1;
+    uint32_t* __restrict__ qd2 = view.qd2;
     WinState* st = a.state + b;
     gpoeo_pd_result* res = a.results + b;
-    int32_t* count = a.q_count + 2 * a.pass;
+    int32_t* count = a.q_count + 2 * pass;
 
     if (tid == 0) {
-        sh.done = a.pass == 0 ? 0 : st->done;
+        sh.done = pass == 0 ? 0 : st->done;
         const double* v2 = a.var + 2 * b * a.num_channels;
         double acc = 0.0;
         for (int32_t c = 0; c < a.num_channels; ++c) acc = acc + (double)w.w[c] * v2[2 * c];
@@ -181,7 +197,7 @@ __global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, 
         sh.r_err = reference_bound(v2, a.num_channels, n, w, sh.r_approx);
     }
     __syncthreads();
-    if (sh.done) return;
+    if (sh.done) return true;
     if (n == 0 || tmax < tmin + 2) {   // empty or too short a slot of a window table
         if (tid == 0) {
             gpoeo_pd_result o = {};
@@ -190,7 +206,7 @@ __global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, 
             *res = o;
             st->done = 1;
         }
-        return;
+        return true;
     }
     const double r_approx = sh.r_approx;
     const double r_err = sh.r_err;
@@ -201,9 +217,9 @@ __global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, 
             *res = o;
             st->done = 1;
         }
-        return;
+        return true;
     }
-    const bool r_exact = a.pass > 0 && st->r_is_exact;
+    const bool r_exact = pass > 0 && st->r_is_exact;
     const double r_x = r_exact ? st->r_exact : 0.0;
     const double c_lag = a.c_lag;
     // the window's lags as bits of the peak cache (bit t - tmin)
@@ -213,11 +229,18 @@ __global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, 
 
     // Queue (window b, lag t) for the next tier; lag -1 queues R.
     auto enqueue = [&](int tier, int32_t t) {
-        const int k = atomicAdd(&count[tier - 1], 1);
-        if (k >= kQueueCap) return false;
-        a.q_win[(tier - 1) * kQueueCap + k] = (int32_t)b;
-        a.q_lag[(tier - 1) * kQueueCap + k] = t;
-        return true;
+        if constexpr (kLocal) {   // the queued bitmaps (and r_queued) are the request
+            (void)tier;
+            (void)t;
+            (void)count;
+            return true;
+        } else {
+            const int k = atomicAdd(&count[tier - 1], 1);
+            if (k >= kQueueCap) return false;
+            a.q_win[(tier - 1) * kQueueCap + k] = (int32_t)b;
+            a.q_lag[(tier - 1) * kQueueCap + k] = t;
+            return true;
+        }
     };
     auto want_r = [&]() {
         if (atomicExch(&st->r_queued, 1) == 0 && !enqueue(2, -1)) atomicExch(&st->r_queued, 0);
@@ -444,8 +467,8 @@ __global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, 
     if (!rescue) {
         done = rule(0.0, 0.0, 0.0, false, o);
     } else {
-        done = rule(a.tau0, a.tau1, r_err, !a.last, o);
-        if (!done && a.last) {
+        done = rule(a.tau0, a.tau1, r_err, !last, o);
+        if (!done && last) {
             done = rule(0.0, 0.0, 0.0, false, o);
             unresolved = true;
         }
@@ -453,10 +476,21 @@ __global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, 
     __syncthreads();
     if (tid == 0 && done) {
         o.n_rescored = st->rescored;
-        o.flags = unresolved ? GPOEO_PD_UNRESOLVED : 0u;
+        o.flags = (unresolved ? GPOEO_PD_UNRESOLVED : 0u) | (st->tier2 ? GPOEO_PD_TIER2 : 0u);
         *res = o;
         st->done = 1;
     }
+    return done;
+}
+
+template <int kSelThreads>
+__global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, Weights w) {
+    __shared__ Shared<kSelThreads> sh;
+    const int64_t b = blockIdx.x;
+    const WindowView view = {a.s64 + b * (int64_t)a.lags, a.tier1 + b * (int64_t)a.words,
+                             a.tier2 + b * (int64_t)a.words, a.queued1 + b * (int64_t)a.words,
+                             a.queued2 + b * (int64_t)a.words};
+    select_window<kSelThreads, false>(a, w, b, a.pass, a.last != 0, sh, view);
 }
 
 // One re-score round: every wavefront takes queued tier-1 requests (one lag
@@ -495,6 +529,7 @@ __global__ __launch_bounds__(kThreads) void rescore_kernel(SelectArgs a, Weights
         if (t < 0) {
             WinState* st = a.state + b;
             st->r_exact = exact_reference(xw, a.num_channels, a.channel_stride, n, w);
+            st->tier2 = 1;
             __threadfence();
             st->r_is_exact = 1;
             continue;
@@ -503,6 +538,7 @@ __global__ __launch_bounds__(kThreads) void rescore_kernel(SelectArgs a, Weights
         uint32_t* t2 = a.tier2 + b * (int64_t)a.words;
         if ((t2[j >> 5] >> (j & 31)) & 1u) continue;
         a.s64[b * (int64_t)a.lags + j] = exact_score(xw, a.num_channels, a.channel_stride, n, t, w);
+        a.state[b].tier2 = 1;
         __threadfence();
         atomicOr(&t2[j >> 5], 1u << (j & 31));
     }
@@ -527,12 +563,180 @@ __global__ __launch_bounds__(kThreads) void select_init_kernel(SelectBuffers sb,
         z.r_queued = 0;
         z.r_is_exact = 0;
         z.rescored = 0;
+        z.tier2 = 0;
         sb.state[b] = z;
     }
     if (blockIdx.x == 0 && (int)threadIdx.x < 2 * kPasses) sb.q_count[threadIdx.x] = 0;
 }
 
+// Re-scores the lags window b's rule marked in its queued bitmaps (and R), on
+// the LDS copies of the fused kernel: tier 1 by the wavefronts (one lag each at
+// a time), tier 2 and R by single lanes, with the same evaluations as
+// rescore_kernel.
+template <int kT>
+__device__ void rescore_window(const SelectArgs& a, const Weights& w, int64_t b, double* s,
+                               uint32_t* t1, uint32_t* t2, const uint32_t* qd1,
+                               const uint32_t* qd2) {
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    WinState* st = a.state + b;
+    const float* __restrict__ xw = a.x + b * a.window_stride;
+    for (int k = wave; k < a.words; k += kT / kWave) {
+        uint32_t m = __builtin_amdgcn_readfirstlane(qd1[k] & ~t1[k]);
+        while (m) {
+            const int bit = __builtin_ctz(m);
+            m &= m - 1;
+            const int64_t j = 32 * (int64_t)k + bit;
+            const double v = wave_score(xw, a.num_channels, a.channel_stride, a.n, a.tmin + j, w,
+                                        lane);
+            if (lane == 0) {
+                s[j] = v;
+                atomicOr(&t1[k], 1u << bit);
+                atomicAdd(&st->rescored, 1);
+            }
+        }
+    }
+    for (int k = tid; k < a.words; k += kT) {
+        uint32_t m = qd2[k] & ~t2[k];
+        while (m) {
+            const int bit = __builtin_ctz(m);
+            m &= m - 1;
+            const int64_t j = 32 * (int64_t)k + bit;
+            s[j] = exact_score(xw, a.num_channels, a.channel_stride, a.n, a.tmin + j, w);
+            st->tier2 = 1;
+            atomicOr(&t2[k], 1u << bit);
+        }
+    }
+    if (tid == 0 && st->r_queued && !st->r_is_exact) {
+        st->r_exact = exact_reference(xw, a.num_channels, a.channel_stride, a.n, w);
+        st->tier2 = 1;
+        st->r_is_exact = 1;
+    }
+}
+
+struct FinishArgs {
+    const double* part;      // lag-score chunk partials
+    double* var;             // [B][C][2], written here
+    float* scores;           // nullable
+    int32_t t0, lags_padded, chunks;
+};
+
+// Everything after the lag scores of a window, in one workgroup: the window
+// statistics (stats::channel_stats, as window_stats_kernel), the finalisation
+// (stats::finalize_lags, as finalize_kernel), the selection state, and up to
+// kPasses evaluations of the rule with this workgroup re-scoring the lags
+// each one marks.  The window's fp64 scores and its four bitmaps live in LDS
+// (dynamic shared memory: lags doubles, then 4 x words words) for the
+// selection.  Same values, decisions and results as the separate kernels;
+// one launch instead of nine, for windows short enough that one workgroup
+// re-scores a lag quickly.
+__global__ __launch_bounds__(stats::kStatsThreads) void finish_kernel(SelectArgs a, FinishArgs f,
+                                                                     Weights w) {
+    constexpr int kT = stats::kStatsThreads;
+    __shared__ Shared<kT> sh;
+    __shared__ double red[kT];
+    extern __shared__ double dyn[];
+    double* s_l = dyn;
+    uint32_t* bits = reinterpret_cast<uint32_t*>(dyn + a.lags);
+    uint32_t* t1 = bits;
+    uint32_t* t2 = bits + a.words;
+    uint32_t* qd1 = bits + 2 * a.words;
+    uint32_t* qd2 = bits + 3 * a.words;
+    const int tid = threadIdx.x;
+    const int64_t b = blockIdx.x;
+    const float* __restrict__ xw = a.x + b * a.window_stride;
+    const bool scores_only = (a.flags & GPOEO_PD_SCORES_ONLY) != 0;
+    if (!scores_only)
+        for (int32_t c = 0; c < a.num_channels; ++c) {
+            const stats::ChannelStats cs =
+                stats::channel_stats(xw + (int64_t)c * a.channel_stride, a.n, red, false);
+            if (tid == 0) {
+                const int64_t bc = b * a.num_channels + c;
+                f.var[2 * bc] = cs.var;
+                f.var[2 * bc + 1] = cs.absmean;
+            }
+        }
+    constexpr int L = stats::kFinalizeLags;
+    for (int32_t j = tid; j < a.lags; j += kT * L) {
+        double v[L];
+        stats::finalize_lags(f.part, w, a.num_channels, b, a.n, (int64_t)a.tmin + j, kT,
+                             (int64_t)a.tmin + a.lags, f.t0, f.lags_padded, f.chunks, v);
+#pragma unroll
+        for (int l = 0; l < L; ++l) {
+            const int64_t jj = j + (int64_t)l * kT;
+            if (jj >= a.lags) break;
+            s_l[jj] = v[l];
+            if (f.scores) f.scores[b * (int64_t)a.lags + jj] = (float)v[l];
+        }
+    }
+    if (scores_only) return;
+    for (int k = tid; k < 4 * a.words; k += kT) bits[k] = 0u;
+    if (tid == 0) {
+        WinState z;
+        z.r_exact = 0.0;
+        z.done = 0;
+        z.r_queued = 0;
+        z.r_is_exact = 0;
+        z.rescored = 0;
+        z.tier2 = 0;
+        a.state[b] = z;
+    }
+    __syncthreads();
+    const int passes = (a.flags & GPOEO_PD_NO_RESCUE) ? 1 : kPasses;
+    const WindowView view = {s_l, t1, t2, qd1, qd2};
+    for (int pass = 0; pass < passes; ++pass) {
+        if (select_window<kT, true>(a, w, b, pass, pass == passes - 1, sh, view)) break;
+        __syncthreads();
+        rescore_window<kT>(a, w, b, s_l, t1, t2, qd1, qd2);
+        __syncthreads();
+    }
+}
+
 }  // namespace
+
+hipError_t launch_finish(const Plan& p, const Weights& w, const float* x, double* var,
+                         const double* part, double* s64, float* scores,
+                         const SelectBuffers& sb, void* results, hipStream_t s) {
+    SelectArgs a = {};
+    a.x = x;
+    a.var = var;
+    a.s64 = s64;
+    a.tier1 = sb.tier1;
+    a.tier2 = sb.tier2;
+    a.queued1 = sb.queued1;
+    a.queued2 = sb.queued2;
+    a.state = sb.state;
+    a.q_win = sb.q_win;
+    a.q_lag = sb.q_lag;
+    a.q_count = sb.q_count;
+    a.results = static_cast<gpoeo_pd_result*>(results);
+    a.n = p.n;
+    a.window_stride = p.window_stride;
+    a.channel_stride = p.channel_stride;
+    a.num_channels = p.num_channels;
+    a.tmin = p.tmin;
+    a.tmax = p.tmax;
+    a.lags = p.lags;
+    a.words = p.bitmap_words;
+    a.c_lag = p.c_lag;
+    a.err_max = p.err_max;
+    a.flags = p.flags;
+    a.tab = p.table;
+    a.tau0 = kScoreRelBound;
+    const double u = 1.1102230246251565e-16;
+    a.tau1 = 1.01 * u * ((double)p.n * (1.0 + 1.0 / 256.0) + 2.0 * p.num_channels + 22.0);
+    FinishArgs f;
+    f.part = part;
+    f.var = var;
+    f.scores = scores;
+    f.t0 = p.t0;
+    f.lags_padded = p.lags_padded;
+    f.chunks = p.chunks;
+    const size_t lds = (size_t)p.lags * sizeof(double) + 4 * (size_t)p.bitmap_words * 4;
+    hipLaunchKernelGGL(finish_kernel, dim3((unsigned)p.num_windows), dim3(stats::kStatsThreads),
+                       lds, s, a, f, w);
+    return hipGetLastError();
+}
 
 hipError_t launch_select_init(const Plan& p, const SelectBuffers& sb, hipStream_t s) {
     const int64_t total = std::max<int64_t>((int64_t)p.bitmap_words * p.num_windows, p.num_windows);

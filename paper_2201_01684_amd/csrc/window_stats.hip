@@ -14,55 +14,15 @@
 #include <algorithm>
 
 #include "internal.h"
+#include "stats.h"
 
 namespace gpoeo {
 namespace {
 
-constexpr int kStatsThreads = 256;
-
-__device__ double block_sum(double v, double* red) {
-    red[threadIdx.x] = v;
-    __syncthreads();
-#pragma unroll
-    for (int w = kStatsThreads / 2; w > 0; w >>= 1) {
-        if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-        __syncthreads();
-    }
-    double r = red[0];
-    __syncthreads();
-    return r;
-}
-
-// Visits x[0..n) once in a fixed order per thread: a scalar head up to 16-byte
-// alignment, then 16-byte groups (thread t takes groups t, t + 256, ..., four
-// loads in flight), then a scalar tail.
-template <typename F>
-__device__ __forceinline__ void visit(const float* __restrict__ xw, int64_t n, F&& f) {
-    const int64_t mis = (int64_t)((reinterpret_cast<uintptr_t>(xw) >> 2) & 3);
-    const int64_t head = ((4 - mis) & 3) < n ? ((4 - mis) & 3) : n;
-    for (int64_t i = threadIdx.x; i < head; i += kStatsThreads) f(xw[i]);
-    const float4* __restrict__ v = reinterpret_cast<const float4*>(xw + head);
-    const int64_t groups = (n - head) >> 2;
-    int64_t g = threadIdx.x;
-    for (; g + 3 * kStatsThreads < groups; g += 4 * kStatsThreads) {
-        const float4 a = v[g], b = v[g + kStatsThreads], c = v[g + 2 * kStatsThreads],
-                     d = v[g + 3 * kStatsThreads];
-        f(a.x); f(a.y); f(a.z); f(a.w);
-        f(b.x); f(b.y); f(b.z); f(b.w);
-        f(c.x); f(c.y); f(c.z); f(c.w);
-        f(d.x); f(d.y); f(d.z); f(d.w);
-    }
-    for (; g < groups; g += kStatsThreads) {
-        const float4 a = v[g];
-        f(a.x); f(a.y); f(a.z); f(a.w);
-    }
-    for (int64_t i = head + (groups << 2) + threadIdx.x; i < n; i += kStatsThreads) f(xw[i]);
-}
-
-__global__ __launch_bounds__(kStatsThreads) void window_stats_kernel(
+__global__ __launch_bounds__(stats::kStatsThreads) void window_stats_kernel(
     const float* __restrict__ x, double* __restrict__ var, int64_t n_all, int64_t window_stride,
     int64_t channel_stride, int32_t num_channels, WindowTable tab, double* __restrict__ fstat) {
-    __shared__ double red[kStatsThreads];
+    __shared__ double red[stats::kStatsThreads];
     const int64_t bc = blockIdx.x;
     const int64_t b = bc / num_channels;
     const int32_t c = (int32_t)(bc % num_channels);
@@ -76,29 +36,14 @@ __global__ __launch_bounds__(kStatsThreads) void window_stats_kernel(
     }
     const float* __restrict__ xw =
         x + table_off(tab, b, window_stride) + (int64_t)c * channel_stride;
-    double s = 0.0, sa = 0.0;
-    visit(xw, n, [&](float x) {
-        const double v = (double)x;
-        s += v;
-        sa += fabs(v);
-    });
-    const double mean = block_sum(s, red) / (double)n;
-    const double absmean = block_sum(sa, red) / (double)n;
-    double q = 0.0, qa = 0.0;
-    visit(xw, n, [&](float x) {
-        const double d = (double)x - mean;
-        q += d * d;
-        qa += fabs(d);
-    });
-    const double sq = block_sum(q, red);
-    const double sabs = fstat ? block_sum(qa, red) : 0.0;
+    const stats::ChannelStats st = stats::channel_stats(xw, n, red, fstat != nullptr);
     if (threadIdx.x == 0) {
-        var[2 * bc] = sq / (double)n;
-        var[2 * bc + 1] = absmean;
+        var[2 * bc] = st.var;
+        var[2 * bc + 1] = st.absmean;
         if (fstat) {   // the FFT scores centre each sequence by this same mean
-            fstat[4 * bc] = mean;
-            fstat[4 * bc + 1] = sq;
-            fstat[4 * bc + 2] = sabs;
+            fstat[4 * bc] = st.mean;
+            fstat[4 * bc + 1] = st.sq;
+            fstat[4 * bc + 2] = st.sabs;
             fstat[4 * bc + 3] = 0.0;
         }
     }
@@ -127,14 +72,8 @@ __global__ __launch_bounds__(256) void finalize_kernel(const double* __restrict_
             continue;
         }
         const int64_t t = (int64_t)tmin + j;
-        double s = 0.0;
-        for (int32_t c = 0; c < num_channels; ++c) {
-            const double* p = part + ((b * num_channels + c) * chunks) * (int64_t)lags_padded +
-                              (t - t0);
-            double d = 0.0;
-            for (int32_t k = 0; k < chunks; ++k) d += p[(int64_t)k * lags_padded];
-            s += (double)w.w[c] * (d / (double)(n - t));
-        }
+        const double s = stats::finalize_lag(part, w, num_channels, b, n, t, t0, lags_padded,
+                                             chunks);
         s64[e] = s;
         if (scores) scores[e] = (float)s;
     }
@@ -191,7 +130,7 @@ hipError_t launch_finalize_blocks(const Plan& p, const Weights& w, const double*
 hipError_t launch_window_stats(const Plan& p, const float* x, double* var, double* fstat,
                                hipStream_t s) {
     const int64_t groups = p.num_windows * p.num_channels;
-    hipLaunchKernelGGL(window_stats_kernel, dim3((unsigned)groups), dim3(kStatsThreads), 0, s, x,
+    hipLaunchKernelGGL(window_stats_kernel, dim3((unsigned)groups), dim3(stats::kStatsThreads), 0, s, x,
                        var, p.n, p.window_stride, p.channel_stride, p.num_channels, p.table, fstat);
     return hipGetLastError();
 }

@@ -98,7 +98,7 @@ def test_workspace_size_valid_and_monotone(lib):
     dict(n=7, tmin=1, tmax=3), dict(tmin=0), dict(tmin=5, tmax=6), dict(tmax=2049),
     dict(window_stride=0), dict(channel_stride=4095), dict(window_stride=-1),
     dict(c_lag=0.0), dict(c_lag=1.0), dict(c_lag=float("nan")), dict(err_max=float("nan")),
-    dict(flags=16), dict(flags=4, n=4 << 20, tmax=2 << 20),
+    dict(flags=32), dict(flags=4, n=4 << 20, tmax=2 << 20),
     # grids that would exceed HIP's 32-bit global size: 2^24 sequences of 256
     # threads, 2^26 lag-score waves of 64
     dict(num_windows=1 << 20, num_channels=16, n=64, tmax=32, window_stride=1024,

@@ -168,7 +168,7 @@ def test_full_size(name):
     torch.cuda.empty_cache()
     gf, rf = out["fft"]
     gd, rd = out["direct"]
-    assert np.all(rf["flags"] == 0)
+    assert np.all(rf["flags"] & pkg.UNRESOLVED == 0)
     for f in ("period", "verdict", "t_cand", "t_low", "t_up", "n_candidates"):
         assert np.array_equal(rf[f], rd[f]), f"{name}: {f} differs from the direct path"
     # both within their bounds of the exact scores: 2.5e-5 + 1e-6 (+ fp32 rounding)

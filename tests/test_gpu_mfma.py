@@ -169,7 +169,7 @@ def test_full_size(name):
     torch.cuda.empty_cache()
     gm, rm = out["mfma"]
     gd, rd = out["direct"]
-    assert np.all(rm["flags"] == 0)
+    assert np.all(rm["flags"] & pkg.UNRESOLVED == 0)
     for f in ("period", "verdict", "t_cand", "t_low", "t_up", "n_candidates"):
         assert np.array_equal(rm[f], rd[f]), f"{name}: {f} differs from the direct path"
     # both within their bounds of the exact scores: 2.5e-5 + 1.25e-5 (+ fp32 rounding)

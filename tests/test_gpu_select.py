@@ -1,0 +1,141 @@
+"""The selection's re-scoring tiers, its queue limit and the fused small-window
+path, through the C ABI, against the oracle.
+
+- Windows of at most GPOEO_PD_FUSED_MAX_N samples run statistics, finalisation
+  and selection in one kernel; GPOEO_PD_UNFUSED runs the separate kernels.
+  Both must give bitwise equal scores and results.
+- A 64-sample integer window whose local-search minimum is an exact tie
+  between two lags: tier-0 and tier-1 intervals of equal values always
+  overlap, so only the plain sequential fp64 sums (tier 2) decide it, and the
+  result must then be the oracle's (the smaller lag), with GPOEO_PD_TIER2 set
+  and no GPOEO_PD_UNRESOLVED.
+- 200,000 copies of that window need 400,000 tier-1 re-scores in the first
+  round, more than the three rounds of global queues hold (3 x 65,536): a
+  window whose requests did not fit is decided on its unwidened values and
+  flagged UNRESOLVED; every unflagged window equals the oracle.
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+import oracle  # noqa: E402
+from gen import make_workload, planted_trace  # noqa: E402
+
+from test_gpu_parity import check_results, check_scores  # noqa: E402
+
+# found by a seeded search over period-like ternary sequences with the oracle:
+# S(T) over the local-search window [16, 29] attains its minimum at two lags
+# with exactly equal rational values
+TIE = np.array([int(c) for c in
+                "1100010001000100010001100100010001000100012001000100210001000100"],
+               dtype=np.float32)
+QUEUE_CAP = 1 << 16          # kQueueCap: global re-score requests per tier and round
+
+
+def _device():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+def run(x_np, lay, flags=0):
+    import paper_2201_01684_amd as pkg
+    dev = _device()
+    x = torch.from_numpy(np.ascontiguousarray(x_np).reshape(-1)).to(dev)
+    desc, keep = pkg.make_desc(lay.num_windows, lay.num_channels, lay.n, lay.window_stride,
+                               lay.channel_stride, lay.tmin, lay.tmax, lay.c_lag, lay.err_max,
+                               lay.weights, flags)
+    det = pkg.Detector(x, desc, keep, want_scores=True)
+    det.run()
+    torch.cuda.synchronize()
+    res = None if flags & pkg.SCORES_ONLY else det.results_numpy()
+    return det.scores.cpu().numpy(), res
+
+
+def test_tie_window_is_an_exact_tie():
+    """The fixture really has two exactly equal minimal scores in its window."""
+    from fractions import Fraction
+    n = TIE.size
+    _, out = oracle.detect(TIE, oracle.Layout(1, 1, n, n, n, 1, n // 2))
+    lo, hi = int(out["t_low"][0]), int(out["t_up"][0])
+    v = [Fraction(int(sum((int(TIE[i]) - int(TIE[i + t])) ** 2 for i in range(n - t))), n - t)
+         for t in range(lo, hi + 1)]
+    m = min(v)
+    assert m > 0 and sum(x == m for x in v) == 2
+    assert out["period"][0] == lo + v.index(m)
+
+
+@pytest.mark.parametrize("unfused", [False, True])
+def test_exact_tie_is_decided_by_sequential_sums(unfused):
+    import paper_2201_01684_amd as pkg
+    n = TIE.size
+    lay = oracle.Layout(1, 1, n, n, n, 1, n // 2)
+    g, res = run(TIE, lay, pkg.UNFUSED if unfused else 0)
+    o, out = oracle.detect(TIE, lay)
+    check_scores(g.astype(np.float64), o, "tie")
+    check_results(res, out, "tie")
+    assert res["flags"][0] & pkg.TIER2, "the tie was not decided on sequential sums"
+    assert res["n_rescored"][0] >= 2
+    assert res["period"][0] == 20
+
+
+def test_queue_overflow_gives_the_documented_outcome():
+    import paper_2201_01684_amd as pkg
+    n, copies = TIE.size, 200_000
+    x = np.tile(TIE, copies)
+    lay = oracle.Layout(copies, 1, n, n, n, 1, n // 2)
+    _, o1 = oracle.detect(TIE, oracle.Layout(1, 1, n, n, n, 1, n // 2))
+    _, res = run(x, lay, pkg.UNFUSED)          # global queues
+    assert 2 * copies > 3 * QUEUE_CAP
+    flagged = (res["flags"] & pkg.UNRESOLVED) != 0
+    assert flagged.any(), "no window ran out of queue space"
+    ok = ~flagged
+    assert ok.any()
+    for f in ("period", "verdict", "t_cand", "t_low", "t_up", "n_candidates"):
+        assert np.all(res[f][ok] == o1[f][0]), f
+    assert np.all(res["flags"][ok] & pkg.TIER2)
+    # the fused path has no shared queue: every window is decided exactly
+    _, rf = run(x, lay)
+    assert not np.any(rf["flags"] & pkg.UNRESOLVED)
+    for f in ("period", "verdict", "t_cand", "t_low", "t_up", "n_candidates"):
+        assert np.all(rf[f] == o1[f][0]), f
+
+
+@pytest.mark.parametrize("case", ["w1", "w2", "w5", "noisy", "no_rescue", "scores_only",
+                                  "ragged"])
+def test_fused_equals_unfused_bitwise(case):
+    import paper_2201_01684_amd as pkg
+    flags = 0
+    if case == "w1":
+        wl = make_workload("w1")
+        x, lay = wl.x, oracle.Layout.of(wl)
+    elif case == "w2":       # length-jittered traces: flat minima, many re-scores
+        wl = make_workload("w2", traces=12, n=16384, tmax=4096, pmax=3000)
+        x, lay = wl.x, oracle.Layout.of(wl)
+    elif case == "w5":       # weighted channels
+        wl = make_workload("w5", traces=3, n=8192, tmax=2048, pmax=1500)
+        x, lay = wl.x, oracle.Layout.of(wl, weights=np.array([1, 2, .5, 1, 1, 3, 1, .25],
+                                                              dtype=np.float32))
+    elif case == "noisy":
+        x = planted_trace(8 * 5000, 211, 5, seed=3, sigma=40.0)
+        lay = oracle.Layout(8, 1, 5000, 5000, 5000, 2, 2500)
+    elif case == "no_rescue":
+        wl = make_workload("w2", traces=4, n=8192, tmax=2048, pmax=1500)
+        x, lay, flags = wl.x, oracle.Layout.of(wl), pkg.NO_RESCUE
+    elif case == "scores_only":
+        wl = make_workload("w1")
+        x, lay, flags = wl.x, oracle.Layout.of(wl), pkg.SCORES_ONLY
+    else:                    # overlapping windows at a stride that shares no blocks
+        x = planted_trace(30011, 97, 4, seed=5, sigma=1.0)
+        lay = oracle.Layout(9, 1, 4099, 3001, 4099, 3, 2049)
+    gf, rf = run(x, lay, flags)
+    gu, ru = run(x, lay, flags | pkg.UNFUSED)
+    assert np.array_equal(gf.view(np.uint32), gu.view(np.uint32)), f"{case}: scores differ"
+    if rf is not None:
+        assert rf.tobytes() == ru.tobytes(), f"{case}: results differ"
+        if not flags:
+            o, out = oracle.detect(x, lay)
+            check_scores(gf.astype(np.float64), o, case)
+            check_results(rf, out, case)
