@@ -92,7 +92,8 @@ __device__ inline double exact_reference(const float* __restrict__ xw, int32_t n
     return 2.0 * acc;
 }
 
-// Tier-1 re-score: S(T) in fp64 by one wavefront.  Lane l accumulates the
+// S(T) in fp64 by one wavefront (the tier-1 re-score of the FFT and
+// matrix-core fix-ups and of the rolling combination).  Lane l accumulates the
 // terms i = l + 64 (4k + r) in four partial sums r = 0..3, which are combined
 // as (p0 + p1) + (p2 + p3) and then across lanes by a fixed shuffle tree; every
 // lane returns lane 0's value.  Each partial sum holds at most M/256 + 1 terms,
@@ -125,6 +126,68 @@ __device__ inline double wave_score(const float* __restrict__ xw, int32_t num_ch
         for (int off = 32; off > 0; off >>= 1) part = part + __shfl_down(part, off);
         part = __shfl(part, 0);
         s = s + (double)w.w[c] * (part / (double)m);
+    }
+    return s;
+}
+
+// Tier-1 re-score by a workgroup of kG lanes (kG/64 wavefronts; every thread
+// calls it; red holds kG/64 doubles): lane l accumulates the terms
+// i = l + kG (4k + r) in four partial sums r = 0..3, combined as
+// (p0 + p1) + (p2 + p3), then a butterfly of lane shuffles in each wavefront,
+// then the wavefront sums in wavefront order.  Each partial sum holds at most
+// M/(4 kG) + 1 terms, so the result is within (M/(4 kG) + 12) u of the exact
+// sum; every thread returns the same value.
+template <int kG>
+__device__ inline double group_score(const float* __restrict__ xw, int32_t num_channels,
+                                     int64_t channel_stride, int64_t n, int64_t t,
+                                     const Weights& w, double* red) {
+    constexpr int kWaves = kG / kWave;
+    const int tid = threadIdx.x;
+    double s = 0.0;
+    for (int32_t c = 0; c < num_channels; ++c) {
+        const float* __restrict__ xc = xw + (int64_t)c * channel_stride;
+        const int64_t m = n - t;
+        double p[4] = {0.0, 0.0, 0.0, 0.0};
+        int64_t i = tid;
+        // the operands of kAhead steps are loaded before they are added (in
+        // the same order), so that a lane has them in flight together
+        constexpr int kAhead = 8;
+        for (; i + (4 * kAhead - 1) * (int64_t)kG < m; i += 4 * kAhead * (int64_t)kG) {
+            float u[4 * kAhead], v[4 * kAhead];
+#pragma unroll
+            for (int q = 0; q < 4 * kAhead; ++q) {
+                u[q] = xc[i + (int64_t)kG * q];
+                v[q] = xc[i + (int64_t)kG * q + t];
+            }
+#pragma unroll
+            for (int q = 0; q < 4 * kAhead; ++q) {
+                const double d = (double)u[q] - (double)v[q];
+                p[q & 3] = p[q & 3] + d * d;
+            }
+        }
+        for (; i + 3 * kG < m; i += 4 * kG) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const double d = (double)xc[i + kG * r] - (double)xc[i + kG * r + t];
+                p[r] = p[r] + d * d;
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int64_t k = i + kG * r;
+            if (k < m) {
+                const double d = (double)xc[k] - (double)xc[k + t];
+                p[r] = p[r] + d * d;
+            }
+        }
+        double part = (p[0] + p[1]) + (p[2] + p[3]);
+        for (int off = kWave / 2; off > 0; off >>= 1) part = part + __shfl_xor(part, off);
+        if ((tid & (kWave - 1)) == 0) red[tid / kWave] = part;
+        __syncthreads();
+        double tot = red[0];
+        for (int v = 1; v < kWaves; ++v) tot = tot + red[v];
+        __syncthreads();
+        s = s + (double)w.w[c] * (tot / (double)m);
     }
     return s;
 }

@@ -47,7 +47,7 @@ namespace {
 using exact::exact_reference;
 using exact::exact_score;
 using exact::reference_bound;
-using exact::wave_score;
+using exact::group_score;
 
 constexpr int kThreads = 256;       // re-score and initialisation kernels and short windows
 // Selection passes run one workgroup per window; from this many lags on, four
@@ -79,6 +79,7 @@ struct SelectArgs {
     uint32_t flags;
     int32_t pass;
     int32_t last;
+    int32_t stage;           // select passes copy a window's scores and tier bitmaps to LDS
     WindowTable tab;
 };
 
@@ -139,6 +140,47 @@ __device__ int64_t block_min_i(int64_t v, int64_t* red) {
 }
 
 
+// The reductions of one step of the rule at once (one exchange through LDS,
+// two barriers): three double minima, two int64 sums and one int64 minimum
+// (unused ones are passed as neutral values).  Butterflies inside each
+// wavefront, then the per-wave values folded in wave order; every thread gets
+// the results.
+template <int kT, typename Sh>
+__device__ void block_reduce(double (&dmin)[3], int64_t (&isum)[2], int64_t& imin, Sh& sh) {
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+#pragma unroll
+        for (int k = 0; k < 3; ++k) dmin[k] = fmin(dmin[k], __shfl_xor(dmin[k], o));
+#pragma unroll
+        for (int k = 0; k < 2; ++k) isum[k] += (int64_t)__shfl_xor((long long)isum[k], o);
+        imin = min(imin, (int64_t)__shfl_xor((long long)imin, o));
+    }
+    const int wv = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+#pragma unroll
+        for (int k = 0; k < 3; ++k) sh.red_md[k][wv] = dmin[k];
+#pragma unroll
+        for (int k = 0; k < 2; ++k) sh.red_ms[k][wv] = isum[k];
+        sh.red_mi[wv] = imin;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        double r = sh.red_md[k][0];
+        for (int w = 1; w < kT / kWave; ++w) r = fmin(r, sh.red_md[k][w]);
+        dmin[k] = r;
+    }
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        int64_t r = sh.red_ms[k][0];
+        for (int w = 1; w < kT / kWave; ++w) r += sh.red_ms[k][w];
+        isum[k] = r;
+    }
+    int64_t r = sh.red_mi[0];
+    for (int w = 1; w < kT / kWave; ++w) r = min(r, sh.red_mi[w]);
+    imin = r;
+    __syncthreads();
+}
+
 // Windows of up to this many lags keep the outcome of the first peak scan
 // (bit t - tmin set: a decided peak) in LDS, so that the later scans test a
 // bit instead of evaluating three score intervals again.
@@ -150,6 +192,9 @@ struct Shared {
     double red_d2[kT / kWave];
     int64_t red_i[kT / kWave];
     int64_t red_j[kT / kWave];
+    double red_md[3][kT / kWave];     // multi-value reductions: double minima,
+    int64_t red_ms[2][kT / kWave];    //   int64 sums,
+    int64_t red_mi[kT / kWave];       //   one int64 minimum
     uint32_t peaks[kPeakWords];
     int done;
     double r_approx;
@@ -235,11 +280,29 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
             (void)count;
             return true;
         } else {
-            const int k = atomicAdd(&count[tier - 1], 1);
-            if (k >= kQueueCap) return false;
-            a.q_win[(tier - 1) * kQueueCap + k] = (int32_t)b;
-            a.q_lag[(tier - 1) * kQueueCap + k] = t;
-            return true;
+            // one atomic per wavefront and tier: the calling lanes of a tier
+            // take consecutive slots from a range their first lane reserves
+            const int lane = threadIdx.x & (kWave - 1);
+            bool ok = true;
+            for (int tr = 1; tr <= 2; ++tr) {
+                const bool mine = tier == tr;
+                const uint64_t m = __ballot(mine);
+                if (m == 0) continue;
+                const int leader = __ffsll((unsigned long long)m) - 1;
+                int base = 0;
+                if (lane == leader) base = atomicAdd(&count[tr - 1], __popcll(m));
+                base = __shfl(base, leader);
+                if (mine) {
+                    const int k = base + __popcll(m & ((uint64_t(1) << lane) - 1));
+                    if (k >= kQueueCap) {
+                        ok = false;
+                    } else {
+                        a.q_win[(tr - 1) * kQueueCap + k] = (int32_t)b;
+                        a.q_lag[(tr - 1) * kQueueCap + k] = t;
+                    }
+                }
+            }
+            return ok;
         }
     };
     auto want_r = [&]() {
@@ -325,11 +388,17 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
                 unk_lo = fmin(unk_lo, z.lo);
             }
         }
-        unk = block_sum_i<kSelThreads>(unk, sh.red_i);
-        npk = block_sum_i<kSelThreads>(npk, sh.red_j);
-        pk_lo = block_min_d<kSelThreads>(pk_lo, sh.red_d);
-        pk_hi = block_min_d<kSelThreads>(pk_hi, sh.red_d2);
-        unk_lo = block_min_d<kSelThreads>(unk_lo, sh.red_d);
+        {
+            double dm[3] = {pk_lo, pk_hi, unk_lo};
+            int64_t is[2] = {unk, npk};
+            int64_t im = 0;
+            block_reduce<kSelThreads>(dm, is, im, sh);
+            pk_lo = dm[0];
+            pk_hi = dm[1];
+            unk_lo = dm[2];
+            unk = is[0];
+            npk = is[1];
+        }
         if (unk > 0) {
             const double cut =
                 npk > 0 ? fmax(r_hi - c_lag * (r_hi - pk_hi) + ulp4 * r_hi, pk_hi) : INFINITY;
@@ -375,9 +444,13 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
                 push(t, z);
             }
         }
-        unk = block_sum_i<kSelThreads>(unk, sh.red_i);
-        ncand = block_sum_i<kSelThreads>(ncand, sh.red_j);
-        tc = block_min_i<kSelThreads>(tc, sh.red_i);
+        {
+            double dm[3] = {INFINITY, INFINITY, INFINITY};
+            int64_t is[2] = {unk, ncand};
+            block_reduce<kSelThreads>(dm, is, tc, sh);
+            unk = is[0];
+            ncand = is[1];
+        }
         if (unk > 0) {
             // the threshold must tighten too: R and every peak that can be
             // the smallest one
@@ -423,9 +496,13 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
                 tbest = min(tbest, t);
             }
         }
-        ncont = block_sum_i<kSelThreads>(ncont, sh.red_i);
-        nopen = block_sum_i<kSelThreads>(nopen, sh.red_j);
-        tbest = block_min_i<kSelThreads>(tbest, sh.red_i);
+        {
+            double dm[3] = {INFINITY, INFINITY, INFINITY};
+            int64_t is[2] = {ncont, nopen};
+            block_reduce<kSelThreads>(dm, is, tbest, sh);
+            ncont = is[0];
+            nopen = is[1];
+        }
         if (ncont > 1 && nopen > 0 && tau0 > 0.0) {
             for (int64_t t = lo + tid; t <= hi; t += kSelThreads) {
                 const Iv z = iv(t);
@@ -483,37 +560,60 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
     return done;
 }
 
+// Windows of at most this many lags are staged in LDS by the selection passes
+// (their fp64 scores and two tier bitmaps: at most about 113 KiB).
+constexpr int32_t kSelLdsLags = 14000;
+constexpr int64_t kSelLdsWindows = 1024;
+
+// One pass of the rule over every window not yet decided.  With a.stage the
+// window's scores and tier bitmaps are first copied to LDS with coalesced
+// loads (all in flight together), so that the rule's scans read LDS.
 template <int kSelThreads>
 __global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, Weights w) {
     __shared__ Shared<kSelThreads> sh;
+    extern __shared__ double dyn[];
     const int64_t b = blockIdx.x;
-    const WindowView view = {a.s64 + b * (int64_t)a.lags, a.tier1 + b * (int64_t)a.words,
-                             a.tier2 + b * (int64_t)a.words, a.queued1 + b * (int64_t)a.words,
-                             a.queued2 + b * (int64_t)a.words};
+    if (a.pass > 0 && a.state[b].done) return;   // decided earlier (the same for every thread)
+    WindowView view = {a.s64 + b * (int64_t)a.lags, a.tier1 + b * (int64_t)a.words,
+                       a.tier2 + b * (int64_t)a.words, a.queued1 + b * (int64_t)a.words,
+                       a.queued2 + b * (int64_t)a.words};
+    if (a.stage) {
+        double* s_l = dyn;
+        uint32_t* t1_l = reinterpret_cast<uint32_t*>(dyn + a.lags);
+        uint32_t* t2_l = t1_l + a.words;
+        for (int32_t j = threadIdx.x; j < a.lags; j += kSelThreads) s_l[j] = view.s[j];
+        for (int32_t k = threadIdx.x; k < a.words; k += kSelThreads) {
+            t1_l[k] = view.t1[k];
+            t2_l[k] = view.t2[k];
+        }
+        __syncthreads();
+        view.s = s_l;
+        view.t1 = t1_l;
+        view.t2 = t2_l;
+    }
     select_window<kSelThreads, false>(a, w, b, a.pass, a.last != 0, sh, view);
 }
 
-// One re-score round: every wavefront takes queued tier-1 requests (one lag
-// per wavefront), then every lane takes queued tier-2 requests (one lag, or
-// one window's R, per lane).
+// One re-score round: every workgroup takes queued tier-1 requests (one lag
+// per workgroup at a time), then every lane takes queued tier-2 requests (one
+// lag, or one window's R, per lane).
 __global__ __launch_bounds__(kThreads) void rescore_kernel(SelectArgs a, Weights w) {
+    __shared__ double red[kThreads / kWave];
     const int32_t* count = a.q_count + 2 * a.pass;
     const int n1 = min(count[0], kQueueCap), n2 = min(count[1], kQueueCap);
     if (n1 == 0 && n2 == 0) return;
-    const int lane = threadIdx.x & (kWave - 1);
-    const int64_t waves = (int64_t)gridDim.x * (kThreads / kWave);
-    const int64_t wave = (int64_t)blockIdx.x * (kThreads / kWave) +
-                         __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    for (int64_t e = wave; e < n1; e += waves) {
+    for (int64_t e = blockIdx.x; e < n1; e += gridDim.x) {
         const int64_t b = a.q_win[e];
         const int64_t t = a.q_lag[e];
         const int64_t j = t - a.tmin;
         uint32_t* t1 = a.tier1 + b * (int64_t)a.words;
-        if ((t1[j >> 5] >> (j & 31)) & 1u) continue;
+        const uint32_t done = (t1[j >> 5] >> (j & 31)) & 1u;
+        __syncthreads();                    // every thread has read the bit
+        if (done) continue;
         const float* __restrict__ xw = a.x + table_off(a.tab, b, a.window_stride);
-        const double v =
-            wave_score(xw, a.num_channels, a.channel_stride, table_n(a.tab, b, a.n), t, w, lane);
-        if (lane == 0) {
+        const double v = group_score<kThreads>(xw, a.num_channels, a.channel_stride,
+                                               table_n(a.tab, b, a.n), t, w, red);
+        if (threadIdx.x == 0) {
             a.s64[b * (int64_t)a.lags + j] = v;
             __threadfence();
             const uint32_t old = atomicOr(&t1[j >> 5], 1u << (j & 31));
@@ -570,31 +670,32 @@ __global__ __launch_bounds__(kThreads) void select_init_kernel(SelectBuffers sb,
 }
 
 // Re-scores the lags window b's rule marked in its queued bitmaps (and R), on
-// the LDS copies of the fused kernel: tier 1 by the wavefronts (one lag each at
+// the LDS copies of the fused kernel: tier 1 by the whole workgroup (one lag at
 // a time), tier 2 and R by single lanes, with the same evaluations as
 // rescore_kernel.
 template <int kT>
 __device__ void rescore_window(const SelectArgs& a, const Weights& w, int64_t b, double* s,
                                uint32_t* t1, uint32_t* t2, const uint32_t* qd1,
-                               const uint32_t* qd2) {
-    const int tid = threadIdx.x, lane = tid & (kWave - 1);
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+                               const uint32_t* qd2, double* red) {
+    const int tid = threadIdx.x;
     WinState* st = a.state + b;
     const float* __restrict__ xw = a.x + b * a.window_stride;
-    for (int k = wave; k < a.words; k += kT / kWave) {
-        uint32_t m = __builtin_amdgcn_readfirstlane(qd1[k] & ~t1[k]);
+    for (int k = 0; k < a.words; ++k) {
+        // read by every thread before group_score's barriers let thread 0 set a bit of k
+        uint32_t m = qd1[k] & ~t1[k];
         while (m) {
             const int bit = __builtin_ctz(m);
             m &= m - 1;
             const int64_t j = 32 * (int64_t)k + bit;
-            const double v = wave_score(xw, a.num_channels, a.channel_stride, a.n, a.tmin + j, w,
-                                        lane);
-            if (lane == 0) {
+            const double v = group_score<kT>(xw, a.num_channels, a.channel_stride, a.n,
+                                             a.tmin + j, w, red);
+            if (tid == 0) {
                 s[j] = v;
                 atomicOr(&t1[k], 1u << bit);
                 atomicAdd(&st->rescored, 1);
             }
         }
+        __syncthreads();
     }
     for (int k = tid; k < a.words; k += kT) {
         uint32_t m = qd2[k] & ~t2[k];
@@ -687,7 +788,7 @@ __global__ __launch_bounds__(stats::kStatsThreads) void finish_kernel(SelectArgs
     for (int pass = 0; pass < passes; ++pass) {
         if (select_window<kT, true>(a, w, b, pass, pass == passes - 1, sh, view)) break;
         __syncthreads();
-        rescore_window<kT>(a, w, b, s_l, t1, t2, qd1, qd2);
+        rescore_window<kT>(a, w, b, s_l, t1, t2, qd1, qd2, red);
         __syncthreads();
     }
 }
@@ -784,13 +885,19 @@ hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const 
     const int passes = rescue ? kPasses : 1;
     const dim3 grid_sel((unsigned)p.num_windows);
     const dim3 grid_re(kRescoreGroups);
+    // (for a few windows each pass is a chain of scans that LDS shortens; for
+    // many windows the copies would cost more occupancy than they save)
+    a.stage = p.lags <= kSelLdsLags && p.num_windows <= kSelLdsWindows;
+    const size_t lds =
+        a.stage ? (size_t)p.lags * sizeof(double) + 2 * (size_t)p.bitmap_words * 4 : 0;
     for (int pass = 0; pass < passes; ++pass) {
         a.pass = pass;
         a.last = pass == passes - 1;
         if (p.lags >= kWideLags && !p.table.n)
-            hipLaunchKernelGGL(select_pass_kernel<1024>, grid_sel, dim3(1024), 0, s, a, w);
+            hipLaunchKernelGGL(select_pass_kernel<1024>, grid_sel, dim3(1024), lds, s, a, w);
         else
-            hipLaunchKernelGGL(select_pass_kernel<kThreads>, grid_sel, dim3(kThreads), 0, s, a, w);
+            hipLaunchKernelGGL(select_pass_kernel<kThreads>, grid_sel, dim3(kThreads), lds, s, a,
+                               w);
         if (!a.last) hipLaunchKernelGGL(rescore_kernel, grid_re, dim3(kThreads), 0, s, a, w);
     }
     return hipGetLastError();
