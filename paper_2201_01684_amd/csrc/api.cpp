@@ -100,7 +100,7 @@ bool launches_fit(const Plan& p) {
             !fits(seqs * ((p.lags + 255) / 256), 256))
             return false;
     } else if (p.sliding) {
-        if (!fits(p.block_tasks, kWave)) return false;
+        if (!fits(2 * p.block_tasks, kWave)) return false;   // the cut launch has twice the waves
     } else if (!fits(p.tasks, kWave)) {
         return false;
     }
@@ -247,7 +247,7 @@ int make_plan(const gpoeo_pd_desc* d, Plan* p, bool ragged = false) {
         p->block_chunk = chunk;
         p->block_chunks = (int32_t)chunks;
         if (!mul_ok(bbase, chunks, &p->block_tasks)) return GPOEO_PD_EINVAL;
-        if (p->block_tasks / p->waves_per_group + 1 > INT32_MAX) return GPOEO_PD_EINVAL;
+        if (2 * p->block_tasks / p->waves_per_group + 1 > INT32_MAX) return GPOEO_PD_EINVAL;
     }
     if (p->fft) {   // one D(T) per (window, channel, lag), lags from tmin
         p->t0 = d->tmin;
@@ -605,7 +605,7 @@ int gpoeo_pd_describe_plan(const gpoeo_pd_desc* desc, gpoeo_pd_plan_info* info) 
     info->score_waves = p.fft ? 0
                         : p.mfma ? (int64_t)p.num_windows * p.num_channels * p.mfma_tiles *
                                        p.mfma_chunks
-                        : (p.sliding ? 2 * p.block_tasks : p.tasks);
+                        : (p.sliding ? 3 * p.block_tasks : p.tasks);
     info->workspace_bytes = p.bytes;
     const double wc = (double)p.num_windows * p.num_channels;
     double defined = 0.0, scored = 0.0;

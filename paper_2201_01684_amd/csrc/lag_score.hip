@@ -141,6 +141,9 @@ __global__ __launch_bounds__(kWave * kWavesPerGroup) void lag_score_kernel(Score
     // shared block partials of overlapping windows the trace end and, for the
     // cut partials, the end of the block the lags' ranges stop in.
     int64_t n = table_n(a.tab, b, a.n);
+    // samples that exist from xw on: the window, or with shared block
+    // partials the rest of the trace (the cut bound below only limits pairs)
+    const int64_t mem_end = a.trace_len > 0 ? a.trace_len - b * a.window_stride : n;
     if (a.trace_len > 0) n = min(n, a.trace_len - b * a.window_stride);
     if (a.cut > 0) n = min(n, ((t_wave - 1) / a.cut + 1) * a.cut);
 
@@ -174,7 +177,7 @@ __global__ __launch_bounds__(kWave * kWavesPerGroup) void lag_score_kernel(Score
     };
     for (int64_t q0 = 0; q0 < nb_full; q0 += runs_per) {
         const int64_t q1 = min(nb_full, q0 + runs_per);
-        if constexpr (kBT == 8) {
+        if constexpr (kBT <= 8) {
             // Two register sets: the loads of the next block are in flight
             // while this block's products run (a wave's own latency stays
             // hidden even when few waves share a SIMD, as for short windows).
@@ -200,19 +203,26 @@ __global__ __launch_bounds__(kWave * kWavesPerGroup) void lag_score_kernel(Score
             acc[j] = 0.0f;
         }
     }
-    // Masked blocks at the end of the lags' ranges.
+    // Masked blocks at the end of the lags' ranges.  A block whose loads stay
+    // below mem_end (the loads of an unmasked block reach at most sample
+    // i + t_wave_hi + 20) loads like one and masks only the arithmetic: the
+    // cut partials of shared blocks, whose pair bound lies inside the trace.
+    // Otherwise no load passes the last sample.
     for (int64_t q0 = nb_full; q0 < nb_any; q0 += runs_per) {
         const int64_t q1 = min(nb_any, q0 + runs_per);
         for (int64_t q = q0; q < q1; ++q) {
             const int64_t i = i_begin + q * kBlockSamples;
-            float xs[16];
-#pragma unroll
-            for (int s = 0; s < 16; ++s) xs[s] = (i + s < n) ? xw[i + s] : 0.0f;
             const int64_t rem64 = n - i - t_lane;   // pair (s, j) valid iff s + j < rem
             const int rem = (int)max((int64_t)-1, min(rem64, (int64_t)64));
-            float y[kW];
+            float xs[16], y[kW];
+            if (i + t_wave_hi + 21 <= mem_end) {
+                load_block(q, xs, y);
+            } else {
 #pragma unroll
-            for (int kk = 0; kk < kW; ++kk) y[kk] = (kk < rem) ? xw[i + t_lane + kk] : 0.0f;
+                for (int s = 0; s < 16; ++s) xs[s] = (i + s < n) ? xw[i + s] : 0.0f;
+#pragma unroll
+                for (int kk = 0; kk < kW; ++kk) y[kk] = (kk < rem) ? xw[i + t_lane + kk] : 0.0f;
+            }
             block_masked<kBT>(xs, y, rem, acc);
         }
 #pragma unroll
@@ -281,14 +291,18 @@ void launch_shifted(const Plan& p, const ScoreArgs& a, hipStream_t s) {
     }
 }
 
-void launch(const Plan& p, const ScoreArgs& a, hipStream_t s) {
-    if (p.lags_per_lane == 8) {
-        if (p.waves_per_group == 1) launch_shifted<8, 1>(p, a, s);
-        else launch_shifted<8, 4>(p, a, s);
-    } else {
-        if (p.waves_per_group == 1) launch_shifted<16, 1>(p, a, s);
-        else launch_shifted<16, 4>(p, a, s);
-    }
+template <int kBT>
+void launch_bt(const Plan& p, const ScoreArgs& a, hipStream_t s) {
+    if (p.waves_per_group == 1) launch_shifted<kBT, 1>(p, a, s);
+    else launch_shifted<kBT, 4>(p, a, s);
+}
+
+// bt: lags per lane of this launch (the plan's, or half of it for the cut
+// partials of shared blocks)
+void launch(const Plan& p, const ScoreArgs& a, hipStream_t s, int bt) {
+    if (bt == 4) launch_bt<4>(p, a, s);
+    else if (bt == 8) launch_bt<8>(p, a, s);
+    else launch_bt<16>(p, a, s);
 }
 
 ScoreArgs common(const Plan& p, const float* x) {
@@ -322,7 +336,7 @@ hipError_t launch_lag_score(const Plan& p, const float* x, double* part, hipStre
         hipLaunchKernelGGL(lag_score_tiny_kernel, dim3((unsigned)groups), dim3(kTinyLags), 0, s,
                            a);
     } else {
-        launch(p, a, s);
+        launch(p, a, s, p.lags_per_lane);
     }
     return hipGetLastError();
 }
@@ -340,10 +354,16 @@ hipError_t launch_lag_score_blocks(const Plan& p, const float* x, double* full, 
     a.chunk = p.block_chunk;
     a.chunks = p.block_chunks;
     a.part = full;                                  // full-block partials F_g(T)
-    launch(p, a, s);
-    a.part = cut;                                   // cut-block partials C_g(T)
+    launch(p, a, s, p.lags_per_lane);
+    // Cut-block partials C_g(T): every pair range of a lag block ends inside
+    // the block, along a diagonal as long as the lag block is wide, which the
+    // masked blocks cover; lag blocks of half the width halve that stretch.
+    // They still start at 1 (mod their width), which divides the stride.
+    a.part = cut;
     a.cut = p.window_stride;
-    launch(p, a, s);
+    a.lag_blocks = 2 * p.lag_blocks;
+    a.tasks = 2 * p.block_tasks;
+    launch(p, a, s, p.lags_per_lane / 2);
     return hipGetLastError();
 }
 
