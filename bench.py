@@ -39,6 +39,10 @@ EM_FLOP = 13
 # add), the centred difference (sub, sub, sub) and its square accumulated (mul, add).
 CENTRED_FLOP = 7
 FLOP_PER_PAIR = 3                 # one subtraction, one multiply, one add per (x[i], x[i+T])
+# Pairs per second the direct kernel can issue at most: one v_sub_f32 and one
+# v_fmac_f32 per pair, two VALU instructions per clock per CU with dual issue,
+# 256 CUs at 2.4 GHz.
+VALU_PAIR_CEILING = 256 * 2.4e9 * 64
 METRIC = "lag·samples/sec and traces/sec for batched period detection; % FP32 peak"
 CSRC = os.path.join(ROOT, "paper_2201_01684_amd", "csrc")
 # committed rocprofv3 HBM counter summaries per score mode (w3), and the source
@@ -461,7 +465,11 @@ def main():
                     "achieved": ops / (score_ms / 1e3) / 1e12, "peak": INT8_MFMA_PEAK_TOPS,
                     "unit": "TOP/s", "frac": ops / (score_ms / 1e3) / 1e12 / INT8_MFMA_PEAK_TOPS,
                     "traffic": counters_traffic(wl.name, "mfma"), "ops_per_launch": ops,
-                    "fp32_equivalent_tflops": FLOP_PER_PAIR * scored / (score_ms / 1e3) / 1e12}
+                    "fp32_equivalent_tflops": FLOP_PER_PAIR * scored / (score_ms / 1e3) / 1e12,
+                    # the method's own unit: (x[i], x[i+T]) pairs per second, against
+                    # the direct kernel's VALU pair ceiling (two instructions per pair)
+                    "pairs_per_s": scored / (score_ms / 1e3),
+                    "vs_valu_pair_ceiling": scored / (score_ms / 1e3) / VALU_PAIR_CEILING}
     else:
         roofline = {"kernel": "lag_score_kernel", "bound": "alu", "achieved": achieved,
                     "peak": FP32_VECTOR_PEAK_TFLOPS, "unit": "TFLOP/s",
@@ -539,6 +547,8 @@ def main():
             line[key] = {"ms_per_step": a_ms, "value": pairs / (a_ms / 1e3),
                          "traces_per_sec": wl.num_windows / (a_ms / 1e3),
                          "selections_equal_direct": bool(same)}
+            if key == "mfma_scores":   # whole call, every pair of the definition
+                line[key]["vs_valu_pair_ceiling"] = pairs / (a_ms / 1e3) / VALU_PAIR_CEILING
             del adet
             torch.cuda.empty_cache()
     if wl.truth is not None:
