@@ -276,27 +276,35 @@ __global__ __launch_bounds__(kThreads) void mfma_edge_kernel(MfmaArgs a) {
 // from one step to the next, so a workgroup stages its digits in LDS a stage
 // of kStageSteps steps at a time: per plane, an A block of the samples
 // [i0s - 64, i0s + 32 kStageSteps + 96) and a B block of the samples
-// [i0s + T0, i0s + T0 + 32 (kStageSteps + 1) + 3072 + 1024), where i0s is the
-// stage's first sample and T0 the first lag of the workgroup's first tile.
-// Samples at or past N are staged as zeros.  The B block is stored as two
+// [i0s + T0', i0s + T0' + 32 (kStageSteps + 1) + 3072 + 1024), where i0s is the
+// stage's first sample and T0' the first lag T0 of the workgroup's first tile
+// rounded down to a multiple of 16, so that every staged chunk is 16 aligned
+// bytes of a plane.  Samples at or past N are staged as zeros.  The B block is stored as two
 // halves, the first and the second 16 bytes of every 32-byte row, so that the
 // lanes of a B read (one 16-byte half of 32 consecutive rows) cover 512
-// contiguous bytes, free of bank conflicts.  Two stage buffers: the next
-// stage's digits are loaded from HBM into registers while this one's products
-// run, then written to the other buffer before the stage's one barrier.
-// Two workgroups share a CU (67 KB of LDS and at most 256 registers a lane
-// each), so one wave's operand reads overlap the other's products.
+// contiguous bytes, free of bank conflicts.
+//
+// The staging goes straight from memory into LDS (global_load_lds_dwordx4:
+// lane l of one instruction writes the 16 bytes at LDS base + 16 l), into the
+// other of two stage buffers while this stage's products run; the stage ends
+// with a wait for those loads and one barrier.  No staging passes through
+// registers, so r(T) stays in registers between flushes, and two workgroups
+// share a CU (68 KB of LDS and at most 256 registers a lane each): one wave's
+// operand reads overlap the other's products.
 constexpr int kStageSteps = 64;
 constexpr int kStageA = 32 * kStageSteps + 160;                  // 2208 bytes
 constexpr int kStageB = 32 * (kStageSteps + 1) + 4 * kMfmaTileLags;   // 6176 bytes
 constexpr int kStageHalf = kStageB / 2;                          // 3088 bytes
 constexpr int kStagePlane = kStageA + kStageB;
-constexpr int kStageBytes = 4 * kStagePlane;                     // 33536 bytes
-constexpr int kStageChunks = kStageBytes / 16;
-constexpr int kStageRounds = (kStageChunks + kThreads - 1) / kThreads;
+constexpr int kStageChunks = 4 * kStagePlane / 16;               // 2096 chunks of 16 bytes
+constexpr int kStageLoads = (kStageChunks + kWave - 1) / kWave;  // 33 wave-wide loads a stage
+constexpr int kStageBytes = kStageLoads * kWave * 16;            // 33792 bytes
 static_assert(kStageA % 16 == 0 && kStageB % 32 == 0 && kStageHalf % 16 == 0,
               "16-byte staging chunks, 32-byte B rows");
 static_assert(kMfmaFlush % kStageSteps == 0 && kStageSteps % 2 == 0, "stage and flush cadence");
+
+typedef __attribute__((address_space(1))) void global_void;
+typedef __attribute__((address_space(3))) void lds_void;
 
 // One wavefront per (sequence, tile of 1024 lags, chunk of sample steps); four
 // tiles of a sequence per workgroup, sharing the staged digits.  With one chunk
@@ -342,91 +350,59 @@ __global__ __launch_bounds__(kThreads, 2) void mfma_xcorr_kernel(MfmaArgs a) {
     const int64_t my_steps = active ? max((int64_t)0, steps_of(t0)) : 0;
     const int64_t stages = (wg_steps + kStageSteps - 1) / kStageSteps;
     const int8_t* __restrict__ seq = a.dig + s * 4 * a.plane + kMfmaPadL;
+    // The steps' samples are moved dl = T0 - T0' (0 .. 15) earlier than i0, so
+    // that B starts on the aligned T0': step i0 pairs, for lag T0 + 32 b + a,
+    // the samples i = i0 - dl - a + k and i + T (k < 32).  Successive steps
+    // still cover every i exactly once, from i = -dl - a <= 0 on.
+    const int dl = (int)(tg0 & 15);
 
-    // staging: 16-byte chunk c of a stage, plane p and chunk j of the plane's
-    // blocks, lands at byte 16 c of its buffer (A), or in the B half j' % 2 at
-    // row j' / 2 (B, with j' = j - kStageA / 16)
-    auto stage_pos = [&](int c) {
-        const int p = c / (kStagePlane / 16), j = c % (kStagePlane / 16);
-        if (j < kStageA / 16) return 16 * c;
-        const int jb = j - kStageA / 16;
-        return p * kStagePlane + kStageA + (jb & 1) * kStageHalf + 16 * (jb >> 1);
-    };
-    // The B block starts at lag tg0 = Tmin + 4096 g, which need not be a
-    // multiple of 16: its chunks are taken from 32 aligned bytes at an offset
-    // shift, the same for every chunk of the launch.
-    const int shift = (int)(tg0 & 15);
-    auto bytes_from = [&](const v4i& lo, const v4i& hi) {
-        const uint32_t w[8] = {(uint32_t)lo[0], (uint32_t)lo[1], (uint32_t)lo[2], (uint32_t)lo[3],
-                               (uint32_t)hi[0], (uint32_t)hi[1], (uint32_t)hi[2], (uint32_t)hi[3]};
-        const int rb = shift & 3;
-        v4i out;
-        switch (shift >> 2) {   // uniform: constant register indices in each case
-#define GPOEO_BYTES_AT(q)                                                     \
-    case q:                                                                   \
-        out[0] = (int)__builtin_amdgcn_alignbyte(w[q + 1], w[q + 0], rb);     \
-        out[1] = (int)__builtin_amdgcn_alignbyte(w[q + 2], w[q + 1], rb);     \
-        out[2] = (int)__builtin_amdgcn_alignbyte(w[q + 3], w[q + 2], rb);     \
-        out[3] = (int)__builtin_amdgcn_alignbyte(w[q + 4], w[q + 3], rb);     \
-        break;
-            GPOEO_BYTES_AT(0)
-            GPOEO_BYTES_AT(1)
-            GPOEO_BYTES_AT(2)
-            default:
-            GPOEO_BYTES_AT(3)
-#undef GPOEO_BYTES_AT
-        }
-        return out;
-    };
-    v4i held[kStageRounds];
-    auto fetch = [&](int64_t st) {
+    // Staging: the 16-byte chunk c of a stage lands at byte 16 c of its buffer.
+    // Per plane p, chunks j < kStageA / 16 are the A block; then the B rows'
+    // first halves, then their second halves.  A chunk that starts at or past
+    // N is read from the zero padding before the plane's first sample, as is
+    // every slot past the last chunk.  Wave w issues the loads w, w + 4, ...
+    auto fetch = [&](int64_t st, int buf) {
         const int64_t i0s = 32 * (kbeg + st * kStageSteps);
-#pragma unroll
-        for (int rr = 0; rr < kStageRounds; ++rr) {
-            const int c = rr * kThreads + threadIdx.x;
-            held[rr] = v4i{0, 0, 0, 0};
-            if (c < kStageChunks) {
-                const int p = c / (kStagePlane / 16), j = c % (kStagePlane / 16);
-                const int8_t* plane = seq + p * a.plane;
-                if (j < kStageA / 16) {   // A: 16-byte aligned (i0s is a multiple of 32)
-                    const int64_t i = i0s - 64 + 16 * j;
-                    // a chunk starting before N: its samples, and zeros from
-                    // the plane's padding past N
-                    if (i < n) held[rr] = *reinterpret_cast<const v4i*>(plane + i);
-                } else {   // B: from the two aligned chunks around it
-                    const int64_t i = i0s + tg0 + 16 * (j - kStageA / 16) - shift;
-                    v4i lo = v4i{0, 0, 0, 0}, hi = v4i{0, 0, 0, 0};
-                    if (i < n) lo = *reinterpret_cast<const v4i*>(plane + i);
-                    if (shift != 0 && i + 16 < n) hi = *reinterpret_cast<const v4i*>(plane + i + 16);
-                    held[rr] = bytes_from(lo, hi);
-                }
+        for (int r = wave; r < kStageLoads; r += kThreads / kWave) {
+            const int c = r * kWave + lane;
+            const int p = c / (kStagePlane / 16), j = c % (kStagePlane / 16);
+            const int8_t* plane = seq + (int64_t)min(p, 3) * a.plane;
+            int64_t i;
+            if (j < kStageA / 16) {
+                i = i0s - 64 + 16 * j;
+            } else {
+                const int jb = j - kStageA / 16;
+                const int half = jb >= kStageHalf / 16 ? 1 : 0;
+                i = i0s + (tg0 - dl) + 32 * (jb - half * (kStageHalf / 16)) + 16 * half;
             }
+            const int8_t* src = (c < kStageChunks && i < n) ? plane + i : seq - 64;
+            __builtin_amdgcn_global_load_lds((global_void*)src,
+                                             (lds_void*)(stage_buf + buf * kStageBytes +
+                                                         r * (kWave * 16)),
+                                             16, 0, 0);
         }
     };
-    auto deposit = [&](int buf) {
-#pragma unroll
-        for (int rr = 0; rr < kStageRounds; ++rr) {
-            const int c = rr * kThreads + threadIdx.x;
-            if (c < kStageChunks)
-                *reinterpret_cast<v4i*>(stage_buf + buf * kStageBytes + stage_pos(c)) = held[rr];
-        }
+    // the stage's loads have landed, for every wave of the workgroup
+    auto stage_barrier = [&]() {
+        __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0); expcnt and lgkmcnt not waited on
+        __syncthreads();
     };
 
     const int m = lane & 31, h = lane >> 5;
-    const int off = (4 - (m & 3)) & 3;   // byte offset of this lane's A row within its first dword
+    const int off = (-dl - m) & 3;   // byte offset of this lane's A row within its first dword
     v16i acc[7];
 #pragma unroll
     for (int g = 0; g < 7; ++g) acc[g] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
-    // Per step, from the stage buffer: A row a = m, bytes i0 - m + 16 h .. + 15
-    // (dword-aligned reads shifted into place); B column b = m, bytes
-    // i0 + T0 + 32 m + 16 h .. + 15.
-    uint32_t w0[4][5];
-    v4i b0[4];
+    // Per step, from the stage buffer: A row a = m, bytes i0 - dl - m + 16 h
+    // .. + 15 (dword-aligned reads shifted into place); B column b = m, bytes
+    // i0 + T0' + 32 m + 16 h .. + 15.
+    uint32_t w0[4][5], w1[4][5];
+    v4i b0[4], b1[4];
     auto load = [&](const int8_t* sb, uint32_t (&w)[4][5], v4i (&bq)[4], int k) {
 #pragma unroll
         for (int p = 0; p < 4; ++p) {
             const uint32_t* src = reinterpret_cast<const uint32_t*>(
-                sb + p * kStagePlane + 32 * k + 64 - m + 16 * h - off);
+                sb + p * kStagePlane + 32 * k + 64 - dl - m + 16 * h - off);
 #pragma unroll
             for (int e = 0; e < 5; ++e) w[p][e] = src[e];
         }
@@ -451,60 +427,54 @@ __global__ __launch_bounds__(kThreads, 2) void mfma_xcorr_kernel(MfmaArgs a) {
                 acc[p + q] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[p], bq[q], acc[p + q], 0, 0, 0);
     };
     // Every kMfmaFlush steps (each group sum stays below 2^31 over that many)
-    // the shift groups are added, scaled by 256^(p+q), into r(T) in fp64.
-    // Between flushes r(T) waits in the lane's own output slot (its D(T) or
-    // S(T), or the chunk's partial), so that two waves fit each SIMD.
-    // Register j of lane (m, h) holds row 8 (j / 4) + 4 h + j % 4, column m.
-    auto slot_of = [&](int64_t t) {
-        return kChunked
-            ? a.rpart + (s * a.chunks + chunk) * ((int64_t)a.tiles * kMfmaTileLags) + (t - a.t0)
-            : (a.s64 ? a.s64 : a.part) + s * a.lags + (t - a.tmin);
-    };
-    auto flush = [&](bool first) {
+    // the shift groups are added, scaled by 256^(p+q), into r(T) in fp64,
+    // which the lane holds in registers.  Register j of lane (m, h) holds row
+    // 8 (j / 4) + 4 h + j % 4, column m: lag t0 + 32 m + row.
+    double r[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) r[j] = 0.0;
+    auto flush = [&]() {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-            const int row = 8 * (j >> 2) + 4 * h + (j & 3);
-            const int64_t t = (int64_t)t0 + 32 * m + row;
-            if (t < a.tmin || t > tm) continue;   // lags past a table window's own: left unwritten
-            double* slot = slot_of(t);
-            double r = first ? 0.0 : *slot;
 #pragma unroll
-            for (int g = 6; g >= 0; --g) r += ldexp((double)acc[g][j], 8 * g);
-            *slot = r;
+            for (int g = 6; g >= 0; --g) r[j] += ldexp((double)acc[g][j], 8 * g);
         }
 #pragma unroll
         for (int g = 0; g < 7; ++g)
             acc[g] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
     };
 
-    if (stages > 0) {
-        fetch(0);
-        deposit(0);
-    }
-    __syncthreads();
+    if (stages > 0) fetch(0, 0);
+    stage_barrier();
     for (int64_t st = 0; st < stages; ++st) {
-        if (st + 1 < stages) fetch(st + 1);   // in flight while this stage's products run
+        // the next stage's loads, into the other buffer (every wave has left
+        // it behind at the last barrier), in flight while this one's products run
+        if (st + 1 < stages) fetch(st + 1, (int)((st + 1) & 1));
         const int8_t* sb = stage_buf + (st & 1) * kStageBytes;
         // this wave's steps in the stage (none once its tile's run out)
         const int nk = (int)min((int64_t)kStageSteps, max((int64_t)0, my_steps - st * kStageSteps));
-        for (int k = 0; k < nk; ++k) {
-            load(sb, w0, b0, k);
+        // two operand sets: the reads of step k + 1 are in flight while the
+        // products of step k run (nk is even)
+        if (nk > 0) load(sb, w0, b0, 0);
+        for (int k = 0; k < nk; k += 2) {
+            load(sb, w1, b1, k + 1);
             step(w0, b0);
+            if (k + 2 < nk) load(sb, w0, b0, k + 2);
+            step(w1, b1);
         }
-        if (active && ((st + 1) % (kMfmaFlush / kStageSteps) == 0 || st + 1 == stages))
-            flush(st < kMfmaFlush / kStageSteps);
-        if (st + 1 < stages) deposit((int)((st + 1) & 1));
-        __syncthreads();
+        if (active && ((st + 1) % (kMfmaFlush / kStageSteps) == 0 || st + 1 == stages)) flush();
+        stage_barrier();
     }
     if (!active) return;
-    if (stages == 0) flush(true);   // a chunk past this tile's steps: r = 0
-    if (kChunked) return;           // the partials stay for the combination
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
         const int row = 8 * (j >> 2) + 4 * h + (j & 3);
         const int64_t t = (int64_t)t0 + 32 * m + row;
-        if (t < a.tmin || t > tm) continue;
-        write_d(a, s, n, t, *slot_of(t));
+        if (t < a.tmin || t > tm) continue;   // lags past a table window's own: left unwritten
+        if (kChunked)   // the partials stay for the combination
+            a.rpart[(s * a.chunks + chunk) * ((int64_t)a.tiles * kMfmaTileLags) + (t - a.t0)] = r[j];
+        else
+            write_d(a, s, n, t, r[j]);
     }
 }
 
