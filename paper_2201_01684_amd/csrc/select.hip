@@ -209,14 +209,21 @@ struct WindowView {
     const uint32_t* t2;
     uint32_t* qd1;
     uint32_t* qd2;
+    // Deferred requests (selection passes of windows of at most 32 kReqWords
+    // lags): qd1 and qd2 above are this pass's request bitmaps in LDS, and
+    // these are the window's queued bitmaps in the workspace, which the
+    // requests join after the rule (one aggregated append per wavefront).
+    uint32_t* gq1;
+    uint32_t* gq2;
 };
 
 // One evaluation of the rule for window b (every thread of the workgroup
 // calls it).  Returns true once the window's result is written (now or in an
 // earlier pass).  Requests for higher tiers are marked in the window's queued
 // bitmaps; kLocal = false also appends them to the global re-score queues
-// (one re-score kernel serves every window), kLocal = true leaves them to the
-// caller, which re-scores the marked lags of its own window.
+// (one re-score kernel serves every window), at once or, with view.gq1 set,
+// all together after the rule; kLocal = true leaves them to the caller, which
+// re-scores the marked lags of its own window.
 template <int kSelThreads, bool kLocal>
 __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, int pass,
                               bool last, Shared<kSelThreads>& sh, const WindowView& view) {
@@ -272,7 +279,9 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
     const bool cache = lag_span <= 32 * (int64_t)kPeakWords;
     const int words_of_window = cache ? (int)((lag_span + 31) >> 5) : 0;
 
-    // Queue (window b, lag t) for the next tier; lag -1 queues R.
+    const bool deferred = !kLocal && view.gq1 != nullptr;
+    // Queue (window b, lag t) for the next tier; lag -1 queues R (never
+    // deferred).
     auto enqueue = [&](int tier, int32_t t) {
         if constexpr (kLocal) {   // the queued bitmaps (and r_queued) are the request
             (void)tier;
@@ -280,6 +289,7 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
             (void)count;
             return true;
         } else {
+            if (deferred && t >= 0) return true;   // the request bitmap holds it
             // one atomic per wavefront and tier: the calling lanes of a tier
             // take consecutive slots from a range their first lane reserves
             const int lane = threadIdx.x & (kWave - 1);
@@ -551,6 +561,50 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
         }
     }
     __syncthreads();
+    if (deferred && !done) {
+        // This pass's requests (marked in the LDS bitmaps, read after the
+        // barrier above) join the window's queued bitmaps; the lags not queued
+        // in an earlier pass go to the global queue, each wavefront's lanes
+        // into consecutive slots that one atomic reserves.  A request that
+        // does not fit is dropped and its queued bit cleared, as at once.
+        const int lane = tid & (kWave - 1);
+        for (int k0 = 0; k0 < a.words; k0 += kSelThreads) {
+            const int k = k0 + tid;
+#pragma unroll
+            for (int tr = 1; tr <= 2; ++tr) {
+                uint32_t* req = tr == 1 ? qd1 : qd2;
+                uint32_t* gq = tr == 1 ? view.gq1 : view.gq2;
+                uint32_t bits = k < a.words ? req[k] : 0u;
+                if (bits) {
+                    bits &= ~atomicOr(&gq[k], bits);
+                    req[k] = 0u;
+                }
+                const int cnt = __popc(bits);
+                int incl = cnt;
+                for (int o = 1; o < kWave; o <<= 1) {
+                    const int u = __shfl_up(incl, o);
+                    if (lane >= o) incl += u;
+                }
+                const int total = __shfl(incl, kWave - 1);
+                if (total == 0) continue;
+                int base = 0;
+                if (lane == kWave - 1) base = atomicAdd(&count[tr - 1], total);
+                base = __shfl(base, kWave - 1);
+                int slot = base + incl - cnt;
+                while (bits) {
+                    const int bit = __builtin_ctz(bits);
+                    bits &= bits - 1;
+                    if (slot < kQueueCap) {
+                        a.q_win[(tr - 1) * kQueueCap + slot] = (int32_t)b;
+                        a.q_lag[(tr - 1) * kQueueCap + slot] = tmin + 32 * k + bit;
+                    } else {
+                        atomicAnd(&gq[k], ~(1u << bit));
+                    }
+                    ++slot;
+                }
+            }
+        }
+    }
     if (tid == 0 && done) {
         o.n_rescored = st->rescored;
         o.flags = (unresolved ? GPOEO_PD_UNRESOLVED : 0u) | (st->tier2 ? GPOEO_PD_TIER2 : 0u);
@@ -559,6 +613,10 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
     }
     return done;
 }
+
+// Windows of at most 32 kReqWords lags collect a selection pass's re-score
+// requests in LDS bitmaps before they join the global queues.
+constexpr int kReqWords = 1024;
 
 // Windows of at most this many lags are staged in LDS by the selection passes
 // (their fp64 scores and two tier bitmaps: at most about 113 KiB).
@@ -571,20 +629,56 @@ constexpr int64_t kSelLdsWindows = 1024;
 template <int kSelThreads>
 __global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, Weights w) {
     __shared__ Shared<kSelThreads> sh;
+    __shared__ uint32_t req[2][kReqWords];
     extern __shared__ double dyn[];
     const int64_t b = blockIdx.x;
     if (a.pass > 0 && a.state[b].done) return;   // decided earlier (the same for every thread)
     WindowView view = {a.s64 + b * (int64_t)a.lags, a.tier1 + b * (int64_t)a.words,
                        a.tier2 + b * (int64_t)a.words, a.queued1 + b * (int64_t)a.words,
-                       a.queued2 + b * (int64_t)a.words};
+                       a.queued2 + b * (int64_t)a.words, nullptr, nullptr};
+    if (a.words <= kReqWords) {   // deferred requests (cleared here; select_window's
+                                  // first barrier orders this before the rule)
+        for (int32_t k = threadIdx.x; k < a.words; k += kSelThreads) req[0][k] = req[1][k] = 0u;
+        view.gq1 = view.qd1;
+        view.gq2 = view.qd2;
+        view.qd1 = req[0];
+        view.qd2 = req[1];
+    }
     if (a.stage) {
         double* s_l = dyn;
         uint32_t* t1_l = reinterpret_cast<uint32_t*>(dyn + a.lags);
         uint32_t* t2_l = t1_l + a.words;
-        for (int32_t j = threadIdx.x; j < a.lags; j += kSelThreads) s_l[j] = view.s[j];
-        for (int32_t k = threadIdx.x; k < a.words; k += kSelThreads) {
-            t1_l[k] = view.t1[k];
-            t2_l[k] = view.t2[k];
+        // kBatch loads of a thread in flight before their LDS stores
+        constexpr int kBatch = 8;
+        for (int32_t j0 = 0; j0 < a.lags; j0 += kBatch * kSelThreads) {
+            double v[kBatch];
+#pragma unroll
+            for (int r = 0; r < kBatch; ++r) {
+                const int32_t j = j0 + r * kSelThreads + (int32_t)threadIdx.x;
+                v[r] = j < a.lags ? view.s[j] : 0.0;
+            }
+#pragma unroll
+            for (int r = 0; r < kBatch; ++r) {
+                const int32_t j = j0 + r * kSelThreads + (int32_t)threadIdx.x;
+                if (j < a.lags) s_l[j] = v[r];
+            }
+        }
+        for (int32_t k0 = 0; k0 < a.words; k0 += kBatch * kSelThreads) {
+            uint32_t u1[kBatch], u2[kBatch];
+#pragma unroll
+            for (int r = 0; r < kBatch; ++r) {
+                const int32_t k = k0 + r * kSelThreads + (int32_t)threadIdx.x;
+                u1[r] = k < a.words ? view.t1[k] : 0u;
+                u2[r] = k < a.words ? view.t2[k] : 0u;
+            }
+#pragma unroll
+            for (int r = 0; r < kBatch; ++r) {
+                const int32_t k = k0 + r * kSelThreads + (int32_t)threadIdx.x;
+                if (k < a.words) {
+                    t1_l[k] = u1[r];
+                    t2_l[k] = u2[r];
+                }
+            }
         }
         __syncthreads();
         view.s = s_l;
