@@ -209,6 +209,32 @@ __device__ __forceinline__ double2 twiddle(const FftArgs& a, int64_t e) {
     return cmul(a.tw[a.tw_hi + (e >> a.lg2)], a.tw[a.tw_lo + (e & ((int64_t(1) << a.lg2) - 1))]);
 }
 
+// The pass twiddles of one 2^lg-point sub-transform (tw[m], m < 2^(lg-1)),
+// copied to LDS at twl by the workgroup: load() issues the loads into
+// registers (with the caller's data loads, all in flight together), store()
+// writes them; the caller's barrier before the transform orders them.
+template <int kTile>
+struct TwiddleCopy {
+    static constexpr int kPer = ((1 << (kTile - 1)) + kTThreads - 1) / kTThreads;
+    double2 v[kPer];
+    __device__ __forceinline__ void load(const double2* __restrict__ tw, int lg) {
+        const int count = 1 << (lg - 1);
+#pragma unroll
+        for (int r = 0; r < kPer; ++r) {
+            const int k = threadIdx.x + r * kTThreads;
+            v[r] = k < count ? tw[k] : make_double2(0.0, 0.0);
+        }
+    }
+    __device__ __forceinline__ void store(double2* twl, int lg) const {
+        const int count = 1 << (lg - 1);
+#pragma unroll
+        for (int r = 0; r < kPer; ++r) {
+            const int k = threadIdx.x + r * kTThreads;
+            if (k < count) twl[k] = v[r];
+        }
+    }
+};
+
 // 4 (|X_a|^2 + i |X_b|^2) at frequency k from Z(k) and Z(L - k).
 __device__ __forceinline__ double2 power_pair(double2 zk, double2 zm) {
     const double ux = zk.x + zm.x, uy = zk.y - zm.y;
@@ -454,7 +480,10 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_fwd_kernel(FftArgs a) {
     const int npts = (1 << a.lg1) * cols;
     const int64_t l2 = int64_t(1) << a.lg2;
     const Seq qa = seq_of(a, 2 * pair), qb = seq_of(a, 2 * pair + 1);
+    double2* twl = lds + npts;   // the pass twiddles, after the tile
     {   // all loads of a thread in flight before its LDS writes
+        TwiddleCopy<kTile> tc;
+        tc.load(a.tw + a.tw_a, a.lg1);
         double2 v[kRegPoints];
 #pragma unroll
         for (int r = 0; r < kRegPoints; ++r) {
@@ -462,6 +491,7 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_fwd_kernel(FftArgs a) {
             const int64_t i = f < npts ? (int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1)) : a.len;
             v[r] = make_double2(centred(qa, i), centred(qb, i));
         }
+        tc.store(twl, a.lg1);
 #pragma unroll
         for (int r = 0; r < kRegPoints; ++r) {
             const int f = threadIdx.x + r * kTThreads;
@@ -469,7 +499,7 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_fwd_kernel(FftArgs a) {
         }
     }
     __syncthreads();
-    lds_fft_fwd<kTile>(lds, a.lg1, a.lgc, a.tw + a.tw_a);
+    lds_fft_fwd<kTile>(lds, a.lg1, a.lgc, twl);
     double2* __restrict__ zp = a.z + pair * a.zstride;
     double2 w[kRegPoints];
 #pragma unroll
@@ -518,7 +548,10 @@ __global__ __launch_bounds__(kTThreads) void fft_rows_kernel(FftArgs a) {
         self = ka == kb;
         return (q & 1) ? kb : ka;
     };
+    double2* twl = lds + npts;   // the pass twiddles, after the tile
     {   // all loads of a thread in flight before its LDS writes
+        TwiddleCopy<kTile> tc;
+        tc.load(a.tw + a.tw_b, a.lg2);
         double2 v[kRegPoints];
 #pragma unroll
         for (int r = 0; r < kRegPoints; ++r) {
@@ -528,6 +561,7 @@ __global__ __launch_bounds__(kTThreads) void fft_rows_kernel(FftArgs a) {
             v[r] = (valid && f < npts) ? zp[(int64_t)bitrev(k1, a.lg1) * l2 + (f >> lgs)]
                                        : make_double2(0.0, 0.0);
         }
+        tc.store(twl, a.lg2);
 #pragma unroll
         for (int r = 0; r < kRegPoints; ++r) {
             const int f = threadIdx.x + r * kTThreads;
@@ -535,7 +569,7 @@ __global__ __launch_bounds__(kTThreads) void fft_rows_kernel(FftArgs a) {
         }
     }
     __syncthreads();
-    lds_fft_fwd<kTile>(lds, a.lg2, lgs, a.tw + a.tw_b);
+    lds_fft_fwd<kTile>(lds, a.lg2, lgs, twl);
     double2 wv[kRegPoints];
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {
@@ -557,7 +591,7 @@ __global__ __launch_bounds__(kTThreads) void fft_rows_kernel(FftArgs a) {
         if (f < npts) lds[f] = wv[r];
     }
     __syncthreads();
-    lds_fft_inv<kTile>(lds, a.lg2, lgs, a.tw + a.tw_b);
+    lds_fft_inv<kTile>(lds, a.lg2, lgs, twl);
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {   // twiddle loads first (wv is free again)
         const int f = threadIdx.x + r * kTThreads;
@@ -622,7 +656,10 @@ __global__ __launch_bounds__(kTThreads) void fft_wrap_rows_kernel(FftArgs a, int
         self = ka == kb;
         return side ? kb : ka;
     };
+    double2* twl = lds + npts;   // the pass twiddles, after the tile
     {
+        TwiddleCopy<kTile> tc;
+        tc.load(a.tw + a.tw_b, a.lg2);
         double2 v[kRegPoints];
 #pragma unroll
         for (int r = 0; r < kRegPoints; ++r) {
@@ -634,6 +671,7 @@ __global__ __launch_bounds__(kTThreads) void fft_wrap_rows_kernel(FftArgs a, int
             v[r] = (valid && f < npts) ? src[(int64_t)bitrev(k1, a.lg1) * l2 + (f >> lgs)]
                                        : make_double2(0.0, 0.0);
         }
+        tc.store(twl, a.lg2);
 #pragma unroll
         for (int r = 0; r < kRegPoints; ++r) {
             const int f = threadIdx.x + r * kTThreads;
@@ -641,7 +679,7 @@ __global__ __launch_bounds__(kTThreads) void fft_wrap_rows_kernel(FftArgs a, int
         }
     }
     __syncthreads();
-    lds_fft_fwd<kTile>(lds, a.lg2, lgs, a.tw + a.tw_b);
+    lds_fft_fwd<kTile>(lds, a.lg2, lgs, twl);
     double2 wv[kRegPoints];
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {   // at the head transform's slots
@@ -665,7 +703,7 @@ __global__ __launch_bounds__(kTThreads) void fft_wrap_rows_kernel(FftArgs a, int
         if (f < npts && (q & 1) == 0) lds[(f >> lgs) * (slots >> 1) + (q >> 1)] = wv[r];
     }
     __syncthreads();
-    lds_fft_inv<kTile>(lds, a.lg2, lgs - 1, a.tw + a.tw_b);
+    lds_fft_inv<kTile>(lds, a.lg2, lgs - 1, twl);
     const int half = npts >> 1;
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {   // twiddle loads first
@@ -705,7 +743,10 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_inv_kernel(FftArgs a) {
     const int npts = (1 << a.lg1) * cols;
     const int64_t l2 = int64_t(1) << a.lg2;
     const double2* __restrict__ zp = a.z + pair * a.zstride;
+    double2* twl = lds + npts;   // the pass twiddles, after the tile
     {   // all loads of a thread in flight before its LDS writes
+        TwiddleCopy<kTile> tc;
+        tc.load(a.tw + a.tw_a, a.lg1);
         double2 v[kRegPoints];
 #pragma unroll
         for (int r = 0; r < kRegPoints; ++r) {
@@ -713,6 +754,7 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_inv_kernel(FftArgs a) {
             v[r] = f < npts ? zp[(int64_t)(f >> a.lgc) * l2 + c0 + (f & (cols - 1))]
                             : make_double2(0.0, 0.0);
         }
+        tc.store(twl, a.lg1);
 #pragma unroll
         for (int r = 0; r < kRegPoints; ++r) {
             const int f = threadIdx.x + r * kTThreads;
@@ -720,7 +762,7 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_inv_kernel(FftArgs a) {
         }
     }
     __syncthreads();
-    lds_fft_inv<kTile>(lds, a.lg1, a.lgc, a.tw + a.tw_a);
+    lds_fft_inv<kTile>(lds, a.lg1, a.lgc, twl);
     if (a.wout) {   // head-tail transform: cc_a(s) + i cc_b(s) for shifts s < wm
         const int rows = (int)min((int64_t)((a.wm - 1) / l2) + 1, int64_t(1) << a.lg1);
         for (int f = threadIdx.x; f < rows * cols; f += kTThreads) {
@@ -1312,9 +1354,10 @@ void launch_transforms(const FftArgs& a, int64_t pairs, hipStream_t s) {
     }
     const int64_t m1 = int64_t(1) << a.lg1, m2 = int64_t(1) << a.lg2, cols = int64_t(1) << a.lgc;
     const int64_t col_groups = pairs * (m2 / cols);
-    const size_t lds_cols = sizeof(double2) * (size_t)(m1 * cols);
+    // tiles, then each kernel's pass twiddles (half a sub-transform)
+    const size_t lds_cols = sizeof(double2) * (size_t)(m1 * cols + m1 / 2);
     const int64_t rp = int64_t(1) << a.lgr;
-    const size_t lds_rows = sizeof(double2) * 2 * (size_t)(rp * m2);
+    const size_t lds_rows = sizeof(double2) * (size_t)(2 * rp * m2 + m2 / 2);
     const int64_t row_groups = pairs * ((m1 / 2 + 1 + rp - 1) / rp);
     hipLaunchKernelGGL((fft_cols_fwd_kernel<kTile, kRagged>), grid(col_groups), dim3(kTThreads),
                        lds_cols, s, a);
@@ -1375,7 +1418,7 @@ void launch_spectrum(const Plan& p, const FftArgs& a, hipStream_t s) {
         return;
     }
     const int64_t col_groups = p.fft_pairs * (p.fft_m2 / p.fft_cols);
-    const size_t lds_cols = sizeof(double2) * (size_t)p.fft_m1 * p.fft_cols;
+    const size_t lds_cols = sizeof(double2) * ((size_t)p.fft_m1 * p.fft_cols + p.fft_m1 / 2);
     const int64_t rp = int64_t(1) << a.lgr;
     const size_t lds_rows = sizeof(double2) * 2 * rp * (size_t)p.fft_m2;
     const int64_t row_groups = p.fft_pairs * ((p.fft_m1 / 2 + 1 + rp - 1) / rp);
@@ -1435,7 +1478,7 @@ void launch_wrap(const Plan& p, FftArgs aw, double2* tw, double2* zw, double* wr
     launch_twiddles(aw, tw, s);
     const int64_t m1 = int64_t(1) << aw.lg1, m2 = int64_t(1) << aw.lg2, cols = int64_t(1) << aw.lgc;
     const int64_t col_groups = p.fft_pairs * (m2 / cols);
-    const size_t lds_cols = sizeof(double2) * (size_t)(m1 * cols);
+    const size_t lds_cols = sizeof(double2) * (size_t)(m1 * cols + m1 / 2);
     aw.seg_len = p.fft_wrap_m;
     aw.seg_start = 0;                                  // heads
     aw.z = zw;
@@ -1454,7 +1497,7 @@ void launch_wrap(const Plan& p, FftArgs aw, double2* tw, double2* zw, double* wr
     if (aw.lgr > aw.lg1 - 1) aw.lgr = aw.lg1 - 1;
     const int64_t rp = int64_t(1) << aw.lgr;
     const int64_t row_groups = p.fft_pairs * ((m1 / 2 + 1 + rp - 1) / rp);
-    const size_t lds_rows = sizeof(double2) * 4 * (size_t)(rp * m2);
+    const size_t lds_rows = sizeof(double2) * (size_t)(4 * rp * m2 + m2 / 2);
     if (rows_tile == kFftSmallTileLog2)
         hipLaunchKernelGGL((fft_wrap_rows_kernel<kFftSmallTileLog2>), dim3((unsigned)row_groups),
                            dim3(kTThreads), lds_rows, s, aw, p.fft_pairs * lw);
