@@ -216,22 +216,36 @@ static void detect_one(const oracle_pd_params* p, const float* xw, int64_t n, in
 
 int32_t oracle_pd_rolling_schedule(int64_t n, int32_t t_init, const oracle_pd_rolling_params* rp,
                                    int64_t* starts, int32_t cap, double* short_next) {
+    /* Algorithm 3 (Sec. 4.1.3) measures suffixes of the trace that start
+     * (2 + c_eval step) periods before its end and then every step periods
+     * later, as long as at least c_measure periods remain.  With u = step T,
+     * s_k = s_0 + k u for s_0 = max(0, D - (2 + c_eval step) T), the suffix k
+     * exists iff D - s_k >= c_measure T, i.e. k <= (D - s_0 - c_measure T) / u:
+     * J = floor of that, plus one, suffixes.  The rounded quotient is checked
+     * against the condition itself on both sides of J. */
     const double t = (double)t_init;
     const double dur = (double)(n - 1);
+    const double need = rp->c_measure * t;
     *short_next = 0.0;
-    if (dur < rp->c_measure * t) {
-        *short_next = rp->c_measure * t - dur;
+    if (dur < need) {
+        *short_next = need - dur;
         return 0;
     }
-    double t_start = dur - (2.0 + rp->c_eval * rp->step) * t;
-    if (t_start < 0.0) t_start = 0.0;
-    int32_t j = 0;
-    while ((dur - t_start) / t >= rp->c_measure) {
-        if (j == cap) return -1;
-        starts[j++] = (int64_t)floor(t_start);
-        t_start += rp->step * t;
+    double s0 = dur - (2.0 + rp->c_eval * rp->step) * t;
+    if (s0 < 0.0) s0 = 0.0;
+    const double u = rp->step * t;
+    if (dur - s0 < need) return 0;
+    double jq = floor((dur - s0 - need) / u);
+    if (jq > (double)cap) return -1;
+    int64_t j = (int64_t)jq + 1;
+    while (j > 1 && !(dur - (s0 + (double)(j - 1) * u) >= need)) --j;
+    while (dur - (s0 + (double)j * u) >= need) {
+        ++j;
+        if (j > cap) return -1;
     }
-    return j;
+    if (j > cap) return -1;
+    for (int64_t k = 0; k < j; ++k) starts[k] = (int64_t)floor(s0 + (double)k * u);
+    return (int32_t)j;
 }
 
 int oracle_pd_rolling(const oracle_pd_params* p, const oracle_pd_rolling_params* rp,

@@ -121,11 +121,11 @@ int oracle_pd_score_list(const oracle_pd_params* p, const float* x, const int64_
  *             PERIODIC the result carries its verdict, period 0 and no windows.
  *   D       = N - 1 (the sampling duration in samples, T_s = 1)
  *   D < c_measure * T_init: too short; period T_init, next = c_measure T_init - D
- *   t_start = max(0, D - (2 + c_eval * step) * T_init)
- *   while (D - t_start) / T_init >= c_measure:
- *       suffix x[floor(t_start) .. N-1] (N_j = N - floor(t_start) samples),
- *       lags [tmin, min(tmax, N_j / 2)], same rule -> T_j, err_j
- *       t_start += step * T_init
+ *   suffix k = 0 .. J-1 starts at s_k = s_0 + k step T_init,
+ *       s_0 = max(0, D - (2 + c_eval * step) * T_init),
+ *       J = the number of k with D - s_k >= c_measure T_init;
+ *       it holds x[floor(s_k) .. N-1] (N_j = N - floor(s_k) samples) and is
+ *       scored on the lags [tmin, min(tmax, N_j / 2)] by the same rule -> T_j, err_j
  *   the suffixes with a PERIODIC verdict form T and Err (none -> APERIODIC)
  *   period  = T_k with err_k = min Err (first such k)
  *   diff    = |max T - min T| / mean T

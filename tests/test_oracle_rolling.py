@@ -36,6 +36,39 @@ def test_default_schedule_has_seven_windows():
     assert durations == [5.25, 4.75, 4.25, 3.75, 3.25, 2.75, 2.25]
 
 
+def brute_schedule(n, t_init, c_measure, step, c_eval):
+    """Algorithm 3's suffix starts by enumeration in exact rationals: start at
+    (2 + c_eval step) periods before the end (at least sample 0) and move on by
+    step periods while at least c_measure periods remain."""
+    from fractions import Fraction as F
+    d, t = F(n - 1), F(t_init)
+    cm, st, ce = F(c_measure), F(step), F(c_eval)
+    if d < cm * t:
+        return [], float(cm * t - d)
+    s = max(F(0), d - (2 + ce * st) * t)
+    out = []
+    while d - s >= cm * t:
+        out.append(math.floor(s))
+        s += st * t
+    return out, 0.0
+
+
+def test_schedule_matches_enumeration_for_other_constants():
+    # dyadic constants: every quantity of the schedule is exact in fp64, so
+    # the oracle must equal the rational enumeration exactly
+    rng = np.random.default_rng(11)
+    for _ in range(3000):
+        n = int(rng.integers(2, 2_000_000))
+        t_init = int(rng.integers(1, max(2, n // 2)))
+        cm = float(rng.choice([1.0, 1.5, 2.0, 3.0]))
+        st = float(rng.choice([0.25, 0.5, 0.75, 1.0, 1.5]))
+        ce = float(rng.choice([0.0, 2.5, 6.5, 12.0]))
+        want = brute_schedule(n, t_init, cm, st, ce)
+        if len(want[0]) > oracle.ROLLING_MAX:
+            continue
+        assert oracle.rolling_schedule(n, t_init, cm, st, ce) == want, (n, t_init, cm, st, ce)
+
+
 def lay1(n, tmax, tmin=2):
     return oracle.Layout(1, 1, n, n, n, tmin, tmax)
 
