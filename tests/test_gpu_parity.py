@@ -263,3 +263,43 @@ def test_detect_period_convenience_returns_scores_period_results():
     scores, period, res = pkg.detect_period(x2, wl.n, wl.tmin, wl.tmax,
                                             pkg.DetectParams(flags=pkg.SCORES_ONLY))
     assert res is None and int(period.abs().sum()) == 0
+
+
+def _random_case(rng):
+    """A seeded random descriptor: batch size, channels, window length, lag
+    range, strides (overlapping or padded windows) and channel weights, with
+    planted-period or noise-only windows."""
+    n = int(rng.choice([40, 97, 300, 1000, 4099, 9000, 17000, 40000]))
+    tmin = int(rng.integers(1, max(2, n // 8)))
+    tmax = int(rng.integers(tmin + 2, n // 2 + 1))      # Tmin + 2 <= Tmax <= N / 2
+    b = int(rng.integers(1, 6))
+    c = int(rng.integers(1, 4))
+    channel_stride = n + int(rng.integers(0, 7))
+    span = (c - 1) * channel_stride + n
+    window_stride = int(rng.choice([span, span + 3, max(1, span // 2)]))
+    total = (b - 1) * window_stride + span
+    period = int(rng.integers(2, max(3, n // 3)))
+    x = planted_trace(total, period, min(period, int(rng.integers(2, 9))),
+                      seed=int(rng.integers(1 << 30)),
+                      sigma=float(rng.choice([0.0, 0.5, 3.0])))
+    w = rng.choice([0.25, 0.5, 1.0, 2.0], size=c).astype(np.float32) if c > 1 else None
+    lay = oracle.Layout(b, c, n, window_stride, channel_stride, tmin, tmax, weights=w)
+    return x.astype(np.float32), lay
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_descriptors(seed):
+    """Random shapes, strides and weights: every score and selection field
+    against the oracle (scores-only and no-rescue runs of the same input
+    must give the same scores)."""
+    import paper_2201_01684_amd as pkg
+    rng = np.random.default_rng(9000 + seed)
+    x, lay = _random_case(rng)
+    where = (f"seed {seed}: B={lay.num_windows} C={lay.num_channels} N={lay.n} "
+             f"T {lay.tmin}..{lay.tmax} strides {lay.window_stride}/{lay.channel_stride}")
+    g, res = gpu_run(x, lay)
+    o, out = oracle.detect(x, lay)
+    check_scores(g, o, where)
+    check_results(res, out, where)
+    g2, _ = gpu_run(x, lay, flags=pkg.SCORES_ONLY)
+    assert np.array_equal(g, g2), f"{where}: scores-only run differs"
