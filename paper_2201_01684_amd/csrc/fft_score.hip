@@ -481,7 +481,51 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_fwd_kernel(FftArgs a) {
     const int64_t l2 = int64_t(1) << a.lg2;
     const Seq qa = seq_of(a, 2 * pair), qb = seq_of(a, 2 * pair + 1);
     double2* twl = lds + npts;   // the pass twiddles, after the tile
-    {   // all loads of a thread in flight before its LDS writes
+    // Tiles of four or more columns whose rows start on 16-byte boundaries: a
+    // thread takes runs of four points of a row (their four samples of each
+    // sequence in one 16-byte load) instead of single points.
+    auto aligned = [&](const Seq& q) {
+        return q.n == 0 || ((reinterpret_cast<uintptr_t>(q.p + c0) & 15) == 0);
+    };
+    const bool rows4 = a.lgc >= 2 && npts == kRegPoints * kTThreads && (l2 & 3) == 0 &&
+                       aligned(qa) && aligned(qb);
+    if (rows4) {   // all loads of a thread in flight before its LDS writes
+        constexpr int kRows = kRegPoints / 4;   // runs of four points a thread
+        const int quads = cols >> 2;            // runs in a row of the tile
+        TwiddleCopy<kTile> tc;
+        tc.load(a.tw + a.tw_a, a.lg1);
+        auto row_of = [&](const Seq& q, int64_t i) -> float4 {
+            if (i + 3 < q.n) return *reinterpret_cast<const float4*>(q.p + i);
+            float4 f4 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            if (i < q.n) f4.x = q.p[i];
+            if (i + 1 < q.n) f4.y = q.p[i + 1];
+            if (i + 2 < q.n) f4.z = q.p[i + 2];
+            return f4;
+        };
+        float4 va[kRows], vb[kRows];
+#pragma unroll
+        for (int k = 0; k < kRows; ++k) {
+            const int qd = threadIdx.x + k * kTThreads;   // points 4 qd .. 4 qd + 3
+            const int64_t i = (int64_t)(qd / quads) * l2 + c0 + 4 * (qd % quads);
+            va[k] = row_of(qa, i);
+            vb[k] = row_of(qb, i);
+        }
+        tc.store(twl, a.lg1);
+#pragma unroll
+        for (int k = 0; k < kRows; ++k) {
+            const int qd = threadIdx.x + k * kTThreads;
+            const int f = 4 * qd;
+            const int64_t i = (int64_t)(qd / quads) * l2 + c0 + 4 * (qd % quads);
+            // the same values as centred(): (double)x - mu inside the sequence, 0 past it
+            auto cv = [&](const Seq& q, float x, int64_t ii) {
+                return ii < q.n ? (double)x - q.mu : 0.0;
+            };
+            lds[f + 0] = make_double2(cv(qa, va[k].x, i), cv(qb, vb[k].x, i));
+            lds[f + 1] = make_double2(cv(qa, va[k].y, i + 1), cv(qb, vb[k].y, i + 1));
+            lds[f + 2] = make_double2(cv(qa, va[k].z, i + 2), cv(qb, vb[k].z, i + 2));
+            lds[f + 3] = make_double2(cv(qa, va[k].w, i + 3), cv(qb, vb[k].w, i + 3));
+        }
+    } else {   // all loads of a thread in flight before its LDS writes
         TwiddleCopy<kTile> tc;
         tc.load(a.tw + a.tw_a, a.lg1);
         double2 v[kRegPoints];
