@@ -235,6 +235,41 @@ struct TwiddleCopy {
     }
 };
 
+// The four-step twiddle tables (tw_lo, 2^lg2 entries, then tw_hi, 2^lg1) in
+// LDS at tl when together they hold at most kFourStepLds entries: copied like
+// the pass twiddles, then read by twiddle_at with the same operations as
+// twiddle().  (The forward column and row kernels; the wrap correction's row
+// kernel keeps the global tables, whose LDS would cost it a workgroup per CU.)
+constexpr int kFourStepLds = 1024;
+__host__ __device__ inline bool four_step_in_lds(int lg1, int lg2) {
+    return (1 << lg1) + (1 << lg2) <= kFourStepLds;
+}
+struct FourStepCopy {
+    static constexpr int kPer = kFourStepLds / kTThreads;
+    double2 v[kPer];
+    __device__ __forceinline__ void load(const FftArgs& a) {
+        const int count = (1 << a.lg1) + (1 << a.lg2);
+#pragma unroll
+        for (int r = 0; r < kPer; ++r) {
+            const int k = threadIdx.x + r * kTThreads;
+            v[r] = k < count ? a.tw[a.tw_lo + k] : make_double2(0.0, 0.0);
+        }
+    }
+    __device__ __forceinline__ void store(const FftArgs& a, double2* tl) const {
+        const int count = (1 << a.lg1) + (1 << a.lg2);
+#pragma unroll
+        for (int r = 0; r < kPer; ++r) {
+            const int k = threadIdx.x + r * kTThreads;
+            if (k < count) tl[k] = v[r];
+        }
+    }
+};
+__device__ __forceinline__ double2 twiddle_at(const FftArgs& a, const double2* tl, bool lds4,
+                                              int64_t e) {
+    if (!lds4) return twiddle(a, e);
+    return cmul(tl[(1 << a.lg2) + (e >> a.lg2)], tl[e & ((int64_t(1) << a.lg2) - 1)]);
+}
+
 // 4 (|X_a|^2 + i |X_b|^2) at frequency k from Z(k) and Z(L - k).
 __device__ __forceinline__ double2 power_pair(double2 zk, double2 zm) {
     const double ux = zk.x + zm.x, uy = zk.y - zm.y;
@@ -489,6 +524,10 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_fwd_kernel(FftArgs a) {
     };
     const bool rows4 = a.lgc >= 2 && npts == kRegPoints * kTThreads && (l2 & 3) == 0 &&
                        aligned(qa) && aligned(qb);
+    const bool lds4 = four_step_in_lds(a.lg1, a.lg2);
+    double2* tl = twl + (1 << (a.lg1 - 1));   // the four-step twiddles, after the pass ones
+    FourStepCopy fc;
+    if (lds4) fc.load(a);
     if (rows4) {   // all loads of a thread in flight before its LDS writes
         constexpr int kRows = kRegPoints / 4;   // runs of four points a thread
         const int quads = cols >> 2;            // runs in a row of the tile
@@ -511,6 +550,7 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_fwd_kernel(FftArgs a) {
             vb[k] = row_of(qb, i);
         }
         tc.store(twl, a.lg1);
+        if (lds4) fc.store(a, tl);
 #pragma unroll
         for (int k = 0; k < kRows; ++k) {
             const int qd = threadIdx.x + k * kTThreads;
@@ -536,6 +576,7 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_fwd_kernel(FftArgs a) {
             v[r] = make_double2(centred(qa, i), centred(qb, i));
         }
         tc.store(twl, a.lg1);
+        if (lds4) fc.store(a, tl);
 #pragma unroll
         for (int r = 0; r < kRegPoints; ++r) {
             const int f = threadIdx.x + r * kTThreads;
@@ -550,7 +591,8 @@ __global__ __launch_bounds__(kTThreads) void fft_cols_fwd_kernel(FftArgs a) {
     for (int r = 0; r < kRegPoints; ++r) {   // twiddle loads first
         const int f = threadIdx.x + r * kTThreads;
         const int64_t k1 = bitrev(f >> a.lgc, a.lg1);
-        w[r] = f < npts ? twiddle(a, k1 * (c0 + (f & (cols - 1)))) : make_double2(1.0, 0.0);
+        w[r] = f < npts ? twiddle_at(a, tl, lds4, k1 * (c0 + (f & (cols - 1))))
+                        : make_double2(1.0, 0.0);
     }
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {
@@ -593,9 +635,13 @@ __global__ __launch_bounds__(kTThreads) void fft_rows_kernel(FftArgs a) {
         return (q & 1) ? kb : ka;
     };
     double2* twl = lds + npts;   // the pass twiddles, after the tile
+    const bool lds4 = four_step_in_lds(a.lg1, a.lg2);
+    double2* tl = twl + (1 << (a.lg2 - 1));   // the four-step twiddles, after the pass ones
     {   // all loads of a thread in flight before its LDS writes
         TwiddleCopy<kTile> tc;
         tc.load(a.tw + a.tw_b, a.lg2);
+        FourStepCopy fc;
+        if (lds4) fc.load(a);
         double2 v[kRegPoints];
 #pragma unroll
         for (int r = 0; r < kRegPoints; ++r) {
@@ -606,6 +652,7 @@ __global__ __launch_bounds__(kTThreads) void fft_rows_kernel(FftArgs a) {
                                        : make_double2(0.0, 0.0);
         }
         tc.store(twl, a.lg2);
+        if (lds4) fc.store(a, tl);
 #pragma unroll
         for (int r = 0; r < kRegPoints; ++r) {
             const int f = threadIdx.x + r * kTThreads;
@@ -641,7 +688,8 @@ __global__ __launch_bounds__(kTThreads) void fft_rows_kernel(FftArgs a) {
         const int f = threadIdx.x + r * kTThreads;
         bool valid, self;
         const uint32_t k1 = k1_of(f & (slots - 1), valid, self);
-        wv[r] = (f < npts && valid) ? twiddle(a, (int64_t)k1 * (f >> lgs)) : make_double2(1.0, 0.0);
+        wv[r] = (f < npts && valid) ? twiddle_at(a, tl, lds4, (int64_t)k1 * (f >> lgs))
+                                    : make_double2(1.0, 0.0);
     }
 #pragma unroll
     for (int r = 0; r < kRegPoints; ++r) {
@@ -1398,13 +1446,16 @@ void launch_transforms(const FftArgs& a, int64_t pairs, hipStream_t s) {
     }
     const int64_t m1 = int64_t(1) << a.lg1, m2 = int64_t(1) << a.lg2, cols = int64_t(1) << a.lgc;
     const int64_t col_groups = pairs * (m2 / cols);
-    // tiles, then each kernel's pass twiddles (half a sub-transform)
+    // tiles, then each kernel's pass twiddles (half a sub-transform), then for
+    // the forward columns and the rows the four-step twiddles when they fit
+    const size_t fs = four_step_in_lds(a.lg1, a.lg2) ? (size_t)(m1 + m2) : 0;
     const size_t lds_cols = sizeof(double2) * (size_t)(m1 * cols + m1 / 2);
+    const size_t lds_cols_fwd = lds_cols + sizeof(double2) * fs;
     const int64_t rp = int64_t(1) << a.lgr;
-    const size_t lds_rows = sizeof(double2) * (size_t)(2 * rp * m2 + m2 / 2);
+    const size_t lds_rows = sizeof(double2) * ((size_t)(2 * rp * m2 + m2 / 2) + fs);
     const int64_t row_groups = pairs * ((m1 / 2 + 1 + rp - 1) / rp);
     hipLaunchKernelGGL((fft_cols_fwd_kernel<kTile, kRagged>), grid(col_groups), dim3(kTThreads),
-                       lds_cols, s, a);
+                       lds_cols_fwd, s, a);
     hipLaunchKernelGGL((fft_rows_kernel<kTile, kRagged>), grid(row_groups), dim3(kTThreads),
                        lds_rows, s, a);
     hipLaunchKernelGGL((fft_cols_inv_kernel<kTile, kRagged>), grid(col_groups), dim3(kTThreads),
@@ -1462,7 +1513,9 @@ void launch_spectrum(const Plan& p, const FftArgs& a, hipStream_t s) {
         return;
     }
     const int64_t col_groups = p.fft_pairs * (p.fft_m2 / p.fft_cols);
-    const size_t lds_cols = sizeof(double2) * ((size_t)p.fft_m1 * p.fft_cols + p.fft_m1 / 2);
+    const size_t lds_cols = sizeof(double2) * ((size_t)p.fft_m1 * p.fft_cols + p.fft_m1 / 2 +
+                                               (four_step_in_lds(a.lg1, a.lg2)
+                                                    ? (size_t)(p.fft_m1 + p.fft_m2) : 0));
     const int64_t rp = int64_t(1) << a.lgr;
     const size_t lds_rows = sizeof(double2) * 2 * rp * (size_t)p.fft_m2;
     const int64_t row_groups = p.fft_pairs * ((p.fft_m1 / 2 + 1 + rp - 1) / rp);
@@ -1522,16 +1575,18 @@ void launch_wrap(const Plan& p, FftArgs aw, double2* tw, double2* zw, double* wr
     launch_twiddles(aw, tw, s);
     const int64_t m1 = int64_t(1) << aw.lg1, m2 = int64_t(1) << aw.lg2, cols = int64_t(1) << aw.lgc;
     const int64_t col_groups = p.fft_pairs * (m2 / cols);
+    const size_t fs = four_step_in_lds(aw.lg1, aw.lg2) ? (size_t)(m1 + m2) : 0;
     const size_t lds_cols = sizeof(double2) * (size_t)(m1 * cols + m1 / 2);
+    const size_t lds_cols_fwd = lds_cols + sizeof(double2) * fs;
     aw.seg_len = p.fft_wrap_m;
     aw.seg_start = 0;                                  // heads
     aw.z = zw;
     hipLaunchKernelGGL((fft_cols_fwd_kernel<kTile, false>), dim3((unsigned)col_groups),
-                       dim3(kTThreads), lds_cols, s, aw);
+                       dim3(kTThreads), lds_cols_fwd, s, aw);
     aw.seg_start = p.n - p.fft_wrap_m;                 // tails
     aw.z = zw + p.fft_pairs * lw;
     hipLaunchKernelGGL((fft_cols_fwd_kernel<kTile, false>), dim3((unsigned)col_groups),
-                       dim3(kTThreads), lds_cols, s, aw);
+                       dim3(kTThreads), lds_cols_fwd, s, aw);
     aw.seg_len = 0;
     aw.z = zw;
     // a row pair holds four rows of m2 points: its two rows in each transform
