@@ -28,9 +28,10 @@ FP32_VECTOR_PEAK_TFLOPS = 157.3   # MI355X published FP32 vector peak
 FP64_VECTOR_PEAK_TFLOPS = 78.6    # MI355X published FP64 vector peak
 HBM_PEAK_GBS = 8000.0              # MI355X published HBM3E bandwidth
 INT8_MFMA_PEAK_TOPS = 5000.0       # MI355X published dense int8 matrix peak
-# Matrix-core scores: 16 digit-pair products (four int8 digits per sample on
-# each side) per (x[i], x[i+T]) pair, one multiply and one add each.
-MFMA_OPS_PER_PAIR = 32
+# Matrix-core scores: 13 digit-pair products (four int8 digits per sample on
+# each side; the three pairs of least weight are left out) per (x[i], x[i+T])
+# pair, one multiply and one add each.
+MFMA_OPS_PER_PAIR = 26
 # Algorithmic fp64 FLOP of the EM per (sample, component, iteration): the
 # log-density (sub, mul, mul, sub), the exponential (counted as one), the
 # normalisation (add, mul) and the three moments (add; mul, add; mul, mul, add).

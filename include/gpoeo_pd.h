@@ -58,11 +58,13 @@
  * matrix instructions: each (window, channel) sequence is centred by its mean
  * rounded to fp32, scaled by a power of two 2^s into integers
  * X_i = rint((x_i - c) 2^s) with |X_i| <= 2^30, and split into four signed
- * base-256 digits; the 16 digit-pair correlations accumulate exactly in int32
- * and are combined in fp64.  When every x_i - c is a multiple of 2^-s (the
- * samples of the sequence span at most about 2^7 in magnitude, as sampled
- * power does) the X_i are the samples exactly and the only error is the fp64
- * combination; otherwise the rounding of X_i adds a bounded error.  Each lag
+ * base-256 digits; the 13 digit-pair correlations of weight 256^2 and above
+ * accumulate exactly in int32 and are combined in fp64 (the three of least
+ * weight, at most 2^23 per sample pair against products up to 2^60, are left
+ * out and bounded).  When every x_i - c is a multiple of 2^-s (the samples of
+ * the sequence span at most about 2^7 in magnitude, as sampled power does) the
+ * X_i are the samples exactly and the only errors are the fp64 combination and
+ * the pairs left out; otherwise the rounding of X_i adds a bounded error.  Each lag
  * whose bound exceeds 1.25e-5 of its score (exact zeros included) is
  * recomputed as an fp64 sum before the selection, which then uses the same
  * tier-0 width as the direct scores.  Selections equal those of the direct

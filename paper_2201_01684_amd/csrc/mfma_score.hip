@@ -11,18 +11,23 @@
 // otherwise the rounding is bounded below.  X splits into four balanced base-256
 // digits d_p in [-128, 127], X = sum_p 256^p d_p, and the cross term is the sum
 // over digit pairs of 256^(p+q) sum_i d_p(i) d_q(i+T), exact int8 products
-// accumulated exactly in int32 by v_mfma_i32_32x32x32_i8.
+// accumulated exactly in int32 by v_mfma_i32_32x32x32_i8.  The three pairs of
+// least weight, p + q <= 1, are left out: per sample pair they add at most
+// 2^14 + 2 * 256 * 2^14 to a product of up to 2^60, so the cross term they
+// drop is within 8404992 (N - T) of r(T), and the fix-up's bound includes it.
 //
 // Tile of one wavefront: 1024 lags T0 + 32 b + a (a, b < 32) over 32-sample
 // steps i0: A[a][k] = d_p(i0 - a + k), B[k][b] = d_q(i0 + T0 + 32 b + k), so
 // (A B)[a][b] sums the products of samples i = i0 - a + k and i + T.  Zero
 // padding around each digit plane makes every read in range and every pair
 // outside [0, N) contribute nothing, so the steps i0 = 0, 32, ... cover each
-// lag's pairs exactly once.  The 16 digit-pair products go to 7 shift groups
-// p + q; every 512 steps the groups are added, scaled by 256^(p+q), into fp64.
+// lag's pairs exactly once.  The 13 digit-pair products go to 5 shift groups
+// p + q = 2 .. 6; every 512 steps the groups are added, scaled by 256^(p+q),
+// into fp64.
 //
 // The fix-up re-scores in fp64 every lag whose error bound (rounding of the
-// fp64 sums, and the quantisation of inexact sequences) is not within half the
+// fp64 sums, the digit pairs left out, and the quantisation of inexact
+// sequences) is not within half the
 // selection's tier-0 width of its score.
 #include <cmath>
 
@@ -37,6 +42,10 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 
 constexpr int kThreads = 256;
 constexpr int kXcds = 8;   // MI355X: workgroups are dealt to its 8 XCDs in turn
+// Shift groups p + q = 2 .. 6 of the 13 digit-pair products kept, and the most
+// the three left out (p + q <= 1) add to one sample pair's product, 128^2 (1 + 2 * 256).
+constexpr int kGroups = 5;
+constexpr double kDroppedPerPair = 8404992.0;
 constexpr int kEdgeTile = 4096;
 constexpr int kEdgePer = kEdgeTile / kThreads;
 constexpr int kEdgeWaves = kThreads / kWave;
@@ -390,9 +399,9 @@ __global__ __launch_bounds__(kThreads, 2) void mfma_xcorr_kernel(MfmaArgs a) {
 
     const int m = lane & 31, h = lane >> 5;
     const int off = (-dl - m) & 3;   // byte offset of this lane's A row within its first dword
-    v16i acc[7];
+    v16i acc[kGroups];   // acc[g] holds shift group p + q = g + 2
 #pragma unroll
-    for (int g = 0; g < 7; ++g) acc[g] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+    for (int g = 0; g < kGroups; ++g) acc[g] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
     // Per step, from the stage buffer: A row a = m, bytes i0 - dl - m + 16 h
     // .. + 15 (dword-aligned reads shifted into place); B column b = m, bytes
     // i0 + T0' + 32 m + 16 h .. + 15.
@@ -424,7 +433,9 @@ __global__ __launch_bounds__(kThreads, 2) void mfma_xcorr_kernel(MfmaArgs a) {
         for (int p = 0; p < 4; ++p)
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-                acc[p + q] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[p], bq[q], acc[p + q], 0, 0, 0);
+                if (p + q >= 2)
+                    acc[p + q - 2] =
+                        __builtin_amdgcn_mfma_i32_32x32x32_i8(A[p], bq[q], acc[p + q - 2], 0, 0, 0);
     };
     // Every kMfmaFlush steps (each group sum stays below 2^31 over that many)
     // the shift groups are added, scaled by 256^(p+q), into r(T) in fp64,
@@ -437,10 +448,10 @@ __global__ __launch_bounds__(kThreads, 2) void mfma_xcorr_kernel(MfmaArgs a) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
 #pragma unroll
-            for (int g = 6; g >= 0; --g) r[j] += ldexp((double)acc[g][j], 8 * g);
+            for (int g = kGroups - 1; g >= 0; --g) r[j] += ldexp((double)acc[g][j], 8 * (g + 2));
         }
 #pragma unroll
-        for (int g = 0; g < 7; ++g)
+        for (int g = 0; g < kGroups; ++g)
             acc[g] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
     };
 
@@ -509,19 +520,20 @@ struct MfixArgs {
 
 // One workgroup per window.  Per channel (X units): the rounding of E and of
 // the edge sums (each within gamma_{N+1} E), of the three operations forming
-// D, and of the fp64 sum of the shift groups into r (7 additions per flush,
+// D, and of the fp64 sum of the shift groups into r (5 additions per flush,
 // over terms whose magnitudes sum to at most (N - T) 2^62 1.008, because a
 // balanced four-digit X has sum_p 256^p |d_p| < 2^31 1.004) give R, lag-
 // independent with N - T <= N.  An inexact sequence adds the quantisation:
 // with |X_i - 2^s (x_i - c)| <= 1/2 + 2^-23, D_X - 2^2s D is at most
-// 4 sqrt(m D_X) + 6 m over m = N - T pairs.  D_X is bounded through the
-// computed score: w_c D_c <= m S + sum_c' w_c' R_c'.  Lags whose total bound,
+// 4 sqrt(m D_X) + 6 m over m = N - T pairs.  Every sequence adds the digit
+// pairs left out of r, L = 2 * 8404992 m in D.  D_X is bounded through the
+// computed score: w_c D_c <= m S + sum_c' w_c' (R_c' + L_c').  Lags whose total bound,
 // divided by m, exceeds tau0 / 2 of the score (the other half covers the
 // finalisation and the fp32 output) are re-scored by a wavefront in fp64 and
 // marked tier 1; so is every score of exactly zero.
 __global__ __launch_bounds__(kThreads) void mfma_fixup_kernel(MfixArgs a, Weights w) {
-    __shared__ double rr[kMaxChannels], qa[kMaxChannels], qb[kMaxChannels];
-    __shared__ double total_r;
+    __shared__ double rr[kMaxChannels], qa[kMaxChannels], qb[kMaxChannels], tr[kMaxChannels];
+    __shared__ double total_r, total_t;
     const int64_t b = blockIdx.x;
     const int64_t n = table_n(a.tab, b, a.n);
     if (n == 0) return;   // an empty slot of a window table
@@ -535,21 +547,26 @@ __global__ __launch_bounds__(kThreads) void mfma_fixup_kernel(MfixArgs a, Weight
         const double sc = a.qstat[4 * sq + 1];
         const double e = a.qstat[4 * sq + 3];
         const double round_x = u * (4.04 * ((double)n + 1.0) + 12.0) * e +
-                               2.0 * (7.0 * flushes + (double)a.chunks) * u * 1.01 * (double)n *
+                               2.0 * (5.0 * flushes + (double)a.chunks) * u * 1.01 * (double)n *
                                    ldexp(1.008, 62);
         rr[c] = 1.01 * ldexp(round_x, -2 * (int)sc);
+        tr[c] = 1.01 * ldexp(2.0 * kDroppedPerPair, -2 * (int)sc);   // per pair, times m
         const bool inexact = a.qstat[4 * sq + 2] == 0.0;
         qa[c] = inexact ? 1.01 * 4.0 * ldexp(1.0, -(int)sc) : 0.0;
         qb[c] = inexact ? 1.01 * 6.0 * ldexp(1.0, -2 * (int)sc) : 0.0;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        double acc = 0.0;
-        for (int32_t c = 0; c < a.num_channels; ++c) acc += (double)w.w[c] * rr[c];
+        double acc = 0.0, acct = 0.0;
+        for (int32_t c = 0; c < a.num_channels; ++c) {
+            acc += (double)w.w[c] * rr[c];
+            acct += (double)w.w[c] * tr[c];
+        }
         total_r = acc * (1.0 + 1e-12);
+        total_t = acct * (1.0 + 1e-12);
     }
     __syncthreads();
-    const double ar = total_r;
+    const double ar = total_r, at = total_t;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x >> 6;
     const float* __restrict__ xw = a.x + table_off(a.tab, b, a.window_stride);
@@ -561,11 +578,12 @@ __global__ __launch_bounds__(kThreads) void mfma_fixup_kernel(MfixArgs a, Weight
             const int64_t t = (int64_t)a.tmin + j;
             const double m = (double)(n - t);
             const double v = a.s64[b * a.lags + j];
-            double bound = ar;
+            const double art = (ar + at * m) * (1.0 + 1e-12);   // all channels' R and left-out pairs
+            double bound = art;
             for (int32_t c = 0; c < a.num_channels; ++c) {
                 if (qa[c] == 0.0) continue;
                 const double wc = (double)w.w[c];
-                const double dup = (m * fmax(v, 0.0) * (1.0 + 1e-12) + ar) / wc + rr[c];
+                const double dup = (m * fmax(v, 0.0) * (1.0 + 1e-12) + art) / wc + rr[c] + tr[c] * m;
                 bound += wc * (qa[c] * sqrt(m * dup) + qb[c] * m);
             }
             fix = !(bound * (1.0 + 1e-12) / m <= 0.5 * a.tau0 * v);

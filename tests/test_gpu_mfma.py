@@ -5,7 +5,9 @@ The path promises every score within 1.25e-5 relative of the exact value
 re-scored in fp64 first), exact zeros where the oracle has them, and
 selections identical to the oracle's.  On sequences whose samples the
 integer scaling represents exactly (every workload here but the normalised
-counters of w5) the only error left is the fp64 combination, so their scores
+counters of w5) the only errors left are the fp64 combination and the three
+digit pairs of least weight left out of the products (at most 2^24 per sample
+pair in D against samples scaled to 2^30, and of random sign), so their scores
 are held to the fp32 output rounding.  Covered: the smallest windows, ragged
 N, lag ranges that start inside a tile and end on, before and after a tile
 boundary, weighted channels at different scales, samples spanning many
@@ -28,7 +30,7 @@ from gen import make_workload, planted_trace  # noqa: E402
 from test_gpu_parity import check_results, gpu_run  # noqa: E402
 
 MFMA_RTOL = 1.25e-5 + 2.0 ** -24     # the fix-up's bound plus the fp32 output rounding
-EXACT_RTOL = 1e-7                    # exactly represented samples: fp64 combination + fp32 output
+EXACT_RTOL = 1e-7                    # exactly represented samples: fp64 combination, left-out pairs, fp32 output
 
 
 def mfma_flag():
@@ -109,6 +111,31 @@ def test_samples_over_many_binades():
                   (1e3 + rng.normal(0, 1e-3, n)).astype(np.float32)])
     g, res, out = mfma_parity(x, oracle.Layout(3, 1, n, n, n, 2, 4096), "mfma binades")
     assert res["period"][0] == 211
+
+
+def test_left_out_pairs_decide_the_fix_up():
+    # Levels below 2^20 in steps of 1/8 (exact in fp32) under noise of 390: the
+    # scale is 2^10, so the lowest digit is not zero, and at multiples of the
+    # period S is about 3e5 against 7e11 elsewhere.  The bound of the three
+    # digit pairs left out of the products, 2 * 8404992 per pair in X units or
+    # about 16 per pair in samples, exceeds 1.25e-5 of the score there (the
+    # fp64 rounding terms alone would not, below about 4e4), so the fix-up
+    # re-scores those lags in fp64; every other lag keeps its certified value.
+    n, period = 8192, 97
+    rng = np.random.default_rng(31)
+    template = rng.integers(-2**20 + 8192, 2**20 - 8192, size=period) + rng.integers(0, 8, period) / 8
+    noise = np.round(rng.normal(0.0, 390.0, n) * 8) / 8
+    x64 = np.tile(template, n // period + 1)[:n] + noise
+    x64[0] -= np.sum(x64) % (n / 8)   # a mean on the 1/8 grid: every x - c exact at scale 2^10
+    x = x64.astype(np.float32)
+    assert np.array_equal(x.astype(np.float64), x64)
+    lay = oracle.Layout(1, 1, n, n, n, 2, 2048)
+    g, res, out = mfma_parity(x[None], lay, "mfma left-out pairs", rtol=EXACT_RTOL)
+    assert res["period"][0] == period
+    at_period = np.arange(period, 2049, period)
+    s_at = g[0, at_period - 2]
+    assert np.all((s_at > 1e5) & (s_at < 1e6))
+    assert res["n_rescored"][0] >= len(at_period)
 
 
 def test_exact_periods_and_constant_windows():
