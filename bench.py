@@ -476,6 +476,10 @@ def main():
                     "peak": FP32_VECTOR_PEAK_TFLOPS, "unit": "TFLOP/s",
                     "frac": achieved / FP32_VECTOR_PEAK_TFLOPS,
                     "traffic": counters_traffic(wl.name)}
+    # HBM bandwidth the stage drew: the counter bytes per launch over the
+    # stage's measured time (null with the traffic)
+    roofline["hbm_gbs"] = (roofline["traffic"] / (score_ms / 1e3) / 1e9
+                           if roofline["traffic"] else None)
 
     line = {
         "metric": METRIC,
