@@ -80,17 +80,27 @@ __device__ __forceinline__ void load_window(const float* __restrict__ p,
     }
 }
 
-// 16 samples x kBT lags, every pair valid.
+// 16 samples x kBT lags, every pair valid.  The differences of four lags go
+// to four registers before their four multiply-adds (the scheduling barriers
+// keep the groups): left alone, the compiler reuses one register for every
+// difference, so each instruction waits on the one before it, and that chain
+// cost the w3 launch about 2.5% of its issue rate.
 template <int kBT>
 __device__ __forceinline__ void block_full(const float (&xs)[16],
                                            const float (&y)[Geometry<kBT>::kW],
                                            float (&acc)[kBT]) {
+    constexpr int kG = kBT < 4 ? kBT : 4;
 #pragma unroll
     for (int s = 0; s < 16; ++s) {
 #pragma unroll
-        for (int j = 0; j < kBT; ++j) {
-            float d = xs[s] - y[s + j];
-            acc[j] = __builtin_fmaf(d, d, acc[j]);
+        for (int j = 0; j < kBT; j += kG) {
+            float d[kG];
+#pragma unroll
+            for (int u = 0; u < kG; ++u) d[u] = xs[s] - y[s + j + u];
+            __builtin_amdgcn_sched_group_barrier(0x2, kG, 0);   // kG VALU: the subtractions
+#pragma unroll
+            for (int u = 0; u < kG; ++u) acc[j + u] = __builtin_fmaf(d[u], d[u], acc[j + u]);
+            __builtin_amdgcn_sched_group_barrier(0x2, kG, 0);   // kG VALU: the multiply-adds
         }
     }
 }
