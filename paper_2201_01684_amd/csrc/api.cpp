@@ -28,8 +28,10 @@ namespace {
 // lags and suits long windows; 8 halves the masked stretch at the end of each
 // lag block (64 * 16 samples at 16 lags per lane) and doubles occupancy (59
 // instead of 92 VGPRs), which pays once that stretch exceeds about 1% of the
-// mean pair range N - T.  Measured on MI355X: 16 is best for 262144-sample
-// windows, 8 for 65536- and 16384-sample windows, equal at 131072.
+// mean pair range N - T.  Measured on MI355X with the grouped differences
+// and the four-wave bound of the sixteen-lag instance: 16 is best for 262144-
+// and 131072-sample windows (1.5% ahead of 8 on the latter), 8 for 65536- and
+// 16384-sample windows (3-6% ahead of 16 on the former).
 int32_t choose_lags_per_lane(int64_t n, int32_t tmin, int32_t tmax) {
     const double mean_range = (double)n - 0.5 * ((double)tmin + (double)tmax);
     return (64.0 * 16.0 > 0.01 * mean_range) ? 8 : 16;
