@@ -80,6 +80,7 @@ struct SelectArgs {
     int32_t pass;
     int32_t last;
     int32_t stage;           // select passes copy a window's scores and tier bitmaps to LDS
+    int32_t chunk;           // ... or stream them through LDS a chunk of lags at a time
     WindowTable tab;
 };
 
@@ -215,6 +216,22 @@ struct WindowView {
     // requests join after the rule (one aggregated append per wavefront).
     uint32_t* gq1;
     uint32_t* gq2;
+    // Windows too long to stage whole: an LDS buffer for the scores and tier
+    // words of one chunk of lags (ChunkGeom), or null.
+    double* cs;
+    uint32_t* ct1;
+    uint32_t* ct2;
+};
+
+// The chunks of a workgroup of kT threads: 4 kT scores (kT - 2 + 3 kT lags and
+// one neighbour either side), four loads a thread, and the tier words they
+// touch.
+template <int kT>
+struct ChunkGeom {
+    static constexpr int kEntries = 4 * kT;
+    static constexpr int kLags = kEntries - 2;
+    static constexpr int kWords = kEntries / 32 + 2;
+    static constexpr size_t kBytes = sizeof(double) * kEntries + 2 * sizeof(uint32_t) * kWords;
 };
 
 // One evaluation of the rule for window b (every thread of the workgroup
@@ -327,23 +344,64 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
         const double r_lo = r_exact ? r_x : r_approx - e_r;
         const double r_hi = r_exact ? r_x : r_approx + e_r;
         const double r_v = r_exact ? r_x : r_approx;
-        auto iv = [&](int64_t t) -> Iv {
-            const int64_t j = t - tmin;
-            const double v = s[j];
+        // the interval of the score v of lag index j with tier words w1, w2
+        auto make_iv = [&](double v, uint32_t w1, uint32_t w2, int64_t j) -> Iv {
             const uint32_t bit = 1u << (j & 31);
             Iv r;
             r.v = v;
-            if (t2[j >> 5] & bit) {
+            if (w2 & bit) {
                 r.exact = true;
                 r.lo = r.hi = v;
             } else {
-                const double e = (t1[j >> 5] & bit) ? tau1 : tau0;
+                const double e = (w1 & bit) ? tau1 : tau0;
                 r.exact = false;
                 r.lo = v * (1.0 - e);
                 r.hi = v * (1.0 + e);
             }
             return r;
         };
+        auto iv = [&](int64_t t) -> Iv {
+            const int64_t j = t - tmin;
+            return make_iv(s[j], t1[j >> 5], t2[j >> 5], j);
+        };
+        // the same from the staged chunk (lag index cj0 at cs[0], word cw0 at ct1[0])
+        int64_t cj0 = 0, cw0 = 0;
+        auto iv_c = [&](int64_t t) -> Iv {
+            const int64_t j = t - tmin;
+            return make_iv(view.cs[j - cj0], view.ct1[(j >> 5) - cw0], view.ct2[(j >> 5) - cw0], j);
+        };
+        // Stage the scores of lags c0 - 1 .. c1 (at most ChunkGeom::kEntries)
+        // and their tier words; every thread calls it.
+        auto stage_chunk = [&](int64_t c0, int64_t c1) {
+            constexpr int kPer = ChunkGeom<kSelThreads>::kEntries / kSelThreads;
+            const int64_t j0 = c0 - 1 - tmin, cnt = c1 - c0 + 2;
+            const int64_t w0 = j0 >> 5, wc = ((c1 - tmin) >> 5) - w0 + 1;
+            __syncthreads();   // the previous chunk's readers are done
+            double v[kPer];
+#pragma unroll
+            for (int r = 0; r < kPer; ++r) {
+                const int64_t k = tid + r * kSelThreads;
+                v[r] = k < cnt ? s[j0 + k] : 0.0;
+            }
+            uint32_t u1 = 0u, u2 = 0u;
+            if (tid < wc) {
+                u1 = t1[w0 + tid];
+                u2 = t2[w0 + tid];
+            }
+#pragma unroll
+            for (int r = 0; r < kPer; ++r) {
+                const int64_t k = tid + r * kSelThreads;
+                if (k < cnt) view.cs[k] = v[r];
+            }
+            if (tid < wc) {
+                view.ct1[tid] = u1;
+                view.ct2[tid] = u2;
+            }
+            cj0 = j0;
+            cw0 = w0;
+            __syncthreads();
+        };
+        const bool chunked = view.cs != nullptr;
         auto push = [&](int64_t t, const Iv& z) {
             if (z.exact || !may_push) return;
             const int64_t j = t - tmin;
@@ -353,10 +411,10 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
             if (atomicOr(&qd[j >> 5], bit) & bit) return;   // already queued
             if (!enqueue(at1 ? 2 : 1, (int32_t)t)) atomicAnd(&qd[j >> 5], ~bit);   // full
         };
-        auto peak = [&](int64_t t, Iv& z, bool do_push) -> Tri {
-            const Iv m = iv(t - 1);
-            z = iv(t);
-            const Iv p = iv(t + 1);
+        auto peak_of = [&](auto&& ivf, int64_t t, Iv& z, bool do_push) -> Tri {
+            const Iv m = ivf(t - 1);
+            z = ivf(t);
+            const Iv p = ivf(t + 1);
             const Tri c1 = lt(z, m), c2 = le(z, p);
             if (c1 == kNo || c2 == kNo) return kNo;
             if (c1 == kYes && c2 == kYes) return kYes;
@@ -367,6 +425,7 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
             }
             return kUnk;
         };
+        auto peak = [&](int64_t t, Iv& z, bool do_push) -> Tri { return peak_of(iv, t, z, do_push); };
         const double ulp4 = 4.0 * 2.220446049250313e-16;
         o = gpoeo_pd_result{};
 
@@ -382,9 +441,7 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
             for (int i = tid; i < words_of_window; i += kSelThreads) sh.peaks[i] = 0u;
             __syncthreads();
         }
-        for (int64_t t = tmin + 1 + tid; t < tmax; t += kSelThreads) {
-            Iv z;
-            const Tri q = peak(t, z, false);
+        auto tally_peak = [&](int64_t t, Tri q, const Iv& z) {
             if (q == kYes) {
                 ++npk;
                 pk_lo = fmin(pk_lo, z.lo);
@@ -396,6 +453,21 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
             } else if (q == kUnk) {
                 ++unk;
                 unk_lo = fmin(unk_lo, z.lo);
+            }
+        };
+        if (chunked) {
+            for (int64_t c0 = tmin + 1; c0 < tmax; c0 += ChunkGeom<kSelThreads>::kLags) {
+                const int64_t c1 = min(c0 + (int64_t)ChunkGeom<kSelThreads>::kLags, (int64_t)tmax);
+                stage_chunk(c0, c1);
+                for (int64_t t = c0 + tid; t < c1; t += kSelThreads) {
+                    Iv z;
+                    tally_peak(t, peak_of(iv_c, t, z, false), z);
+                }
+            }
+        } else {
+            for (int64_t t = tmin + 1 + tid; t < tmax; t += kSelThreads) {
+                Iv z;
+                tally_peak(t, peak(t, z, false), z);
             }
         }
         {
@@ -436,14 +508,14 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
         thr.exact = thr.lo == thr.hi;
         int64_t ncand = 0, tc = INT64_MAX;
         unk = 0;
-        for (int64_t t = tmin + 1 + tid; t < tmax; t += kSelThreads) {
+        auto cand = [&](auto&& ivf, int64_t t) {
             Iv z;
             if (cache) {
                 const int64_t j = t - tmin;
-                if (!((sh.peaks[j >> 5] >> (j & 31)) & 1u)) continue;
-                z = iv(t);
-            } else if (peak(t, z, false) != kYes) {
-                continue;
+                if (!((sh.peaks[j >> 5] >> (j & 31)) & 1u)) return;
+                z = ivf(t);
+            } else if (peak_of(ivf, t, z, false) != kYes) {
+                return;
             }
             const Tri q = lt(z, thr);
             if (q == kYes) {
@@ -453,6 +525,15 @@ __device__ bool select_window(const SelectArgs& a, const Weights& w, int64_t b, 
                 ++unk;
                 push(t, z);
             }
+        };
+        if (chunked) {
+            for (int64_t c0 = tmin + 1; c0 < tmax; c0 += ChunkGeom<kSelThreads>::kLags) {
+                const int64_t c1 = min(c0 + (int64_t)ChunkGeom<kSelThreads>::kLags, (int64_t)tmax);
+                stage_chunk(c0, c1);
+                for (int64_t t = c0 + tid; t < c1; t += kSelThreads) cand(iv_c, t);
+            }
+        } else {
+            for (int64_t t = tmin + 1 + tid; t < tmax; t += kSelThreads) cand(iv, t);
         }
         {
             double dm[3] = {INFINITY, INFINITY, INFINITY};
@@ -635,7 +716,13 @@ __global__ __launch_bounds__(kSelThreads) void select_pass_kernel(SelectArgs a, 
     if (a.pass > 0 && a.state[b].done) return;   // decided earlier (the same for every thread)
     WindowView view = {a.s64 + b * (int64_t)a.lags, a.tier1 + b * (int64_t)a.words,
                        a.tier2 + b * (int64_t)a.words, a.queued1 + b * (int64_t)a.words,
-                       a.queued2 + b * (int64_t)a.words, nullptr, nullptr};
+                       a.queued2 + b * (int64_t)a.words, nullptr, nullptr,
+                       nullptr, nullptr, nullptr};
+    if (a.chunk) {
+        view.cs = dyn;
+        view.ct1 = reinterpret_cast<uint32_t*>(dyn + ChunkGeom<kSelThreads>::kEntries);
+        view.ct2 = view.ct1 + ChunkGeom<kSelThreads>::kWords;
+    }
     if (a.words <= kReqWords) {   // deferred requests (cleared here; select_window's
                                   // first barrier orders this before the rule)
         for (int32_t k = threadIdx.x; k < a.words; k += kSelThreads) req[0][k] = req[1][k] = 0u;
@@ -982,12 +1069,19 @@ hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const 
     // (for a few windows each pass is a chain of scans that LDS shortens; for
     // many windows the copies would cost more occupancy than they save)
     a.stage = p.lags <= kSelLdsLags && p.num_windows <= kSelLdsWindows;
+    // (windows too long for that stream their two full scans through LDS:
+    // a chunk's loads all in flight together, instead of a dependent load per
+    // lag and thread)
+    a.chunk = !a.stage && p.lags > kSelLdsLags;
+    const bool wide = p.lags >= kWideLags && !p.table.n;
     const size_t lds =
-        a.stage ? (size_t)p.lags * sizeof(double) + 2 * (size_t)p.bitmap_words * 4 : 0;
+        a.stage ? (size_t)p.lags * sizeof(double) + 2 * (size_t)p.bitmap_words * 4
+        : a.chunk ? (wide ? ChunkGeom<1024>::kBytes : ChunkGeom<kThreads>::kBytes)
+                  : 0;
     for (int pass = 0; pass < passes; ++pass) {
         a.pass = pass;
         a.last = pass == passes - 1;
-        if (p.lags >= kWideLags && !p.table.n)
+        if (wide)
             hipLaunchKernelGGL(select_pass_kernel<1024>, grid_sel, dim3(1024), lds, s, a, w);
         else
             hipLaunchKernelGGL(select_pass_kernel<kThreads>, grid_sel, dim3(kThreads), lds, s, a,

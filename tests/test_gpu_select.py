@@ -13,6 +13,12 @@ path, through the C ABI, against the oracle.
   round, more than the three rounds of global queues hold (3 x 65,536): a
   window whose requests did not fit is decided on its unwidened values and
   flagged UNRESOLVED; every unflagged window equals the oracle.
+- Windows with more lags than a selection pass stages whole in LDS (14,000)
+  stream their two full scans through LDS a chunk of lags at a time (4,094
+  lags with 1024 threads, 1,022 with the 256 threads of window tables).
+  Batches of 15,999 lags, with plateaus of near-equal scores that tier 1 must
+  decide, equal the oracle with direct and FFT scores, and so does rolling
+  detection over such a trace (its suffix windows run as a window table).
 """
 import numpy as np
 import pytest
@@ -139,3 +145,44 @@ def test_fused_equals_unfused_bitwise(case):
             o, out = oracle.detect(x, lay)
             check_scores(gf.astype(np.float64), o, case)
             check_results(rf, out, case)
+
+
+LONG_N, LONG_TMAX = 40000, 16000
+
+
+def _long_batch():
+    rows = [planted_trace(LONG_N, 4094, 6, seed=11, integer=True),   # period = one chunk
+            planted_trace(LONG_N, 1500, 8, seed=12, integer=True),
+            planted_trace(LONG_N, 5000, 9, seed=13, sigma=3.0),
+            planted_trace(LONG_N, 777, 5, seed=14, sigma=5.0)]
+    # jittered repeats: flat minima whose peak tests tier 0 leaves open
+    jit = make_workload("w2", traces=8, n=LONG_N, tmax=LONG_TMAX, pmax=5000)
+    return np.concatenate([np.stack(rows), jit.x.reshape(8, LONG_N)]).astype(np.float32)
+
+
+@pytest.mark.parametrize("mode", ["direct", "fft"])
+def test_long_windows_match_oracle(mode):
+    import paper_2201_01684_amd as pkg
+    x = _long_batch()
+    lay = oracle.Layout(x.shape[0], 1, LONG_N, LONG_N, LONG_N, 2, LONG_TMAX)
+    g, res = run(x, lay, pkg.FFT_SCORES if mode == "fft" else 0)
+    o, out = oracle.detect(x, lay)
+    check_scores(g.astype(np.float64), o, f"long windows, {mode} scores")
+    check_results(res, out, f"long windows, {mode} scores")
+    assert not np.any(res["flags"] & pkg.UNRESOLVED)
+    assert np.array_equal(res["period"][:4], [4094, 1500, 5000, 777])
+    if mode == "direct":   # open tests: the passes after a re-score round ran too
+        assert res["n_rescored"][4:].sum() > 0
+
+
+def test_long_window_rolling_matches_oracle():
+    from test_gpu_rolling import check, gpu_rolling
+    n = 2 * LONG_N
+    rows = [planted_trace(n, 2600, 7, seed=15, sigma=3.0),
+            np.concatenate([planted_trace(n - 9000, 1800, 6, seed=16, sigma=2.0),
+                            planted_trace(9000, 2900, 6, seed=17, sigma=2.0)])]
+    x = np.stack(rows).astype(np.float32)
+    lay = oracle.Layout(len(rows), 1, n, n, n, 2, LONG_TMAX)
+    g = gpu_rolling(x, lay)
+    o = oracle.rolling(x, lay)
+    check(g, o, "long-window rolling")
