@@ -56,6 +56,7 @@ constexpr int kThreads = 256;       // re-score and initialisation kernels and s
 // the narrow workgroups: more windows in flight at once.
 constexpr int kWideLags = 4096;
 constexpr int kRescoreGroups = 1024;   // workgroups of one re-score round
+constexpr int64_t kChunkWideWindows = 256;   // MI355X's CUs: one 1024-thread workgroup each
 
 struct SelectArgs {
     const float* x;
@@ -1073,7 +1074,12 @@ hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const 
     // a chunk's loads all in flight together, instead of a dependent load per
     // lag and thread)
     a.chunk = !a.stage && p.lags > kSelLdsLags;
-    const bool wide = p.lags >= kWideLags && !p.table.n;
+    // Chunked scans are paced by their barriers and interval tests: a batch
+    // with more windows than the GPU has CUs runs them in 256-thread
+    // workgroups, several windows a CU (1024 windows of 32,767 lags: 290 ->
+    // 215 us a pass), a smaller batch keeps the 1024 threads a window.
+    const bool wide = p.lags >= kWideLags && !p.table.n &&
+                      !(a.chunk && p.num_windows > kChunkWideWindows);
     const size_t lds =
         a.stage ? (size_t)p.lags * sizeof(double) + 2 * (size_t)p.bitmap_words * 4
         : a.chunk ? (wide ? ChunkGeom<1024>::kBytes : ChunkGeom<kThreads>::kBytes)
