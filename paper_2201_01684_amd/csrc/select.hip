@@ -53,7 +53,8 @@ constexpr int kThreads = 256;       // re-score and initialisation kernels and s
 // Selection passes run one workgroup per window; from this many lags on, four
 // times as many threads keep more of a window's scores in flight.  A window
 // table (suffix windows, mostly far shorter than the plan's lag range) keeps
-// the narrow workgroups: more windows in flight at once.
+// the narrow workgroups: more windows in flight at once; so does a batch of
+// more than kChunkWideWindows windows too long to stage in LDS whole.
 constexpr int kWideLags = 4096;
 constexpr int kRescoreGroups = 1024;   // workgroups of one re-score round
 constexpr int64_t kChunkWideWindows = 256;   // MI355X's CUs: one 1024-thread workgroup each
@@ -224,9 +225,8 @@ struct WindowView {
     uint32_t* ct2;
 };
 
-// The chunks of a workgroup of kT threads: 4 kT scores (kT - 2 + 3 kT lags and
-// one neighbour either side), four loads a thread, and the tier words they
-// touch.
+// The chunks of a workgroup of kT threads: 4 kT scores (4 kT - 2 lags and one
+// neighbour either side), four loads a thread, and the tier words they touch.
 template <int kT>
 struct ChunkGeom {
     static constexpr int kEntries = 4 * kT;
