@@ -104,13 +104,61 @@ __device__ __forceinline__ Tri le(const Iv& a, const Iv& b) {
     return kUnk;
 }
 
-// Block reductions: a butterfly of lane shuffles inside each wavefront, the
-// per-wave results through LDS, then every thread folds them in wave order.
-// (min and integer sums: the result does not depend on the order.)
+// Wavefront reductions with DPP lane moves (VALU operations, where a lane
+// shuffle is a round trip through the LDS unit): a butterfly inside each quad,
+// then each lane with its mirror in the other half row and in the other half
+// of the row, so that every lane of a row of 16 holds the row's value; then
+// lane 15 of rows 0 and 2 into rows 1 and 3, and lane 31 into rows 2 and 3,
+// so that lane 63 holds the wavefront's value.  Rows a broadcast does not
+// enable take the operation's identity.  (min and integer sums: the result
+// does not depend on the order.)
+constexpr int kDppQuadXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+constexpr int kDppQuadXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int kDppRowHalfMirror = 0x141;
+constexpr int kDppRowMirror = 0x140;
+constexpr int kDppRowBcast15 = 0x142;
+constexpr int kDppRowBcast31 = 0x143;
+
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v, uint64_t old) {
+    const int lo = __builtin_amdgcn_update_dpp((int)(uint32_t)old, (int)(uint32_t)v, kCtrl,
+                                               kRowMask, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp((int)(uint32_t)(old >> 32), (int)(uint32_t)(v >> 32),
+                                               kCtrl, kRowMask, 0xF, false);
+    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+
+// op(v, v of the lane kCtrl selects) for the three kinds of value
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ double dpp_min_d(double v) {
+    const uint64_t id = (uint64_t)__double_as_longlong(INFINITY);
+    return fmin(v, __longlong_as_double((long long)dpp64<kCtrl, kRowMask>(
+                       (uint64_t)__double_as_longlong(v), id)));
+}
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ int64_t dpp_sum_i(int64_t v) {
+    return v + (int64_t)dpp64<kCtrl, kRowMask>((uint64_t)v, 0u);
+}
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ int64_t dpp_min_i(int64_t v) {
+    return min(v, (int64_t)dpp64<kCtrl, kRowMask>((uint64_t)v, (uint64_t)INT64_MAX));
+}
+
+__device__ __forceinline__ double wave_min_d(double v) {
+    v = dpp_min_d<kDppQuadXor1, 0xF>(v);
+    v = dpp_min_d<kDppQuadXor2, 0xF>(v);
+    v = dpp_min_d<kDppRowHalfMirror, 0xF>(v);
+    v = dpp_min_d<kDppRowMirror, 0xF>(v);
+    v = dpp_min_d<kDppRowBcast15, 0xA>(v);
+    return dpp_min_d<kDppRowBcast31, 0xC>(v);
+}
+
+// Block reductions: the wavefront reductions above, the per-wave results
+// (lane 63) through LDS, then every thread folds them in wave order.
 template <int kT>
 __device__ double block_min_d(double v, double* red) {
-    for (int o = kWave / 2; o > 0; o >>= 1) v = fmin(v, __shfl_xor(v, o));
-    if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = v;
+    v = wave_min_d(v);
+    if ((threadIdx.x & (kWave - 1)) == kWave - 1) red[threadIdx.x / kWave] = v;
     __syncthreads();
     double r = red[0];
     for (int w = 1; w < kT / kWave; ++w) r = fmin(r, red[w]);
@@ -118,47 +166,29 @@ __device__ double block_min_d(double v, double* red) {
     return r;
 }
 
-template <int kT>
-__device__ int64_t block_sum_i(int64_t v, int64_t* red) {
-    long long x = v;
-    for (int o = kWave / 2; o > 0; o >>= 1) x += __shfl_xor(x, o);
-    if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = x;
-    __syncthreads();
-    int64_t r = red[0];
-    for (int w = 1; w < kT / kWave; ++w) r += red[w];
-    __syncthreads();
-    return r;
-}
-
-template <int kT>
-__device__ int64_t block_min_i(int64_t v, int64_t* red) {
-    long long x = v;
-    for (int o = kWave / 2; o > 0; o >>= 1) x = min(x, __shfl_xor(x, o));
-    if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = x;
-    __syncthreads();
-    int64_t r = red[0];
-    for (int w = 1; w < kT / kWave; ++w) r = min(r, red[w]);
-    __syncthreads();
-    return r;
-}
-
-
 // The reductions of one step of the rule at once (one exchange through LDS,
 // two barriers): three double minima, two int64 sums and one int64 minimum
-// (unused ones are passed as neutral values).  Butterflies inside each
-// wavefront, then the per-wave values folded in wave order; every thread gets
-// the results.
+// (unused ones are passed as neutral values).  Wavefront reductions, then the
+// per-wave values folded in wave order; every thread gets the results.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ void reduce_step(double (&dmin)[3], int64_t (&isum)[2], int64_t& imin) {
+#pragma unroll
+    for (int k = 0; k < 3; ++k) dmin[k] = dpp_min_d<kCtrl, kRowMask>(dmin[k]);
+#pragma unroll
+    for (int k = 0; k < 2; ++k) isum[k] = dpp_sum_i<kCtrl, kRowMask>(isum[k]);
+    imin = dpp_min_i<kCtrl, kRowMask>(imin);
+}
+
 template <int kT, typename Sh>
 __device__ void block_reduce(double (&dmin)[3], int64_t (&isum)[2], int64_t& imin, Sh& sh) {
-    for (int o = kWave / 2; o > 0; o >>= 1) {
-#pragma unroll
-        for (int k = 0; k < 3; ++k) dmin[k] = fmin(dmin[k], __shfl_xor(dmin[k], o));
-#pragma unroll
-        for (int k = 0; k < 2; ++k) isum[k] += (int64_t)__shfl_xor((long long)isum[k], o);
-        imin = min(imin, (int64_t)__shfl_xor((long long)imin, o));
-    }
+    reduce_step<kDppQuadXor1, 0xF>(dmin, isum, imin);
+    reduce_step<kDppQuadXor2, 0xF>(dmin, isum, imin);
+    reduce_step<kDppRowHalfMirror, 0xF>(dmin, isum, imin);
+    reduce_step<kDppRowMirror, 0xF>(dmin, isum, imin);
+    reduce_step<kDppRowBcast15, 0xA>(dmin, isum, imin);
+    reduce_step<kDppRowBcast31, 0xC>(dmin, isum, imin);
     const int wv = threadIdx.x / kWave;
-    if ((threadIdx.x & (kWave - 1)) == 0) {
+    if ((threadIdx.x & (kWave - 1)) == kWave - 1) {
 #pragma unroll
         for (int k = 0; k < 3; ++k) sh.red_md[k][wv] = dmin[k];
 #pragma unroll
