@@ -54,7 +54,8 @@ constexpr int kThreads = 256;       // re-score and initialisation kernels and s
 // times as many threads keep more of a window's scores in flight.  A window
 // table (suffix windows, mostly far shorter than the plan's lag range) keeps
 // the narrow workgroups: more windows in flight at once; so does a batch of
-// more than kChunkWideWindows windows too long to stage in LDS whole.
+// more than kChunkWideWindows windows whose scans stream through LDS in
+// chunks.
 constexpr int kWideLags = 4096;
 constexpr int kRescoreGroups = 1024;   // workgroups of one re-score round
 constexpr int64_t kChunkWideWindows = 256;   // MI355X's CUs: one 1024-thread workgroup each
@@ -248,8 +249,8 @@ struct WindowView {
     // requests join after the rule (one aggregated append per wavefront).
     uint32_t* gq1;
     uint32_t* gq2;
-    // Windows too long to stage whole: an LDS buffer for the scores and tier
-    // words of one chunk of lags (ChunkGeom), or null.
+    // Windows not staged whole (too long, or too many of them): an LDS buffer
+    // for the scores and tier words of one chunk of lags (ChunkGeom), or null.
     double* cs;
     uint32_t* ct1;
     uint32_t* ct2;
@@ -1100,10 +1101,10 @@ hipError_t launch_select(const Plan& p, const Weights& w, const float* x, const 
     // (for a few windows each pass is a chain of scans that LDS shortens; for
     // many windows the copies would cost more occupancy than they save)
     a.stage = p.lags <= kSelLdsLags && p.num_windows <= kSelLdsWindows;
-    // (windows too long for that stream their two full scans through LDS:
-    // a chunk's loads all in flight together, instead of a dependent load per
-    // lag and thread)
-    a.chunk = !a.stage && p.lags > kSelLdsLags;
+    // (windows too long for that, or too many of them, stream their two full
+    // scans through LDS: a chunk's loads all in flight together, instead of a
+    // dependent load per lag and thread)
+    a.chunk = !a.stage;
     // Chunked scans are paced by their barriers and interval tests: a batch
     // with more windows than the GPU has CUs runs them in 256-thread
     // workgroups, several windows a CU (1024 windows of 32,767 lags: 290 ->
