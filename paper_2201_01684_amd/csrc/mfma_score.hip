@@ -143,10 +143,25 @@ __global__ __launch_bounds__(kThreads) void mfma_prep_kernel(MfmaArgs a) {
         }
         return;
     }
+    // Each thread visits i = tid, tid + kThreads, ... in order; the samples of
+    // kPrepBatch consecutive visits are loaded together (all in flight).
+    constexpr int kPrepBatch = 8;
     double sum = 0.0;
     float mn = INFINITY, mx = -INFINITY;
-    for (int64_t i = threadIdx.x; i < n; i += kThreads) {
-        const float v = xs[i];
+    int64_t i1 = threadIdx.x;
+    for (; i1 + (kPrepBatch - 1) * kThreads < n; i1 += kPrepBatch * kThreads) {
+        float v[kPrepBatch];
+#pragma unroll
+        for (int r = 0; r < kPrepBatch; ++r) v[r] = xs[i1 + r * kThreads];
+#pragma unroll
+        for (int r = 0; r < kPrepBatch; ++r) {
+            sum += (double)v[r];
+            mn = fminf(mn, v[r]);
+            mx = fmaxf(mx, v[r]);
+        }
+    }
+    for (; i1 < n; i1 += kThreads) {
+        const float v = xs[i1];
         sum += (double)v;
         mn = fminf(mn, v);
         mx = fmaxf(mx, v);
@@ -166,12 +181,24 @@ __global__ __launch_bounds__(kThreads) void mfma_prep_kernel(MfmaArgs a) {
     // four consecutive samples per thread and step: one 32-bit store per digit
     // plane (samples past N, in the padding, get zero digits)
     const int64_t n4 = (n + 3) & ~int64_t(3);
+    // the samples of two consecutive steps of a thread are loaded together
+    // (zeros past N, which no step below uses)
+    float nxt[4];
+    auto load4 = [&](int64_t i, float (&v)[4]) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = i + k < n ? xs[i + k] : 0.0f;
+    };
+    if (4 * (int64_t)threadIdx.x < n4) load4(4 * (int64_t)threadIdx.x, nxt);
     for (int64_t i = 4 * (int64_t)threadIdx.x; i < n4; i += 4 * kThreads) {
+        float cur[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) cur[k] = nxt[k];
+        if (i + 4 * kThreads < n4) load4(i + 4 * kThreads, nxt);
         uint32_t word[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             if (i + k >= n) break;
-            const double xv = (double)xs[i + k];
+            const double xv = (double)cur[k];
             const double y = xv - c;
             const double bb = y - xv;                          // two-sum error of xv + (-c)
             const double err = (xv - (y - bb)) + (-c - bb);
