@@ -598,13 +598,25 @@ __global__ __launch_bounds__(kThreads) void mfma_fixup_kernel(MfixArgs a, Weight
     const int wave = threadIdx.x >> 6;
     const float* __restrict__ xw = a.x + table_off(a.tab, b, a.window_stride);
     const int32_t nlags = tm - a.tmin + 1;
-    for (int32_t j0 = wave * kWave; j0 < nlags; j0 += kThreads) {
+    // wavefront w tests lags j0 + lane, j0 = 64 w + 256 k; the scores of
+    // kFixBatch consecutive k are loaded together (all in flight), then tested
+    constexpr int kFixBatch = 8;
+    for (int32_t jb = wave * kWave; jb < nlags; jb += kThreads * kFixBatch) {
+    double vb[kFixBatch];
+#pragma unroll
+    for (int r = 0; r < kFixBatch; ++r) {
+        const int32_t j = jb + r * kThreads + lane;
+        vb[r] = j < nlags ? a.s64[b * a.lags + j] : 0.0;
+    }
+#pragma unroll
+    for (int r = 0; r < kFixBatch; ++r) {
+        const int32_t j0 = jb + r * kThreads;
         const int32_t j = j0 + lane;
         bool fix = false;
         if (j < nlags) {
             const int64_t t = (int64_t)a.tmin + j;
             const double m = (double)(n - t);
-            const double v = a.s64[b * a.lags + j];
+            const double v = vb[r];
             const double art = (ar + at * m) * (1.0 + 1e-12);   // all channels' R and left-out pairs
             double bound = art;
             for (int32_t c = 0; c < a.num_channels; ++c) {
@@ -630,6 +642,7 @@ __global__ __launch_bounds__(kThreads) void mfma_fixup_kernel(MfixArgs a, Weight
                 atomicAdd(&a.state[b].rescored, 1);
             }
         }
+    }
     }
 }
 
