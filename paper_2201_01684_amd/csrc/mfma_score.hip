@@ -261,14 +261,22 @@ __global__ __launch_bounds__(kThreads) void mfma_edge_kernel(MfmaArgs a) {
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     if (threadIdx.x == 0) out[0] = 0.0;
     double carry = 0.0;
+    // the next tile's samples are loaded while this tile is scanned
+    float nxt[kEdgePer];
+    auto load_tile = [&](int64_t k0, float (&v)[kEdgePer]) {
+#pragma unroll
+        for (int r = 0; r < kEdgePer; ++r) {
+            const int64_t kk = k0 + (int)threadIdx.x + r * kThreads;
+            v[r] = kk < span - 1 ? p[side == 0 ? kk : n - 1 - kk] : 0.0f;
+        }
+    };
+    if (span - 1 > 0) load_tile(0, nxt);
     for (int64_t k0 = 0; k0 < span - 1; k0 += kEdgeTile) {
         {
             float v[kEdgePer];
 #pragma unroll
-            for (int r = 0; r < kEdgePer; ++r) {
-                const int64_t kk = k0 + (int)threadIdx.x + r * kThreads;
-                v[r] = kk < span - 1 ? p[side == 0 ? kk : n - 1 - kk] : 0.0f;
-            }
+            for (int r = 0; r < kEdgePer; ++r) v[r] = nxt[r];
+            if (k0 + kEdgeTile < span - 1) load_tile(k0 + kEdgeTile, nxt);
 #pragma unroll
             for (int r = 0; r < kEdgePer; ++r) {
                 const int k = (int)threadIdx.x + r * kThreads;
