@@ -1,7 +1,7 @@
 """Pins of the oracle's Algorithm 2 similarity error (GMM groups + SMAPE).
 
 The paper prints no worked example, and the EM details of the Gaussian mixture
-(initialisation, iterations) are this build's reading.  Pinned: cases whose
+(initialisation, iterations) are not given there and are fixed here.  Pinned: cases whose
 answer does not depend on those details (well-separated clusters, which any
 mixture fit recovers; a single group; exact periods; the invariances of the
 definition), and the EM trajectory itself on overlapping clusters against
