@@ -122,7 +122,7 @@ __device__ __forceinline__ void block_masked(const float (&xs)[16],
 
 // Sixteen lags a lane run at most four waves a SIMD: that leaves the compiler
 // 128 registers (it uses 109 instead of 92 at five waves), 0.6-0.9% faster on
-// the 1024- and 256-trace workloads (A/B on one box).  The same bound slows the
+// the 1024- and 256-trace workloads (A/B on one GPU).  The same bound slows the
 // eight-lag instance by 4%, so the others keep the default.
 template <int kBT, int kWavesPerGroup, int kShift>
 __global__ __launch_bounds__(kWave * kWavesPerGroup)
